@@ -1,0 +1,204 @@
+"""Plain fp64 CPU oracle of Jacap scoring, top-B selection and KV compaction.
+
+TEST INFRASTRUCTURE ONLY. Only the tests, the package smoke check and the
+benchmark's CPU-baseline leg may import or run this module; the product path
+(the HIP library and its Python binding) never does. It shares no code with
+the HIP path.
+
+It follows Algorithm 1 (Jacap) of Sec. 3.4 and the equations it is built from
+(centre attention, Eq. 8 importance weight, Eq. 9 capacity matrix, Eq. 10
+leverage score), step by step, in float64. Readings of points the paper leaves
+open (all listed in the design doc):
+
+* ridge: A = ridge*I + sum_j w_j u_j u_j^T with w_j from Eq. 8. ridge=1 is
+  Eq. 9; ridge=1/d reproduces Algorithm 1 literally (it drops the 1/d_k of
+  Eq. 8); ridge=0 is the plain statistical leverage form of App. B.2.
+* query statistics: sample mean and the 1/N (maximum-likelihood) covariance of
+  the observation-window queries (Sec. 3.4 end: estimated from observed
+  queries; App. B.2: diagonal covariance in practice).
+* GQA: the G query heads sharing a KV head are pooled into one sample of
+  G*w queries.
+* u_i = v_i (Sec. 3.4 end: the proxy used when W_O is not applied).
+* TOP-B: order by (fp32 score desc, index asc), NaN lowest, -0 == +0, and
+  return the kept indices in ascending order; |C| = min(B, n).
+"""
+
+from __future__ import annotations
+
+import math
+
+import numpy as np
+import scipy.linalg
+
+DIAG = "diag"
+FULL = "full"
+
+
+# ---------------------------------------------------------------------------
+# Step 0: query statistics (mu_Q, Lambda_Q)
+# ---------------------------------------------------------------------------
+
+def pool_queries(q_group: np.ndarray) -> np.ndarray:
+    """Stack the window queries of the G query heads of one KV head: (G, w, d) -> (G*w, d)."""
+    q_group = np.asarray(q_group, dtype=np.float64)
+    return q_group.reshape(-1, q_group.shape[-1])
+
+
+def query_statistics(Qs: np.ndarray, cov_mode: str = DIAG):
+    """Centre mu_Q and covariance Lambda_Q of the local query model q = mu_Q + dq,
+    dq ~ N(0, Lambda_Q) (Sec. 3.3), estimated from the observed window queries
+    (Sec. 3.4, last paragraph). DIAG returns the per-channel variances (App. B.2:
+    diagonal covariance in practice); FULL returns the d x d matrix."""
+    Qs = np.asarray(Qs, dtype=np.float64)
+    N = Qs.shape[0]
+    mu = Qs.sum(axis=0) / N
+    dev = Qs - mu
+    if cov_mode == DIAG:
+        return mu, (dev * dev).sum(axis=0) / N
+    if cov_mode == FULL:
+        return mu, dev.T @ dev / N
+    raise ValueError(cov_mode)
+
+
+# ---------------------------------------------------------------------------
+# Algorithm 1, step 1: attention at the query centre over the full pool
+# ---------------------------------------------------------------------------
+
+def centre_logits(K: np.ndarray, mu: np.ndarray, tau: float) -> np.ndarray:
+    """Logits k_i^T mu_Q / (tau sqrt(d_k)) of the subset-independent centre
+    attention (Sec. 3.4, definition of bar-alpha; Algorithm 1, first step)."""
+    d = K.shape[1]
+    return (K @ mu) / (tau * math.sqrt(d))
+
+
+def centre_attention(z: np.ndarray):
+    """bar-alpha = softmax(z) over every cached token, and 1 - bar-alpha.
+
+    1 - bar-alpha_i is formed as (Z - e_i) / Z, the mass of the other tokens,
+    so that it does not cancel when bar-alpha_i approaches 1."""
+    m = z.max()
+    e = np.exp(z - m)
+    Z = e.sum()
+    return e / Z, (Z - e) / Z
+
+
+# ---------------------------------------------------------------------------
+# Algorithm 1, step 2: softmax-sensitive importance weight (Eq. 8)
+# ---------------------------------------------------------------------------
+
+def query_response(K: np.ndarray, lam: np.ndarray) -> np.ndarray:
+    """kappa_i = k_i^T Lambda_Q k_i (Sec. 3.4, diagonal query response)."""
+    K = np.asarray(K, dtype=np.float64)
+    if lam.ndim == 1:
+        return (K * K) @ lam
+    return np.einsum("ia,ab,ib->i", K, lam, K)
+
+
+def importance_weights(alpha: np.ndarray, one_minus_alpha: np.ndarray,
+                       kappa: np.ndarray, d: int) -> np.ndarray:
+    """w_i = (1/d_k) rho_i^2 kappa_i with rho_i = bar-alpha_i (1 - bar-alpha_i)
+    (Eq. 8; rho is the diagonal softmax sensitivity of Sec. 3.4)."""
+    rho = alpha * one_minus_alpha
+    return rho * rho * kappa / d
+
+
+# ---------------------------------------------------------------------------
+# Algorithm 1, steps 3-4: capacity matrix (Eq. 9) and leverage score (Eq. 10)
+# ---------------------------------------------------------------------------
+
+def capacity_matrix(U: np.ndarray, w: np.ndarray, ridge: float) -> np.ndarray:
+    """A = ridge * I + sum_j w_j u_j u_j^T over the whole candidate pool (Eq. 9)."""
+    U = np.asarray(U, dtype=np.float64)
+    d = U.shape[1]
+    return ridge * np.eye(d) + U.T @ (w[:, None] * U)
+
+
+def leverage_scores(U: np.ndarray, w: np.ndarray, A: np.ndarray):
+    """score_i = w_i u_i^T A^{-1} u_i (Eq. 10), evaluated as w_i ||L^{-1} u_i||^2
+    with A = L L^T. Returns (scores, singular); when A is not positive definite
+    (ridge 0 and a rank-deficient weighted Gram) the Moore-Penrose inverse of A
+    is used instead and singular is True."""
+    U = np.asarray(U, dtype=np.float64)
+    try:
+        L = np.linalg.cholesky(A)
+    except np.linalg.LinAlgError:
+        return leverage_scores_eigh(U, w, A), True
+    Y = scipy.linalg.solve_triangular(L, U.T, lower=True)
+    return w * (Y * Y).sum(axis=0), False
+
+
+def leverage_scores_eigh(U: np.ndarray, w: np.ndarray, A: np.ndarray,
+                         rcond: float = 1e-12) -> np.ndarray:
+    """The same score through the eigendecomposition A = Q diag(s) Q^T:
+    w_i sum_j (q_j^T u_i)^2 / s_j, dropping s_j <= rcond * max(s) (pseudo-inverse)."""
+    s, Q = np.linalg.eigh(A)
+    keep = s > rcond * max(float(s.max()), 0.0)
+    P = np.asarray(U, dtype=np.float64) @ Q[:, keep]
+    return w * (P * P / s[keep]).sum(axis=1)
+
+
+# ---------------------------------------------------------------------------
+# Algorithm 1, step 5: TOP-B, then the retained cache Z_C (Sec. 3.1)
+# ---------------------------------------------------------------------------
+
+def to_fp32(scores: np.ndarray) -> np.ndarray:
+    """Round fp64 scores once to fp32 (round to nearest even); selection is
+    decided on these."""
+    return np.asarray(scores, dtype=np.float64).astype(np.float32)
+
+
+def select_top(scores32: np.ndarray, budget: int) -> np.ndarray:
+    """Indices of the min(budget, n) best tokens by (score desc, index asc), NaN
+    ranked lowest and -0 equal to +0, returned in ascending index order (int32)."""
+    s = np.asarray(scores32, dtype=np.float32).astype(np.float64)
+    n = s.shape[0]
+    b = max(0, min(int(budget), n))
+    nan = np.isnan(s)
+    key = np.where(nan, 0.0, s) + 0.0        # +0.0 turns -0 into +0
+    # lexsort: last key is primary -> NaN flag, then -score, then index.
+    order = np.lexsort((np.arange(n), -key, nan))
+    return np.sort(order[:b]).astype(np.int32)
+
+
+def compact(K: np.ndarray, V: np.ndarray, idx: np.ndarray):
+    """Retained cache Z_C = {(k_i, v_i)}_{i in C} (Sec. 3.1): an exact gather."""
+    return K[idx], V[idx]
+
+
+# ---------------------------------------------------------------------------
+# One unit (sequence, layer, KV head) end to end
+# ---------------------------------------------------------------------------
+
+def score_unit(q_group, K, V, *, tau: float = 10.0, ridge: float = 1.0,
+               cov_mode: str = DIAG) -> dict:
+    """Jacap scores of one KV head (Algorithm 1 steps 1-4) with every
+    intermediate, in float64. q_group is (G, w, d) or (N, d); K and V are (n, d)."""
+    K = np.asarray(K, dtype=np.float64)
+    V = np.asarray(V, dtype=np.float64)
+    n, d = K.shape
+    Qs = pool_queries(q_group)
+    mu, lam = query_statistics(Qs, cov_mode)
+    out = {"mu": mu, "lam": lam, "n": n, "d": d}
+    if n == 0:
+        out.update(scores=np.zeros(0), w=np.zeros(0), singular=False,
+                   A=ridge * np.eye(d))
+        return out
+    z = centre_logits(K, mu, tau)
+    alpha, one_minus = centre_attention(z)
+    kappa = query_response(K, lam)
+    w = importance_weights(alpha, one_minus, kappa, d)
+    A = capacity_matrix(V, w, ridge)
+    scores, singular = leverage_scores(V, w, A)
+    out.update(z=z, alpha=alpha, one_minus_alpha=one_minus, kappa=kappa, w=w,
+               A=A, scores=scores, singular=singular)
+    return out
+
+
+def evict_unit(q_group, K, V, budget: int, **kw) -> dict:
+    """score_unit, then TOP-B on the fp32 scores and the compacted K', V'."""
+    out = score_unit(q_group, K, V, **kw)
+    s32 = to_fp32(out["scores"])
+    idx = select_top(s32, budget)
+    Kc, Vc = compact(np.asarray(K), np.asarray(V), idx)
+    out.update(scores32=s32, idx=idx, k_out=Kc, v_out=Vc)
+    return out
