@@ -1,0 +1,171 @@
+"""Benchmark of the Jacap eviction pass (score + select + compact) on one MI355X.
+
+One step = jacap_evict over the whole synthetic batch (every layer and KV
+head): window statistics, centre attention, Eq. 8 weights, weighted Gram,
+Cholesky, leverage scores, top-B selection and K/V compaction. Inputs are
+resident in HBM before timing starts.
+
+Prints one JSON line ("Measurement"):
+  value        cached tokens scored+selected per second (full-model tokens:
+               one token = its K/V rows in every layer and KV head)
+  roofline     algorithmic HBM bytes (K and V read once) / step time
+  cpu_baseline the fp64 oracle timed on this host on a bounded sample
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+import torch
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_HBM_GBS = 8000.0
+METRIC = "cached tokens scored+selected/sec per GPU; achieved HBM GB/s vs peak"
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="long128k")
+    ap.add_argument("--budget", type=int, default=None)
+    ap.add_argument("--ridge", type=float, default=1.0)
+    ap.add_argument("--tau", type=float, default=10.0)
+    ap.add_argument("--cpu-seconds", type=float, default=15.0,
+                    help="time budget of the oracle CPU baseline sample")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    return ap.parse_args()
+
+
+def ensure_built():
+    lib = os.path.join(ROOT, "paper_2609_08131_amd", "libjacap.so")
+    if not os.path.exists(lib):
+        from paper_2609_08131_amd import build
+        build.build()
+
+
+def cpu_baseline(case, budget, tau, ridge, seconds):
+    """Time the fp64 oracle on as many units (sequence, layer, KV head) of the
+    same workload as fit in `seconds`; scale to full-model tokens/s."""
+    from oracle import jacap_oracle as jo
+    try:
+        import threadpoolctl
+        info = threadpoolctl.threadpool_info()
+        cores = max([i.get("num_threads", 1) for i in info] + [1])
+    except Exception:
+        cores = os.cpu_count() or 1
+    w = case.workload
+    units = [(b, l, h) for b in range(case.num_seqs) for l in range(w.num_layers)
+             for h in range(w.num_kv_heads)]
+    rng = np.random.default_rng(0)
+    order = rng.permutation(len(units))
+    done_tokens, done_units = 0, 0
+    t_total = 0.0
+    for i in order:
+        b, l, h = units[i]
+        q, k, v = case.unit_arrays(b, l, h)          # host copy, not timed
+        t0 = time.perf_counter()
+        jo.evict_unit(q, k, v, budget, tau=tau, ridge=ridge)
+        t_total += time.perf_counter() - t0
+        done_tokens += k.shape[0]
+        done_units += 1
+        if t_total >= seconds:
+            break
+    entries_per_s = done_tokens / t_total
+    tokens_per_s = entries_per_s / (w.num_layers * w.num_kv_heads)
+    return {"value": tokens_per_s, "unit": "tokens/s", "cores": int(cores), "kind": "oracle",
+            "sample": f"{done_units} of {len(units)} units (seq, layer, kv head) of {w.name}, "
+                      f"{done_tokens} token-entries in {t_total:.1f} s; tokens/s = "
+                      f"entries/s / (layers*kv_heads)",
+            "entries_per_s": entries_per_s}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1",
+                          "n_gpus": args.gpus}))
+        sys.exit(2)
+    ensure_built()
+    from jacap_synth import make_case
+    from paper_2609_08131_amd import jacap
+
+    torch.cuda.set_device(0)
+    case = make_case(args.workload, device="cuda")
+    w = case.workload
+    budget = args.budget if args.budget is not None else w.budget_k
+    params = jacap.Params(budget_k=budget, temperature=args.tau, ridge=args.ridge)
+    prob = jacap.prepare(case.q_win, case.k, case.v, case.seq_offsets, case.seq_lens, params)
+    stream = torch.cuda.current_stream()
+    torch.cuda.synchronize()
+
+    for _ in range(args.warmup):
+        jacap.run_evict(prob, case.q_win, case.k, case.v, stream)
+    flags = jacap.read_status(prob.ws, stream)
+    torch.cuda.synchronize()
+
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter()
+    for s, e in ev:
+        s.record(stream)
+        jacap.run_evict(prob, case.q_win, case.k, case.v, stream)
+        e.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t_wall
+    times = np.array([s.elapsed_time(e) for s, e in ev])   # ms
+    ms = float(times.mean())
+
+    esize = case.k.element_size()
+    d = w.head_dim
+    entries = case.total_tokens * w.num_layers * w.num_kv_heads
+    alg_bytes = 2 * entries * d * esize                    # K and V read once
+    tokens_per_s = case.total_tokens / (ms * 1e-3)
+    achieved = alg_bytes / (ms * 1e-3) / 1e9
+
+    out = {
+        "metric": METRIC,
+        "value": tokens_per_s,
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms,
+        "ms_per_step_min": float(times.min()),
+        "wall_s": wall,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": w.dtype,
+        "data": "synthetic",
+        "entries_per_s": entries / (ms * 1e-3),
+        "status_flags": flags,
+        "config": {
+            "workload": w.name, "num_seqs": case.num_seqs, "layers": w.num_layers,
+            "kv_heads": w.num_kv_heads, "q_heads": w.num_q_heads, "head_dim": d,
+            "tokens": case.total_tokens, "window": w.window, "budget_k": budget,
+            "tau": args.tau, "ridge": args.ridge, "cov_mode": "diag",
+        },
+        "roofline": {
+            "bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+            "frac": achieved / PEAK_HBM_GBS, "traffic": None,
+            "scope": "whole jacap_evict step (all kernels); algorithmic bytes = K+V read once",
+            "alg_bytes_per_step": alg_bytes,
+        },
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(case, budget, args.tau, args.ridge, args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,177 @@
+/*
+ * jacap.h -- C ABI of libjacap.so: Jacap KV-cache eviction scoring, top-B
+ * selection and compaction on AMD Instinct MI355X (gfx950).
+ *
+ * The method is Algorithm 1 of the Jacap paper (Sec. 3.4): for every cached
+ * token i of one (sequence, layer, KV head) -- a "unit" --
+ *
+ *   bar-alpha_i = softmax_i( k_i . mu_Q / (tau sqrt(d)) )      centre attention
+ *   kappa_i     = k_i^T Lambda_Q k_i                           query response
+ *   w_i         = bar-alpha_i^2 (1 - bar-alpha_i)^2 kappa_i / d   (Eq. 8)
+ *   A           = ridge I + sum_j w_j v_j v_j^T                (Eq. 9)
+ *   score_i     = w_i v_i^T A^{-1} v_i                         (Eq. 10)
+ *
+ * then keeps the B highest-scoring tokens (Algorithm 1, TOP-B) and gathers
+ * the retained cache Z_C = {(k_i, v_i)}_{i in C} (Sec. 3.1). The query
+ * statistics (mu_Q, Lambda_Q) are the sample mean and 1/N covariance of the
+ * observation-window queries (Sec. 3.4, last paragraph); the G = H_q / H_kv
+ * query heads that share a KV head are pooled into one sample of G*w queries.
+ * u_i = v_i is the output-direction proxy the paper uses when W_O is not
+ * applied (Sec. 3.4).
+ *
+ * ridge: ridge = 1 is Eq. 9 as printed; ridge = 1/d gives exactly the scores
+ * of Algorithm 1 as printed (whose weight omits the 1/d of Eq. 8); ridge = 0
+ * is the plain statistical leverage score of App. B.1/B.2.
+ *
+ * Conventions common to every entry point
+ * ---------------------------------------
+ * - All data pointers are DEVICE pointers on the current HIP device, except
+ *   the two descriptor structs and `flags` of jacap_read_status, which are
+ *   host pointers read (or written) during the call only.
+ * - The caller owns every buffer. The library allocates no memory, keeps no
+ *   pointer after returning and holds no global state; all work is enqueued
+ *   asynchronously on `stream` (a hipStream_t; NULL = the null stream).
+ *   Calls on different streams are independent if they use distinct
+ *   workspaces.
+ * - Host-detectable errors (null or misaligned pointers, bad shapes or
+ *   strides, unsupported head_dim or dtype, too small a workspace) return an
+ *   error code and enqueue nothing. A failed launch returns JACAP_ERR_HIP.
+ * - Data-dependent problems are reported through sticky device flags in the
+ *   workspace (read with jacap_read_status): JACAP_FLAG_NONFINITE when a
+ *   query, key or value is NaN/Inf, JACAP_FLAG_SINGULAR when A is not
+ *   numerically positive definite (only possible at ridge 0). The scores of
+ *   an affected unit are NaN, and NaN ranks lowest in selection.
+ *
+ * Layouts (element strides, head_dim contiguous, base pointers 16-byte
+ * aligned, every stride a multiple of 8 elements):
+ *   K, V      : element (layer l, kv head h, packed token t, channel c) at
+ *               l*kv_stride_layer + h*kv_stride_head + t*kv_stride_token + c.
+ *               Sequence b owns packed tokens seq_offsets[b] .. seq_offsets[b+1]-1.
+ *               Default [L][H_kv][T_total][d].
+ *   Q window  : element (seq b, layer l, query head g, position p, channel c)
+ *               at b*q_stride_seq + l*q_stride_layer + g*q_stride_head +
+ *               p*q_stride_pos + c. Default [B][L][H_q][w][d]. Query heads
+ *               h*G .. h*G+G-1 serve KV head h.
+ *   scores    : float32 [L][H_kv][T_total] (dense), the per-token scores.
+ *   idx       : int32 [B][L][H_kv][budget_k] (dense): kept token positions
+ *               (0-based within the sequence), ascending; slots past
+ *               min(budget_k, n_b) hold -1.
+ *   K', V'    : row j of unit (b, l, h) at b*out_stride_seq +
+ *               l*out_stride_layer + h*out_stride_head + j*out_stride_row.
+ *               Default [B][L][H_kv][budget_k][d]. Rows past min(budget_k, n_b)
+ *               are left untouched.
+ */
+#ifndef JACAP_H
+#define JACAP_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum jacap_status {
+  JACAP_OK = 0,
+  JACAP_ERR_INVALID_ARG = 1, /* null/misaligned pointer, bad shape/stride/parameter */
+  JACAP_ERR_UNSUPPORTED = 2, /* head_dim not in {64, 128}, or unknown dtype / cov_mode */
+  JACAP_ERR_WORKSPACE = 3,   /* workspace smaller than jacap_workspace_size() */
+  JACAP_ERR_HIP = 4          /* a HIP launch or runtime call failed */
+} jacap_status;
+
+enum jacap_cov_mode {
+  JACAP_COV_DIAG = 0, /* Lambda_Q = per-channel variances (App. B.2 "in practice") */
+  JACAP_COV_FULL = 1  /* Lambda_Q = full d x d covariance (Algorithm 1 input) */
+};
+
+enum jacap_dtype {
+  JACAP_DTYPE_FP32 = 0, /* K, V, Q stored as float32 */
+  JACAP_DTYPE_BF16 = 1  /* K, V, Q stored as bfloat16 */
+};
+
+enum jacap_flags {
+  JACAP_FLAG_NONFINITE = 1u << 0, /* a NaN/Inf input reached a unit's statistics */
+  JACAP_FLAG_SINGULAR = 1u << 1,  /* A = ridge I + M numerically singular: a Cholesky
+                                     pivot fell below 1e-4 (bf16 inputs, fp32-accumulated
+                                     Gram) or 1e-12 (fp32 inputs, fp64 Gram) of its
+                                     diagonal entry; in practice ridge 0 with a
+                                     rank-deficient weighted Gram */
+  JACAP_FLAG_BAD_OFFSETS = 1u << 2 /* a sequence's offsets contradict max_seq_len /
+                                      total_tokens; it was treated as empty */
+};
+
+/* Method and shape parameters (host struct). */
+typedef struct jacap_config {
+  int32_t num_layers;   /* L >= 1 */
+  int32_t num_kv_heads; /* H_kv >= 1 */
+  int32_t num_q_heads;  /* H_q, a positive multiple of H_kv */
+  int32_t head_dim;     /* d: 64 or 128 */
+  int32_t window;       /* w >= 1 observation-window queries per query head */
+  int32_t budget_k;     /* B >= 0 tokens kept per unit (Algorithm 1 budget) */
+  float temperature;    /* tau > 0 (the paper's best value is 10, Sec. 4.4) */
+  float ridge;          /* ridge >= 0 (see the header comment) */
+  int32_t cov_mode;     /* enum jacap_cov_mode */
+  int32_t dtype;        /* enum jacap_dtype */
+} jacap_config;
+
+/* Batch geometry and strides (host struct; seq_offsets is a device pointer). */
+typedef struct jacap_batch {
+  int32_t num_seqs;           /* B >= 1 */
+  int32_t max_seq_len;        /* >= every n_b = seq_offsets[b+1]-seq_offsets[b] */
+  int64_t total_tokens;       /* T_total = seq_offsets[B] */
+  const int32_t* seq_offsets; /* device int32 [B+1], non-decreasing, [0] = 0 */
+  int64_t k_stride_layer, k_stride_head, k_stride_token;
+  int64_t v_stride_layer, v_stride_head, v_stride_token;
+  int64_t q_stride_seq, q_stride_layer, q_stride_head, q_stride_pos;
+  int64_t out_stride_seq, out_stride_layer, out_stride_head, out_stride_row;
+} jacap_batch;
+
+/* Bytes of device workspace that jacap_score / jacap_select / jacap_evict
+ * need for this configuration and batch (an upper bound that depends only on
+ * the host fields). Returns JACAP_ERR_INVALID_ARG / _UNSUPPORTED for an
+ * invalid configuration. Workspace base pointers must be 256-byte aligned. */
+jacap_status jacap_workspace_size(const jacap_config* cfg, const jacap_batch* batch,
+                                  size_t* bytes);
+
+/* Algorithm 1 steps 1-4 (centre attention, Eq. 8 weights, Eq. 9 capacity
+ * matrix, Eq. 10 leverage scores) for every unit: writes scores[L][H_kv][T]
+ * (float32). q_win, k, v are in cfg->dtype. Resets the workspace status
+ * flags first. */
+jacap_status jacap_score(const jacap_config* cfg, const jacap_batch* batch,
+                         const void* q_win, const void* k, const void* v, float* scores,
+                         void* ws, size_t ws_bytes, void* stream);
+
+/* Algorithm 1 step 5 (TOP-B): for each unit keeps min(budget_k, n_b) tokens
+ * ordered by (score descending, position ascending), NaN lowest and -0 equal
+ * to +0, and writes their positions in ascending order to idx (-1 padding).
+ * Bit-exact and deterministic for given scores. */
+jacap_status jacap_select(const jacap_config* cfg, const jacap_batch* batch,
+                          const float* scores, int32_t* idx, void* ws, size_t ws_bytes,
+                          void* stream);
+
+/* Retained cache Z_C (Sec. 3.1): K'[j] = K[idx[j]], V'[j] = V[idx[j]], exact
+ * copies in cfg->dtype, for every idx[j] >= 0. */
+jacap_status jacap_compact(const jacap_config* cfg, const jacap_batch* batch,
+                           const int32_t* idx, const void* k, const void* v, void* k_out,
+                           void* v_out, void* stream);
+
+/* jacap_score, jacap_select and jacap_compact enqueued as one launch
+ * sequence on `stream`. */
+jacap_status jacap_evict(const jacap_config* cfg, const jacap_batch* batch,
+                         const void* q_win, const void* k, const void* v, float* scores,
+                         int32_t* idx, void* k_out, void* v_out, void* ws, size_t ws_bytes,
+                         void* stream);
+
+/* Synchronises `stream` and returns the sticky device flags (enum
+ * jacap_flags, OR-ed) written by the last jacap_score / jacap_evict that used
+ * this workspace. */
+jacap_status jacap_read_status(const void* ws, void* stream, uint32_t* flags);
+
+/* Static, human-readable name of a status code. */
+const char* jacap_status_string(jacap_status s);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* JACAP_H */

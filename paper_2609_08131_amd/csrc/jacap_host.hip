@@ -1,0 +1,233 @@
+// C-ABI entry points of libjacap.so: argument validation, workspace layout
+// and the launch sequences of jacap_score / jacap_select / jacap_compact /
+// jacap_evict. Host-detectable errors return before anything is enqueued.
+#include <math.h>
+#include <string.h>
+
+#include "jacap_internal.hpp"
+
+using namespace jacap;
+
+namespace {
+
+inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+inline bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+jacap_status check_config(const jacap_config* c) {
+  if (!c) return JACAP_ERR_INVALID_ARG;
+  if (c->num_layers < 1 || c->num_kv_heads < 1 || c->num_q_heads < 1) return JACAP_ERR_INVALID_ARG;
+  if (c->num_q_heads % c->num_kv_heads != 0) return JACAP_ERR_INVALID_ARG;
+  if (c->window < 1 || c->budget_k < 0) return JACAP_ERR_INVALID_ARG;
+  if (!(c->temperature > 0.0f) || !isfinite(c->temperature)) return JACAP_ERR_INVALID_ARG;
+  if (!(c->ridge >= 0.0f) || !isfinite(c->ridge)) return JACAP_ERR_INVALID_ARG;
+  if (c->head_dim != 64 && c->head_dim != 128) return JACAP_ERR_UNSUPPORTED;
+  if (c->dtype != JACAP_DTYPE_FP32 && c->dtype != JACAP_DTYPE_BF16) return JACAP_ERR_UNSUPPORTED;
+  if (c->cov_mode != JACAP_COV_DIAG && c->cov_mode != JACAP_COV_FULL) return JACAP_ERR_UNSUPPORTED;
+  return JACAP_OK;
+}
+
+jacap_status check_batch(const jacap_config* c, const jacap_batch* b) {
+  if (!b || !b->seq_offsets) return JACAP_ERR_INVALID_ARG;
+  if (b->num_seqs < 1 || b->max_seq_len < 0 || b->total_tokens < 0) return JACAP_ERR_INVALID_ARG;
+  if ((int64_t)b->num_seqs * c->num_layers * c->num_kv_heads > 65535) return JACAP_ERR_UNSUPPORTED;
+  if (b->total_tokens > (int64_t)INT32_MAX) return JACAP_ERR_UNSUPPORTED;
+  const int64_t st[] = {b->k_stride_layer, b->k_stride_head, b->k_stride_token,
+                        b->v_stride_layer, b->v_stride_head, b->v_stride_token,
+                        b->q_stride_seq, b->q_stride_layer, b->q_stride_head, b->q_stride_pos,
+                        b->out_stride_seq, b->out_stride_layer, b->out_stride_head,
+                        b->out_stride_row};
+  for (int64_t s : st)
+    if (s < 0 || (s % 8) != 0) return JACAP_ERR_INVALID_ARG;
+  if (b->k_stride_token < c->head_dim || b->v_stride_token < c->head_dim) return JACAP_ERR_INVALID_ARG;
+  if (b->q_stride_pos < c->head_dim || b->out_stride_row < c->head_dim) return JACAP_ERR_INVALID_ARG;
+  return JACAP_OK;
+}
+
+Workspace layout(const jacap_config* c, const jacap_batch* b) {
+  Workspace w{};
+  const int64_t U = (int64_t)b->num_seqs * c->num_layers * c->num_kv_heads;
+  const int64_t D = c->head_dim;
+  const int64_t LHT = (int64_t)c->num_layers * c->num_kv_heads * b->total_tokens;
+  const int maxn = b->max_seq_len;
+  w.mfma = c->dtype == JACAP_DTYPE_BF16;
+  w.kchunks = (maxn + kKChunk - 1) / kKChunk;
+  w.gchunk = w.mfma ? kGChunkMfma : kGChunkPrecise;
+  w.gchunks = (maxn + w.gchunk - 1) / w.gchunk;
+  w.gparts = w.mfma ? kMfmaGramParts : 1;
+  w.lchunks = (maxn + kLChunk - 1) / kLChunk;
+  const int64_t NB = D / 16;
+  const int64_t npair = NB * (NB + 1) / 2;
+  const int64_t part_bytes = w.mfma ? (int64_t)kMfmaGramParts * npair * 256 * 4 : D * D * 8;
+  size_t o = 0;
+  auto take = [&](size_t bytes) { size_t r = o; o = align256(o + bytes); return r; };
+  w.status = take(4);
+  w.uflags = take(4 * U);
+  w.mu = take(8 * U * D);
+  w.lam = take(8 * U * D);
+  w.lamfull = take(c->cov_mode == JACAP_COV_FULL ? 4 * U * D * D : 4);
+  w.smax_m = take(4 * U);
+  w.smax_z = take(8 * U);
+  w.z = take(4 * LHT);
+  w.kappa = take(4 * LHT);
+  w.cstat = take(8 * U * (int64_t)w.kchunks);
+  w.gram = take((size_t)(U * (int64_t)w.gchunks * part_bytes));
+  w.linv64 = take(8 * U * D * D);
+  w.linv32 = take(4 * U * D * D);
+  w.total = o;
+  return w;
+}
+
+Geo make_geo(const jacap_config* c, const jacap_batch* b) {
+  Geo g{};
+  g.L = c->num_layers;
+  g.H = c->num_kv_heads;
+  g.Hq = c->num_q_heads;
+  g.G = c->num_q_heads / c->num_kv_heads;
+  g.D = c->head_dim;
+  g.w = c->window;
+  g.B = b->num_seqs;
+  g.U = b->num_seqs * c->num_layers * c->num_kv_heads;
+  g.maxn = b->max_seq_len;
+  g.T = b->total_tokens;
+  g.seq_off = b->seq_offsets;
+  g.ksl = b->k_stride_layer; g.ksh = b->k_stride_head; g.kst = b->k_stride_token;
+  g.vsl = b->v_stride_layer; g.vsh = b->v_stride_head; g.vst = b->v_stride_token;
+  g.qss = b->q_stride_seq; g.qsl = b->q_stride_layer; g.qsh = b->q_stride_head; g.qsp = b->q_stride_pos;
+  g.oss = b->out_stride_seq; g.osl = b->out_stride_layer; g.osh = b->out_stride_head; g.osr = b->out_stride_row;
+  return g;
+}
+
+jacap_status prepare(const jacap_config* c, const jacap_batch* b, void* ws, size_t ws_bytes,
+                     void* stream, Launch* L) {
+  jacap_status s = check_config(c);
+  if (s != JACAP_OK) return s;
+  s = check_batch(c, b);
+  if (s != JACAP_OK) return s;
+  L->cfg = c;
+  L->geo = make_geo(c, b);
+  L->ws = layout(c, b);
+  L->wsp = static_cast<char*>(ws);
+  L->stream = static_cast<hipStream_t>(stream);
+  if (ws != nullptr || ws_bytes != 0) {
+    if (!ws || (reinterpret_cast<uintptr_t>(ws) & 255u)) return JACAP_ERR_INVALID_ARG;
+    if (ws_bytes < L->ws.total) return JACAP_ERR_WORKSPACE;
+  }
+  return JACAP_OK;
+}
+
+#define JACAP_TRY(expr)                         \
+  do {                                          \
+    if ((expr) != hipSuccess) return JACAP_ERR_HIP; \
+  } while (0)
+
+jacap_status run_score(const Launch& L, const void* q, const void* k, const void* v, float* scores) {
+  JACAP_TRY(launch_init(L));
+  JACAP_TRY(launch_qstats(L, q));
+  JACAP_TRY(launch_kpass(L, k));
+  JACAP_TRY(launch_softmax_merge(L));
+  JACAP_TRY(launch_gram(L, v));
+  JACAP_TRY(launch_factor(L));
+  JACAP_TRY(launch_leverage(L, v, scores));
+  return JACAP_OK;
+}
+
+bool score_ptrs_ok(const void* q, const void* k, const void* v, const float* scores) {
+  return q && k && v && scores && aligned16(q) && aligned16(k) && aligned16(v) && aligned16(scores);
+}
+
+}  // namespace
+
+extern "C" {
+
+jacap_status jacap_workspace_size(const jacap_config* cfg, const jacap_batch* batch, size_t* bytes) {
+  if (!bytes) return JACAP_ERR_INVALID_ARG;
+  jacap_status s = check_config(cfg);
+  if (s != JACAP_OK) return s;
+  s = check_batch(cfg, batch);
+  if (s != JACAP_OK) return s;
+  *bytes = layout(cfg, batch).total;
+  return JACAP_OK;
+}
+
+jacap_status jacap_score(const jacap_config* cfg, const jacap_batch* batch, const void* q_win,
+                         const void* k, const void* v, float* scores, void* ws, size_t ws_bytes,
+                         void* stream) {
+  Launch L;
+  if (!ws) return JACAP_ERR_INVALID_ARG;
+  jacap_status s = prepare(cfg, batch, ws, ws_bytes, stream, &L);
+  if (s != JACAP_OK) return s;
+  if (!score_ptrs_ok(q_win, k, v, scores)) return JACAP_ERR_INVALID_ARG;
+  if (batch->total_tokens == 0) return launch_init(L) == hipSuccess ? JACAP_OK : JACAP_ERR_HIP;
+  return run_score(L, q_win, k, v, scores);
+}
+
+jacap_status jacap_select(const jacap_config* cfg, const jacap_batch* batch, const float* scores,
+                          int32_t* idx, void* ws, size_t ws_bytes, void* stream) {
+  Launch L;
+  jacap_status s = prepare(cfg, batch, ws, ws_bytes, stream, &L);
+  if (s != JACAP_OK) return s;
+  if (cfg->budget_k == 0) return JACAP_OK;
+  if (!idx || (!scores && batch->total_tokens > 0)) return JACAP_ERR_INVALID_ARG;
+  if (!aligned16(idx) || (scores && !aligned16(scores))) return JACAP_ERR_INVALID_ARG;
+  return launch_select(L, scores, idx) == hipSuccess ? JACAP_OK : JACAP_ERR_HIP;
+}
+
+jacap_status jacap_compact(const jacap_config* cfg, const jacap_batch* batch, const int32_t* idx,
+                           const void* k, const void* v, void* k_out, void* v_out, void* stream) {
+  Launch L;
+  jacap_status s = prepare(cfg, batch, nullptr, 0, stream, &L);
+  if (s != JACAP_OK) return s;
+  if (cfg->budget_k == 0) return JACAP_OK;
+  if (!idx || !k || !v || !k_out || !v_out) return JACAP_ERR_INVALID_ARG;
+  if (!aligned16(k) || !aligned16(v) || !aligned16(k_out) || !aligned16(v_out)) return JACAP_ERR_INVALID_ARG;
+  return launch_compact(L, idx, k, v, k_out, v_out) == hipSuccess ? JACAP_OK : JACAP_ERR_HIP;
+}
+
+jacap_status jacap_evict(const jacap_config* cfg, const jacap_batch* batch, const void* q_win,
+                         const void* k, const void* v, float* scores, int32_t* idx, void* k_out,
+                         void* v_out, void* ws, size_t ws_bytes, void* stream) {
+  Launch L;
+  if (!ws) return JACAP_ERR_INVALID_ARG;
+  jacap_status s = prepare(cfg, batch, ws, ws_bytes, stream, &L);
+  if (s != JACAP_OK) return s;
+  if (!score_ptrs_ok(q_win, k, v, scores)) return JACAP_ERR_INVALID_ARG;
+  if (cfg->budget_k > 0) {
+    if (!idx || !k_out || !v_out) return JACAP_ERR_INVALID_ARG;
+    if (!aligned16(idx) || !aligned16(k_out) || !aligned16(v_out)) return JACAP_ERR_INVALID_ARG;
+  }
+  if (batch->total_tokens > 0) {
+    s = run_score(L, q_win, k, v, scores);
+    if (s != JACAP_OK) return s;
+  } else if (launch_init(L) != hipSuccess) {
+    return JACAP_ERR_HIP;
+  }
+  if (cfg->budget_k == 0) return JACAP_OK;
+  JACAP_TRY(launch_select(L, scores, idx));
+  JACAP_TRY(launch_compact(L, idx, k, v, k_out, v_out));
+  return JACAP_OK;
+}
+
+jacap_status jacap_read_status(const void* ws, void* stream, uint32_t* flags) {
+  if (!ws || !flags || (reinterpret_cast<uintptr_t>(ws) & 255u)) return JACAP_ERR_INVALID_ARG;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  uint32_t host = 0;
+  if (hipMemcpyAsync(&host, ws, sizeof(uint32_t), hipMemcpyDeviceToHost, st) != hipSuccess)
+    return JACAP_ERR_HIP;
+  if (hipStreamSynchronize(st) != hipSuccess) return JACAP_ERR_HIP;
+  *flags = host;
+  return JACAP_OK;
+}
+
+const char* jacap_status_string(jacap_status s) {
+  switch (s) {
+    case JACAP_OK: return "JACAP_OK";
+    case JACAP_ERR_INVALID_ARG: return "JACAP_ERR_INVALID_ARG";
+    case JACAP_ERR_UNSUPPORTED: return "JACAP_ERR_UNSUPPORTED";
+    case JACAP_ERR_WORKSPACE: return "JACAP_ERR_WORKSPACE";
+    case JACAP_ERR_HIP: return "JACAP_ERR_HIP";
+  }
+  return "JACAP_ERR_UNKNOWN";
+}
+
+}  // extern "C"

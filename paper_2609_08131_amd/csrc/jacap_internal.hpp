@@ -1,0 +1,191 @@
+// Internal definitions shared by the HIP kernels and the C-ABI host code of
+// libjacap.so (gfx950 / CDNA4 only).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "jacap.h"
+
+namespace jacap {
+
+// ---------------------------------------------------------------------------
+// Tiling constants
+// ---------------------------------------------------------------------------
+constexpr int kThreads = 256;        // 4 wave64 per workgroup
+constexpr int kKChunk = 256;         // tokens per workgroup in the K pass
+constexpr int kGChunkMfma = 8192;    // tokens per workgroup in the MFMA Gram pass
+constexpr int kGChunkPrecise = 1024; // tokens per workgroup in the fp64 Gram pass
+constexpr int kLChunk = 1024;        // tokens per workgroup in the leverage pass
+constexpr int kMfmaGramParts = 4;    // one partial Gram per wave
+
+// Unit flags (per (seq, layer, kv head)); the public flags are the OR of all.
+constexpr uint32_t kUnitNonfinite = JACAP_FLAG_NONFINITE;
+constexpr uint32_t kUnitSingular = JACAP_FLAG_SINGULAR;
+
+// ---------------------------------------------------------------------------
+// Geometry passed by value to every kernel
+// ---------------------------------------------------------------------------
+struct Geo {
+  int L, H, Hq, G, D, w, B, U;  // U = B * L * H units
+  int maxn;                     // host-declared max sequence length
+  int64_t T;                    // packed tokens per (layer, head)
+  const int32_t* seq_off;       // device [B+1]
+  int64_t ksl, ksh, kst;
+  int64_t vsl, vsh, vst;
+  int64_t qss, qsl, qsh, qsp;
+  int64_t oss, osl, osh, osr;
+};
+
+struct Unit {
+  int b, l, h;
+  int64_t t0;  // first packed token of the sequence
+  int n;       // tokens of the sequence
+};
+
+// A sequence whose offsets are inconsistent with the host-declared geometry is
+// treated as empty (and reported by the query-statistics kernel), so no kernel
+// ever indexes outside [0, T) or past the chunk grid sized from maxn.
+__device__ __forceinline__ bool offsets_ok(const Geo& g, int32_t a, int32_t e) {
+  return a >= 0 && e >= a && (int64_t)e <= g.T && e - a <= g.maxn;
+}
+
+__device__ __forceinline__ Unit decode_unit(const Geo& g, int u) {
+  Unit r;
+  r.h = u % g.H;
+  r.l = (u / g.H) % g.L;
+  r.b = u / (g.H * g.L);
+  const int32_t a = g.seq_off[r.b];
+  const int32_t e = g.seq_off[r.b + 1];
+  r.t0 = a;
+  r.n = offsets_ok(g, a, e) ? e - a : 0;
+  return r;
+}
+
+// Offset of per-token arrays laid out like the scores: [L][H][T].
+__device__ __forceinline__ int64_t token_row(const Geo& g, const Unit& un) {
+  return ((int64_t)un.l * g.H + un.h) * g.T + un.t0;
+}
+
+// ---------------------------------------------------------------------------
+// Workspace layout (byte offsets from the workspace base; 256-byte aligned)
+// ---------------------------------------------------------------------------
+struct Workspace {
+  size_t status;   // uint32: OR of the public flags
+  size_t uflags;   // uint32 [U]
+  size_t mu;       // double [U][D]
+  size_t lam;      // double [U][D]          (diagonal covariance)
+  size_t lamfull;  // float  [U][D][D]       (full covariance, FULL mode only)
+  size_t smax_m;   // float  [U]             global logit max
+  size_t smax_z;   // double [U]             global sum of exp(z - m)
+  size_t z;        // float  [L][H][T]       centre logits
+  size_t kappa;    // float  [L][H][T]       query response
+  size_t cstat;    // float2 [U][kchunks]    per-chunk (max, sum exp)
+  size_t gram;     // partial Gram matrices, format depends on the path
+  size_t linv64;   // double [U][D][D]       L^{-1} (lower, zeros above)
+  size_t linv32;   // float  [U][D][D]
+  size_t total;
+  int kchunks, gchunks, gchunk, gparts, lchunks;
+  bool mfma;       // bf16 path (MFMA Gram and leverage)
+};
+
+// ---------------------------------------------------------------------------
+// Small device helpers
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ float bf16_to_f32(uint16_t b) {
+  return __uint_as_float(((uint32_t)b) << 16);
+}
+
+// float -> bfloat16, round to nearest even (inputs here are finite).
+__device__ __forceinline__ uint16_t f32_to_bf16(float f) {
+  uint32_t u = __float_as_uint(f);
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
+template <typename T>
+__device__ __forceinline__ float to_f32(T x);
+template <>
+__device__ __forceinline__ float to_f32<float>(float x) { return x; }
+template <>
+__device__ __forceinline__ float to_f32<uint16_t>(uint16_t x) { return bf16_to_f32(x); }
+
+// Importance weight of Eq. 8 from the stored logit z and query response kappa,
+// given the unit's logit max m and softmax normaliser Z:
+//   e = exp(z - m), alpha = e / Z, 1 - alpha = (Z - e) / Z,
+//   w = (alpha (1 - alpha))^2 kappa / d.
+// Shared by the Gram and leverage passes so both see bit-identical weights.
+__device__ __forceinline__ double importance_weight(float z, float kappa, float m, double Z,
+                                                    double inv_d) {
+  double e = exp((double)z - (double)m);
+  double a = e / Z;
+  double oma = (Z - e) / Z;
+  double rho = a * oma;
+  return rho * rho * (double)kappa * inv_d;
+}
+
+// Wave64 butterfly reductions: every lane ends with the same, order-fixed value
+// (IEEE addition is commutative, so partner lanes compute identical sums).
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
+  return v;
+}
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  return v;
+}
+__device__ __forceinline__ double wave_sum(double v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  return v;
+}
+
+// Block (kThreads = 4 waves) reductions with a fixed combination order.
+template <typename T, typename Op>
+__device__ __forceinline__ T block_combine(T wave_val, T* red, Op op) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  __syncthreads();
+  if (lane == 0) red[wave] = wave_val;
+  __syncthreads();
+  T r = red[0];
+#pragma unroll
+  for (int i = 1; i < kThreads / 64; ++i) r = op(r, red[i]);
+  return r;
+}
+
+__device__ __forceinline__ void raise_flags(uint32_t* status, uint32_t* uflags, int u,
+                                            uint32_t f) {
+  atomicOr(status, f);
+  atomicOr(uflags + u, f);
+}
+
+// ---------------------------------------------------------------------------
+// Launchers (defined in the kernel translation units)
+// ---------------------------------------------------------------------------
+struct Launch {
+  const jacap_config* cfg;
+  Geo geo;
+  Workspace ws;
+  char* wsp;  // workspace base
+  hipStream_t stream;
+};
+
+hipError_t launch_init(const Launch& L);
+hipError_t launch_qstats(const Launch& L, const void* q);
+hipError_t launch_kpass(const Launch& L, const void* k);
+hipError_t launch_softmax_merge(const Launch& L);
+hipError_t launch_gram(const Launch& L, const void* v);
+hipError_t launch_factor(const Launch& L);
+hipError_t launch_leverage(const Launch& L, const void* v, float* scores);
+hipError_t launch_select(const Launch& L, const float* scores, int32_t* idx);
+hipError_t launch_compact(const Launch& L, const int32_t* idx, const void* k, const void* v,
+                          void* ko, void* vo);
+
+template <typename T>
+__host__ __device__ __forceinline__ T* ws_ptr(char* base, size_t off) {
+  return reinterpret_cast<T*>(base + off);
+}
+
+}  // namespace jacap

@@ -1,0 +1,179 @@
+// Leverage score of Eq. 10: score_i = w_i v_i^T A^{-1} v_i = w_i ||L^{-1} v_i||^2.
+//
+// bf16 inputs: Y = V L^{-T} on MFMA 16x16x32 bf16. The token dimension is the
+// MFMA row dimension, so each lane loads 8 consecutive channels of one token
+// straight from HBM (16 bytes, no transpose). L^{-1} is split into bf16
+// hi + lo and kept in registers; only the K-blocks with b <= a of the lower
+// triangle are multiplied. The squared row norm is reduced across the 16
+// lanes that share a token.
+//
+// fp32 inputs: fp64 VALU, L^{-1} in LDS, 8 threads per token.
+#include "jacap_internal.hpp"
+
+namespace jacap {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+
+template <int D>
+__global__ __launch_bounds__(kThreads) void leverage_mfma_kernel(
+    Geo g, const uint16_t* __restrict__ v, const float* __restrict__ zbuf,
+    const float* __restrict__ kbuf, const float* __restrict__ m_u, const double* __restrict__ z_u,
+    const float* __restrict__ linv32, const uint32_t* __restrict__ uflags,
+    float* __restrict__ scores, double inv_d) {
+  constexpr int NB = D / 16;  // output blocks of 16 channels (a)
+  constexpr int NK = D / 32;  // K blocks of 32 channels (b)
+  const int u = blockIdx.y, chunk = blockIdx.x;
+  const Unit un = decode_unit(g, u);
+  const int base = chunk * kLChunk;
+  if (base >= un.n) return;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int ch = lane & 15, kg = lane >> 4;
+  const int64_t trow = token_row(g, un);
+  const int end = min(un.n, base + kLChunk);
+
+  if (uflags[u] != 0u) {  // unit failed (non-finite input or singular A): NaN scores
+    for (int t = base + threadIdx.x; t < end; t += kThreads) scores[trow + t] = __builtin_nanf("");
+    return;
+  }
+
+  // B fragments: lane holds L^{-1}[a = 16 j + ch][b = 32 kb + 8 kg + q], q = 0..7.
+  bf16x8 bh[NB][NK], bl[NB][NK];
+  const float* Li = linv32 + (int64_t)u * D * D;
+#pragma unroll
+  for (int j = 0; j < NB; ++j)
+#pragma unroll
+    for (int kb = 0; kb < NK; ++kb) {
+      if (32 * kb > 16 * j + 15) continue;  // block entirely above the diagonal
+      const float* src = Li + (16 * j + ch) * D + 32 * kb + 8 * kg;
+#pragma unroll
+      for (int q = 0; q < 8; ++q) {
+        const float x = src[q];
+        const __bf16 h = (__bf16)x;
+        bh[j][kb][q] = h;
+        bl[j][kb][q] = (__bf16)(x - (float)h);
+      }
+    }
+
+  const float m = m_u[u];
+  const double Z = z_u[u];
+  const uint16_t* vb = v + un.l * g.vsl + un.h * g.vsh;
+
+  for (int t0 = base + wave * 16; t0 < end; t0 += 16 * (kThreads / 64)) {
+    const int tok = t0 + ch;  // A-operand row of this lane
+    bf16x8 a[NK];
+#pragma unroll
+    for (int kb = 0; kb < NK; ++kb) {
+      uint4 raw = make_uint4(0u, 0u, 0u, 0u);
+      if (tok < end) raw = *reinterpret_cast<const uint4*>(vb + (un.t0 + tok) * g.vst + 32 * kb + 8 * kg);
+      a[kb] = *reinterpret_cast<const bf16x8*>(&raw);
+    }
+    float ss[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int j = 0; j < NB; ++j) {
+      floatx4 y = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int kb = 0; kb < NK; ++kb) {
+        if (32 * kb > 16 * j + 15) continue;
+        y = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[kb], bh[j][kb], y, 0, 0, 0);
+        y = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[kb], bl[j][kb], y, 0, 0, 0);
+      }
+#pragma unroll
+      for (int r = 0; r < 4; ++r) ss[r] += y[r] * y[r];
+    }
+    // lane holds Y[token t0 + 4 kg + r][a = 16 j + ch]: reduce over ch.
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+#pragma unroll
+      for (int o = 1; o < 16; o <<= 1) ss[r] += __shfl_xor(ss[r], o);
+    if (ch < 4) {
+      const int t = t0 + 4 * kg + ch;
+      float s = ss[0];
+#pragma unroll
+      for (int r = 1; r < 4; ++r)
+        if (ch == r) s = ss[r];
+      if (t < end) {
+        const double w = importance_weight(zbuf[trow + t], kbuf[trow + t], m, Z, inv_d);
+        scores[trow + t] = (float)(w * (double)s);
+      }
+    }
+  }
+}
+
+template <int D>
+__global__ __launch_bounds__(kThreads) void leverage_precise_kernel(
+    Geo g, const float* __restrict__ v, const float* __restrict__ zbuf,
+    const float* __restrict__ kbuf, const float* __restrict__ m_u, const double* __restrict__ z_u,
+    const double* __restrict__ linv64, const uint32_t* __restrict__ uflags,
+    float* __restrict__ scores, double inv_d) {
+  constexpr int LD = D + 1;
+  constexpr int TPT = 8;                 // threads per token
+  constexpr int TOK = kThreads / TPT;    // tokens per tile
+  const int u = blockIdx.y, chunk = blockIdx.x;
+  const Unit un = decode_unit(g, u);
+  const int base = chunk * kLChunk;
+  if (base >= un.n) return;
+  const int tid = threadIdx.x;
+  const int64_t trow = token_row(g, un);
+  const int end = min(un.n, base + kLChunk);
+  if (uflags[u] != 0u) {
+    for (int t = base + tid; t < end; t += kThreads) scores[trow + t] = __builtin_nanf("");
+    return;
+  }
+  __shared__ double X[D * LD];
+  __shared__ float vs[TOK][D];
+  const double* Li = linv64 + (int64_t)u * D * D;
+  for (int e = tid; e < D * D; e += kThreads) X[(e / D) * LD + (e % D)] = Li[e];
+  const float m = m_u[u];
+  const double Z = z_u[u];
+  const float* vb = v + un.l * g.vsl + un.h * g.vsh;
+  const int my_tok = tid / TPT, sub = tid % TPT;
+  for (int t0 = base; t0 < end; t0 += TOK) {
+    __syncthreads();
+    for (int e = tid; e < TOK * D; e += kThreads) {
+      const int tk = e / D, c = e % D;
+      vs[tk][c] = (t0 + tk < end) ? vb[(un.t0 + t0 + tk) * g.vst + c] : 0.0f;
+    }
+    __syncthreads();
+    double ss = 0.0;
+    for (int a = sub; a < D; a += TPT) {
+      double y = 0.0;
+      for (int b = 0; b <= a; ++b) y += X[a * LD + b] * (double)vs[my_tok][b];
+      ss += y * y;
+    }
+#pragma unroll
+    for (int o = 1; o < TPT; o <<= 1) ss += __shfl_xor(ss, o);
+    const int t = t0 + my_tok;
+    if (sub == 0 && t < end) {
+      const double w = importance_weight(zbuf[trow + t], kbuf[trow + t], m, Z, inv_d);
+      scores[trow + t] = (float)(w * ss);
+    }
+  }
+}
+
+hipError_t launch_leverage(const Launch& L, const void* v, float* scores) {
+  const Geo& g = L.geo;
+  const dim3 grid(L.ws.lchunks, g.U);
+  const double inv_d = 1.0 / (double)g.D;
+  const float* zb = ws_ptr<float>(L.wsp, L.ws.z);
+  const float* kb = ws_ptr<float>(L.wsp, L.ws.kappa);
+  const float* mu = ws_ptr<float>(L.wsp, L.ws.smax_m);
+  const double* zu = ws_ptr<double>(L.wsp, L.ws.smax_z);
+  const uint32_t* uf = ws_ptr<uint32_t>(L.wsp, L.ws.uflags);
+  if (L.ws.mfma) {
+    const float* l32 = ws_ptr<float>(L.wsp, L.ws.linv32);
+    if (g.D == 128)
+      leverage_mfma_kernel<128><<<grid, kThreads, 0, L.stream>>>(g, (const uint16_t*)v, zb, kb, mu, zu, l32, uf, scores, inv_d);
+    else
+      leverage_mfma_kernel<64><<<grid, kThreads, 0, L.stream>>>(g, (const uint16_t*)v, zb, kb, mu, zu, l32, uf, scores, inv_d);
+  } else {
+    const double* l64 = ws_ptr<double>(L.wsp, L.ws.linv64);
+    if (g.D == 128)
+      leverage_precise_kernel<128><<<grid, kThreads, 0, L.stream>>>(g, (const float*)v, zb, kb, mu, zu, l64, uf, scores, inv_d);
+    else
+      leverage_precise_kernel<64><<<grid, kThreads, 0, L.stream>>>(g, (const float*)v, zb, kb, mu, zu, l64, uf, scores, inv_d);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace jacap

@@ -1,0 +1,288 @@
+// Query statistics, centre-attention logits, query response and the global
+// softmax normaliser (Algorithm 1, first two steps; Sec. 3.4).
+#include <type_traits>
+
+#include "jacap_internal.hpp"
+
+namespace jacap {
+
+// Clears the sticky status word and the per-unit flags. A fill kernel rather
+// than hipMemsetAsync so that the launch sequence can be captured in a graph.
+__global__ void init_kernel(uint32_t* __restrict__ status, uint32_t* __restrict__ uflags, int U) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i == 0) status[0] = 0u;
+  if (i < U) uflags[i] = 0u;
+}
+
+hipError_t launch_init(const Launch& L) {
+  const int U = L.geo.U;
+  init_kernel<<<(U + kThreads - 1) / kThreads, kThreads, 0, L.stream>>>(
+      ws_ptr<uint32_t>(L.wsp, L.ws.status), ws_ptr<uint32_t>(L.wsp, L.ws.uflags), U);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// mu_Q and Lambda_Q of the pooled window (G query heads x w positions):
+// sample mean and 1/N covariance, accumulated in fp64 in a fixed order.
+// ---------------------------------------------------------------------------
+template <typename T, int D>
+__global__ __launch_bounds__(kThreads) void qstats_kernel(Geo g, const T* __restrict__ q,
+                                                          double* __restrict__ mu_out,
+                                                          double* __restrict__ lam_out,
+                                                          float* __restrict__ lamfull, int full,
+                                                          uint32_t* status, uint32_t* uflags) {
+  const int u = blockIdx.x;
+  const int tid = threadIdx.x;
+  const Unit un = decode_unit(g, u);
+  if (tid == 0 && un.n == 0 &&
+      !offsets_ok(g, g.seq_off[un.b], g.seq_off[un.b + 1]))
+    atomicOr(status, (uint32_t)JACAP_FLAG_BAD_OFFSETS);
+  const int Ns = g.G * g.w;
+  const T* qb = q + un.b * g.qss + un.l * g.qsl + (int64_t)un.h * g.G * g.qsh;
+  __shared__ double smu[D];
+  if (tid < D) {
+    double s = 0.0;
+    for (int r = 0; r < Ns; ++r) {
+      const int gq = r / g.w, p = r - gq * g.w;
+      s += (double)to_f32(qb[gq * g.qsh + p * g.qsp + tid]);
+    }
+    const double m = s / Ns;
+    double v = 0.0;
+    for (int r = 0; r < Ns; ++r) {
+      const int gq = r / g.w, p = r - gq * g.w;
+      const double dv = (double)to_f32(qb[gq * g.qsh + p * g.qsp + tid]) - m;
+      v += dv * dv;
+    }
+    v /= Ns;
+    smu[tid] = m;
+    mu_out[(int64_t)u * D + tid] = m;
+    lam_out[(int64_t)u * D + tid] = v;
+    if (!isfinite(m) || !isfinite(v)) raise_flags(status, uflags, u, kUnitNonfinite);
+  }
+  if (!full) return;
+  // Full covariance: each thread owns D*D/kThreads entries; rows are staged,
+  // centred, 32 at a time in LDS.
+  constexpr int PER = D * D / kThreads;
+  __shared__ double qt[32][D];
+  double acc[PER];
+#pragma unroll
+  for (int k = 0; k < PER; ++k) acc[k] = 0.0;
+  for (int r0 = 0; r0 < Ns; r0 += 32) {
+    __syncthreads();
+    for (int e = tid; e < 32 * D; e += kThreads) {
+      const int rr = e / D, c = e - rr * D, r = r0 + rr;
+      double x = 0.0;
+      if (r < Ns) {
+        const int gq = r / g.w, p = r - gq * g.w;
+        x = (double)to_f32(qb[gq * g.qsh + p * g.qsp + c]) - smu[c];
+      }
+      qt[rr][c] = x;
+    }
+    __syncthreads();
+    const int nr = min(32, Ns - r0);
+    for (int rr = 0; rr < nr; ++rr) {
+#pragma unroll
+      for (int k = 0; k < PER; ++k) {
+        const int e = tid + k * kThreads;
+        acc[k] += qt[rr][e / D] * qt[rr][e % D];
+      }
+    }
+  }
+#pragma unroll
+  for (int k = 0; k < PER; ++k) {
+    const int e = tid + k * kThreads;
+    lamfull[(int64_t)u * D * D + e] = (float)(acc[k] / Ns);
+  }
+}
+
+hipError_t launch_qstats(const Launch& L, const void* q) {
+  const Geo& g = L.geo;
+  const int full = L.cfg->cov_mode == JACAP_COV_FULL;
+  double* mu = ws_ptr<double>(L.wsp, L.ws.mu);
+  double* lam = ws_ptr<double>(L.wsp, L.ws.lam);
+  float* lf = ws_ptr<float>(L.wsp, L.ws.lamfull);
+  uint32_t* st = ws_ptr<uint32_t>(L.wsp, L.ws.status);
+  uint32_t* uf = ws_ptr<uint32_t>(L.wsp, L.ws.uflags);
+  const bool bf = L.cfg->dtype == JACAP_DTYPE_BF16;
+  if (g.D == 128) {
+    if (bf)
+      qstats_kernel<uint16_t, 128><<<g.U, kThreads, 0, L.stream>>>(g, (const uint16_t*)q, mu, lam, lf, full, st, uf);
+    else
+      qstats_kernel<float, 128><<<g.U, kThreads, 0, L.stream>>>(g, (const float*)q, mu, lam, lf, full, st, uf);
+  } else {
+    if (bf)
+      qstats_kernel<uint16_t, 64><<<g.U, kThreads, 0, L.stream>>>(g, (const uint16_t*)q, mu, lam, lf, full, st, uf);
+    else
+      qstats_kernel<float, 64><<<g.U, kThreads, 0, L.stream>>>(g, (const float*)q, mu, lam, lf, full, st, uf);
+  }
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// K pass: z_i = k_i . mu / (tau sqrt d) and kappa_i = k_i^T Lambda k_i for a
+// chunk of kKChunk tokens, then the chunk's (max z, sum exp(z - max)).
+// One 16-byte load per lane: a token row is spread over LPT lanes.
+// ---------------------------------------------------------------------------
+template <typename T, int D, bool FULL>
+__global__ __launch_bounds__(kThreads) void kpass_kernel(
+    Geo g, const T* __restrict__ k, const double* __restrict__ mu, const double* __restrict__ lam,
+    const float* __restrict__ lamfull, float* __restrict__ zout, float* __restrict__ kout,
+    float2* __restrict__ cstat, int kchunks, double inv_scale, uint32_t* status,
+    uint32_t* uflags) {
+  const int u = blockIdx.y, chunk = blockIdx.x;
+  const Unit un = decode_unit(g, u);
+  const int base = chunk * kKChunk;
+  if (base >= un.n) return;
+
+  constexpr int VEC = 16 / sizeof(T);
+  constexpr int LPT = D / VEC;
+  constexpr int TPW = 64 / LPT;
+  constexpr int TPB = TPW * (kThreads / 64);
+  using Acc = typename std::conditional<std::is_same<T, float>::value, double, float>::type;
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int sub = lane % LPT, tiw = lane / LPT;
+
+  Acc muv[VEC], lamv[VEC];
+#pragma unroll
+  for (int e = 0; e < VEC; ++e) {
+    muv[e] = (Acc)mu[(int64_t)u * D + sub * VEC + e];
+    lamv[e] = (Acc)lam[(int64_t)u * D + sub * VEC + e];
+  }
+
+  __shared__ float zsh[kKChunk];
+  __shared__ float red[kThreads / 64];
+  __shared__ float lamsh[FULL ? D * (D + 1) : 1];
+  __shared__ float ksh[FULL ? TPB : 1][FULL ? D : 1];
+  if constexpr (FULL) {
+    for (int e = tid; e < D * D; e += kThreads)
+      lamsh[(e / D) * (D + 1) + (e % D)] = lamfull[(int64_t)u * D * D + e];
+  }
+
+  const T* kb = k + un.l * g.ksl + un.h * g.ksh;
+  const int64_t trow = token_row(g, un);
+
+  for (int it = 0; it < kKChunk; it += TPB) {
+    const int tl = it + wave * TPW + tiw;
+    const int i = base + tl;
+    const bool valid = i < un.n;
+    Acc x[VEC];
+    if (valid) {
+      const uint4 raw = *reinterpret_cast<const uint4*>(kb + (un.t0 + i) * g.kst + sub * VEC);
+      const T* xv = reinterpret_cast<const T*>(&raw);
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) x[e] = (Acc)to_f32(xv[e]);
+    } else {
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) x[e] = (Acc)0;
+    }
+    Acc dot = 0, kap = 0;
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) dot += muv[e] * x[e];
+    if constexpr (!FULL) {
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) kap += lamv[e] * x[e] * x[e];
+    } else {
+      __syncthreads();
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) ksh[wave * TPW + tiw][sub * VEC + e] = (float)x[e];
+      __syncthreads();
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) {
+        const float* row = lamsh + (sub * VEC + e) * (D + 1);
+        Acc t = 0;
+        for (int bb = 0; bb < D; ++bb) t += (Acc)row[bb] * (Acc)ksh[wave * TPW + tiw][bb];
+        kap += x[e] * t;
+      }
+    }
+#pragma unroll
+    for (int o = LPT / 2; o > 0; o >>= 1) {
+      dot += __shfl_xor(dot, o);
+      kap += __shfl_xor(kap, o);
+    }
+    if (sub == 0) {
+      const float z = valid ? (float)((double)dot * inv_scale) : -INFINITY;
+      zsh[tl] = z;
+      if (valid) {
+        zout[trow + i] = z;
+        kout[trow + i] = (float)kap;
+        if (!isfinite(z) || !isfinite((float)kap)) raise_flags(status, uflags, u, kUnitNonfinite);
+      }
+    }
+  }
+  __syncthreads();
+  static_assert(kKChunk == kThreads, "one logit per thread in the chunk reduction");
+  const float zv = zsh[tid];
+  const float m = block_combine(wave_max(zv), red, [](float a, float b) { return fmaxf(a, b); });
+  const float ex = (zv == -INFINITY) ? 0.0f : expf(zv - m);
+  const float s = block_combine(wave_sum(ex), red, [](float a, float b) { return a + b; });
+  if (tid == 0) cstat[(int64_t)u * kchunks + chunk] = make_float2(m, s);
+}
+
+template <typename T, int D>
+static void kpass_dispatch(const Launch& L, const void* k, bool full, dim3 grid, double inv_scale) {
+  const Geo& g = L.geo;
+  auto args = [&](auto kern) {
+    kern<<<grid, kThreads, 0, L.stream>>>(
+        g, (const T*)k, ws_ptr<double>(L.wsp, L.ws.mu), ws_ptr<double>(L.wsp, L.ws.lam),
+        ws_ptr<float>(L.wsp, L.ws.lamfull), ws_ptr<float>(L.wsp, L.ws.z),
+        ws_ptr<float>(L.wsp, L.ws.kappa), ws_ptr<float2>(L.wsp, L.ws.cstat), L.ws.kchunks,
+        inv_scale, ws_ptr<uint32_t>(L.wsp, L.ws.status), ws_ptr<uint32_t>(L.wsp, L.ws.uflags));
+  };
+  if (full)
+    args(kpass_kernel<T, D, true>);
+  else
+    args(kpass_kernel<T, D, false>);
+}
+
+hipError_t launch_kpass(const Launch& L, const void* k) {
+  const Geo& g = L.geo;
+  const bool full = L.cfg->cov_mode == JACAP_COV_FULL;
+  const double inv_scale = 1.0 / ((double)L.cfg->temperature * sqrt((double)g.D));
+  const dim3 grid(L.ws.kchunks, g.U);
+  const bool bf = L.cfg->dtype == JACAP_DTYPE_BF16;
+  if (g.D == 128) {
+    if (bf) kpass_dispatch<uint16_t, 128>(L, k, full, grid, inv_scale);
+    else kpass_dispatch<float, 128>(L, k, full, grid, inv_scale);
+  } else {
+    if (bf) kpass_dispatch<uint16_t, 64>(L, k, full, grid, inv_scale);
+    else kpass_dispatch<float, 64>(L, k, full, grid, inv_scale);
+  }
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Global softmax normaliser per unit: m = max_c m_c, Z = sum_c Z_c exp(m_c - m)
+// (fp64, fixed order).
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(kThreads) void softmax_merge_kernel(Geo g,
+                                                                 const float2* __restrict__ cstat,
+                                                                 int kchunks, float* m_out,
+                                                                 double* z_out) {
+  const int u = blockIdx.x, tid = threadIdx.x;
+  const Unit un = decode_unit(g, u);
+  __shared__ float redf[kThreads / 64];
+  __shared__ double redd[kThreads / 64];
+  if (un.n == 0) {
+    if (tid == 0) { m_out[u] = 0.0f; z_out[u] = 1.0; }
+    return;
+  }
+  const int nch = (un.n + kKChunk - 1) / kKChunk;
+  const float2* cs = cstat + (int64_t)u * kchunks;
+  float m = -INFINITY;
+  for (int c = tid; c < nch; c += kThreads) m = fmaxf(m, cs[c].x);
+  m = block_combine(wave_max(m), redf, [](float a, float b) { return fmaxf(a, b); });
+  double s = 0.0;
+  for (int c = tid; c < nch; c += kThreads) s += (double)cs[c].y * exp((double)cs[c].x - (double)m);
+  s = block_combine(wave_sum(s), redd, [](double a, double b) { return a + b; });
+  if (tid == 0) { m_out[u] = m; z_out[u] = s; }
+}
+
+hipError_t launch_softmax_merge(const Launch& L) {
+  softmax_merge_kernel<<<L.geo.U, kThreads, 0, L.stream>>>(
+      L.geo, ws_ptr<float2>(L.wsp, L.ws.cstat), L.ws.kchunks, ws_ptr<float>(L.wsp, L.ws.smax_m),
+      ws_ptr<double>(L.wsp, L.ws.smax_z));
+  return hipGetLastError();
+}
+
+}  // namespace jacap

@@ -8,7 +8,15 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 
+def _ensure_library():
+    lib = os.path.join(ROOT, "paper_2609_08131_amd", "libjacap.so")
+    if not os.path.exists(lib):
+        from paper_2609_08131_amd import build
+        build.build()
+
+
 def pytest_configure(config):
+    _ensure_library()
     config.addinivalue_line("markers", "gpu: needs an MI355X (gfx950) and the built HIP library")
     config.addinivalue_line("markers", "slow: full-size cases (minutes of CPU oracle time)")
 

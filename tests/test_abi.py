@@ -1,0 +1,138 @@
+"""Host-side checks of the C ABI (no GPU needed, no compute calls).
+
+* libjacap.so loads and exports every function include/jacap.h declares;
+* the ctypes structs match the C layout (compiled with gcc from the header);
+* host-detectable errors are returned before anything touches the device.
+"""
+
+import ctypes
+import os
+import re
+import subprocess
+import tempfile
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "jacap.h")
+
+jacap = pytest.importorskip("paper_2609_08131_amd.jacap")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(jacap_[a-z_]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_function():
+    names = declared_functions()
+    assert "jacap_score" in names and "jacap_evict" in names
+    lib = ctypes.CDLL(jacap.LIB_PATH)
+    missing = [n for n in names if not hasattr(lib, n)]
+    assert not missing, missing
+    assert set(names) == set(jacap.EXPORTED)
+
+
+def test_struct_layout_matches_header():
+    prog = r"""
+#include <stdio.h>
+#include <stddef.h>
+#include "jacap.h"
+#define F(S, m) printf(#m " %zu\n", offsetof(S, m));
+int main(void) {
+  printf("sizeof_config %zu\nsizeof_batch %zu\n", sizeof(jacap_config), sizeof(jacap_batch));
+  F(jacap_config, temperature) F(jacap_config, ridge) F(jacap_config, dtype)
+  F(jacap_batch, total_tokens) F(jacap_batch, seq_offsets) F(jacap_batch, k_stride_layer)
+  F(jacap_batch, q_stride_pos) F(jacap_batch, out_stride_row)
+  return 0;
+}
+"""
+    with tempfile.TemporaryDirectory() as d:
+        src, exe = os.path.join(d, "t.c"), os.path.join(d, "t")
+        open(src, "w").write(prog)
+        subprocess.run(["gcc", "-I", os.path.dirname(HEADER), src, "-o", exe], check=True)
+        out = dict(line.split() for line in subprocess.run([exe], capture_output=True, text=True,
+                                                          check=True).stdout.splitlines())
+    assert int(out["sizeof_config"]) == ctypes.sizeof(jacap.Config)
+    assert int(out["sizeof_batch"]) == ctypes.sizeof(jacap.Batch)
+    for s, m in (("Config", "temperature"), ("Config", "ridge"), ("Config", "dtype"),
+                 ("Batch", "total_tokens"), ("Batch", "seq_offsets"), ("Batch", "k_stride_layer"),
+                 ("Batch", "q_stride_pos"), ("Batch", "out_stride_row")):
+        assert int(out[m]) == getattr(getattr(jacap, s), m).offset, m
+
+
+def _cfg(**kw):
+    base = dict(num_layers=1, num_kv_heads=1, num_q_heads=1, head_dim=64, window=16, budget_k=8,
+                temperature=10.0, ridge=1.0, cov_mode=0, dtype=0)
+    base.update(kw)
+    return jacap.Config(**base)
+
+
+def _batch(**kw):
+    b = jacap.Batch()
+    b.num_seqs, b.max_seq_len, b.total_tokens = 1, 100, 100
+    b.seq_offsets = 0x1000
+    b.k_stride_layer = b.v_stride_layer = 6400
+    b.k_stride_head = b.v_stride_head = 6400
+    b.k_stride_token = b.v_stride_token = 64
+    b.q_stride_seq, b.q_stride_layer, b.q_stride_head, b.q_stride_pos = 1024, 1024, 1024, 64
+    b.out_stride_seq, b.out_stride_layer, b.out_stride_head, b.out_stride_row = 512, 512, 512, 64
+    for k, v in kw.items():
+        setattr(b, k, v)
+    return b
+
+
+def _ws_size(cfg, b):
+    n = ctypes.c_size_t(0)
+    return jacap._lib.jacap_workspace_size(ctypes.byref(cfg), ctypes.byref(b), ctypes.byref(n)), n.value
+
+
+def test_workspace_size_and_validation():
+    code, n = _ws_size(_cfg(), _batch())
+    assert code == jacap.OK and n > 0 and n % 256 == 0
+    code2, n2 = _ws_size(_cfg(dtype=1), _batch(max_seq_len=20000, total_tokens=20000))
+    assert code2 == jacap.OK and n2 > n
+    bad = [
+        (_cfg(head_dim=96), jacap.ERR_UNSUPPORTED),
+        (_cfg(dtype=7), jacap.ERR_UNSUPPORTED),
+        (_cfg(cov_mode=3), jacap.ERR_UNSUPPORTED),
+        (_cfg(num_q_heads=3, num_kv_heads=2), jacap.ERR_INVALID_ARG),
+        (_cfg(window=0), jacap.ERR_INVALID_ARG),
+        (_cfg(budget_k=-1), jacap.ERR_INVALID_ARG),
+        (_cfg(temperature=0.0), jacap.ERR_INVALID_ARG),
+        (_cfg(temperature=float("nan")), jacap.ERR_INVALID_ARG),
+        (_cfg(ridge=-1.0), jacap.ERR_INVALID_ARG),
+    ]
+    for cfg, want in bad:
+        assert _ws_size(cfg, _batch())[0] == want
+    assert _ws_size(_cfg(), _batch(k_stride_token=60))[0] == jacap.ERR_INVALID_ARG
+    assert _ws_size(_cfg(), _batch(seq_offsets=0))[0] == jacap.ERR_INVALID_ARG
+    assert _ws_size(_cfg(), _batch(num_seqs=0))[0] == jacap.ERR_INVALID_ARG
+    assert jacap._lib.jacap_workspace_size(ctypes.byref(_cfg()), ctypes.byref(_batch()), None) == jacap.ERR_INVALID_ARG
+
+
+def test_entry_points_reject_bad_pointers_before_launch():
+    cfg, b = _cfg(), _batch()
+    _, n = _ws_size(cfg, b)
+    P = ctypes.c_void_p
+    lib = jacap._lib
+    good = P(0x100000)
+    # null workspace, misaligned workspace, too small workspace
+    assert lib.jacap_score(ctypes.byref(cfg), ctypes.byref(b), good, good, good, good, None, n, None) == jacap.ERR_INVALID_ARG
+    assert lib.jacap_score(ctypes.byref(cfg), ctypes.byref(b), good, good, good, good, P(0x100010), n, None) == jacap.ERR_INVALID_ARG
+    assert lib.jacap_score(ctypes.byref(cfg), ctypes.byref(b), good, good, good, good, good, n - 256, None) == jacap.ERR_WORKSPACE
+    # null / misaligned data pointers
+    assert lib.jacap_score(ctypes.byref(cfg), ctypes.byref(b), None, good, good, good, good, n, None) == jacap.ERR_INVALID_ARG
+    assert lib.jacap_score(ctypes.byref(cfg), ctypes.byref(b), good, P(0x100004), good, good, good, n, None) == jacap.ERR_INVALID_ARG
+    assert lib.jacap_evict(ctypes.byref(cfg), ctypes.byref(b), good, good, good, good, None, good, good, good, n, None) == jacap.ERR_INVALID_ARG
+    assert lib.jacap_compact(ctypes.byref(cfg), ctypes.byref(b), good, None, good, good, good, None) == jacap.ERR_INVALID_ARG
+    assert lib.jacap_select(ctypes.byref(cfg), ctypes.byref(b), good, None, None, 0, None) == jacap.ERR_INVALID_ARG
+    assert lib.jacap_read_status(None, None, ctypes.byref(ctypes.c_uint32())) == jacap.ERR_INVALID_ARG
+    assert lib.jacap_read_status(good, None, None) == jacap.ERR_INVALID_ARG
+
+
+def test_status_strings():
+    for code, name in ((0, "JACAP_OK"), (1, "JACAP_ERR_INVALID_ARG"), (2, "JACAP_ERR_UNSUPPORTED"),
+                       (3, "JACAP_ERR_WORKSPACE"), (4, "JACAP_ERR_HIP"), (99, "JACAP_ERR_UNKNOWN")):
+        assert jacap.status_string(code) == name
