@@ -5,10 +5,12 @@
 // bf16 inputs: MFMA 16x16x32 bf16 with fp32 accumulation. The reduction runs
 // over tokens, so both operands need 8 consecutive tokens of one channel per
 // lane: each wave stages 32 tokens of V transposed ([channel][token]) in LDS.
-// V is exact in bf16; the weighted operand x = w v is split as
-// x_hi + x_lo (two bf16), so M = V^T X_hi + V^T X_lo carries ~2^-17 relative
-// error instead of the 2^-9 of a single rounding. Only the upper-triangular
-// 16x16 blocks are formed.
+// V is exact in bf16; the weighted operand x = w v (fp32) is split into three
+// bf16 terms x1 + x2 + x3 (24 significant bits, like fp32), so
+// M = V^T X1 + V^T X2 + V^T X3 matches an fp32 Gram: the capacity matrix of a
+// short or ridge-0 unit can have cond(A) ~ 1e5-1e6, and a two-term split
+// (2^-17) then costs more than the 1e-3 score tolerance. Only the
+// upper-triangular 16x16 blocks are formed.
 //
 // fp32 inputs: fp64 VALU accumulation (8x8 or 4x4 register tiles per thread).
 #include "jacap_internal.hpp"
@@ -88,19 +90,23 @@ __global__ __launch_bounds__(kThreads) void gram_mfma_kernel(
     for (int i = 0; i < NB; ++i) a[i] = *reinterpret_cast<const bf16x8*>(&vt[wave][i * 16 + ch][kg * 8]);
 #pragma unroll
     for (int j = 0; j < NB; ++j) {
-      bf16x8 xh, xl;
+      bf16x8 x1, x2, x3;
 #pragma unroll
       for (int q = 0; q < 8; ++q) {
         const float x = (float)a[j][q] * wl[q];
-        const __bf16 h = (__bf16)x;
-        xh[q] = h;
-        xl[q] = (__bf16)(x - (float)h);
+        const __bf16 h1 = (__bf16)x;
+        const float r1 = x - (float)h1;
+        const __bf16 h2 = (__bf16)r1;
+        x1[q] = h1;
+        x2[q] = h2;
+        x3[q] = (__bf16)(r1 - (float)h2);
       }
 #pragma unroll
       for (int i = 0; i <= j; ++i) {
         const int p = pair_index(i, j, NB);
-        acc[p] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], xh, acc[p], 0, 0, 0);
-        acc[p] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], xl, acc[p], 0, 0, 0);
+        acc[p] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], x3, acc[p], 0, 0, 0);
+        acc[p] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], x2, acc[p], 0, 0, 0);
+        acc[p] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], x1, acc[p], 0, 0, 0);
       }
     }
     wave_lds_sync();
