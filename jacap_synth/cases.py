@@ -131,6 +131,12 @@ class Case:
     def max_seq_len(self) -> int:
         return int(max(self.seq_lens)) if self.seq_lens else 0
 
+    def to(self, device) -> "Case":
+        """The same case with every tensor moved to `device` (values unchanged)."""
+        return Case(workload=self.workload, q_win=self.q_win.to(device), k=self.k.to(device),
+                    v=self.v.to(device), seq_lens=list(self.seq_lens),
+                    seq_offsets=self.seq_offsets.to(device))
+
     def unit_arrays(self, b: int, layer: int, head: int):
         """Host fp64 copies (exact widening) of one unit's Q window, K and V."""
         w = self.workload

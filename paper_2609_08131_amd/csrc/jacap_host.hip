@@ -54,11 +54,13 @@ Workspace layout(const jacap_config* c, const jacap_batch* b) {
   w.kchunks = (maxn + kKChunk - 1) / kKChunk;
   w.gchunk = w.mfma ? kGChunkMfma : kGChunkPrecise;
   w.gchunks = (maxn + w.gchunk - 1) / w.gchunk;
-  w.gparts = w.mfma ? kMfmaGramParts : 1;
-  w.lchunks = (maxn + kLChunk - 1) / kLChunk;
+  w.gparts = 1;
+  const int lchunk = w.mfma ? kLChunkMfma : kLChunkPrecise;
+  w.lchunks = (maxn + lchunk - 1) / lchunk;
   const int64_t NB = D / 16;
   const int64_t npair = NB * (NB + 1) / 2;
-  const int64_t part_bytes = w.mfma ? (int64_t)kMfmaGramParts * npair * 256 * 4 : D * D * 8;
+  const int64_t nlp = (NB / 2) * (NB / 2 + 1);
+  const int64_t part_bytes = npair * 256 * (w.mfma ? 4 : 8);
   size_t o = 0;
   auto take = [&](size_t bytes) { size_t r = o; o = align256(o + bytes); return r; };
   w.status = take(4);
@@ -72,8 +74,9 @@ Workspace layout(const jacap_config* c, const jacap_batch* b) {
   w.kappa = take(4 * LHT);
   w.cstat = take(8 * U * (int64_t)w.kchunks);
   w.gram = take((size_t)(U * (int64_t)w.gchunks * part_bytes));
-  w.linv64 = take(8 * U * D * D);
-  w.linv32 = take(4 * U * D * D);
+  w.gram_red = take(8 * U * npair * 256);
+  w.linv64 = take(w.mfma ? 8 : 8 * U * D * D);
+  w.lfrag = take(w.mfma ? 2 * U * nlp * 2 * 64 * 8 : 8);
   w.total = o;
   return w;
 }
@@ -126,8 +129,14 @@ jacap_status run_score(const Launch& L, const void* q, const void* k, const void
   JACAP_TRY(launch_qstats(L, q));
   JACAP_TRY(launch_kpass(L, k));
   JACAP_TRY(launch_softmax_merge(L));
-  JACAP_TRY(launch_gram(L, v));
-  JACAP_TRY(launch_factor(L));
+  JACAP_TRY(launch_gram(L, v, false));
+  JACAP_TRY(launch_gram_reduce(L, false));
+  JACAP_TRY(launch_factor(L, false));
+  if (L.ws.mfma) {  // recompute the Gram of ill-conditioned units with the exact split
+    JACAP_TRY(launch_gram(L, v, true));
+    JACAP_TRY(launch_gram_reduce(L, true));
+    JACAP_TRY(launch_factor(L, true));
+  }
   JACAP_TRY(launch_leverage(L, v, scores));
   return JACAP_OK;
 }

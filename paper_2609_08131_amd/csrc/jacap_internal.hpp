@@ -14,14 +14,18 @@ namespace jacap {
 // ---------------------------------------------------------------------------
 constexpr int kThreads = 256;        // 4 wave64 per workgroup
 constexpr int kKChunk = 256;         // tokens per workgroup in the K pass
-constexpr int kGChunkMfma = 8192;    // tokens per workgroup in the MFMA Gram pass
+constexpr int kGChunkMfma = 4096;    // tokens per workgroup in the MFMA Gram pass
 constexpr int kGChunkPrecise = 1024; // tokens per workgroup in the fp64 Gram pass
-constexpr int kLChunk = 1024;        // tokens per workgroup in the leverage pass
-constexpr int kMfmaGramParts = 4;    // one partial Gram per wave
+constexpr int kLChunkMfma = 4096;    // tokens per workgroup in the MFMA leverage pass
+constexpr int kLChunkPrecise = 1024; // tokens per workgroup in the fp64 leverage pass
 
 // Unit flags (per (seq, layer, kv head)); the public flags are the OR of all.
 constexpr uint32_t kUnitNonfinite = JACAP_FLAG_NONFINITE;
 constexpr uint32_t kUnitSingular = JACAP_FLAG_SINGULAR;
+// Internal: the unit's capacity matrix is ill-conditioned enough that its Gram
+// is recomputed with the exact three-term split (bf16 path only).
+constexpr uint32_t kUnitRefine = 1u << 8;
+constexpr uint32_t kUnitFailed = kUnitNonfinite | kUnitSingular;
 
 // ---------------------------------------------------------------------------
 // Geometry passed by value to every kernel
@@ -81,9 +85,10 @@ struct Workspace {
   size_t z;        // float  [L][H][T]       centre logits
   size_t kappa;    // float  [L][H][T]       query response
   size_t cstat;    // float2 [U][kchunks]    per-chunk (max, sum exp)
-  size_t gram;     // partial Gram matrices, format depends on the path
-  size_t linv64;   // double [U][D][D]       L^{-1} (lower, zeros above)
-  size_t linv32;   // float  [U][D][D]
+  size_t gram;     // per-chunk partial Grams [U][gchunks][NPAIR*256], fp32 (bf16 path) or fp64
+  size_t gram_red; // double [U][NPAIR*256]  reduced Gram, block-lane layout
+  size_t linv64;   // double [U][D][D]       L^{-1} (lower, zeros above), fp32-input path
+  size_t lfrag;    // bf16 [U][NLP][2][64][8] L^{-1} hi/lo MFMA B fragments, bf16 path
   size_t total;
   int kchunks, gchunks, gchunk, gparts, lchunks;
   bool mfma;       // bf16 path (MFMA Gram and leverage)
@@ -176,8 +181,9 @@ hipError_t launch_init(const Launch& L);
 hipError_t launch_qstats(const Launch& L, const void* q);
 hipError_t launch_kpass(const Launch& L, const void* k);
 hipError_t launch_softmax_merge(const Launch& L);
-hipError_t launch_gram(const Launch& L, const void* v);
-hipError_t launch_factor(const Launch& L);
+hipError_t launch_gram(const Launch& L, const void* v, bool refine);
+hipError_t launch_gram_reduce(const Launch& L, bool refine);
+hipError_t launch_factor(const Launch& L, bool refine);
 hipError_t launch_leverage(const Launch& L, const void* v, float* scores);
 hipError_t launch_select(const Launch& L, const float* scores, int32_t* idx);
 hipError_t launch_compact(const Launch& L, const int32_t* idx, const void* k, const void* v,

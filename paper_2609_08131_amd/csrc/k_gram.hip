@@ -1,24 +1,32 @@
 // Weighted Gram M = sum_i w_i v_i v_i^T over a unit's tokens (the data term of
-// the capacity matrix, Eq. 9), as per-chunk partial sums that the factor
-// kernel adds in a fixed order.
+// the capacity matrix, Eq. 9), as one partial per workgroup (a chunk of
+// tokens) that the reduce kernel adds in a fixed order.
+//
+// Partial layout ("block-lane"): the upper-triangular 16x16 blocks (i <= j) of
+// M, block pair p = pair_index(i, j), 256 entries per block in MFMA 16x16
+// output order: entry p*256 + lane*4 + r holds M[16i + 4(lane/16) + r][16j + lane%16].
 //
 // bf16 inputs: MFMA 16x16x32 bf16 with fp32 accumulation. The reduction runs
-// over tokens, so both operands need 8 consecutive tokens of one channel per
-// lane: each wave stages 32 tokens of V transposed ([channel][token]) in LDS.
-// V is exact in bf16; the weighted operand x = w v (fp32) is split into three
-// bf16 terms x1 + x2 + x3 (24 significant bits, like fp32), so
-// M = V^T X1 + V^T X2 + V^T X3 matches an fp32 Gram: the capacity matrix of a
-// short or ridge-0 unit can have cond(A) ~ 1e5-1e6, and a two-term split
-// (2^-17) then costs more than the 1e-3 score tolerance. Only the
-// upper-triangular 16x16 blocks are formed.
+// over tokens, so a lane's operand fragment is 8 consecutive tokens of one
+// channel: it is gathered straight from HBM with 16-bit loads (four rows x 32
+// bytes per wave instruction), so no LDS transpose is needed. V is exact in
+// bf16; the weighted operand x = w v (fp32) is split exactly into three bf16
+// terms by truncation (x = x1 + x2 + x3), so M = V^T X1 + V^T X2 + V^T X3 is
+// an fp32-accurate Gram: the capacity matrix of a short or ridge-0 unit can
+// reach cond(A) ~ 1e5-1e6, where a two-term split (2^-17) costs more than
+// the 1e-3 score tolerance. The next step's fragments are loaded while the
+// current step's MFMAs run. The four waves' accumulators are reduced in LDS.
 //
-// fp32 inputs: fp64 VALU accumulation (8x8 or 4x4 register tiles per thread).
+// fp32 inputs: fp64 VALU accumulation (register tiles), same partial layout.
+#include <type_traits>
+
 #include "jacap_internal.hpp"
 
 namespace jacap {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float floatx4 __attribute__((ext_vector_type(4)));
+typedef uint16_t u16x8 __attribute__((ext_vector_type(8)));
 
 // Per-wave barrier for LDS traffic that stays inside one wave.
 __device__ __forceinline__ void wave_lds_sync() {
@@ -27,94 +35,232 @@ __device__ __forceinline__ void wave_lds_sync() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
-// Index of the upper-triangular block pair (i <= j) among NB x NB blocks.
-__host__ __device__ constexpr int pair_index(int i, int j, int NB) {
-  return i * NB - (i * (i - 1)) / 2 + (j - i);
+// Three-term exact split of x into bf16 pieces by truncation: each piece takes
+// the next 8 significant bits, the remainder of the last one is exactly zero.
+__device__ __forceinline__ void split3(float x, uint16_t& h1, uint16_t& h2, uint16_t& h3) {
+  const uint32_t b0 = __float_as_uint(x) & 0xFFFF0000u;
+  const float r1 = x - __uint_as_float(b0);
+  const uint32_t b1 = __float_as_uint(r1) & 0xFFFF0000u;
+  const float r2 = r1 - __uint_as_float(b1);
+  h1 = (uint16_t)(b0 >> 16);
+  h2 = (uint16_t)(b1 >> 16);
+  h3 = (uint16_t)(__float_as_uint(r2) >> 16);
 }
 
-template <int D>
-__global__ __launch_bounds__(kThreads) void gram_mfma_kernel(
+// The workgroup walks its chunk in steps of 32 tokens. Each step is loaded
+// with coalesced 16-byte loads (prefetched two steps ahead), staged in LDS
+// (double-buffered, one barrier per step) and shared by the four waves. The
+// upper 16x16 block pairs (i <= j) are split between the waves by column
+// pairs {w, NB-1-w}, which gives every wave the same number of pairs (9 at
+// d = 128), so no cross-wave reduction is needed. Token <-> MFMA K-slot
+// mapping: lane (ch, kg) element q is token 4 q + kg of the step (the same
+// mapping for both operands); with a 288-byte row pitch the four kg groups of
+// a fragment read fall in disjoint LDS banks. Each wave accumulates in fp32
+// for kGramFlush steps, then adds that into a second fp32 accumulator, so the
+// rounding chains stay short (the Gram of an ill-conditioned ridge-0 unit
+// needs it).
+constexpr int kGramStep = 32;
+constexpr int kGramPitch = 144;  // u16 elements per staged token row (288 bytes)
+constexpr int kGramFlush = 4;
+
+struct GramArgs {
+  const uint16_t* vb;   // V of the unit, at its first token
+  int64_t vst;
+  const float* zbuf;
+  const float* kbuf;
+  int64_t trow;
+  float m;
+  double Z;
+  double inv_d;
+  int base, end, nsteps;
+  float* out;           // this chunk's partial (block-lane layout)
+};
+
+// Split x into NT bf16 terms, smallest first (x = sum of the terms up to the
+// split error): NT = 2 rounds to nearest (error <= 2^-18 |x|); NT = 3
+// truncates (exact).
+template <int NT>
+__device__ __forceinline__ void split_terms(float x, uint16_t (&h)[NT]) {
+  if constexpr (NT == 2) {
+    const __bf16 a = (__bf16)x;
+    const __bf16 b = (__bf16)(x - (float)a);
+    h[0] = __builtin_bit_cast(uint16_t, b);
+    h[1] = __builtin_bit_cast(uint16_t, a);
+  } else {
+    uint16_t h1, h2, h3;
+    split3(x, h1, h2, h3);
+    h[0] = h3; h[1] = h2; h[2] = h1;
+  }
+}
+
+// Whole chunk for wave W: it owns columns JA = W and JB = NB-1-W (if distinct).
+template <int D, int W, int NT>
+__device__ __forceinline__ void gram_wave(const GramArgs& ga, uint16_t* tiles, float* wts) {
+  constexpr int NB = D / 16;
+  constexpr int OCT = D / 8;                            // 16-byte pieces per token row
+  constexpr int LOADS = kGramStep * OCT / kThreads;     // 16-byte loads per thread per step
+  constexpr int TILE = kGramStep * kGramPitch;          // u16 per staged step
+  constexpr int JA = W, JB = NB - 1 - W;
+  constexpr bool HAS_A = JA < NB && JA <= JB;
+  constexpr bool HAS_B = JB > JA;
+  constexpr int PA = HAS_A ? JA + 1 : 0;                // pairs of column JA
+  constexpr int PB = HAS_B ? JB + 1 : 0;                // pairs of column JB
+  constexpr int NP = PA + PB > 0 ? PA + PB : 1;
+  constexpr int NA = HAS_B ? JB + 1 : (HAS_A ? JA + 1 : 0);  // fragments needed
+  constexpr int WPW = kGramStep / (kThreads / 64);      // weights computed per wave per step
+  static_assert(LOADS >= 1, "step too small");
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int ch = lane & 15, kg = lane >> 4;
+
+  // Two-level fp32 accumulation: MFMAs accumulate into acc32 for
+  // kGramFlush steps, which is then added into acc2 (short rounding chains).
+  floatx4 acc32[NP], acc2[NP];
+#pragma unroll
+  for (int p = 0; p < NP; ++p) {
+    acc32[p] = floatx4{0.f, 0.f, 0.f, 0.f};
+    acc2[p] = floatx4{0.f, 0.f, 0.f, 0.f};
+  }
+
+  struct Pre { uint4 v[LOADS]; float z, k; };
+  auto gload = [&](int st, Pre& buf) {
+    const int t0 = ga.base + st * kGramStep;
+#pragma unroll
+    for (int r = 0; r < LOADS; ++r) {
+      const int flat = r * kThreads + tid, tok = flat / OCT, oc = flat % OCT;
+      buf.v[r] = make_uint4(0u, 0u, 0u, 0u);
+      if (t0 + tok < ga.end) buf.v[r] = *reinterpret_cast<const uint4*>(ga.vb + (int64_t)(t0 + tok) * ga.vst + oc * 8);
+    }
+    const int tw = t0 + W * WPW + lane;
+    buf.z = 0.f;
+    buf.k = 0.f;
+    if (lane < WPW && tw < ga.end) { buf.z = ga.zbuf[ga.trow + tw]; buf.k = ga.kbuf[ga.trow + tw]; }
+  };
+  // Stage V and this wave's share of the weights; token t of the step goes to
+  // weight slot (t % 4) * 8 + t / 4, so lane (ch, kg) reads slots 8 kg .. 8 kg + 7.
+  auto stage = [&](int st, const Pre& buf, uint16_t* tile, float* wt) {
+#pragma unroll
+    for (int r = 0; r < LOADS; ++r) {
+      const int flat = r * kThreads + tid, tok = flat / OCT, oc = flat % OCT;
+      *reinterpret_cast<uint4*>(tile + tok * kGramPitch + oc * 8) = buf.v[r];
+    }
+    if (lane < WPW) {
+      const int t = W * WPW + lane;
+      const int tw = ga.base + st * kGramStep + t;
+      const float w = tw < ga.end ? (float)importance_weight(buf.z, buf.k, ga.m, ga.Z, ga.inv_d) : 0.0f;
+      wt[(t % 4) * 8 + t / 4] = w;
+    }
+  };
+  auto column = [&](auto jc, auto pbc, const u16x8 (&a)[NA > 0 ? NA : 1], const float (&wl)[8]) {
+    constexpr int J = decltype(jc)::value, PBASE = decltype(pbc)::value;
+    u16x8 xt[NT];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      uint16_t h[NT];
+      split_terms<NT>(bf16_to_f32(a[J][q]) * wl[q], h);
+#pragma unroll
+      for (int t = 0; t < NT; ++t) xt[t][q] = h[t];
+    }
+    // term-outer order (smallest term first): consecutive MFMAs write
+    // different accumulators
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+      const bf16x8 c = __builtin_bit_cast(bf16x8, xt[t]);
+#pragma unroll
+      for (int i = 0; i <= J; ++i)
+        acc32[PBASE + i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a[i]), c,
+                                                                   acc32[PBASE + i], 0, 0, 0);
+    }
+  };
+  auto flush = [&]() {
+#pragma unroll
+    for (int p = 0; p < NP; ++p) {
+      acc2[p] = acc2[p] + acc32[p];
+      acc32[p] = floatx4{0.f, 0.f, 0.f, 0.f};
+    }
+  };
+  auto compute = [&](const uint16_t* tile, const float* wt) {
+    if constexpr (NA > 0) {
+      float wl[8];
+      const floatx4 w0 = *reinterpret_cast<const floatx4*>(wt + kg * 8);
+      const floatx4 w1 = *reinterpret_cast<const floatx4*>(wt + kg * 8 + 4);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) { wl[q] = w0[q]; wl[q + 4] = w1[q]; }
+      u16x8 a[NA];
+#pragma unroll
+      for (int i = 0; i < NA; ++i)
+#pragma unroll
+        for (int q = 0; q < 8; ++q) a[i][q] = tile[(4 * q + kg) * kGramPitch + 16 * i + ch];
+      if constexpr (HAS_A) column(std::integral_constant<int, JA>{}, std::integral_constant<int, 0>{}, a, wl);
+      if constexpr (HAS_B) column(std::integral_constant<int, JB>{}, std::integral_constant<int, PA>{}, a, wl);
+    }
+  };
+
+  Pre b0, b1;
+  gload(0, b0);
+  if (ga.nsteps > 1) gload(1, b1);
+  for (int st = 0; st < ga.nsteps; st += 2) {
+    stage(st, b0, tiles, wts);
+    __syncthreads();
+    if (st + 2 < ga.nsteps) gload(st + 2, b0);
+    compute(tiles, wts);
+    if ((st + 1) % kGramFlush == 0) flush();
+    if (st + 1 >= ga.nsteps) break;
+    stage(st + 1, b1, tiles + TILE, wts + kGramStep);
+    __syncthreads();
+    if (st + 3 < ga.nsteps) gload(st + 3, b1);
+    compute(tiles + TILE, wts + kGramStep);
+    if ((st + 2) % kGramFlush == 0) flush();
+  }
+  flush();
+  // Emit: column j, row block i -> global pair index of (i, j).
+  auto emit = [&](auto jc, auto pbc) {
+    constexpr int J = decltype(jc)::value, PBASE = decltype(pbc)::value;
+#pragma unroll
+    for (int i = 0; i <= J; ++i) {
+      const int p = i * NB - (i * (i - 1)) / 2 + (J - i);
+      *reinterpret_cast<floatx4*>(ga.out + p * 256 + lane * 4) = acc2[PBASE + i];
+    }
+  };
+  if constexpr (HAS_A) emit(std::integral_constant<int, JA>{}, std::integral_constant<int, 0>{});
+  if constexpr (HAS_B) emit(std::integral_constant<int, JB>{}, std::integral_constant<int, PA>{});
+}
+
+// NT = 2: first pass over every unit. NT = 3: refinement pass over the units
+// the factor kernel marked (kUnitRefine), which rewrites their partials.
+template <int D, int NT>
+__global__ __launch_bounds__(kThreads, 2) void gram_mfma_kernel(
     Geo g, const uint16_t* __restrict__ v, const float* __restrict__ zbuf,
     const float* __restrict__ kbuf, const float* __restrict__ m_u, const double* __restrict__ z_u,
-    float* __restrict__ partials, int gchunks, double inv_d) {
+    const uint32_t* __restrict__ uflags, float* __restrict__ partials, int gchunks, double inv_d) {
   constexpr int NB = D / 16;
   constexpr int NPAIR = NB * (NB + 1) / 2;
-  constexpr int TSTEP = 32;                 // tokens per wave step (MFMA K)
-  constexpr int PITCH = TSTEP + 8;          // padded LDS row (u16 elements)
-  constexpr int LOADS = TSTEP * D / 8 / 64; // 16-byte loads per lane per step
+  constexpr int TILE = kGramStep * kGramPitch;
   const int u = blockIdx.y, chunk = blockIdx.x;
+  if (NT == 3 && !(uflags[u] & kUnitRefine)) return;
   const Unit un = decode_unit(g, u);
   const int base = chunk * kGChunkMfma;
   if (base >= un.n) return;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int ch = lane & 15, kg = lane >> 4;
-
-  __shared__ __attribute__((aligned(16))) uint16_t vt[kThreads / 64][D][PITCH];
-  __shared__ float wsh[kThreads / 64][TSTEP];
-
-  const float m = m_u[u];
-  const double Z = z_u[u];
-  const uint16_t* vb = v + un.l * g.vsl + un.h * g.vsh;
-  const int64_t trow = token_row(g, un);
-  const int end = min(un.n, base + kGChunkMfma);
-
-  floatx4 acc[NPAIR];
-#pragma unroll
-  for (int p = 0; p < NPAIR; ++p) acc[p] = floatx4{0.f, 0.f, 0.f, 0.f};
-
-  for (int t0 = base + wave * TSTEP; t0 < end; t0 += TSTEP * (kThreads / 64)) {
-    // Stage 32 tokens x D channels, transposed, into this wave's LDS tile.
-#pragma unroll
-    for (int r = 0; r < LOADS; ++r) {
-      const int flat = r * 64 + lane;
-      const int tok = flat / (D / 8), oct = flat % (D / 8);
-      uint4 raw = make_uint4(0u, 0u, 0u, 0u);
-      if (t0 + tok < end) raw = *reinterpret_cast<const uint4*>(vb + (un.t0 + t0 + tok) * g.vst + oct * 8);
-      const uint16_t* e = reinterpret_cast<const uint16_t*>(&raw);
-#pragma unroll
-      for (int q = 0; q < 8; ++q) vt[wave][oct * 8 + q][tok] = e[q];
-    }
-    if (lane < TSTEP) {
-      const int t = t0 + lane;
-      float wv = 0.0f;
-      if (t < end) wv = (float)importance_weight(zbuf[trow + t], kbuf[trow + t], m, Z, inv_d);
-      wsh[wave][lane] = wv;
-    }
-    wave_lds_sync();
-
-    float wl[8];
-#pragma unroll
-    for (int q = 0; q < 8; ++q) wl[q] = wsh[wave][kg * 8 + q];
-    bf16x8 a[NB];
-#pragma unroll
-    for (int i = 0; i < NB; ++i) a[i] = *reinterpret_cast<const bf16x8*>(&vt[wave][i * 16 + ch][kg * 8]);
-#pragma unroll
-    for (int j = 0; j < NB; ++j) {
-      bf16x8 x1, x2, x3;
-#pragma unroll
-      for (int q = 0; q < 8; ++q) {
-        const float x = (float)a[j][q] * wl[q];
-        const __bf16 h1 = (__bf16)x;
-        const float r1 = x - (float)h1;
-        const __bf16 h2 = (__bf16)r1;
-        x1[q] = h1;
-        x2[q] = h2;
-        x3[q] = (__bf16)(r1 - (float)h2);
-      }
-#pragma unroll
-      for (int i = 0; i <= j; ++i) {
-        const int p = pair_index(i, j, NB);
-        acc[p] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], x3, acc[p], 0, 0, 0);
-        acc[p] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], x2, acc[p], 0, 0, 0);
-        acc[p] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], x1, acc[p], 0, 0, 0);
-      }
-    }
-    wave_lds_sync();
+  __shared__ __attribute__((aligned(16))) uint16_t tiles[2 * TILE];
+  __shared__ __attribute__((aligned(16))) float wts[2 * kGramStep];
+  GramArgs ga;
+  ga.vb = v + un.l * g.vsl + un.h * g.vsh + un.t0 * g.vst;
+  ga.vst = g.vst;
+  ga.zbuf = zbuf;
+  ga.kbuf = kbuf;
+  ga.trow = token_row(g, un);
+  ga.m = m_u[u];
+  ga.Z = z_u[u];
+  ga.inv_d = inv_d;
+  ga.base = base;
+  ga.end = min(un.n, base + kGChunkMfma);
+  ga.nsteps = (ga.end - base + kGramStep - 1) / kGramStep;
+  ga.out = partials + ((int64_t)u * gchunks + chunk) * (NPAIR * 256);
+  switch (threadIdx.x >> 6) {
+    case 0: gram_wave<D, 0, NT>(ga, tiles, wts); break;
+    case 1: gram_wave<D, 1, NT>(ga, tiles, wts); break;
+    case 2: gram_wave<D, 2, NT>(ga, tiles, wts); break;
+    default: gram_wave<D, 3, NT>(ga, tiles, wts); break;
   }
-  // Partial of this wave: block p, lane, element r -> M[16 i + 4 kg + r][16 j + ch].
-  float* out = partials + (((int64_t)u * gchunks + chunk) * kMfmaGramParts + wave) * (NPAIR * 256);
-#pragma unroll
-  for (int p = 0; p < NPAIR; ++p) *reinterpret_cast<floatx4*>(out + p * 256 + lane * 4) = acc[p];
 }
 
 // fp64 Gram for fp32 inputs: thread (ty, tx) of a 16 x 16 grid owns a
@@ -125,6 +271,8 @@ __global__ __launch_bounds__(kThreads) void gram_precise_kernel(
     const float* __restrict__ kbuf, const float* __restrict__ m_u, const double* __restrict__ z_u,
     double* __restrict__ partials, int gchunks, double inv_d) {
   constexpr int R = D / 16;
+  constexpr int NB = D / 16;
+  constexpr int NPAIR = NB * (NB + 1) / 2;
   const int u = blockIdx.y, chunk = blockIdx.x;
   const Unit un = decode_unit(g, u);
   const int base = chunk * kGChunkPrecise;
@@ -166,14 +314,21 @@ __global__ __launch_bounds__(kThreads) void gram_precise_kernel(
         for (int b = 0; b < R; ++b) acc[a][b] += xa[a] * vb2[b];
     }
   }
-  double* out = partials + ((int64_t)u * gchunks + chunk) * D * D;
+  double* out = partials + ((int64_t)u * gchunks + chunk) * (NPAIR * 256);
 #pragma unroll
   for (int a = 0; a < R; ++a)
 #pragma unroll
-    for (int b = 0; b < R; ++b) out[(ty * R + a) * D + tx * R + b] = acc[a][b];
+    for (int b = 0; b < R; ++b) {
+      const int row = ty * R + a, col = tx * R + b;
+      const int i = row / 16, j = col / 16;
+      if (i > j) continue;
+      const int p = i * NB - (i * (i - 1)) / 2 + (j - i);
+      const int ln = ((row % 16) / 4) * 16 + (col % 16);
+      out[p * 256 + ln * 4 + (row % 4)] = acc[a][b];
+    }
 }
 
-hipError_t launch_gram(const Launch& L, const void* v) {
+hipError_t launch_gram(const Launch& L, const void* v, bool refine) {
   const Geo& g = L.geo;
   const dim3 grid(L.ws.gchunks, g.U);
   const double inv_d = 1.0 / (double)g.D;
@@ -181,18 +336,66 @@ hipError_t launch_gram(const Launch& L, const void* v) {
   const float* kb = ws_ptr<float>(L.wsp, L.ws.kappa);
   const float* mu = ws_ptr<float>(L.wsp, L.ws.smax_m);
   const double* zu = ws_ptr<double>(L.wsp, L.ws.smax_z);
+  const uint32_t* uf = ws_ptr<uint32_t>(L.wsp, L.ws.uflags);
   if (L.ws.mfma) {
     float* part = ws_ptr<float>(L.wsp, L.ws.gram);
-    if (g.D == 128)
-      gram_mfma_kernel<128><<<grid, kThreads, 0, L.stream>>>(g, (const uint16_t*)v, zb, kb, mu, zu, part, L.ws.gchunks, inv_d);
-    else
-      gram_mfma_kernel<64><<<grid, kThreads, 0, L.stream>>>(g, (const uint16_t*)v, zb, kb, mu, zu, part, L.ws.gchunks, inv_d);
+    const uint16_t* vv = (const uint16_t*)v;
+    if (g.D == 128) {
+      if (refine) gram_mfma_kernel<128, 3><<<grid, kThreads, 0, L.stream>>>(g, vv, zb, kb, mu, zu, uf, part, L.ws.gchunks, inv_d);
+      else gram_mfma_kernel<128, 2><<<grid, kThreads, 0, L.stream>>>(g, vv, zb, kb, mu, zu, uf, part, L.ws.gchunks, inv_d);
+    } else {
+      if (refine) gram_mfma_kernel<64, 3><<<grid, kThreads, 0, L.stream>>>(g, vv, zb, kb, mu, zu, uf, part, L.ws.gchunks, inv_d);
+      else gram_mfma_kernel<64, 2><<<grid, kThreads, 0, L.stream>>>(g, vv, zb, kb, mu, zu, uf, part, L.ws.gchunks, inv_d);
+    }
   } else {
+    if (refine) return hipSuccess;
     double* part = ws_ptr<double>(L.wsp, L.ws.gram);
     if (g.D == 128)
       gram_precise_kernel<128><<<grid, kThreads, 0, L.stream>>>(g, (const float*)v, zb, kb, mu, zu, part, L.ws.gchunks, inv_d);
     else
       gram_precise_kernel<64><<<grid, kThreads, 0, L.stream>>>(g, (const float*)v, zb, kb, mu, zu, part, L.ws.gchunks, inv_d);
+  }
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Reduce the per-chunk partials of each unit, entry by entry, in chunk order
+// (fp64). grid = (NPAIR, U): one 16x16 block pair per workgroup.
+// ---------------------------------------------------------------------------
+template <typename P, int D>
+__global__ __launch_bounds__(kThreads) void gram_reduce_kernel(Geo g, const P* __restrict__ partials,
+                                                               int gchunks, int gchunk,
+                                                               const uint32_t* __restrict__ uflags,
+                                                               int refine, double* __restrict__ red) {
+  constexpr int NB = D / 16;
+  constexpr int NPAIR = NB * (NB + 1) / 2;
+  const int p = blockIdx.x, u = blockIdx.y;
+  if (refine && !(uflags[u] & kUnitRefine)) return;
+  const Unit un = decode_unit(g, u);
+  const int nch = (un.n + gchunk - 1) / gchunk;
+  const P* src = partials + (int64_t)u * gchunks * (NPAIR * 256) + p * 256 + threadIdx.x;
+  double s = 0.0;
+#pragma unroll 8
+  for (int c = 0; c < nch; ++c) s += (double)src[(int64_t)c * (NPAIR * 256)];
+  red[(int64_t)u * (NPAIR * 256) + p * 256 + threadIdx.x] = s;
+}
+
+hipError_t launch_gram_reduce(const Launch& L, bool refine) {
+  const Geo& g = L.geo;
+  if (refine && !L.ws.mfma) return hipSuccess;
+  const uint32_t* uf = ws_ptr<uint32_t>(L.wsp, L.ws.uflags);
+  const int rf = refine ? 1 : 0;
+  const int NB = g.D / 16, npair = NB * (NB + 1) / 2;
+  const dim3 grid(npair, g.U);
+  double* red = ws_ptr<double>(L.wsp, L.ws.gram_red);
+  if (L.ws.mfma) {
+    const float* part = ws_ptr<float>(L.wsp, L.ws.gram);
+    if (g.D == 128) gram_reduce_kernel<float, 128><<<grid, kThreads, 0, L.stream>>>(g, part, L.ws.gchunks, L.ws.gchunk, uf, rf, red);
+    else gram_reduce_kernel<float, 64><<<grid, kThreads, 0, L.stream>>>(g, part, L.ws.gchunks, L.ws.gchunk, uf, rf, red);
+  } else {
+    const double* part = ws_ptr<double>(L.wsp, L.ws.gram);
+    if (g.D == 128) gram_reduce_kernel<double, 128><<<grid, kThreads, 0, L.stream>>>(g, part, L.ws.gchunks, L.ws.gchunk, uf, rf, red);
+    else gram_reduce_kernel<double, 64><<<grid, kThreads, 0, L.stream>>>(g, part, L.ws.gchunks, L.ws.gchunk, uf, rf, red);
   }
   return hipGetLastError();
 }

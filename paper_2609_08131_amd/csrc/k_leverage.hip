@@ -16,87 +16,95 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float floatx4 __attribute__((ext_vector_type(4)));
 
 template <int D>
-__global__ __launch_bounds__(kThreads) void leverage_mfma_kernel(
+__global__ __launch_bounds__(kThreads, 2) void leverage_mfma_kernel(
     Geo g, const uint16_t* __restrict__ v, const float* __restrict__ zbuf,
     const float* __restrict__ kbuf, const float* __restrict__ m_u, const double* __restrict__ z_u,
-    const float* __restrict__ linv32, const uint32_t* __restrict__ uflags,
+    const uint16_t* __restrict__ lfrag, const uint32_t* __restrict__ uflags,
     float* __restrict__ scores, double inv_d) {
-  constexpr int NB = D / 16;  // output blocks of 16 channels (a)
-  constexpr int NK = D / 32;  // K blocks of 32 channels (b)
+  constexpr int NB = D / 16;                    // output blocks of 16 channels (a)
+  constexpr int NK = D / 32;                    // K blocks of 32 channels (b)
+  constexpr int NLP = (NB / 2) * (NB / 2 + 1);  // lower (j, kb) block pairs
   const int u = blockIdx.y, chunk = blockIdx.x;
   const Unit un = decode_unit(g, u);
-  const int base = chunk * kLChunk;
+  const int base = chunk * kLChunkMfma;
   if (base >= un.n) return;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int ch = lane & 15, kg = lane >> 4;
   const int64_t trow = token_row(g, un);
-  const int end = min(un.n, base + kLChunk);
+  const int end = min(un.n, base + kLChunkMfma);
 
-  if (uflags[u] != 0u) {  // unit failed (non-finite input or singular A): NaN scores
+  if (uflags[u] & kUnitFailed) {  // unit failed (non-finite input or singular A): NaN scores
     for (int t = base + threadIdx.x; t < end; t += kThreads) scores[trow + t] = __builtin_nanf("");
     return;
   }
 
-  // B fragments: lane holds L^{-1}[a = 16 j + ch][b = 32 kb + 8 kg + q], q = 0..7.
-  bf16x8 bh[NB][NK], bl[NB][NK];
-  const float* Li = linv32 + (int64_t)u * D * D;
+  // B fragments, pre-split by the factor kernel in lane order.
+  bf16x8 bh[NLP], bl[NLP];
+  const uint16_t* lf = lfrag + (int64_t)u * NLP * 2 * 64 * 8;
 #pragma unroll
-  for (int j = 0; j < NB; ++j)
-#pragma unroll
-    for (int kb = 0; kb < NK; ++kb) {
-      if (32 * kb > 16 * j + 15) continue;  // block entirely above the diagonal
-      const float* src = Li + (16 * j + ch) * D + 32 * kb + 8 * kg;
-#pragma unroll
-      for (int q = 0; q < 8; ++q) {
-        const float x = src[q];
-        const __bf16 h = (__bf16)x;
-        bh[j][kb][q] = h;
-        bl[j][kb][q] = (__bf16)(x - (float)h);
-      }
-    }
+  for (int q = 0; q < NLP; ++q) {
+    bh[q] = *reinterpret_cast<const bf16x8*>(lf + ((int64_t)(q * 2 + 0) * 64 + lane) * 8);
+    bl[q] = *reinterpret_cast<const bf16x8*>(lf + ((int64_t)(q * 2 + 1) * 64 + lane) * 8);
+  }
 
   const float m = m_u[u];
   const double Z = z_u[u];
-  const uint16_t* vb = v + un.l * g.vsl + un.h * g.vsh;
+  const uint16_t* vb = v + un.l * g.vsl + un.h * g.vsh + un.t0 * g.vst;
 
-  for (int t0 = base + wave * 16; t0 < end; t0 += 16 * (kThreads / 64)) {
+  // A step is 16 tokens (one MFMA row tile); the next step's V rows are
+  // loaded while this one computes. MFMAs are issued kb-outer so that
+  // consecutive MFMAs update different output blocks.
+  auto load = [&](int t0, bf16x8 (&a)[NK]) {
     const int tok = t0 + ch;  // A-operand row of this lane
-    bf16x8 a[NK];
 #pragma unroll
     for (int kb = 0; kb < NK; ++kb) {
       uint4 raw = make_uint4(0u, 0u, 0u, 0u);
-      if (tok < end) raw = *reinterpret_cast<const uint4*>(vb + (un.t0 + tok) * g.vst + 32 * kb + 8 * kg);
-      a[kb] = *reinterpret_cast<const bf16x8*>(&raw);
+      if (tok < end) raw = *reinterpret_cast<const uint4*>(vb + (int64_t)tok * g.vst + 32 * kb + 8 * kg);
+      a[kb] = __builtin_bit_cast(bf16x8, raw);
     }
+  };
+  constexpr int WSTRIDE = 16 * (kThreads / 64);
+  int t0 = base + wave * 16;
+  bf16x8 cur[NK], nxt[NK];
+  if (t0 < end) load(t0, cur);
+  for (; t0 < end; t0 += WSTRIDE) {
+    if (t0 + WSTRIDE < end) load(t0 + WSTRIDE, nxt);
+    const int tw = t0 + 4 * kg + (ch & 3);
+    float zt = 0.f, kt = 0.f;
+    if (ch < 4 && tw < end) { zt = zbuf[trow + tw]; kt = kbuf[trow + tw]; }
+    // Output blocks j = 2 jp and 2 jp + 1 share the K-block range kb <= jp:
+    // their two accumulation chains are interleaved.
     float ss[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int j = 0; j < NB; ++j) {
-      floatx4 y = {0.f, 0.f, 0.f, 0.f};
+    for (int jp = 0; jp < NB / 2; ++jp) {
+      floatx4 y0 = {0.f, 0.f, 0.f, 0.f}, y1 = {0.f, 0.f, 0.f, 0.f};
+      const int q0 = jp * (jp + 1) * 1 + jp * 0;        // pair index of (2 jp, 0)
+      const int q1 = jp * (jp + 1) + (jp + 1);          // pair index of (2 jp + 1, 0)
 #pragma unroll
-      for (int kb = 0; kb < NK; ++kb) {
-        if (32 * kb > 16 * j + 15) continue;
-        y = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[kb], bh[j][kb], y, 0, 0, 0);
-        y = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[kb], bl[j][kb], y, 0, 0, 0);
+      for (int kb = 0; kb <= jp; ++kb) {
+        y0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(cur[kb], bh[q0 + kb], y0, 0, 0, 0);
+        y1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(cur[kb], bh[q1 + kb], y1, 0, 0, 0);
+        y0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(cur[kb], bl[q0 + kb], y0, 0, 0, 0);
+        y1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(cur[kb], bl[q1 + kb], y1, 0, 0, 0);
       }
 #pragma unroll
-      for (int r = 0; r < 4; ++r) ss[r] += y[r] * y[r];
+      for (int r = 0; r < 4; ++r) ss[r] += y0[r] * y0[r] + y1[r] * y1[r];
     }
     // lane holds Y[token t0 + 4 kg + r][a = 16 j + ch]: reduce over ch.
 #pragma unroll
     for (int r = 0; r < 4; ++r)
 #pragma unroll
       for (int o = 1; o < 16; o <<= 1) ss[r] += __shfl_xor(ss[r], o);
-    if (ch < 4) {
-      const int t = t0 + 4 * kg + ch;
-      float s = ss[0];
+    if (ch < 4 && tw < end) {
+      float sv = ss[0];
 #pragma unroll
       for (int r = 1; r < 4; ++r)
-        if (ch == r) s = ss[r];
-      if (t < end) {
-        const double w = importance_weight(zbuf[trow + t], kbuf[trow + t], m, Z, inv_d);
-        scores[trow + t] = (float)(w * (double)s);
-      }
+        if (ch == r) sv = ss[r];
+      const double w = importance_weight(zt, kt, m, Z, inv_d);
+      scores[trow + tw] = (float)(w * (double)sv);
     }
+#pragma unroll
+    for (int kb = 0; kb < NK; ++kb) cur[kb] = nxt[kb];
   }
 }
 
@@ -111,12 +119,12 @@ __global__ __launch_bounds__(kThreads) void leverage_precise_kernel(
   constexpr int TOK = kThreads / TPT;    // tokens per tile
   const int u = blockIdx.y, chunk = blockIdx.x;
   const Unit un = decode_unit(g, u);
-  const int base = chunk * kLChunk;
+  const int base = chunk * kLChunkPrecise;
   if (base >= un.n) return;
   const int tid = threadIdx.x;
   const int64_t trow = token_row(g, un);
-  const int end = min(un.n, base + kLChunk);
-  if (uflags[u] != 0u) {
+  const int end = min(un.n, base + kLChunkPrecise);
+  if (uflags[u] & kUnitFailed) {
     for (int t = base + tid; t < end; t += kThreads) scores[trow + t] = __builtin_nanf("");
     return;
   }
@@ -161,11 +169,11 @@ hipError_t launch_leverage(const Launch& L, const void* v, float* scores) {
   const double* zu = ws_ptr<double>(L.wsp, L.ws.smax_z);
   const uint32_t* uf = ws_ptr<uint32_t>(L.wsp, L.ws.uflags);
   if (L.ws.mfma) {
-    const float* l32 = ws_ptr<float>(L.wsp, L.ws.linv32);
+    const uint16_t* lf = ws_ptr<uint16_t>(L.wsp, L.ws.lfrag);
     if (g.D == 128)
-      leverage_mfma_kernel<128><<<grid, kThreads, 0, L.stream>>>(g, (const uint16_t*)v, zb, kb, mu, zu, l32, uf, scores, inv_d);
+      leverage_mfma_kernel<128><<<grid, kThreads, 0, L.stream>>>(g, (const uint16_t*)v, zb, kb, mu, zu, lf, uf, scores, inv_d);
     else
-      leverage_mfma_kernel<64><<<grid, kThreads, 0, L.stream>>>(g, (const uint16_t*)v, zb, kb, mu, zu, l32, uf, scores, inv_d);
+      leverage_mfma_kernel<64><<<grid, kThreads, 0, L.stream>>>(g, (const uint16_t*)v, zb, kb, mu, zu, lf, uf, scores, inv_d);
   } else {
     const double* l64 = ws_ptr<double>(L.wsp, L.ws.linv64);
     if (g.D == 128)
