@@ -52,6 +52,7 @@ Workspace layout(const jacap_config* c, const jacap_batch* b) {
   const int maxn = b->max_seq_len;
   w.mfma = c->dtype == JACAP_DTYPE_BF16;
   w.kchunks = (maxn + kKChunk - 1) / kKChunk;
+  w.wchunks = (maxn + kWChunk - 1) / kWChunk;
   w.gchunk = w.mfma ? kGChunkMfma : kGChunkPrecise;
   w.gchunks = (maxn + w.gchunk - 1) / w.gchunk;
   w.gparts = 1;
@@ -73,6 +74,7 @@ Workspace layout(const jacap_config* c, const jacap_batch* b) {
   w.z = take(4 * LHT);
   w.kappa = take(4 * LHT);
   w.cstat = take(8 * U * (int64_t)w.kchunks);
+  w.wgt = take(4 * LHT);
   w.gram = take((size_t)(U * (int64_t)w.gchunks * part_bytes));
   w.gram_red = take(8 * U * npair * 256);
   w.linv64 = take(w.mfma ? 8 : 8 * U * D * D);
@@ -128,7 +130,7 @@ jacap_status run_score(const Launch& L, const void* q, const void* k, const void
   JACAP_TRY(launch_init(L));
   JACAP_TRY(launch_qstats(L, q));
   JACAP_TRY(launch_kpass(L, k));
-  JACAP_TRY(launch_softmax_merge(L));
+  JACAP_TRY(launch_softmax_weights(L));
   JACAP_TRY(launch_gram(L, v, false));
   JACAP_TRY(launch_gram_reduce(L, false));
   JACAP_TRY(launch_factor(L, false));

@@ -18,6 +18,7 @@ constexpr int kGChunkMfma = 4096;    // tokens per workgroup in the MFMA Gram pa
 constexpr int kGChunkPrecise = 1024; // tokens per workgroup in the fp64 Gram pass
 constexpr int kLChunkMfma = 4096;    // tokens per workgroup in the MFMA leverage pass
 constexpr int kLChunkPrecise = 1024; // tokens per workgroup in the fp64 leverage pass
+constexpr int kWChunk = 4096;        // tokens per workgroup in the weight pass
 
 // Unit flags (per (seq, layer, kv head)); the public flags are the OR of all.
 constexpr uint32_t kUnitNonfinite = JACAP_FLAG_NONFINITE;
@@ -85,12 +86,13 @@ struct Workspace {
   size_t z;        // float  [L][H][T]       centre logits
   size_t kappa;    // float  [L][H][T]       query response
   size_t cstat;    // float2 [U][kchunks]    per-chunk (max, sum exp)
+  size_t wgt;      // float  [L][H][T]       importance weights (Eq. 8)
   size_t gram;     // per-chunk partial Grams [U][gchunks][NPAIR*256], fp32 (bf16 path) or fp64
   size_t gram_red; // double [U][NPAIR*256]  reduced Gram, block-lane layout
   size_t linv64;   // double [U][D][D]       L^{-1} (lower, zeros above), fp32-input path
   size_t lfrag;    // bf16 [U][NLP][2][64][8] L^{-1} hi/lo MFMA B fragments, bf16 path
   size_t total;
-  int kchunks, gchunks, gchunk, gparts, lchunks;
+  int kchunks, wchunks, gchunks, gchunk, gparts, lchunks;
   bool mfma;       // bf16 path (MFMA Gram and leverage)
 };
 
@@ -180,7 +182,7 @@ struct Launch {
 hipError_t launch_init(const Launch& L);
 hipError_t launch_qstats(const Launch& L, const void* q);
 hipError_t launch_kpass(const Launch& L, const void* k);
-hipError_t launch_softmax_merge(const Launch& L);
+hipError_t launch_softmax_weights(const Launch& L);
 hipError_t launch_gram(const Launch& L, const void* v, bool refine);
 hipError_t launch_gram_reduce(const Launch& L, bool refine);
 hipError_t launch_factor(const Launch& L, bool refine);

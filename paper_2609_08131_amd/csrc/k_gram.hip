@@ -6,16 +6,13 @@
 // M, block pair p = pair_index(i, j), 256 entries per block in MFMA 16x16
 // output order: entry p*256 + lane*4 + r holds M[16i + 4(lane/16) + r][16j + lane%16].
 //
-// bf16 inputs: MFMA 16x16x32 bf16 with fp32 accumulation. The reduction runs
-// over tokens, so a lane's operand fragment is 8 consecutive tokens of one
-// channel: it is gathered straight from HBM with 16-bit loads (four rows x 32
-// bytes per wave instruction), so no LDS transpose is needed. V is exact in
-// bf16; the weighted operand x = w v (fp32) is split exactly into three bf16
-// terms by truncation (x = x1 + x2 + x3), so M = V^T X1 + V^T X2 + V^T X3 is
-// an fp32-accurate Gram: the capacity matrix of a short or ridge-0 unit can
-// reach cond(A) ~ 1e5-1e6, where a two-term split (2^-17) costs more than
-// the 1e-3 score tolerance. The next step's fragments are loaded while the
-// current step's MFMAs run. The four waves' accumulators are reduced in LDS.
+// bf16 inputs: MFMA 16x16x32 bf16 with fp32 accumulation; the contraction runs
+// over tokens. V is exact in bf16; the weighted operand x = w v (fp32) is split
+// into bf16 terms, so M = sum_t V^T X_t. The first pass uses two terms rounded
+// to nearest (x = x1 + x2 to 2^-17 relative); the factor kernel then marks
+// the units whose capacity matrix is ill-conditioned enough for that to show
+// in the scores, and a second pass recomputes only those with an exact
+// three-term split by truncation.
 //
 // fp32 inputs: fp64 VALU accumulation (register tiles), same partial layout.
 #include <type_traits>
@@ -27,13 +24,9 @@ namespace jacap {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float floatx4 __attribute__((ext_vector_type(4)));
 typedef uint16_t u16x8 __attribute__((ext_vector_type(8)));
-
-// Per-wave barrier for LDS traffic that stays inside one wave.
-__device__ __forceinline__ void wave_lds_sync() {
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-  __builtin_amdgcn_wave_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-}
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float float2v __attribute__((ext_vector_type(2)));
 
 // Three-term exact split of x into bf16 pieces by truncation: each piece takes
 // the next 8 significant bits, the remainder of the last one is exactly zero.
@@ -47,37 +40,8 @@ __device__ __forceinline__ void split3(float x, uint16_t& h1, uint16_t& h2, uint
   h3 = (uint16_t)(__float_as_uint(r2) >> 16);
 }
 
-// The workgroup walks its chunk in steps of 32 tokens. Each step is loaded
-// with coalesced 16-byte loads (prefetched two steps ahead), staged in LDS
-// (double-buffered, one barrier per step) and shared by the four waves. The
-// upper 16x16 block pairs (i <= j) are split between the waves by column
-// pairs {w, NB-1-w}, which gives every wave the same number of pairs (9 at
-// d = 128), so no cross-wave reduction is needed. Token <-> MFMA K-slot
-// mapping: lane (ch, kg) element q is token 4 q + kg of the step (the same
-// mapping for both operands); with a 288-byte row pitch the four kg groups of
-// a fragment read fall in disjoint LDS banks. Each wave accumulates in fp32
-// for kGramFlush steps, then adds that into a second fp32 accumulator, so the
-// rounding chains stay short (the Gram of an ill-conditioned ridge-0 unit
-// needs it).
-constexpr int kGramStep = 32;
-constexpr int kGramPitch = 144;  // u16 elements per staged token row (288 bytes)
-constexpr int kGramFlush = 4;
-
-struct GramArgs {
-  const uint16_t* vb;   // V of the unit, at its first token
-  int64_t vst;
-  const float* zbuf;
-  const float* kbuf;
-  int64_t trow;
-  float m;
-  double Z;
-  double inv_d;
-  int base, end, nsteps;
-  float* out;           // this chunk's partial (block-lane layout)
-};
-
 // Split x into NT bf16 terms, smallest first (x = sum of the terms up to the
-// split error): NT = 2 rounds to nearest (error <= 2^-18 |x|); NT = 3
+// split error): NT = 2 rounds to nearest (error <= 2^-17 |x|); NT = 3
 // truncates (exact).
 template <int NT>
 __device__ __forceinline__ void split_terms(float x, uint16_t (&h)[NT]) {
@@ -93,6 +57,43 @@ __device__ __forceinline__ void split_terms(float x, uint16_t (&h)[NT]) {
   }
 }
 
+// Transposing 64-bit LDS read (gfx950): inside each group of 16 lanes, lane i
+// receives element i % 4 of the 4 x 16-bit values addressed by lanes
+// i / 4, 4 + i / 4, 8 + i / 4 and 12 + i / 4 of its group, in that order.
+__device__ __forceinline__ s16x4 lds_read_tr16(const uint16_t* p) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (__attribute__((address_space(3))) s16x4*)(p));
+}
+
+// The workgroup walks its chunk in steps of 32 tokens. Each step is loaded
+// with coalesced 16-byte loads (prefetched two steps ahead) and staged in LDS
+// token-major (double-buffered, one barrier per step); the four waves share
+// it. The upper 16x16 block pairs (i <= j) are split between the waves by
+// column pairs {w, NB-1-w}, which gives every wave the same number of pairs
+// (9 at d = 128), so no cross-wave reduction is needed.
+//
+// Token <-> MFMA K-slot mapping: lane (ch, kg) slot q holds token 8 kg + q of
+// the step, for both operands. The operand fragment of a 16-channel block is
+// read with two transposing LDS reads: lane (i, kg) addresses token
+// 8 kg + i / 4 (+ 4), channels 4 (i % 4) .. + 3 of the block, and receives
+// channel i of tokens 8 kg .. 8 kg + 3 (8 kg + 4 .. 8 kg + 7). With a 288-byte
+// row pitch, the 16 lanes of a group touch 32 distinct banks.
+//
+// Accumulation: fp32 MFMA chains of kGramFlush steps, each added into a
+// second fp32 accumulator (short rounding chains; an ill-conditioned ridge-0
+// unit needs them).
+constexpr int kGramStep = 32;
+constexpr int kGramPitch = 144;  // u16 elements per staged token row (288 bytes)
+constexpr int kGramFlush = 4;
+
+struct GramArgs {
+  const uint16_t* vb;   // V of the unit, at its first token
+  int64_t vst;
+  const float* wrow;    // importance weights of the unit, at its first token
+  int base, end, nsteps;  // nsteps: a multiple of kGramFlush
+  float* out;           // this chunk's partial (block-lane layout)
+};
+
 // Whole chunk for wave W: it owns columns JA = W and JB = NB-1-W (if distinct).
 template <int D, int W, int NT>
 __device__ __forceinline__ void gram_wave(const GramArgs& ga, uint16_t* tiles, float* wts) {
@@ -107,58 +108,74 @@ __device__ __forceinline__ void gram_wave(const GramArgs& ga, uint16_t* tiles, f
   constexpr int PB = HAS_B ? JB + 1 : 0;                // pairs of column JB
   constexpr int NP = PA + PB > 0 ? PA + PB : 1;
   constexpr int NA = HAS_B ? JB + 1 : (HAS_A ? JA + 1 : 0);  // fragments needed
-  constexpr int WPW = kGramStep / (kThreads / 64);      // weights computed per wave per step
+  constexpr int WPW = kGramStep / (kThreads / 64);      // weights loaded per wave per step
   static_assert(LOADS >= 1, "step too small");
+  static_assert((WPW & (WPW - 1)) == 0, "weights per wave must be a power of two");
   const int tid = threadIdx.x, lane = tid & 63;
-  const int ch = lane & 15, kg = lane >> 4;
+  const int kg = lane >> 4, il = lane & 15;
+  // This lane's address inside a staged step for the transposing reads.
+  const int tr_off = (8 * kg + (il >> 2)) * kGramPitch + 4 * (il & 3);
 
-  // Two-level fp32 accumulation: MFMAs accumulate into acc32 for
-  // kGramFlush steps, which is then added into acc2 (short rounding chains).
   floatx4 acc32[NP], acc2[NP];
 #pragma unroll
-  for (int p = 0; p < NP; ++p) {
-    acc32[p] = floatx4{0.f, 0.f, 0.f, 0.f};
-    acc2[p] = floatx4{0.f, 0.f, 0.f, 0.f};
-  }
+  for (int p = 0; p < NP; ++p) acc2[p] = floatx4{0.f, 0.f, 0.f, 0.f};
 
-  struct Pre { uint4 v[LOADS]; float z, k; };
-  auto gload = [&](int st, Pre& buf) {
+  // Tokens past the chunk end are loaded from the last token (in bounds) and
+  // get weight 0: x = 0 in their K-slots, so they add exactly nothing.
+  struct Pre { uint4 v[LOADS]; float w; };
+  auto gload = [&](int st) {
+    Pre buf;
     const int t0 = ga.base + st * kGramStep;
+    const int last = ga.end - 1;
 #pragma unroll
     for (int r = 0; r < LOADS; ++r) {
       const int flat = r * kThreads + tid, tok = flat / OCT, oc = flat % OCT;
-      buf.v[r] = make_uint4(0u, 0u, 0u, 0u);
-      if (t0 + tok < ga.end) buf.v[r] = *reinterpret_cast<const uint4*>(ga.vb + (int64_t)(t0 + tok) * ga.vst + oc * 8);
+      const int t = min(t0 + tok, last);
+      buf.v[r] = *reinterpret_cast<const uint4*>(ga.vb + (int64_t)t * ga.vst + oc * 8);
     }
-    const int tw = t0 + W * WPW + lane;
-    buf.z = 0.f;
-    buf.k = 0.f;
-    if (lane < WPW && tw < ga.end) { buf.z = ga.zbuf[ga.trow + tw]; buf.k = ga.kbuf[ga.trow + tw]; }
+    const int tw = t0 + W * WPW + (lane & (WPW - 1));
+    const float w = ga.wrow[min(tw, last)];
+    buf.w = tw <= last ? w : 0.f;
+    return buf;
   };
-  // Stage V and this wave's share of the weights; token t of the step goes to
-  // weight slot (t % 4) * 8 + t / 4, so lane (ch, kg) reads slots 8 kg .. 8 kg + 7.
-  auto stage = [&](int st, const Pre& buf, uint16_t* tile, float* wt) {
+  auto stage = [&](const Pre& buf, uint16_t* tile, float* wt) {
 #pragma unroll
     for (int r = 0; r < LOADS; ++r) {
       const int flat = r * kThreads + tid, tok = flat / OCT, oc = flat % OCT;
       *reinterpret_cast<uint4*>(tile + tok * kGramPitch + oc * 8) = buf.v[r];
     }
-    if (lane < WPW) {
-      const int t = W * WPW + lane;
-      const int tw = ga.base + st * kGramStep + t;
-      const float w = tw < ga.end ? (float)importance_weight(buf.z, buf.k, ga.m, ga.Z, ga.inv_d) : 0.0f;
-      wt[(t % 4) * 8 + t / 4] = w;
-    }
+    if (lane < WPW) wt[W * WPW + lane] = buf.w;
   };
-  auto column = [&](auto jc, auto pbc, const u16x8 (&a)[NA > 0 ? NA : 1], const float (&wl)[8]) {
+  // Column J of the step: B operand x = w v of block J, split into NT terms,
+  // against the A fragments of blocks 0..J. FIRST: the chain restarts.
+  auto column = [&](auto jc, auto pbc, auto firstc, const u16x8 (&a)[NA > 0 ? NA : 1],
+                    const float (&wl)[8]) {
     constexpr int J = decltype(jc)::value, PBASE = decltype(pbc)::value;
+    constexpr bool FIRST = decltype(firstc)::value;
     u16x8 xt[NT];
+    if constexpr (NT == 2) {
+      // Pairwise: hi = RNE(x) for two elements with one packed convert, the
+      // residual x - hi from an fma on the exact product.
 #pragma unroll
-    for (int q = 0; q < 8; ++q) {
-      uint16_t h[NT];
-      split_terms<NT>(bf16_to_f32(a[J][q]) * wl[q], h);
+      for (int q = 0; q < 8; q += 2) {
+        const float v0 = bf16_to_f32(a[J][q]), v1 = bf16_to_f32(a[J][q + 1]);
+        const float2v x = {v0 * wl[q], v1 * wl[q + 1]};
+        const bf16x2 hi = __builtin_convertvector(x, bf16x2);
+        const uint32_t hb = __builtin_bit_cast(uint32_t, hi);
+        const float h0 = __uint_as_float(hb << 16), h1 = __uint_as_float(hb & 0xFFFF0000u);
+        const float2v r = {fmaf(v0, wl[q], -h0), fmaf(v1, wl[q + 1], -h1)};
+        const uint32_t lb = __builtin_bit_cast(uint32_t, __builtin_convertvector(r, bf16x2));
+        xt[0][q] = (uint16_t)lb; xt[0][q + 1] = (uint16_t)(lb >> 16);
+        xt[1][q] = (uint16_t)hb; xt[1][q + 1] = (uint16_t)(hb >> 16);
+      }
+    } else {
 #pragma unroll
-      for (int t = 0; t < NT; ++t) xt[t][q] = h[t];
+      for (int q = 0; q < 8; ++q) {
+        uint16_t h[NT];
+        split_terms<NT>(bf16_to_f32(a[J][q]) * wl[q], h);
+#pragma unroll
+        for (int t = 0; t < NT; ++t) xt[t][q] = h[t];
+      }
     }
     // term-outer order (smallest term first): consecutive MFMAs write
     // different accumulators
@@ -166,52 +183,54 @@ __device__ __forceinline__ void gram_wave(const GramArgs& ga, uint16_t* tiles, f
     for (int t = 0; t < NT; ++t) {
       const bf16x8 c = __builtin_bit_cast(bf16x8, xt[t]);
 #pragma unroll
-      for (int i = 0; i <= J; ++i)
-        acc32[PBASE + i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a[i]), c,
-                                                                   acc32[PBASE + i], 0, 0, 0);
+      for (int i = 0; i <= J; ++i) {
+        const bf16x8 ai = __builtin_bit_cast(bf16x8, a[i]);
+        if (FIRST && t == 0)
+          acc32[PBASE + i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ai, c, floatx4{0.f, 0.f, 0.f, 0.f}, 0, 0, 0);
+        else
+          acc32[PBASE + i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ai, c, acc32[PBASE + i], 0, 0, 0);
+      }
     }
   };
-  auto flush = [&]() {
-#pragma unroll
-    for (int p = 0; p < NP; ++p) {
-      acc2[p] = acc2[p] + acc32[p];
-      acc32[p] = floatx4{0.f, 0.f, 0.f, 0.f};
-    }
-  };
-  auto compute = [&](const uint16_t* tile, const float* wt) {
+  auto compute = [&](const uint16_t* tile, const float* wt, auto firstc) {
     if constexpr (NA > 0) {
       float wl[8];
-      const floatx4 w0 = *reinterpret_cast<const floatx4*>(wt + kg * 8);
-      const floatx4 w1 = *reinterpret_cast<const floatx4*>(wt + kg * 8 + 4);
+      const floatx4 w0 = *reinterpret_cast<const floatx4*>(wt + 8 * kg);
+      const floatx4 w1 = *reinterpret_cast<const floatx4*>(wt + 8 * kg + 4);
 #pragma unroll
       for (int q = 0; q < 4; ++q) { wl[q] = w0[q]; wl[q + 4] = w1[q]; }
       u16x8 a[NA];
+      const uint16_t* tb = tile + tr_off;
 #pragma unroll
-      for (int i = 0; i < NA; ++i)
+      for (int i = 0; i < NA; ++i) {
+        const s16x4 lo = lds_read_tr16(tb + 16 * i);
+        const s16x4 hi = lds_read_tr16(tb + 16 * i + 4 * kGramPitch);
 #pragma unroll
-        for (int q = 0; q < 8; ++q) a[i][q] = tile[(4 * q + kg) * kGramPitch + 16 * i + ch];
-      if constexpr (HAS_A) column(std::integral_constant<int, JA>{}, std::integral_constant<int, 0>{}, a, wl);
-      if constexpr (HAS_B) column(std::integral_constant<int, JB>{}, std::integral_constant<int, PA>{}, a, wl);
+        for (int q = 0; q < 4; ++q) { a[i][q] = (uint16_t)lo[q]; a[i][q + 4] = (uint16_t)hi[q]; }
+      }
+      if constexpr (HAS_A) column(std::integral_constant<int, JA>{}, std::integral_constant<int, 0>{}, firstc, a, wl);
+      if constexpr (HAS_B) column(std::integral_constant<int, JB>{}, std::integral_constant<int, PA>{}, firstc, a, wl);
     }
   };
+  // One step: stage the prefetched data, barrier, prefetch two steps ahead,
+  // compute. The two buffers alternate with the step parity.
+  auto step = [&](int st, Pre& buf, int half, auto firstc) {
+    stage(buf, tiles + half * TILE, wts + half * kGramStep);
+    __syncthreads();
+    if (st + 2 < ga.nsteps) buf = gload(st + 2);
+    compute(tiles + half * TILE, wts + half * kGramStep, firstc);
+  };
 
-  Pre b0, b1;
-  gload(0, b0);
-  if (ga.nsteps > 1) gload(1, b1);
-  for (int st = 0; st < ga.nsteps; st += 2) {
-    stage(st, b0, tiles, wts);
-    __syncthreads();
-    if (st + 2 < ga.nsteps) gload(st + 2, b0);
-    compute(tiles, wts);
-    if ((st + 1) % kGramFlush == 0) flush();
-    if (st + 1 >= ga.nsteps) break;
-    stage(st + 1, b1, tiles + TILE, wts + kGramStep);
-    __syncthreads();
-    if (st + 3 < ga.nsteps) gload(st + 3, b1);
-    compute(tiles + TILE, wts + kGramStep);
-    if ((st + 2) % kGramFlush == 0) flush();
+  static_assert(kGramFlush == 4, "the step loop below is unrolled by four");
+  Pre b0 = gload(0), b1 = gload(1);
+  for (int st = 0; st < ga.nsteps; st += kGramFlush) {
+    step(st, b0, 0, std::true_type{});
+    step(st + 1, b1, 1, std::false_type{});
+    step(st + 2, b0, 0, std::false_type{});
+    step(st + 3, b1, 1, std::false_type{});
+#pragma unroll
+    for (int p = 0; p < NP; ++p) acc2[p] = acc2[p] + acc32[p];
   }
-  flush();
   // Emit: column j, row block i -> global pair index of (i, j).
   auto emit = [&](auto jc, auto pbc) {
     constexpr int J = decltype(jc)::value, PBASE = decltype(pbc)::value;
@@ -229,9 +248,8 @@ __device__ __forceinline__ void gram_wave(const GramArgs& ga, uint16_t* tiles, f
 // the factor kernel marked (kUnitRefine), which rewrites their partials.
 template <int D, int NT>
 __global__ __launch_bounds__(kThreads, 2) void gram_mfma_kernel(
-    Geo g, const uint16_t* __restrict__ v, const float* __restrict__ zbuf,
-    const float* __restrict__ kbuf, const float* __restrict__ m_u, const double* __restrict__ z_u,
-    const uint32_t* __restrict__ uflags, float* __restrict__ partials, int gchunks, double inv_d) {
+    Geo g, const uint16_t* __restrict__ v, const float* __restrict__ wbuf,
+    const uint32_t* __restrict__ uflags, float* __restrict__ partials, int gchunks) {
   constexpr int NB = D / 16;
   constexpr int NPAIR = NB * (NB + 1) / 2;
   constexpr int TILE = kGramStep * kGramPitch;
@@ -245,15 +263,11 @@ __global__ __launch_bounds__(kThreads, 2) void gram_mfma_kernel(
   GramArgs ga;
   ga.vb = v + un.l * g.vsl + un.h * g.vsh + un.t0 * g.vst;
   ga.vst = g.vst;
-  ga.zbuf = zbuf;
-  ga.kbuf = kbuf;
-  ga.trow = token_row(g, un);
-  ga.m = m_u[u];
-  ga.Z = z_u[u];
-  ga.inv_d = inv_d;
+  ga.wrow = wbuf + token_row(g, un);
   ga.base = base;
   ga.end = min(un.n, base + kGChunkMfma);
-  ga.nsteps = (ga.end - base + kGramStep - 1) / kGramStep;
+  constexpr int SPAN = kGramStep * kGramFlush;
+  ga.nsteps = (ga.end - base + SPAN - 1) / SPAN * kGramFlush;
   ga.out = partials + ((int64_t)u * gchunks + chunk) * (NPAIR * 256);
   switch (threadIdx.x >> 6) {
     case 0: gram_wave<D, 0, NT>(ga, tiles, wts); break;
@@ -267,9 +281,8 @@ __global__ __launch_bounds__(kThreads, 2) void gram_mfma_kernel(
 // (D/16) x (D/16) register tile of M; V is staged 32 tokens at a time.
 template <int D>
 __global__ __launch_bounds__(kThreads) void gram_precise_kernel(
-    Geo g, const float* __restrict__ v, const float* __restrict__ zbuf,
-    const float* __restrict__ kbuf, const float* __restrict__ m_u, const double* __restrict__ z_u,
-    double* __restrict__ partials, int gchunks, double inv_d) {
+    Geo g, const float* __restrict__ v, const float* __restrict__ wbuf,
+    double* __restrict__ partials, int gchunks) {
   constexpr int R = D / 16;
   constexpr int NB = D / 16;
   constexpr int NPAIR = NB * (NB + 1) / 2;
@@ -280,8 +293,6 @@ __global__ __launch_bounds__(kThreads) void gram_precise_kernel(
   const int tid = threadIdx.x, ty = tid / 16, tx = tid % 16;
   __shared__ float vs[32][D];
   __shared__ double ws[32];
-  const float m = m_u[u];
-  const double Z = z_u[u];
   const float* vb = v + un.l * g.vsl + un.h * g.vsh;
   const int64_t trow = token_row(g, un);
   const int end = min(un.n, base + kGChunkPrecise);
@@ -298,7 +309,7 @@ __global__ __launch_bounds__(kThreads) void gram_precise_kernel(
     }
     if (tid < 32) {
       const int t = t0 + tid;
-      ws[tid] = (t < end) ? importance_weight(zbuf[trow + t], kbuf[trow + t], m, Z, inv_d) : 0.0;
+      ws[tid] = (t < end) ? (double)wbuf[trow + t] : 0.0;
     }
     __syncthreads();
     for (int tok = 0; tok < 32; ++tok) {
@@ -331,29 +342,25 @@ __global__ __launch_bounds__(kThreads) void gram_precise_kernel(
 hipError_t launch_gram(const Launch& L, const void* v, bool refine) {
   const Geo& g = L.geo;
   const dim3 grid(L.ws.gchunks, g.U);
-  const double inv_d = 1.0 / (double)g.D;
-  const float* zb = ws_ptr<float>(L.wsp, L.ws.z);
-  const float* kb = ws_ptr<float>(L.wsp, L.ws.kappa);
-  const float* mu = ws_ptr<float>(L.wsp, L.ws.smax_m);
-  const double* zu = ws_ptr<double>(L.wsp, L.ws.smax_z);
+  const float* wb = ws_ptr<float>(L.wsp, L.ws.wgt);
   const uint32_t* uf = ws_ptr<uint32_t>(L.wsp, L.ws.uflags);
   if (L.ws.mfma) {
     float* part = ws_ptr<float>(L.wsp, L.ws.gram);
     const uint16_t* vv = (const uint16_t*)v;
     if (g.D == 128) {
-      if (refine) gram_mfma_kernel<128, 3><<<grid, kThreads, 0, L.stream>>>(g, vv, zb, kb, mu, zu, uf, part, L.ws.gchunks, inv_d);
-      else gram_mfma_kernel<128, 2><<<grid, kThreads, 0, L.stream>>>(g, vv, zb, kb, mu, zu, uf, part, L.ws.gchunks, inv_d);
+      if (refine) gram_mfma_kernel<128, 3><<<grid, kThreads, 0, L.stream>>>(g, vv, wb, uf, part, L.ws.gchunks);
+      else gram_mfma_kernel<128, 2><<<grid, kThreads, 0, L.stream>>>(g, vv, wb, uf, part, L.ws.gchunks);
     } else {
-      if (refine) gram_mfma_kernel<64, 3><<<grid, kThreads, 0, L.stream>>>(g, vv, zb, kb, mu, zu, uf, part, L.ws.gchunks, inv_d);
-      else gram_mfma_kernel<64, 2><<<grid, kThreads, 0, L.stream>>>(g, vv, zb, kb, mu, zu, uf, part, L.ws.gchunks, inv_d);
+      if (refine) gram_mfma_kernel<64, 3><<<grid, kThreads, 0, L.stream>>>(g, vv, wb, uf, part, L.ws.gchunks);
+      else gram_mfma_kernel<64, 2><<<grid, kThreads, 0, L.stream>>>(g, vv, wb, uf, part, L.ws.gchunks);
     }
   } else {
     if (refine) return hipSuccess;
     double* part = ws_ptr<double>(L.wsp, L.ws.gram);
     if (g.D == 128)
-      gram_precise_kernel<128><<<grid, kThreads, 0, L.stream>>>(g, (const float*)v, zb, kb, mu, zu, part, L.ws.gchunks, inv_d);
+      gram_precise_kernel<128><<<grid, kThreads, 0, L.stream>>>(g, (const float*)v, wb, part, L.ws.gchunks);
     else
-      gram_precise_kernel<64><<<grid, kThreads, 0, L.stream>>>(g, (const float*)v, zb, kb, mu, zu, part, L.ws.gchunks, inv_d);
+      gram_precise_kernel<64><<<grid, kThreads, 0, L.stream>>>(g, (const float*)v, wb, part, L.ws.gchunks);
   }
   return hipGetLastError();
 }

@@ -17,10 +17,9 @@ typedef float floatx4 __attribute__((ext_vector_type(4)));
 
 template <int D>
 __global__ __launch_bounds__(kThreads, 2) void leverage_mfma_kernel(
-    Geo g, const uint16_t* __restrict__ v, const float* __restrict__ zbuf,
-    const float* __restrict__ kbuf, const float* __restrict__ m_u, const double* __restrict__ z_u,
+    Geo g, const uint16_t* __restrict__ v, const float* __restrict__ wbuf,
     const uint16_t* __restrict__ lfrag, const uint32_t* __restrict__ uflags,
-    float* __restrict__ scores, double inv_d) {
+    float* __restrict__ scores) {
   constexpr int NB = D / 16;                    // output blocks of 16 channels (a)
   constexpr int NK = D / 32;                    // K blocks of 32 channels (b)
   constexpr int NLP = (NB / 2) * (NB / 2 + 1);  // lower (j, kb) block pairs
@@ -47,8 +46,6 @@ __global__ __launch_bounds__(kThreads, 2) void leverage_mfma_kernel(
     bl[q] = *reinterpret_cast<const bf16x8*>(lf + ((int64_t)(q * 2 + 1) * 64 + lane) * 8);
   }
 
-  const float m = m_u[u];
-  const double Z = z_u[u];
   const uint16_t* vb = v + un.l * g.vsl + un.h * g.vsh + un.t0 * g.vst;
 
   // A step is 16 tokens (one MFMA row tile); the next step's V rows are
@@ -70,8 +67,8 @@ __global__ __launch_bounds__(kThreads, 2) void leverage_mfma_kernel(
   for (; t0 < end; t0 += WSTRIDE) {
     if (t0 + WSTRIDE < end) load(t0 + WSTRIDE, nxt);
     const int tw = t0 + 4 * kg + (ch & 3);
-    float zt = 0.f, kt = 0.f;
-    if (ch < 4 && tw < end) { zt = zbuf[trow + tw]; kt = kbuf[trow + tw]; }
+    float wt = 0.f;
+    if (ch < 4 && tw < end) wt = wbuf[trow + tw];
     // Output blocks j = 2 jp and 2 jp + 1 share the K-block range kb <= jp:
     // their two accumulation chains are interleaved.
     float ss[4] = {0.f, 0.f, 0.f, 0.f};
@@ -100,8 +97,7 @@ __global__ __launch_bounds__(kThreads, 2) void leverage_mfma_kernel(
 #pragma unroll
       for (int r = 1; r < 4; ++r)
         if (ch == r) sv = ss[r];
-      const double w = importance_weight(zt, kt, m, Z, inv_d);
-      scores[trow + tw] = (float)(w * (double)sv);
+      scores[trow + tw] = wt * sv;
     }
 #pragma unroll
     for (int kb = 0; kb < NK; ++kb) cur[kb] = nxt[kb];
@@ -110,10 +106,9 @@ __global__ __launch_bounds__(kThreads, 2) void leverage_mfma_kernel(
 
 template <int D>
 __global__ __launch_bounds__(kThreads) void leverage_precise_kernel(
-    Geo g, const float* __restrict__ v, const float* __restrict__ zbuf,
-    const float* __restrict__ kbuf, const float* __restrict__ m_u, const double* __restrict__ z_u,
+    Geo g, const float* __restrict__ v, const float* __restrict__ wbuf,
     const double* __restrict__ linv64, const uint32_t* __restrict__ uflags,
-    float* __restrict__ scores, double inv_d) {
+    float* __restrict__ scores) {
   constexpr int LD = D + 1;
   constexpr int TPT = 8;                 // threads per token
   constexpr int TOK = kThreads / TPT;    // tokens per tile
@@ -132,8 +127,6 @@ __global__ __launch_bounds__(kThreads) void leverage_precise_kernel(
   __shared__ float vs[TOK][D];
   const double* Li = linv64 + (int64_t)u * D * D;
   for (int e = tid; e < D * D; e += kThreads) X[(e / D) * LD + (e % D)] = Li[e];
-  const float m = m_u[u];
-  const double Z = z_u[u];
   const float* vb = v + un.l * g.vsl + un.h * g.vsh;
   const int my_tok = tid / TPT, sub = tid % TPT;
   for (int t0 = base; t0 < end; t0 += TOK) {
@@ -153,8 +146,7 @@ __global__ __launch_bounds__(kThreads) void leverage_precise_kernel(
     for (int o = 1; o < TPT; o <<= 1) ss += __shfl_xor(ss, o);
     const int t = t0 + my_tok;
     if (sub == 0 && t < end) {
-      const double w = importance_weight(zbuf[trow + t], kbuf[trow + t], m, Z, inv_d);
-      scores[trow + t] = (float)(w * ss);
+      scores[trow + t] = (float)((double)wbuf[trow + t] * ss);
     }
   }
 }
@@ -162,24 +154,20 @@ __global__ __launch_bounds__(kThreads) void leverage_precise_kernel(
 hipError_t launch_leverage(const Launch& L, const void* v, float* scores) {
   const Geo& g = L.geo;
   const dim3 grid(L.ws.lchunks, g.U);
-  const double inv_d = 1.0 / (double)g.D;
-  const float* zb = ws_ptr<float>(L.wsp, L.ws.z);
-  const float* kb = ws_ptr<float>(L.wsp, L.ws.kappa);
-  const float* mu = ws_ptr<float>(L.wsp, L.ws.smax_m);
-  const double* zu = ws_ptr<double>(L.wsp, L.ws.smax_z);
+  const float* wb = ws_ptr<float>(L.wsp, L.ws.wgt);
   const uint32_t* uf = ws_ptr<uint32_t>(L.wsp, L.ws.uflags);
   if (L.ws.mfma) {
     const uint16_t* lf = ws_ptr<uint16_t>(L.wsp, L.ws.lfrag);
     if (g.D == 128)
-      leverage_mfma_kernel<128><<<grid, kThreads, 0, L.stream>>>(g, (const uint16_t*)v, zb, kb, mu, zu, lf, uf, scores, inv_d);
+      leverage_mfma_kernel<128><<<grid, kThreads, 0, L.stream>>>(g, (const uint16_t*)v, wb, lf, uf, scores);
     else
-      leverage_mfma_kernel<64><<<grid, kThreads, 0, L.stream>>>(g, (const uint16_t*)v, zb, kb, mu, zu, lf, uf, scores, inv_d);
+      leverage_mfma_kernel<64><<<grid, kThreads, 0, L.stream>>>(g, (const uint16_t*)v, wb, lf, uf, scores);
   } else {
     const double* l64 = ws_ptr<double>(L.wsp, L.ws.linv64);
     if (g.D == 128)
-      leverage_precise_kernel<128><<<grid, kThreads, 0, L.stream>>>(g, (const float*)v, zb, kb, mu, zu, l64, uf, scores, inv_d);
+      leverage_precise_kernel<128><<<grid, kThreads, 0, L.stream>>>(g, (const float*)v, wb, l64, uf, scores);
     else
-      leverage_precise_kernel<64><<<grid, kThreads, 0, L.stream>>>(g, (const float*)v, zb, kb, mu, zu, l64, uf, scores, inv_d);
+      leverage_precise_kernel<64><<<grid, kThreads, 0, L.stream>>>(g, (const float*)v, wb, l64, uf, scores);
   }
   return hipGetLastError();
 }

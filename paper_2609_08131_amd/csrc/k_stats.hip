@@ -252,21 +252,26 @@ hipError_t launch_kpass(const Launch& L, const void* k) {
 }
 
 // ---------------------------------------------------------------------------
-// Global softmax normaliser per unit: m = max_c m_c, Z = sum_c Z_c exp(m_c - m)
-// (fp64, fixed order).
+// Global softmax normaliser per unit, m = max_c m_c and
+// Z = sum_c Z_c exp(m_c - m) (fp64, fixed order), then the Eq. 8 importance
+// weight of every token of the block's chunk (fp64, stored as fp32).
+// grid = (wchunks, U). Every block of a unit merges the chunk statistics in the
+// same order, so all of them use bit-identical (m, Z); block 0 stores them.
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(kThreads) void softmax_merge_kernel(Geo g,
-                                                                 const float2* __restrict__ cstat,
-                                                                 int kchunks, float* m_out,
-                                                                 double* z_out) {
-  const int u = blockIdx.x, tid = threadIdx.x;
+__global__ __launch_bounds__(kThreads) void softmax_weights_kernel(
+    Geo g, const float2* __restrict__ cstat, int kchunks, const float* __restrict__ zbuf,
+    const float* __restrict__ kbuf, double inv_d, float* __restrict__ m_out,
+    double* __restrict__ z_out, float* __restrict__ wout) {
+  const int u = blockIdx.y, chunk = blockIdx.x, tid = threadIdx.x;
   const Unit un = decode_unit(g, u);
   __shared__ float redf[kThreads / 64];
   __shared__ double redd[kThreads / 64];
   if (un.n == 0) {
-    if (tid == 0) { m_out[u] = 0.0f; z_out[u] = 1.0; }
+    if (chunk == 0 && tid == 0) { m_out[u] = 0.0f; z_out[u] = 1.0; }
     return;
   }
+  const int base = chunk * kWChunk;
+  if (base >= un.n) return;
   const int nch = (un.n + kKChunk - 1) / kKChunk;
   const float2* cs = cstat + (int64_t)u * kchunks;
   float m = -INFINITY;
@@ -275,13 +280,19 @@ __global__ __launch_bounds__(kThreads) void softmax_merge_kernel(Geo g,
   double s = 0.0;
   for (int c = tid; c < nch; c += kThreads) s += (double)cs[c].y * exp((double)cs[c].x - (double)m);
   s = block_combine(wave_sum(s), redd, [](double a, double b) { return a + b; });
-  if (tid == 0) { m_out[u] = m; z_out[u] = s; }
+  if (chunk == 0 && tid == 0) { m_out[u] = m; z_out[u] = s; }
+  const int64_t trow = token_row(g, un);
+  const int end = min(un.n, base + kWChunk);
+  for (int t = base + tid; t < end; t += kThreads)
+    wout[trow + t] = (float)importance_weight(zbuf[trow + t], kbuf[trow + t], m, s, inv_d);
 }
 
-hipError_t launch_softmax_merge(const Launch& L) {
-  softmax_merge_kernel<<<L.geo.U, kThreads, 0, L.stream>>>(
-      L.geo, ws_ptr<float2>(L.wsp, L.ws.cstat), L.ws.kchunks, ws_ptr<float>(L.wsp, L.ws.smax_m),
-      ws_ptr<double>(L.wsp, L.ws.smax_z));
+hipError_t launch_softmax_weights(const Launch& L) {
+  const dim3 grid(L.ws.wchunks > 0 ? L.ws.wchunks : 1, L.geo.U);
+  softmax_weights_kernel<<<grid, kThreads, 0, L.stream>>>(
+      L.geo, ws_ptr<float2>(L.wsp, L.ws.cstat), L.ws.kchunks, ws_ptr<float>(L.wsp, L.ws.z),
+      ws_ptr<float>(L.wsp, L.ws.kappa), 1.0 / (double)L.geo.D, ws_ptr<float>(L.wsp, L.ws.smax_m),
+      ws_ptr<double>(L.wsp, L.ws.smax_z), ws_ptr<float>(L.wsp, L.ws.wgt));
   return hipGetLastError();
 }
 
