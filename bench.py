@@ -5,16 +5,23 @@ head): window statistics, centre attention, Eq. 8 weights, weighted Gram,
 Cholesky, leverage scores, top-B selection and K/V compaction. Inputs are
 resident in HBM before timing starts.
 
-Prints one JSON line ("Measurement"):
+Prints one JSON line:
   value        cached tokens scored+selected per second (full-model tokens:
                one token = its K/V rows in every layer and KV head)
-  roofline     algorithmic HBM bytes (K and V read once) / step time
+  roofline     the dominant phase's algorithmic HBM bytes per launch / its
+               average GPU duration, timed with HIP events that the library
+               records around that phase on the launch stream inside the
+               timed region; "traffic" is its measured HBM bytes per launch
+               (rocprofv3 FETCH_SIZE + WRITE_SIZE, scaled by a plain copy of
+               known size) when the recorded counters match the current
+               kernel source, else null
   cpu_baseline the fp64 oracle timed on this host on a bounded sample
 """
 
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import os
 import sys
@@ -42,7 +49,65 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="time budget of the oracle CPU baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="first run a plain 1 GiB elementwise copy (torch.neg; the "
+                         "reference kernel for scaling rocprofv3 FETCH_SIZE / WRITE_SIZE)")
     return ap.parse_args()
+
+
+COPY_BYTES = 1 << 30
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic.json")
+# Source files whose kernels each phase launches (a change voids recorded counters).
+PHASE_SOURCES = {
+    "qstats": "k_stats.hip", "kpass": "k_stats.hip", "weights": "k_stats.hip",
+    "gram": "k_gram.hip", "gram_reduce": "k_gram.hip", "factor": "k_factor.hip",
+    "leverage": "k_leverage.hip", "select": "k_select.hip", "compact": "k_select.hip",
+}
+
+
+def source_sha(phase):
+    f = PHASE_SOURCES.get(phase)
+    if f is None:
+        return None
+    path = os.path.join(ROOT, "paper_2609_08131_amd", "csrc", f)
+    with open(path, "rb") as fh:
+        return hashlib.sha256(fh.read()).hexdigest()[:16]
+
+
+def recorded_traffic(phase, workload):
+    """HBM bytes per launch of `phase` from the committed counter summary, if
+    it was taken on this workload with the current kernel source; else None."""
+    try:
+        with open(TRAFFIC_FILE) as fh:
+            rec = json.load(fh).get(phase)
+    except (OSError, ValueError):
+        return None
+    if not rec or rec.get("workload") != workload or rec.get("source_sha") != source_sha(phase):
+        return None
+    return rec.get("hbm_bytes_per_launch")
+
+
+def phase_bytes(phase, case, budget, prob):
+    """Algorithmic HBM bytes of one launch of `phase` over the whole batch:
+    every input read once and every output written once."""
+    w = case.workload
+    e = case.k.element_size()
+    d = w.head_dim
+    entries = case.total_tokens * w.num_layers * w.num_kv_heads
+    units = case.num_seqs * w.num_layers * w.num_kv_heads
+    nb = d // 16
+    npair = nb * (nb + 1) // 2
+    kept = sum(min(budget, n) for n in case.seq_lens) * w.num_layers * w.num_kv_heads
+    return {
+        "qstats": case.q_win.numel() * e,
+        "kpass": entries * (d * e + 8),                    # K rows; z, kappa out
+        "weights": entries * 12,                            # z, kappa in; w out
+        "gram": entries * (d * e + 4),                      # V rows, w
+        "leverage": entries * (d * e + 8),                  # V rows, w; score out
+        "select": entries * 4 + units * budget * 4,         # scores in; idx out
+        "compact": 2 * kept * d * e * 2,                    # K, V rows in and out
+        "gram_reduce": None, "factor": units * npair * 256 * 8, "refine": None, "init": None,
+    }.get(phase)
 
 
 def ensure_built():
@@ -107,14 +172,30 @@ def main():
     stream = torch.cuda.current_stream()
     torch.cuda.synchronize()
 
+    if args.copy_calibration:
+        src = torch.empty(COPY_BYTES // 4, dtype=torch.float32, device="cuda").fill_(1.0)
+        dst = torch.empty_like(src)
+        torch.neg(src, out=dst)   # one elementwise kernel: reads and writes 1 GiB
+        torch.cuda.synchronize()
+        del src, dst
+
     for _ in range(args.warmup):
         jacap.run_evict(prob, case.q_win, case.k, case.v, stream)
     flags = jacap.read_status(prob.ws, stream)
     torch.cuda.synchronize()
 
+    # Which phase dominates: two untimed steps with every phase recorded.
+    jacap.timing_start()
+    for _ in range(2):
+        jacap.run_evict(prob, case.q_win, case.k, case.v, stream)
+    per_phase = {k: ms / n for k, (ms, n) in jacap.timing_stop().items()}
+    dominant = max(per_phase, key=per_phase.get)
+
+    # Timed region: K steps; the library records the dominant phase only.
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
           for _ in range(args.steps)]
     torch.cuda.synchronize()
+    jacap.timing_start([dominant])
     t_wall = time.perf_counter()
     for s, e in ev:
         s.record(stream)
@@ -122,15 +203,19 @@ def main():
         e.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t_wall
+    dom_ms, dom_calls = jacap.timing_stop()[dominant]
+    dom_avg = dom_ms / dom_calls
     times = np.array([s.elapsed_time(e) for s, e in ev])   # ms
     ms = float(times.mean())
 
     esize = case.k.element_size()
     d = w.head_dim
     entries = case.total_tokens * w.num_layers * w.num_kv_heads
-    alg_bytes = 2 * entries * d * esize                    # K and V read once
+    step_bytes = 2 * entries * d * esize                   # K and V read once
     tokens_per_s = case.total_tokens / (ms * 1e-3)
-    achieved = alg_bytes / (ms * 1e-3) / 1e9
+    dom_bytes = phase_bytes(dominant, case, budget, prob)
+    achieved = dom_bytes / (dom_avg * 1e-3) / 1e9 if dom_bytes else None
+    traffic = recorded_traffic(dominant, w.name)
 
     out = {
         "metric": METRIC,
@@ -157,10 +242,13 @@ def main():
         },
         "roofline": {
             "bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
-            "frac": achieved / PEAK_HBM_GBS, "traffic": None,
-            "scope": "whole jacap_evict step (all kernels); algorithmic bytes = K+V read once",
-            "alg_bytes_per_step": alg_bytes,
+            "frac": achieved / PEAK_HBM_GBS if achieved else None, "traffic": traffic,
+            "kernel": dominant, "kernel_ms": dom_avg, "kernel_launches": dom_calls,
+            "alg_bytes_per_launch": dom_bytes,
+            "traffic_over_alg": traffic / dom_bytes if traffic and dom_bytes else None,
         },
+        "phases_ms": {k: round(v, 4) for k, v in per_phase.items()},
+        "step_hbm_gbs": step_bytes / (ms * 1e-3) / 1e9,
     }
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(case, budget, args.tau, args.ridge, args.cpu_seconds)

@@ -170,6 +170,47 @@ jacap_status jacap_read_status(const void* ws, void* stream, uint32_t* flags);
 /* Static, human-readable name of a status code. */
 const char* jacap_status_string(jacap_status s);
 
+/* ------------------------------------------------------------------------
+ * Per-phase GPU timing, for measurement tools (off by default; nothing here
+ * is needed to use the entry points above).
+ *
+ * While timing is on, every jacap_score / jacap_select / jacap_compact /
+ * jacap_evict call records a HIP event before and after each phase whose bit
+ * (1u << phase) is set in the mask, on the stream the phase's kernels are
+ * launched on; the elapsed time between the two events is that phase's GPU
+ * duration. Events are created on the device that is current when the call
+ * is made. Timing state is process-wide and guarded by a lock; calls that
+ * overlap on several host threads are all recorded.
+ * ------------------------------------------------------------------------ */
+enum jacap_phase {
+  JACAP_PHASE_INIT = 0,        /* status/flag reset */
+  JACAP_PHASE_QSTATS = 1,      /* window statistics mu, Lambda (Eq. 6-7) */
+  JACAP_PHASE_KPASS = 2,       /* centre logits and query response per token */
+  JACAP_PHASE_WEIGHTS = 3,     /* softmax normaliser and Eq. 8 weights */
+  JACAP_PHASE_GRAM = 4,        /* weighted Gram partials (Eq. 9) */
+  JACAP_PHASE_GRAM_REDUCE = 5, /* fixed-order sum of the Gram partials */
+  JACAP_PHASE_FACTOR = 6,      /* Cholesky factor and L^{-1} */
+  JACAP_PHASE_REFINE = 7,      /* exact-split Gram, reduce and factor of ill-conditioned units */
+  JACAP_PHASE_LEVERAGE = 8,    /* leverage scores (Eq. 10) */
+  JACAP_PHASE_SELECT = 9,      /* TOP-B selection */
+  JACAP_PHASE_COMPACT = 10,    /* K/V compaction */
+  JACAP_NUM_PHASES = 11
+};
+
+/* Clears the accumulated times and starts recording the phases in
+ * phase_mask (0 stops recording). Returns JACAP_ERR_INVALID_ARG for bits at
+ * or above JACAP_NUM_PHASES. */
+jacap_status jacap_timing_start(uint32_t phase_mask);
+
+/* Stops recording, waits for every recorded event, and writes per phase the
+ * summed GPU milliseconds (ms[JACAP_NUM_PHASES]) and the number of recorded
+ * calls (calls[JACAP_NUM_PHASES]); either pointer may be NULL. The records
+ * are cleared. Returns JACAP_ERR_HIP if an event query failed. */
+jacap_status jacap_timing_stop(double* ms, int32_t* calls);
+
+/* Static name of a phase ("gram", "leverage", ...), or "unknown". */
+const char* jacap_phase_name(int32_t phase);
+
 #ifdef __cplusplus
 }
 #endif

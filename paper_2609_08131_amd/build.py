@@ -30,7 +30,7 @@ CFLAGS = [
     f"-I{INCLUDE}", f"-I{CSRC}",
 ]
 
-SOURCES = ["jacap_host.hip", "k_stats.hip", "k_gram.hip", "k_factor.hip",
+SOURCES = ["jacap_host.hip", "jacap_timing.hip", "k_stats.hip", "k_gram.hip", "k_factor.hip",
            "k_leverage.hip", "k_select.hip"]
 
 

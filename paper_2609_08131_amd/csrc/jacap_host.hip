@@ -126,20 +126,28 @@ jacap_status prepare(const jacap_config* c, const jacap_batch* b, void* ws, size
     if ((expr) != hipSuccess) return JACAP_ERR_HIP; \
   } while (0)
 
+// Runs `expr` inside a timed scope of phase `ph`.
+#define JACAP_PHASE(ph, expr)               \
+  do {                                      \
+    TimedPhase tp_(L.stream, (ph));         \
+    JACAP_TRY(expr);                        \
+  } while (0)
+
 jacap_status run_score(const Launch& L, const void* q, const void* k, const void* v, float* scores) {
-  JACAP_TRY(launch_init(L));
-  JACAP_TRY(launch_qstats(L, q));
-  JACAP_TRY(launch_kpass(L, k));
-  JACAP_TRY(launch_softmax_weights(L));
-  JACAP_TRY(launch_gram(L, v, false));
-  JACAP_TRY(launch_gram_reduce(L, false));
-  JACAP_TRY(launch_factor(L, false));
+  JACAP_PHASE(JACAP_PHASE_INIT, launch_init(L));
+  JACAP_PHASE(JACAP_PHASE_QSTATS, launch_qstats(L, q));
+  JACAP_PHASE(JACAP_PHASE_KPASS, launch_kpass(L, k));
+  JACAP_PHASE(JACAP_PHASE_WEIGHTS, launch_softmax_weights(L));
+  JACAP_PHASE(JACAP_PHASE_GRAM, launch_gram(L, v, false));
+  JACAP_PHASE(JACAP_PHASE_GRAM_REDUCE, launch_gram_reduce(L, false));
+  JACAP_PHASE(JACAP_PHASE_FACTOR, launch_factor(L, false));
   if (L.ws.mfma) {  // recompute the Gram of ill-conditioned units with the exact split
+    TimedPhase tp(L.stream, JACAP_PHASE_REFINE);
     JACAP_TRY(launch_gram(L, v, true));
     JACAP_TRY(launch_gram_reduce(L, true));
     JACAP_TRY(launch_factor(L, true));
   }
-  JACAP_TRY(launch_leverage(L, v, scores));
+  JACAP_PHASE(JACAP_PHASE_LEVERAGE, launch_leverage(L, v, scores));
   return JACAP_OK;
 }
 
@@ -169,7 +177,10 @@ jacap_status jacap_score(const jacap_config* cfg, const jacap_batch* batch, cons
   jacap_status s = prepare(cfg, batch, ws, ws_bytes, stream, &L);
   if (s != JACAP_OK) return s;
   if (!score_ptrs_ok(q_win, k, v, scores)) return JACAP_ERR_INVALID_ARG;
-  if (batch->total_tokens == 0) return launch_init(L) == hipSuccess ? JACAP_OK : JACAP_ERR_HIP;
+  if (batch->total_tokens == 0) {
+    TimedPhase tp(L.stream, JACAP_PHASE_INIT);
+    return launch_init(L) == hipSuccess ? JACAP_OK : JACAP_ERR_HIP;
+  }
   return run_score(L, q_win, k, v, scores);
 }
 
@@ -181,6 +192,7 @@ jacap_status jacap_select(const jacap_config* cfg, const jacap_batch* batch, con
   if (cfg->budget_k == 0) return JACAP_OK;
   if (!idx || (!scores && batch->total_tokens > 0)) return JACAP_ERR_INVALID_ARG;
   if (!aligned16(idx) || (scores && !aligned16(scores))) return JACAP_ERR_INVALID_ARG;
+  TimedPhase tp(L.stream, JACAP_PHASE_SELECT);
   return launch_select(L, scores, idx) == hipSuccess ? JACAP_OK : JACAP_ERR_HIP;
 }
 
@@ -192,6 +204,7 @@ jacap_status jacap_compact(const jacap_config* cfg, const jacap_batch* batch, co
   if (cfg->budget_k == 0) return JACAP_OK;
   if (!idx || !k || !v || !k_out || !v_out) return JACAP_ERR_INVALID_ARG;
   if (!aligned16(k) || !aligned16(v) || !aligned16(k_out) || !aligned16(v_out)) return JACAP_ERR_INVALID_ARG;
+  TimedPhase tp(L.stream, JACAP_PHASE_COMPACT);
   return launch_compact(L, idx, k, v, k_out, v_out) == hipSuccess ? JACAP_OK : JACAP_ERR_HIP;
 }
 
@@ -210,12 +223,12 @@ jacap_status jacap_evict(const jacap_config* cfg, const jacap_batch* batch, cons
   if (batch->total_tokens > 0) {
     s = run_score(L, q_win, k, v, scores);
     if (s != JACAP_OK) return s;
-  } else if (launch_init(L) != hipSuccess) {
-    return JACAP_ERR_HIP;
+  } else {
+    JACAP_PHASE(JACAP_PHASE_INIT, launch_init(L));
   }
   if (cfg->budget_k == 0) return JACAP_OK;
-  JACAP_TRY(launch_select(L, scores, idx));
-  JACAP_TRY(launch_compact(L, idx, k, v, k_out, v_out));
+  JACAP_PHASE(JACAP_PHASE_SELECT, launch_select(L, scores, idx));
+  JACAP_PHASE(JACAP_PHASE_COMPACT, launch_compact(L, idx, k, v, k_out, v_out));
   return JACAP_OK;
 }
 

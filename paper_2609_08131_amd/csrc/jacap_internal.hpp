@@ -169,6 +169,23 @@ __device__ __forceinline__ void raise_flags(uint32_t* status, uint32_t* uflags, 
 }
 
 // ---------------------------------------------------------------------------
+// Optional per-phase event timing (jacap_timing_start / _stop): records a HIP
+// event pair around the scope on `stream` when the phase is enabled.
+// ---------------------------------------------------------------------------
+class TimedPhase {
+ public:
+  TimedPhase(hipStream_t stream, int phase);
+  ~TimedPhase();
+  TimedPhase(const TimedPhase&) = delete;
+  TimedPhase& operator=(const TimedPhase&) = delete;
+
+ private:
+  hipStream_t stream_;
+  int phase_;
+  hipEvent_t begin_ = nullptr, end_ = nullptr;
+};
+
+// ---------------------------------------------------------------------------
 // Launchers (defined in the kernel translation units)
 // ---------------------------------------------------------------------------
 struct Launch {

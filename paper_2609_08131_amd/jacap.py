@@ -91,12 +91,20 @@ def _load() -> ctypes.CDLL:
         fn.restype = ctypes.c_int
     lib.jacap_status_string.argtypes = [ctypes.c_int]
     lib.jacap_status_string.restype = ctypes.c_char_p
+    lib.jacap_timing_start.argtypes = [ctypes.c_uint32]
+    lib.jacap_timing_start.restype = ctypes.c_int
+    lib.jacap_timing_stop.argtypes = [ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int32)]
+    lib.jacap_timing_stop.restype = ctypes.c_int
+    lib.jacap_phase_name.argtypes = [ctypes.c_int32]
+    lib.jacap_phase_name.restype = ctypes.c_char_p
     return lib
 
 
 _lib = _load()
 EXPORTED = ("jacap_workspace_size", "jacap_score", "jacap_select", "jacap_compact",
-            "jacap_evict", "jacap_read_status", "jacap_status_string")
+            "jacap_evict", "jacap_read_status", "jacap_status_string", "jacap_timing_start",
+            "jacap_timing_stop", "jacap_phase_name")
+NUM_PHASES = 11   # enum jacap_phase
 
 
 def status_string(code: int) -> str:
@@ -258,3 +266,30 @@ def prepare(q_win, k, v, seq_offsets, seq_lens, params: Params) -> Problem:
 def run_evict(prob: Problem, q_win, k, v, stream=None) -> None:
     evict(prob.cfg, prob.batch, q_win, k, v, prob.scores, prob.idx, prob.k_out, prob.v_out,
           prob.ws, stream)
+
+
+# ---------------------------------------------------------------------------
+# Per-phase GPU timing (jacap_timing_start / jacap_timing_stop)
+# ---------------------------------------------------------------------------
+def phase_name(phase: int) -> str:
+    return _lib.jacap_phase_name(int(phase)).decode()
+
+
+PHASES = tuple(phase_name(p) for p in range(NUM_PHASES))
+
+
+def timing_start(phases=None) -> None:
+    """Start recording the named phases (all when None); clears old records."""
+    names = PHASES if phases is None else phases
+    mask = 0
+    for n in names:
+        mask |= 1 << PHASES.index(n)
+    _check("jacap_timing_start", _lib.jacap_timing_start(mask))
+
+
+def timing_stop() -> dict:
+    """Stop recording; {phase: (summed GPU ms, recorded calls)} for recorded phases."""
+    ms = (ctypes.c_double * NUM_PHASES)()
+    calls = (ctypes.c_int32 * NUM_PHASES)()
+    _check("jacap_timing_stop", _lib.jacap_timing_stop(ms, calls))
+    return {PHASES[p]: (ms[p], calls[p]) for p in range(NUM_PHASES) if calls[p] > 0}

@@ -136,3 +136,16 @@ def test_status_strings():
     for code, name in ((0, "JACAP_OK"), (1, "JACAP_ERR_INVALID_ARG"), (2, "JACAP_ERR_UNSUPPORTED"),
                        (3, "JACAP_ERR_WORKSPACE"), (4, "JACAP_ERR_HIP"), (99, "JACAP_ERR_UNKNOWN")):
         assert jacap.status_string(code) == name
+
+
+def test_timing_api_host_side():
+    """Phase names follow enum jacap_phase; bad masks are rejected; an empty
+    recording returns no phases."""
+    assert jacap.PHASES[0] == "init" and jacap.PHASES[4] == "gram"
+    assert jacap.PHASES[8] == "leverage" and len(jacap.PHASES) == jacap.NUM_PHASES
+    assert jacap.phase_name(jacap.NUM_PHASES) == "unknown"
+    lib = ctypes.CDLL(jacap.LIB_PATH)
+    lib.jacap_timing_start.argtypes = [ctypes.c_uint32]
+    assert lib.jacap_timing_start(1 << jacap.NUM_PHASES) == 1   # JACAP_ERR_INVALID_ARG
+    jacap.timing_start(["gram", "leverage"])
+    assert jacap.timing_stop() == {}
