@@ -77,7 +77,8 @@ __device__ __forceinline__ s16x4 lds_read_tr16(const uint16_t* p) {
 // read with two transposing LDS reads: lane (i, kg) addresses token
 // 8 kg + i / 4 (+ 4), channels 4 (i % 4) .. + 3 of the block, and receives
 // channel i of tokens 8 kg .. 8 kg + 3 (8 kg + 4 .. 8 kg + 7). With a 288-byte
-// row pitch, the 16 lanes of a group touch 32 distinct banks.
+// row pitch the 16 lanes of a group touch 32 distinct banks; the chunk
+// swizzle of odd 8-token groups separates the groups served together.
 //
 // Accumulation: fp32 MFMA chains of kGramFlush steps, each added into a
 // second fp32 accumulator (short rounding chains; an ill-conditioned ridge-0
@@ -113,8 +114,14 @@ __device__ __forceinline__ void gram_wave(const GramArgs& ga, uint16_t* tiles, f
   static_assert((WPW & (WPW - 1)) == 0, "weights per wave must be a power of two");
   const int tid = threadIdx.x, lane = tid & 63;
   const int kg = lane >> 4, il = lane & 15;
-  // This lane's address inside a staged step for the transposing reads.
+  // This lane's address inside a staged step for the transposing reads. Rows
+  // of odd 8-token groups hold their 32-byte channel chunks XOR-swizzled by 4
+  // (chunk c at position c ^ 4), so the two 16-lane groups that the LDS
+  // serves together read disjoint banks. Chunk i < 4 sits at i + sw, chunk
+  // i >= 4 at i - sw.
+  const int sw = 4 * (kg & 1);
   const int tr_off = (8 * kg + (il >> 2)) * kGramPitch + 4 * (il & 3);
+  const int tr_lo = tr_off + 16 * sw, tr_hi = tr_off - 16 * sw;
 
   floatx4 acc32[NP], acc2[NP];
 #pragma unroll
@@ -142,7 +149,8 @@ __device__ __forceinline__ void gram_wave(const GramArgs& ga, uint16_t* tiles, f
 #pragma unroll
     for (int r = 0; r < LOADS; ++r) {
       const int flat = r * kThreads + tid, tok = flat / OCT, oc = flat % OCT;
-      *reinterpret_cast<uint4*>(tile + tok * kGramPitch + oc * 8) = buf.v[r];
+      const int pc = oc ^ (8 * ((tok >> 3) & 1));  // 16-byte piece, chunk swizzle
+      *reinterpret_cast<uint4*>(tile + tok * kGramPitch + pc * 8) = buf.v[r];
     }
     if (lane < WPW) wt[W * WPW + lane] = buf.w;
   };
@@ -200,11 +208,11 @@ __device__ __forceinline__ void gram_wave(const GramArgs& ga, uint16_t* tiles, f
 #pragma unroll
       for (int q = 0; q < 4; ++q) { wl[q] = w0[q]; wl[q + 4] = w1[q]; }
       u16x8 a[NA];
-      const uint16_t* tb = tile + tr_off;
 #pragma unroll
       for (int i = 0; i < NA; ++i) {
-        const s16x4 lo = lds_read_tr16(tb + 16 * i);
-        const s16x4 hi = lds_read_tr16(tb + 16 * i + 4 * kGramPitch);
+        const uint16_t* tb = tile + (i < 4 ? tr_lo : tr_hi) + 16 * i;
+        const s16x4 lo = lds_read_tr16(tb);
+        const s16x4 hi = lds_read_tr16(tb + 4 * kGramPitch);
 #pragma unroll
         for (int q = 0; q < 4; ++q) { a[i][q] = (uint16_t)lo[q]; a[i][q + 4] = (uint16_t)hi[q]; }
       }
