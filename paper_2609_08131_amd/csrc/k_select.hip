@@ -2,16 +2,30 @@
 // Z_C = {(k_i, v_i)}_{i in C} (Sec. 3.1).
 //
 // Selection is exact integer work on order-preserving 32-bit keys of the fp32
-// scores (NaN -> 0, the lowest key; -0 -> +0). A three-pass LDS radix select
-// (11 + 11 + 10 bits, MSB first) finds the budget-th largest key T and how many
-// tokens equal to T must be kept; a final ordered pass emits every token with
-// key > T and the lowest-position tokens with key == T, in ascending position
-// order, using block prefix sums over contiguous per-thread segments.
+// scores (NaN -> 0, the lowest key; -0 -> +0): the budget-th largest key T,
+// then every token with key > T and the lowest-position tokens with key == T,
+// written in ascending position order. One workgroup per unit.
+//
+// Fast path (sample select): keys of a fixed sample of the unit (up to 128
+// blocks of 64 contiguous tokens, evenly spaced) bracket T between two sample
+// order statistics lo <= T <= hi. One ordered pass over the scores then
+// collects, in position order, the tokens with key > hi (kept for sure) and
+// the band lo <= key <= hi (candidates) into LDS; T and the emission are
+// finished in LDS. The pass checks that the bracket holds (fewer than budget
+// tokens above hi, at least budget at or above lo) and that both lists fit;
+// otherwise the unit takes the general path: a three-pass radix select over
+// the scores (11 + 11 + 10 bits, MSB first) and an ordered emission pass.
+// Both paths give the same, deterministic result.
 #include "jacap_internal.hpp"
 
 namespace jacap {
 
 constexpr int kSelThreads = 1024;
+constexpr int kSelPer = 8;                          // tokens per thread per staged chunk
+constexpr int kSelChunk = kSelPer * kSelThreads;    // 8192
+constexpr int kCandCap = 8192;                      // candidate band capacity
+constexpr int kSureCap = 8192;                      // kept-for-sure list capacity
+constexpr int kSampleBlocks = 128;                  // sample: <= 128 blocks of 64 tokens
 
 __device__ __forceinline__ uint32_t score_key(float f) {
   if (f != f) return 0u;          // NaN ranks lowest
@@ -19,6 +33,16 @@ __device__ __forceinline__ uint32_t score_key(float f) {
   const uint32_t b = __float_as_uint(f);
   return (b & 0x80000000u) ? ~b : (b | 0x80000000u);
 }
+
+struct SelShared {
+  uint32_t stage[kSelChunk];  // staged chunk keys / sample keys / kept candidate positions
+  uint32_t ckey[kCandCap];    // candidate keys (position order)
+  int32_t cpos[kCandCap];     // candidate positions
+  int32_t gpos[kSureCap];     // kept-for-sure positions (position order)
+  uint32_t hist[2048];
+  uint32_t scan[kSelThreads / 64 + 1];
+  uint32_t bc[2];
+};
 
 // Exclusive prefix sum over kSelThreads values (one per thread), fixed order.
 __device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t x, uint32_t* sh, uint32_t& total) {
@@ -46,8 +70,99 @@ __device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t x, uint32_t* s
   return sh[wave] + incl - x;
 }
 
+// Radix select (11 + 11 + 10 bits, MSB first): the key of rank `rank`
+// (1 = largest, rank <= cnt) among key_at(0 .. cnt-1); `need` = how many keys
+// equal to it fall within the top `rank`.
+template <class KeyAt>
+__device__ uint32_t radix_rank(KeyAt key_at, int cnt, uint32_t rank, SelShared& sh,
+                               uint32_t& need) {
+  const int tid = threadIdx.x;
+  uint32_t prefix = 0u, pmask = 0u, remaining = rank;
+  const int shifts[3] = {21, 10, 0};
+  const int widths[3] = {11, 11, 10};
+  for (int pass = 0; pass < 3; ++pass) {
+    const int shf = shifts[pass];
+    const uint32_t nb = 1u << widths[pass];
+    const uint32_t dmask = nb - 1u;
+    for (uint32_t i = tid; i < nb; i += kSelThreads) sh.hist[i] = 0u;
+    if (tid == 0) { sh.bc[0] = 0u; sh.bc[1] = 0u; }
+    __syncthreads();
+    for (int i = tid; i < cnt; i += kSelThreads) {
+      const uint32_t key = key_at(i);
+      if ((key & pmask) == prefix) atomicAdd(&sh.hist[(key >> shf) & dmask], 1u);
+    }
+    __syncthreads();
+    // Suffix counts from the top digit down: each thread owns a contiguous run
+    // of bins (descending digit order), then a block scan.
+    const uint32_t per = nb / kSelThreads;  // 2 or 1
+    uint32_t local = 0;
+    for (uint32_t q = 0; q < per; ++q) local += sh.hist[nb - 1 - (tid * per + q)];
+    uint32_t tot;
+    uint32_t above = block_exclusive_scan(local, sh.scan, tot);
+    for (uint32_t q = 0; q < per; ++q) {
+      const uint32_t d = nb - 1 - (tid * per + q);
+      const uint32_t c = sh.hist[d];
+      if (above < remaining && remaining <= above + c) {
+        sh.bc[0] = d;
+        sh.bc[1] = above;
+      }
+      above += c;
+    }
+    __syncthreads();
+    prefix |= sh.bc[0] << shf;
+    pmask |= dmask << shf;
+    remaining -= sh.bc[1];
+    __syncthreads();
+  }
+  need = remaining;
+  return prefix;
+}
+
+// General path: radix select over the scores, then an ordered emission pass
+// over contiguous per-thread segments.
+__device__ void select_general(const float* s, int n, int kk, int32_t* out, SelShared& sh) {
+  const int tid = threadIdx.x;
+  uint32_t need;
+  const uint32_t T = radix_rank([&](int i) { return score_key(s[i]); }, n, (uint32_t)kk, sh, need);
+  const int seg = (n + kSelThreads - 1) / kSelThreads;
+  const int lo = min(n, tid * seg), hi = min(n, lo + seg);
+  uint32_t cgt = 0, ceq = 0;
+  for (int i = lo; i < hi; ++i) {
+    const uint32_t key = score_key(s[i]);
+    cgt += key > T;
+    ceq += key == T;
+  }
+  uint32_t tot;
+  uint32_t gt_before = block_exclusive_scan(cgt, sh.scan, tot);
+  uint32_t eq_before = block_exclusive_scan(ceq, sh.scan, tot);
+  for (int i = lo; i < hi; ++i) {
+    const uint32_t key = score_key(s[i]);
+    if (key > T) {
+      const uint32_t pos = gt_before + min(eq_before, need);
+      if (pos < (uint32_t)kk) out[pos] = i;
+      ++gt_before;
+    } else if (key == T) {
+      const uint32_t pos = gt_before + eq_before;
+      if (eq_before < need && pos < (uint32_t)kk) out[pos] = i;
+      ++eq_before;
+    }
+  }
+}
+
+// Number of entries of the ascending list a[0 .. cnt) that are < p.
+__device__ __forceinline__ int lower_bound_lds(const int32_t* a, int cnt, int32_t p) {
+  int lo = 0, hi = cnt;
+  while (lo < hi) {
+    const int mid = (lo + hi) >> 1;
+    if (a[mid] < p) lo = mid + 1;
+    else hi = mid;
+  }
+  return lo;
+}
+
 __global__ __launch_bounds__(kSelThreads) void select_kernel(Geo g, const float* __restrict__ scores,
                                                              int32_t* __restrict__ idx, int budget) {
+  __shared__ SelShared sh;
   const int u = blockIdx.x, tid = threadIdx.x;
   const Unit un = decode_unit(g, u);
   int32_t* out = idx + (int64_t)u * budget;
@@ -62,74 +177,109 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(Geo g, const float*
     return;
   }
 
-  __shared__ uint32_t hist[2048];
-  __shared__ uint32_t scan_sh[kSelThreads / 64 + 1];
-  __shared__ uint32_t sel_digit, sel_above;
-
-  uint32_t prefix = 0u, pmask = 0u;
-  uint32_t remaining = (uint32_t)kk;  // rank (1-based) of T among keys matching the prefix
-  const int shifts[3] = {21, 10, 0};
-  const int widths[3] = {11, 11, 10};
-  for (int pass = 0; pass < 3; ++pass) {
-    const int sh = shifts[pass];
-    const uint32_t nb = 1u << widths[pass];
-    const uint32_t dmask = nb - 1u;
-    for (uint32_t i = tid; i < nb; i += kSelThreads) hist[i] = 0u;
-    if (tid == 0) { sel_digit = 0u; sel_above = 0u; }
+  // Bracket [lo, hi] of T from the sample (the whole unit if it fits the band).
+  uint32_t lo = 0u, hi = 0xFFFFFFFFu;
+  if (n > kCandCap) {
+    const int nb64 = (n + 63) / 64;
+    const int q = (nb64 + kSampleBlocks - 1) / kSampleBlocks;  // every q-th 64-token block
+    const int nsb = (nb64 + q - 1) / q;
+    const int last_start = (nsb - 1) * q * 64;
+    const int S = (nsb - 1) * 64 + min(64, n - last_start);   // valid samples form a prefix
+    for (int j = tid; j < S; j += kSelThreads)
+      sh.stage[j] = score_key(s[(j >> 6) * q * 64 + (j & 63)]);
     __syncthreads();
-    for (int i = tid; i < n; i += kSelThreads) {
-      const uint32_t key = score_key(s[i]);
-      if ((key & pmask) == prefix) atomicAdd(&hist[(key >> sh) & dmask], 1u);
+    const double ks = (double)kk * (double)S / (double)n;
+    const int delta = (int)(4.0 * sqrt(ks)) + 16;
+    const int kr = max(1, (int)(ks + 0.5));
+    const uint32_t r_lo = (uint32_t)min(S, kr + delta);
+    uint32_t dummy;
+    // When the band reaches the top of the sample there is no upper bound:
+    // tokens above the sample maximum are candidates too.
+    if (kr - delta >= 1)
+      hi = radix_rank([&](int i) { return sh.stage[i]; }, S, (uint32_t)(kr - delta), sh, dummy);
+    lo = radix_rank([&](int i) { return sh.stage[i]; }, S, r_lo, sh, dummy);
+  }
+
+  // One ordered pass: kept-for-sure (key > hi) and candidates (lo <= key <= hi).
+  uint32_t gcnt = 0, ccnt = 0;
+  for (int base = 0; base < n; base += kSelChunk) {
+#pragma unroll
+    for (int j = 0; j < kSelPer; ++j) {
+      const int p = base + j * kSelThreads + tid;
+      sh.stage[j * kSelThreads + tid] = p < n ? score_key(s[p]) : 0u;
     }
     __syncthreads();
-    // Suffix counts from the top digit down: each thread owns a contiguous run
-    // of bins (descending digit order), then a block scan.
-    const uint32_t per = nb / kSelThreads;  // 2 or 1
-    uint32_t local = 0;
-    for (uint32_t q = 0; q < per; ++q) local += hist[nb - 1 - (tid * per + q)];
+    uint32_t k8[kSelPer];
+    uint32_t ng = 0, nc = 0;
+#pragma unroll
+    for (int qd = 0; qd < kSelPer; ++qd) {
+      const int p = base + kSelPer * tid + qd;
+      k8[qd] = sh.stage[kSelPer * tid + qd];
+      const bool valid = p < n;
+      ng += valid && k8[qd] > hi;
+      nc += valid && k8[qd] >= lo && k8[qd] <= hi;
+    }
     uint32_t tot;
-    uint32_t above = block_exclusive_scan(local, scan_sh, tot);
-    for (uint32_t q = 0; q < per; ++q) {
-      const uint32_t d = nb - 1 - (tid * per + q);
-      const uint32_t c = hist[d];
-      if (above < remaining && remaining <= above + c) {
-        sel_digit = d;
-        sel_above = above;
+    const uint32_t off = block_exclusive_scan((ng << 16) | nc, sh.scan, tot);
+    uint32_t go = gcnt + (off >> 16), co = ccnt + (off & 0xFFFFu);
+#pragma unroll
+    for (int qd = 0; qd < kSelPer; ++qd) {
+      const int p = base + kSelPer * tid + qd;
+      if (p >= n) continue;
+      if (k8[qd] > hi) {
+        if (go < (uint32_t)kSureCap) sh.gpos[go] = p;
+        ++go;
+      } else if (k8[qd] >= lo) {
+        if (co < (uint32_t)kCandCap) { sh.ckey[co] = k8[qd]; sh.cpos[co] = p; }
+        ++co;
       }
-      above += c;
     }
-    __syncthreads();
-    prefix |= sel_digit << sh;
-    pmask |= dmask << sh;
-    remaining -= sel_above;
+    gcnt += tot >> 16;
+    ccnt += tot & 0xFFFFu;
     __syncthreads();
   }
-  const uint32_t T = prefix;
-  const uint32_t need = remaining;  // tokens with key == T to keep, lowest positions first
+  const bool ok = gcnt < (uint32_t)kk && gcnt + ccnt >= (uint32_t)kk &&
+                  gcnt <= (uint32_t)kSureCap && ccnt <= (uint32_t)kCandCap;
+  if (!ok) {  // uniform: every thread holds the same counts
+    select_general(s, n, kk, out, sh);
+    return;
+  }
 
-  // Ordered emission over contiguous segments.
-  const int seg = (n + kSelThreads - 1) / kSelThreads;
-  const int lo = min(n, tid * seg), hi = min(n, lo + seg);
-  uint32_t cgt = 0, ceq = 0;
-  for (int i = lo; i < hi; ++i) {
-    const uint32_t key = score_key(s[i]);
-    cgt += key > T;
-    ceq += key == T;
-  }
+  // T among the candidates: rank kk - gcnt.
+  const uint32_t r = (uint32_t)kk - gcnt;
+  uint32_t need;
+  const uint32_t T = radix_rank([&](int i) { return sh.ckey[i]; }, (int)ccnt, r, sh, need);
+  // Kept candidates, in position order, into stage[0 .. r).
+  const int per = ((int)ccnt + kSelThreads - 1) / kSelThreads;
+  const int c0 = min((int)ccnt, tid * per), c1 = min((int)ccnt, c0 + per);
+  uint32_t ceq = 0;
+  for (int i = c0; i < c1; ++i) ceq += sh.ckey[i] == T;
   uint32_t tot;
-  uint32_t gt_before = block_exclusive_scan(cgt, scan_sh, tot);
-  uint32_t eq_before = block_exclusive_scan(ceq, scan_sh, tot);
-  for (int i = lo; i < hi; ++i) {
-    const uint32_t key = score_key(s[i]);
-    if (key > T) {
-      const uint32_t pos = gt_before + min(eq_before, need);
-      if (pos < (uint32_t)kk) out[pos] = i;
-      ++gt_before;
-    } else if (key == T) {
-      const uint32_t pos = gt_before + eq_before;
-      if (eq_before < need && pos < (uint32_t)kk) out[pos] = i;
-      ++eq_before;
-    }
+  uint32_t eq_before = block_exclusive_scan(ceq, sh.scan, tot);
+  uint32_t csel = 0;
+  for (int i = c0, e = eq_before; i < c1; ++i) {
+    const uint32_t key = sh.ckey[i];
+    if (key > T) ++csel;
+    else if (key == T) { csel += (uint32_t)e < need; ++e; }
+  }
+  uint32_t sel_before = block_exclusive_scan(csel, sh.scan, tot);
+  for (int i = c0, e = eq_before; i < c1; ++i) {
+    const uint32_t key = sh.ckey[i];
+    bool keep = false;
+    if (key > T) keep = true;
+    else if (key == T) { keep = (uint32_t)e < need; ++e; }
+    if (keep) sh.stage[sel_before++] = (uint32_t)sh.cpos[i];
+  }
+  __syncthreads();
+  // Merge the two position-ordered lists into out[0 .. kk).
+  const int32_t* kept_c = reinterpret_cast<const int32_t*>(sh.stage);
+  for (int a = tid; a < (int)gcnt; a += kSelThreads) {
+    const int32_t p = sh.gpos[a];
+    out[a + lower_bound_lds(kept_c, (int)r, p)] = p;
+  }
+  for (int b = tid; b < (int)r; b += kSelThreads) {
+    const int32_t p = kept_c[b];
+    out[b + lower_bound_lds(sh.gpos, (int)gcnt, p)] = p;
   }
 }
 

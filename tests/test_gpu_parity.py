@@ -233,3 +233,55 @@ def test_select_ties_nan_negzero(jacap):
                 got = prob.idx[b, 0, h].cpu().numpy()
                 assert np.array_equal(got[:len(want)], want), (budget, b, h)
                 assert np.all(got[len(want):] == -1)
+
+
+@pytest.mark.gpu
+def test_select_large_units_both_paths(jacap):
+    """Large units exercise the sampled fast path (spread-out, sorted and
+    NaN/-0/inf mixes) and the general radix path (heavy ties, budget n - 1);
+    the kept positions must equal the oracle's ranking bit for bit."""
+    lens = [8193, 20000, 131072]
+    case = make_case("ragged16", device="cuda", seq_lens=lens, num_layers=1,
+                     num_kv_heads=4, num_q_heads=4, head_dim=64, window=2)
+    rng = np.random.default_rng(7)
+    T = sum(lens)
+    kinds = {
+        0: lambda n: np.exp(rng.normal(0.0, 5.0, n)),
+        1: lambda n: np.sort(np.exp(rng.normal(0.0, 3.0, n))),
+        2: lambda n: rng.integers(0, 5, n).astype(np.float64),
+        3: lambda n: np.exp(rng.normal(0.0, 3.0, n)),
+    }
+    for budget in (1, 1024, 2048, 20000):
+        p = jacap.Params(budget_k=budget)
+        prob = jacap.prepare(case.q_win, case.k, case.v, case.seq_offsets, case.seq_lens, p)
+        s = np.zeros((1, 4, T), np.float32)
+        for b, n in enumerate(lens):
+            lo, hi = token_slice(case, b)
+            for h in range(4):
+                x = kinds[h](n).astype(np.float32)
+                if h == 3:
+                    x[rng.random(n) < 0.1] = np.nan
+                    x[rng.random(n) < 0.05] = -0.0
+                    x[rng.random(n) < 0.05] = 0.0
+                    x[rng.random(n) < 0.01] = np.inf
+                s[0, h, lo:hi] = x
+        print(f"[select] budget {budget}", flush=True)
+        jacap.select(prob.cfg, prob.batch, torch.from_numpy(s).cuda(), prob.idx)
+        torch.cuda.synchronize()
+        for b in range(len(lens)):
+            lo, hi = token_slice(case, b)
+            for h in range(4):
+                want = jo.select_top(s[0, h, lo:hi], budget)
+                got = prob.idx[b, 0, h].cpu().numpy()
+                assert np.array_equal(got[:len(want)], want), (budget, b, h)
+                assert np.all(got[len(want):] == -1)
+    # budget = n - 1 on the large unit (the kept-for-sure list cannot hold it)
+    n = lens[2]
+    p = jacap.Params(budget_k=n - 1)
+    prob = jacap.prepare(case.q_win, case.k, case.v, case.seq_offsets, case.seq_lens, p)
+    s = np.exp(rng.normal(0.0, 5.0, (1, 4, T))).astype(np.float32)
+    jacap.select(prob.cfg, prob.batch, torch.from_numpy(s).cuda(), prob.idx)
+    torch.cuda.synchronize()
+    lo, hi = token_slice(case, 2)
+    want = jo.select_top(s[0, 1, lo:hi], n - 1)
+    assert np.array_equal(prob.idx[2, 0, 1].cpu().numpy()[:n - 1], want)
