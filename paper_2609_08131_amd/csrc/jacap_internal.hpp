@@ -13,7 +13,7 @@ namespace jacap {
 // Tiling constants
 // ---------------------------------------------------------------------------
 constexpr int kThreads = 256;        // 4 wave64 per workgroup
-constexpr int kKChunk = 256;         // tokens per workgroup in the K pass
+constexpr int kKChunk = 1024;        // tokens per workgroup in the K pass
 constexpr int kGChunkMfma = 4096;    // tokens per workgroup in the MFMA Gram pass
 constexpr int kGChunkPrecise = 1024; // tokens per workgroup in the fp64 Gram pass
 constexpr int kLChunkMfma = 4096;    // tokens per workgroup in the MFMA leverage pass
@@ -166,6 +166,16 @@ __device__ __forceinline__ void raise_flags(uint32_t* status, uint32_t* uflags, 
                                             uint32_t f) {
   atomicOr(status, f);
   atomicOr(uflags + u, f);
+}
+
+// Waits for every outstanding vector-memory load of this wave. Placed after a
+// kernel's prologue loads (values used throughout a pipelined loop), so that
+// the compiler's wait analysis does not carry them into the loop, where it
+// would otherwise wait for all loads -- the prefetched ones included -- in
+// every trip.
+__device__ __forceinline__ void drain_vmem() {
+  // s_waitcnt encoding (gfx9): vmcnt = 0, expcnt = 7, lgkmcnt = 15 (no wait).
+  __builtin_amdgcn_s_waitcnt(0x0F70);
 }
 
 // ---------------------------------------------------------------------------

@@ -225,7 +225,8 @@ __device__ __forceinline__ void gram_wave(const GramArgs& ga, uint16_t* tiles, f
   auto step = [&](int st, Pre& buf, int half, auto firstc) {
     stage(buf, tiles + half * TILE, wts + half * kGramStep);
     __syncthreads();
-    if (st + 2 < ga.nsteps) buf = gload(st + 2);
+    buf = gload(min(st + 2, ga.nsteps - 1));  // unconditional: static wait counts
+    __builtin_amdgcn_sched_barrier(0);        // keep the loads ahead of this step's MFMAs
     compute(tiles + half * TILE, wts + half * kGramStep, firstc);
   };
 

@@ -45,38 +45,40 @@ __global__ __launch_bounds__(kThreads, 2) void leverage_mfma_kernel(
     bh[q] = *reinterpret_cast<const bf16x8*>(lf + ((int64_t)(q * 2 + 0) * 64 + lane) * 8);
     bl[q] = *reinterpret_cast<const bf16x8*>(lf + ((int64_t)(q * 2 + 1) * 64 + lane) * 8);
   }
+  drain_vmem();
 
   const uint16_t* vb = v + un.l * g.vsl + un.h * g.vsh + un.t0 * g.vst;
 
-  // A step is 16 tokens (one MFMA row tile); the next step's V rows are
-  // loaded while this one computes. MFMAs are issued kb-outer so that
-  // consecutive MFMAs update different output blocks.
-  auto load = [&](int t0, bf16x8 (&a)[NK]) {
-    const int tok = t0 + ch;  // A-operand row of this lane
+  // A step is 16 tokens (one MFMA row tile). V rows are prefetched two
+  // steps ahead into three rotating register buffers (the loop is unrolled
+  // by three so the buffers stay in fixed registers). Every load in the loop
+  // is issued unconditionally (past-the-end rows are clamped and unused): a
+  // load skipped on some path would make the compiler wait for the newest
+  // loads, i.e. drain the prefetch, in every step. MFMAs are issued kb-outer
+  // so that consecutive MFMAs update different output blocks.
+  // One prefetched step: the lane's V row pieces and the weight of the token
+  // whose score this lane writes.
+  struct Buf { bf16x8 a[NK]; float w; };
+  auto load = [&](int t0, Buf& b) {
+    const int tok = min(t0 + ch, end - 1);  // A-operand row of this lane (clamped; result unused)
 #pragma unroll
-    for (int kb = 0; kb < NK; ++kb) {
-      uint4 raw = make_uint4(0u, 0u, 0u, 0u);
-      if (tok < end) raw = *reinterpret_cast<const uint4*>(vb + (int64_t)tok * g.vst + 32 * kb + 8 * kg);
-      a[kb] = __builtin_bit_cast(bf16x8, raw);
-    }
+    for (int kb = 0; kb < NK; ++kb)
+      b.a[kb] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(vb + (int64_t)tok * g.vst + 32 * kb + 8 * kg));
+    b.w = wbuf[trow + min(t0 + 4 * kg + (ch & 3), end - 1)];
+    __builtin_amdgcn_sched_barrier(0);  // issue here, ahead of the MFMAs that follow
   };
-  constexpr int WSTRIDE = 16 * (kThreads / 64);
-  int t0 = base + wave * 16;
-  bf16x8 cur[NK], nxt[NK];
-  if (t0 < end) load(t0, cur);
-  for (; t0 < end; t0 += WSTRIDE) {
-    if (t0 + WSTRIDE < end) load(t0 + WSTRIDE, nxt);
+  auto step = [&](int t0, const Buf& b) {
     const int tw = t0 + 4 * kg + (ch & 3);
-    float wt = 0.f;
-    if (ch < 4 && tw < end) wt = wbuf[trow + tw];
+    const float wt = b.w;
+    const bf16x8 (&cur)[NK] = b.a;
     // Output blocks j = 2 jp and 2 jp + 1 share the K-block range kb <= jp:
     // their two accumulation chains are interleaved.
     float ss[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int jp = 0; jp < NB / 2; ++jp) {
       floatx4 y0 = {0.f, 0.f, 0.f, 0.f}, y1 = {0.f, 0.f, 0.f, 0.f};
-      const int q0 = jp * (jp + 1) * 1 + jp * 0;        // pair index of (2 jp, 0)
-      const int q1 = jp * (jp + 1) + (jp + 1);          // pair index of (2 jp + 1, 0)
+      const int q0 = jp * (jp + 1);             // pair index of (2 jp, 0)
+      const int q1 = jp * (jp + 1) + (jp + 1);  // pair index of (2 jp + 1, 0)
 #pragma unroll
       for (int kb = 0; kb <= jp; ++kb) {
         y0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(cur[kb], bh[q0 + kb], y0, 0, 0, 0);
@@ -99,8 +101,22 @@ __global__ __launch_bounds__(kThreads, 2) void leverage_mfma_kernel(
         if (ch == r) sv = ss[r];
       scores[trow + tw] = wt * sv;
     }
-#pragma unroll
-    for (int kb = 0; kb < NK; ++kb) cur[kb] = nxt[kb];
+  };
+  constexpr int WSTRIDE = 16 * (kThreads / 64);
+  const int t_first = base + wave * 16;
+  if (t_first >= end) return;
+  Buf b0, b1, b2;
+  load(t_first, b0);
+  load(t_first + WSTRIDE, b1);
+  for (int t0 = t_first; t0 < end; t0 += 3 * WSTRIDE) {
+    load(t0 + 2 * WSTRIDE, b2);
+    step(t0, b0);
+    if (t0 + WSTRIDE >= end) break;
+    load(t0 + 3 * WSTRIDE, b0);
+    step(t0 + WSTRIDE, b1);
+    if (t0 + 2 * WSTRIDE >= end) break;
+    load(t0 + 4 * WSTRIDE, b1);
+    step(t0 + 2 * WSTRIDE, b2);
   }
 }
 

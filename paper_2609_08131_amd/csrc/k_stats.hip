@@ -162,59 +162,76 @@ __global__ __launch_bounds__(kThreads) void kpass_kernel(
   const T* kb = k + un.l * g.ksl + un.h * g.ksh;
   const int64_t trow = token_row(g, un);
 
-  for (int it = 0; it < kKChunk; it += TPB) {
-    const int tl = it + wave * TPW + tiw;
-    const int i = base + tl;
-    const bool valid = i < un.n;
-    Acc x[VEC];
-    if (valid) {
-      const uint4 raw = *reinterpret_cast<const uint4*>(kb + (un.t0 + i) * g.kst + sub * VEC);
-      const T* xv = reinterpret_cast<const T*>(&raw);
+  // UNR iterations per loop trip, their loads issued first (FULL mode keeps
+  // one: it stages each token row in LDS between barriers).
+  constexpr int UNR = FULL ? 1 : 4;
+  static_assert(kKChunk % (UNR * TPB) == 0, "chunk must be whole unrolled trips");
+  for (int it0 = 0; it0 < kKChunk; it0 += UNR * TPB) {
+    uint4 raw[UNR];
 #pragma unroll
-      for (int e = 0; e < VEC; ++e) x[e] = (Acc)to_f32(xv[e]);
-    } else {
-#pragma unroll
-      for (int e = 0; e < VEC; ++e) x[e] = (Acc)0;
+    for (int j = 0; j < UNR; ++j) {
+      const int i = base + it0 + j * TPB + wave * TPW + tiw;
+      const int ic = min(i, un.n - 1);  // in bounds; the value is unused when i >= n
+      raw[j] = *reinterpret_cast<const uint4*>(kb + (un.t0 + ic) * g.kst + sub * VEC);
     }
-    Acc dot = 0, kap = 0;
 #pragma unroll
-    for (int e = 0; e < VEC; ++e) dot += muv[e] * x[e];
-    if constexpr (!FULL) {
+    for (int j = 0; j < UNR; ++j) {
+      const int tl = it0 + j * TPB + wave * TPW + tiw;
+      const int i = base + tl;
+      const bool valid = i < un.n;
+      Acc x[VEC];
+      const T* xv = reinterpret_cast<const T*>(&raw[j]);
 #pragma unroll
-      for (int e = 0; e < VEC; ++e) kap += lamv[e] * x[e] * x[e];
-    } else {
-      __syncthreads();
+      for (int e = 0; e < VEC; ++e) x[e] = valid ? (Acc)to_f32(xv[e]) : (Acc)0;
+      Acc dot = 0, kap = 0;
 #pragma unroll
-      for (int e = 0; e < VEC; ++e) ksh[wave * TPW + tiw][sub * VEC + e] = (float)x[e];
-      __syncthreads();
+      for (int e = 0; e < VEC; ++e) dot += muv[e] * x[e];
+      if constexpr (!FULL) {
 #pragma unroll
-      for (int e = 0; e < VEC; ++e) {
-        const float* row = lamsh + (sub * VEC + e) * (D + 1);
-        Acc t = 0;
-        for (int bb = 0; bb < D; ++bb) t += (Acc)row[bb] * (Acc)ksh[wave * TPW + tiw][bb];
-        kap += x[e] * t;
+        for (int e = 0; e < VEC; ++e) kap += lamv[e] * x[e] * x[e];
+      } else {
+        __syncthreads();
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) ksh[wave * TPW + tiw][sub * VEC + e] = (float)x[e];
+        __syncthreads();
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) {
+          const float* row = lamsh + (sub * VEC + e) * (D + 1);
+          Acc t = 0;
+          for (int bb = 0; bb < D; ++bb) t += (Acc)row[bb] * (Acc)ksh[wave * TPW + tiw][bb];
+          kap += x[e] * t;
+        }
       }
-    }
 #pragma unroll
-    for (int o = LPT / 2; o > 0; o >>= 1) {
-      dot += __shfl_xor(dot, o);
-      kap += __shfl_xor(kap, o);
-    }
-    if (sub == 0) {
-      const float z = valid ? (float)((double)dot * inv_scale) : -INFINITY;
-      zsh[tl] = z;
-      if (valid) {
-        zout[trow + i] = z;
-        kout[trow + i] = (float)kap;
-        if (!isfinite(z) || !isfinite((float)kap)) raise_flags(status, uflags, u, kUnitNonfinite);
+      for (int o = LPT / 2; o > 0; o >>= 1) {
+        dot += __shfl_xor(dot, o);
+        kap += __shfl_xor(kap, o);
+      }
+      if (sub == 0) {
+        const float z = valid ? (float)((double)dot * inv_scale) : -INFINITY;
+        zsh[tl] = z;
+        if (valid) {
+          zout[trow + i] = z;
+          kout[trow + i] = (float)kap;
+          if (!isfinite(z) || !isfinite((float)kap)) raise_flags(status, uflags, u, kUnitNonfinite);
+        }
       }
     }
   }
   __syncthreads();
-  static_assert(kKChunk == kThreads, "one logit per thread in the chunk reduction");
-  const float zv = zsh[tid];
-  const float m = block_combine(wave_max(zv), red, [](float a, float b) { return fmaxf(a, b); });
-  const float ex = (zv == -INFINITY) ? 0.0f : expf(zv - m);
+  static_assert(kKChunk % kThreads == 0, "whole logits per thread in the chunk reduction");
+  constexpr int ZPT = kKChunk / kThreads;
+  float zv[ZPT];
+  float mloc = -INFINITY;
+#pragma unroll
+  for (int q = 0; q < ZPT; ++q) {
+    zv[q] = zsh[q * kThreads + tid];
+    mloc = fmaxf(mloc, zv[q]);
+  }
+  const float m = block_combine(wave_max(mloc), red, [](float a, float b) { return fmaxf(a, b); });
+  float ex = 0.0f;
+#pragma unroll
+  for (int q = 0; q < ZPT; ++q) ex += (zv[q] == -INFINITY) ? 0.0f : expf(zv[q] - m);
   const float s = block_combine(wave_sum(ex), red, [](float a, float b) { return a + b; });
   if (tid == 0) cstat[(int64_t)u * kchunks + chunk] = make_float2(m, s);
 }
