@@ -118,6 +118,43 @@ hipError_t launch_qstats(const Launch& L, const void* q) {
   return hipGetLastError();
 }
 
+// Sum over aligned groups of G lanes (G = 8, 16 or 32); every lane of a group
+// ends with the same value. Within a 16-lane row the partners come from DPP
+// (quad swaps, then the half-row and row mirrors: one VALU instruction per
+// level); groups of 32 add one cross-row exchange.
+__device__ __forceinline__ float dpp_f32(float v, int ctrl_sel) {
+  const int x = __builtin_bit_cast(int, v);
+  int r;
+  switch (ctrl_sel) {  // dpp_ctrl must be a constant
+    case 0: r = __builtin_amdgcn_update_dpp(0, x, 0xB1, 0xF, 0xF, true); break;   // quad_perm [1,0,3,2]
+    case 1: r = __builtin_amdgcn_update_dpp(0, x, 0x4E, 0xF, 0xF, true); break;   // quad_perm [2,3,0,1]
+    case 2: r = __builtin_amdgcn_update_dpp(0, x, 0x141, 0xF, 0xF, true); break;  // row_half_mirror
+    default: r = __builtin_amdgcn_update_dpp(0, x, 0x140, 0xF, 0xF, true); break; // row_mirror
+  }
+  return __builtin_bit_cast(float, r);
+}
+__device__ __forceinline__ double dpp_f64(double v, int ctrl_sel) {
+  const uint64_t b = __builtin_bit_cast(uint64_t, v);
+  const float lo = dpp_f32(__builtin_bit_cast(float, (uint32_t)b), ctrl_sel);
+  const float hi = dpp_f32(__builtin_bit_cast(float, (uint32_t)(b >> 32)), ctrl_sel);
+  return __builtin_bit_cast(double, ((uint64_t)__builtin_bit_cast(uint32_t, hi) << 32) |
+                                        __builtin_bit_cast(uint32_t, lo));
+}
+template <int G, typename F>
+__device__ __forceinline__ F group_sum(F v) {
+  static_assert(G == 8 || G == 16 || G == 32, "group of 8, 16 or 32 lanes");
+  auto step = [&](int sel) {
+    if constexpr (sizeof(F) == 4) v += dpp_f32(v, sel);
+    else v += dpp_f64(v, sel);
+  };
+  step(0);
+  step(1);
+  step(2);
+  if constexpr (G >= 16) step(3);
+  if constexpr (G == 32) v += __shfl_xor(v, 16);
+  return v;
+}
+
 // ---------------------------------------------------------------------------
 // K pass: z_i = k_i . mu / (tau sqrt d) and kappa_i = k_i^T Lambda k_i for a
 // chunk of kKChunk tokens, then the chunk's (max z, sum exp(z - max)).
@@ -151,6 +188,7 @@ __global__ __launch_bounds__(kThreads) void kpass_kernel(
   }
 
   __shared__ float zsh[kKChunk];
+  __shared__ float ksq[kKChunk];
   __shared__ float red[kThreads / 64];
   __shared__ float lamsh[FULL ? D * (D + 1) : 1];
   __shared__ float ksh[FULL ? TPB : 1][FULL ? D : 1];
@@ -178,11 +216,11 @@ __global__ __launch_bounds__(kThreads) void kpass_kernel(
     for (int j = 0; j < UNR; ++j) {
       const int tl = it0 + j * TPB + wave * TPW + tiw;
       const int i = base + tl;
-      const bool valid = i < un.n;
+      const bool valid = i < un.n;  // rows past the end were loaded clamped: finite, discarded
       Acc x[VEC];
       const T* xv = reinterpret_cast<const T*>(&raw[j]);
 #pragma unroll
-      for (int e = 0; e < VEC; ++e) x[e] = valid ? (Acc)to_f32(xv[e]) : (Acc)0;
+      for (int e = 0; e < VEC; ++e) x[e] = (Acc)to_f32(xv[e]);
       Acc dot = 0, kap = 0;
 #pragma unroll
       for (int e = 0; e < VEC; ++e) dot += muv[e] * x[e];
@@ -202,22 +240,27 @@ __global__ __launch_bounds__(kThreads) void kpass_kernel(
           kap += x[e] * t;
         }
       }
-#pragma unroll
-      for (int o = LPT / 2; o > 0; o >>= 1) {
-        dot += __shfl_xor(dot, o);
-        kap += __shfl_xor(kap, o);
-      }
+      dot = group_sum<LPT>(dot);
+      kap = group_sum<LPT>(kap);
       if (sub == 0) {
-        const float z = valid ? (float)((double)dot * inv_scale) : -INFINITY;
-        zsh[tl] = z;
-        if (valid) {
-          zout[trow + i] = z;
-          kout[trow + i] = (float)kap;
-          if (!isfinite(z) || !isfinite((float)kap)) raise_flags(status, uflags, u, kUnitNonfinite);
-        }
+        zsh[tl] = valid ? (float)((double)dot * inv_scale) : -INFINITY;
+        ksq[tl] = (float)kap;
       }
     }
   }
+  // z and kappa of the chunk: coalesced stores, one non-finite check.
+  __syncthreads();
+  bool bad = false;
+  for (int tl = tid; tl < kKChunk; tl += kThreads) {
+    const int i = base + tl;
+    if (i < un.n) {
+      const float z = zsh[tl], kq = ksq[tl];
+      zout[trow + i] = z;
+      kout[trow + i] = kq;
+      bad |= !isfinite(z) || !isfinite(kq);
+    }
+  }
+  if (__any(bad) && (threadIdx.x & 63) == 0) raise_flags(status, uflags, u, kUnitNonfinite);
   __syncthreads();
   static_assert(kKChunk % kThreads == 0, "whole logits per thread in the chunk reduction");
   constexpr int ZPT = kKChunk / kThreads;
