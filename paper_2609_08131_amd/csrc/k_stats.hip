@@ -39,34 +39,67 @@ __global__ __launch_bounds__(kThreads) void qstats_kernel(Geo g, const T* __rest
     atomicOr(status, (uint32_t)JACAP_FLAG_BAD_OFFSETS);
   const int Ns = g.G * g.w;
   const T* qb = q + un.b * g.qss + un.l * g.qsl + (int64_t)un.h * g.G * g.qsh;
+  // Thread (cl, rp): 16-byte piece cl of rows rp, rp + RP, ...; partial sums
+  // are combined over rp in a fixed order through LDS (fp64).
+  constexpr int VEC = 16 / sizeof(T);
+  constexpr int CL = D / VEC;           // lanes per row
+  constexpr int RP = kThreads / CL;     // row parts
+  const int cl = tid % CL, rp = tid / CL;
   __shared__ double smu[D];
+  __shared__ double part[RP][D];
+  auto row_piece = [&](int r, double (&x)[VEC]) {
+    const int gq = r / g.w, p = r - gq * g.w;
+    const uint4 raw = *reinterpret_cast<const uint4*>(qb + gq * g.qsh + p * g.qsp + cl * VEC);
+    const T* xv = reinterpret_cast<const T*>(&raw);
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) x[e] = (double)to_f32(xv[e]);
+  };
+  auto combine = [&](const double (&acc)[VEC], double* out) {
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) part[rp][cl * VEC + e] = acc[e];
+    __syncthreads();
+    if (tid < D) {
+      double t = 0.0;
+      for (int k = 0; k < RP; ++k) t += part[k][tid];
+      out[tid] = t / Ns;
+    }
+    __syncthreads();
+  };
+  double acc[VEC];
+#pragma unroll
+  for (int e = 0; e < VEC; ++e) acc[e] = 0.0;
+  for (int r = rp; r < Ns; r += RP) {
+    double x[VEC];
+    row_piece(r, x);
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) acc[e] += x[e];
+  }
+  combine(acc, smu);
+  double m[VEC];
+#pragma unroll
+  for (int e = 0; e < VEC; ++e) { m[e] = smu[cl * VEC + e]; acc[e] = 0.0; }
+  for (int r = rp; r < Ns; r += RP) {
+    double x[VEC];
+    row_piece(r, x);
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) acc[e] += (x[e] - m[e]) * (x[e] - m[e]);
+  }
+  __shared__ double svar[D];
+  combine(acc, svar);
   if (tid < D) {
-    double s = 0.0;
-    for (int r = 0; r < Ns; ++r) {
-      const int gq = r / g.w, p = r - gq * g.w;
-      s += (double)to_f32(qb[gq * g.qsh + p * g.qsp + tid]);
-    }
-    const double m = s / Ns;
-    double v = 0.0;
-    for (int r = 0; r < Ns; ++r) {
-      const int gq = r / g.w, p = r - gq * g.w;
-      const double dv = (double)to_f32(qb[gq * g.qsh + p * g.qsp + tid]) - m;
-      v += dv * dv;
-    }
-    v /= Ns;
-    smu[tid] = m;
-    mu_out[(int64_t)u * D + tid] = m;
+    const double mm = smu[tid], v = svar[tid];
+    mu_out[(int64_t)u * D + tid] = mm;
     lam_out[(int64_t)u * D + tid] = v;
-    if (!isfinite(m) || !isfinite(v)) raise_flags(status, uflags, u, kUnitNonfinite);
+    if (!isfinite(mm) || !isfinite(v)) raise_flags(status, uflags, u, kUnitNonfinite);
   }
   if (!full) return;
   // Full covariance: each thread owns D*D/kThreads entries; rows are staged,
   // centred, 32 at a time in LDS.
   constexpr int PER = D * D / kThreads;
   __shared__ double qt[32][D];
-  double acc[PER];
+  double cacc[PER];
 #pragma unroll
-  for (int k = 0; k < PER; ++k) acc[k] = 0.0;
+  for (int k = 0; k < PER; ++k) cacc[k] = 0.0;
   for (int r0 = 0; r0 < Ns; r0 += 32) {
     __syncthreads();
     for (int e = tid; e < 32 * D; e += kThreads) {
@@ -84,14 +117,14 @@ __global__ __launch_bounds__(kThreads) void qstats_kernel(Geo g, const T* __rest
 #pragma unroll
       for (int k = 0; k < PER; ++k) {
         const int e = tid + k * kThreads;
-        acc[k] += qt[rr][e / D] * qt[rr][e % D];
+        cacc[k] += qt[rr][e / D] * qt[rr][e % D];
       }
     }
   }
 #pragma unroll
   for (int k = 0; k < PER; ++k) {
     const int e = tid + k * kThreads;
-    lamfull[(int64_t)u * D * D + e] = (float)(acc[k] / Ns);
+    lamfull[(int64_t)u * D * D + e] = (float)(cacc[k] / Ns);
   }
 }
 
