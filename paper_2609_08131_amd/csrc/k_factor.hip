@@ -11,44 +11,52 @@
 // Blocked algorithm on 16x16 blocks (the sequential chain is what bounds a
 // single workgroup, so the work between barriers is made as wide as possible):
 //   Cholesky, for each block column k:
-//     1. wave 0 factors the diagonal block (16 pivots, wave-synchronous);
+//     1. the diagonal block is factored in registers by 16 lanes of wave 0
+//        (lane s holds row s; each pivot's column is broadcast by DPP);
 //     2. the panel below it is solved against it by forward substitution,
 //        one row per thread;
 //     3. the trailing lower triangle takes the rank-16 update, 4x4 register
 //        tiles per thread.
 //   Inverse X = L^{-1}:
-//     4. the diagonal blocks are inverted independently (one column per lane);
-//     5. off-diagonal blocks follow block diagonal by block diagonal:
-//        X_ij = -X_ii (sum_{k=j}^{i-1} L_ik X_kj).
-// LDS holds A (pitch D + 1) with L in its lower triangle; X is written
-// transposed into the upper triangle (X[r][c] at A[c][r], r > c) and its
-// diagonal 1 / L_rr is kept in idg.
+//     4. the diagonal 16x16 blocks are inverted independently (one column per
+//        lane);
+//     5. recursive doubling: for blocks of h = 16, 32, 64 rows, each pair
+//        [L11 0; L21 L22] gets X21 = -X22 L21 X11 from the halves' inverses
+//        (two triangular products, 4x4 register tiles).
+// LDS holds A (pitch D + 1) with L in its lower triangle; X replaces L there
+// block by block as each part of L is consumed. The upper triangle holds
+// temporaries.
 #include "jacap_internal.hpp"
 
 namespace jacap {
 
-// Orders LDS accesses of the lanes of one wave (no workgroup barrier).
-__device__ __forceinline__ void wave_sync_lds() {
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-  __builtin_amdgcn_wave_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-}
-
-// x <- y / ||y||; returns ||y|| (uniform).
-template <int D>
-__device__ __forceinline__ double normalize(double* x, const double* y, double* red) {
-  const int tid = threadIdx.x;
-  const double v = tid < D ? y[tid] * y[tid] : 0.0;
-  const double nrm = sqrt(block_combine(wave_sum(v), red, [](double a, double b) { return a + b; }));
-  if (tid < D) x[tid] = nrm > 0.0 ? y[tid] / nrm : 0.0;
-  __syncthreads();
-  return nrm;
-}
-
-constexpr int kPowerIters = 8;
-// cond(A) estimate above which the bf16 path recomputes the unit's Gram with
-// the exact three-term split (its two-term error grows like ~1e-8 cond(A)).
+// cond(A) bound above which the bf16 path recomputes the unit's Gram with the
+// exact three-term split (its two-term error grows like ~1e-8 cond(A)).
 constexpr double kRefineCond = 2e3;
+
+__device__ __forceinline__ double readlane_f64(double v, int lane) {
+  const uint64_t b = __builtin_bit_cast(uint64_t, v);
+  const uint32_t lo = __builtin_amdgcn_readlane((int)(uint32_t)b, lane);
+  const uint32_t hi = __builtin_amdgcn_readlane((int)(uint32_t)(b >> 32), lane);
+  return __builtin_bit_cast(double, ((uint64_t)hi << 32) | lo);
+}
+
+// Lane N of each 16-lane row, broadcast to the row (DPP row_newbcast).
+template <int N>
+__device__ __forceinline__ double row_bcast_f64(double v) {
+  const uint64_t b = __builtin_bit_cast(uint64_t, v);
+  const uint32_t lo = __builtin_amdgcn_update_dpp(0, (int)(uint32_t)b, 0x150 + N, 0xF, 0xF, false);
+  const uint32_t hi = __builtin_amdgcn_update_dpp(0, (int)(uint32_t)(b >> 32), 0x150 + N, 0xF, 0xF, false);
+  return __builtin_bit_cast(double, ((uint64_t)hi << 32) | lo);
+}
+
+// 1 / sqrt(x) to full fp64 accuracy: hardware estimate, two Newton steps.
+__device__ __forceinline__ double rsqrt_f64(double x) {
+  double y = __builtin_amdgcn_rsq(x);
+  y = y * (1.5 - 0.5 * x * y * y);
+  y = y * (1.5 - 0.5 * x * y * y);
+  return y;
+}
 
 // Lower-triangle index e -> (row i, column j), j <= i (row-major over the triangle).
 __device__ __forceinline__ void tri_index(int e, int& i, int& j) {
@@ -81,23 +89,21 @@ __global__ __launch_bounds__(kThreads) void factor_kernel(Geo g, const double* _
   __shared__ double A[D * LD];
   __shared__ double dg[D];   // diagonal of A before factorisation
   __shared__ double idg[D];  // 1 / L_rr
-  __shared__ double px[D], py[D], pred[kThreads / 64];
+  __shared__ double red_sh[kThreads / 64];
   __shared__ int bad;        // 0, or the unit flag that stops the factorisation
 
-  // Lower triangle of A = ridge I + M from the upper blocks of M.
+  // Lower triangle of A = ridge I + M from the upper blocks of M: pass p
+  // copies block pair p (uniform), thread tid one entry of it.
   const double* R = red + (int64_t)u * (NPAIR * 256);
-  for (int e = tid; e < NPAIR * 256; e += kThreads) {
-    const int p = e / 256, rem = e % 256, ln = rem / 4, r = rem % 4;
-    int i = 0, j = 0, q = p;
-    for (int ii = 0; ii < NB; ++ii) {
-      const int cnt = NB - ii;
-      if (q < cnt) { i = ii; j = ii + q; break; }
-      q -= cnt;
+  {
+    int bi = 0, bj = 0;
+    for (int p = 0; p < NPAIR; ++p) {
+      const int ln = tid / 4, r = tid % 4;
+      const int row = bi * 16 + (ln >> 4) * 4 + r;
+      const int col = bj * 16 + (ln & 15);
+      if (row <= col) A[col * LD + row] = R[p * 256 + tid];  // diagonal block: upper half only
+      if (++bj == NB) { ++bi; bj = bi; }
     }
-    const int row = i * 16 + (ln >> 4) * 4 + r;
-    const int col = j * 16 + (ln & 15);
-    if (row > col) continue;       // diagonal block: keep the upper half
-    A[col * LD + row] = R[e];      // lower-triangle slot (col >= row)
   }
   if (tid == 0) bad = 0;
   __syncthreads();
@@ -112,56 +118,79 @@ __global__ __launch_bounds__(kThreads) void factor_kernel(Geo g, const double* _
     return;
   }
 
-  // lambda_max(A) by power iteration (a lower estimate); A is symmetric with
-  // its lower triangle stored.
-  constexpr int TPR = kThreads / D;  // threads per row in the matrix-vector products
+  // max over rows of sum_c |A[r][c]| (>= lambda_max(A), A symmetric with its
+  // lower triangle stored); TPR threads per row.
+  constexpr int TPR = kThreads / D;
   const int prow = tid / TPR, ppart = tid % TPR;
-  double lam_max = 0.0;
+  auto block_max = [&](double v) {
+    return block_combine(wave_max_f64(v), red_sh, [](double a, double b) { return fmax(a, b); });
+  };
+  double anorm = 0.0;
   if (may_refine) {
-    if (tid < D) px[tid] = 1.0 + 0.01 * tid;
-    __syncthreads();
-    normalize<D>(px, px, pred);
-    for (int it = 0; it < kPowerIters; ++it) {
-      double s = 0.0;
-      for (int b = ppart; b < D; b += TPR)
-        s += ((b <= prow) ? A[prow * LD + b] : A[b * LD + prow]) * px[b];
+    double sr = 0.0;
+    for (int b = ppart; b < D; b += TPR) sr += fabs((b <= prow) ? A[prow * LD + b] : A[b * LD + prow]);
 #pragma unroll
-      for (int o = 1; o < TPR; o <<= 1) s += __shfl_xor(s, o);
-      if (ppart == 0) py[prow] = s;
-      __syncthreads();
-      lam_max = normalize<D>(px, py, pred);
-    }
+    for (int o = 1; o < TPR; o <<= 1) sr += __shfl_xor(sr, o);
+    anorm = block_max(sr);
   }
 
   // ---------------- Cholesky A = L L^T (L overwrites the lower triangle) ----
   for (int kb = 0; kb < NB; ++kb) {
     const int c = 16 * kb;
-    // 1. Diagonal block, by wave 0.
+    // 1. Diagonal block, in registers of wave 0: lane s (mod 16) holds row s.
     if (wave == 0) {
+      const int s = lane & 15;
+      double a[16];
+#pragma unroll
+      for (int q = 0; q < 16; ++q) a[q] = (q <= s) ? A[(c + s) * LD + c + q] : 0.0;
+      // No early exit (the loop must stay fully unrolled so that a[] lives in
+      // registers): after a failed pivot the rest is computed on a stand-in
+      // pivot and discarded.
+      int code = 0;
+#pragma unroll
       for (int t = 0; t < 16; ++t) {
-        const int jj = c + t;
-        const double piv = A[jj * LD + jj];
+        const double piv = readlane_f64(a[t], t);  // A[t][t], uniform
         // A pivot that has lost all but piv_rel of its diagonal entry is within
         // the rounding noise of the accumulated Gram: A is numerically singular
         // at the path's working precision (rank-deficient M with ridge 0).
-        if (!(piv > piv_rel * dg[jj]) || !(piv > 0.0)) {
-          if (lane == 0) bad = !isfinite(piv) ? (int)kUnitNonfinite
-                               : (may_refine ? (int)kUnitRefine : (int)kUnitSingular);
-          break;  // uniform: every lane read the same pivot
+        const bool ok = piv > piv_rel * dg[c + t] && piv > 0.0;
+        if (!ok && code == 0)
+          code = !isfinite(piv) ? (int)kUnitNonfinite
+                                : (may_refine ? (int)kUnitRefine : (int)kUnitSingular);
+        const double y = rsqrt_f64(ok ? piv : 1.0);
+        if (lane == 0) idg[c + t] = y;
+        a[t] = (s == t) ? piv * y : a[t] * y;  // column t of L (rows s < t: unused)
+        // a[q] -= L[s][t] L[q][t] for q > t; L[q][t] is lane q's a[t]. Entries
+        // with q > s are outside row s's lower part and never stored.
+#pragma unroll
+        for (int q = t + 1; q < 16; ++q) {
+          double lq;
+          switch (q) {
+            case 1: lq = row_bcast_f64<1>(a[t]); break;
+            case 2: lq = row_bcast_f64<2>(a[t]); break;
+            case 3: lq = row_bcast_f64<3>(a[t]); break;
+            case 4: lq = row_bcast_f64<4>(a[t]); break;
+            case 5: lq = row_bcast_f64<5>(a[t]); break;
+            case 6: lq = row_bcast_f64<6>(a[t]); break;
+            case 7: lq = row_bcast_f64<7>(a[t]); break;
+            case 8: lq = row_bcast_f64<8>(a[t]); break;
+            case 9: lq = row_bcast_f64<9>(a[t]); break;
+            case 10: lq = row_bcast_f64<10>(a[t]); break;
+            case 11: lq = row_bcast_f64<11>(a[t]); break;
+            case 12: lq = row_bcast_f64<12>(a[t]); break;
+            case 13: lq = row_bcast_f64<13>(a[t]); break;
+            case 14: lq = row_bcast_f64<14>(a[t]); break;
+            default: lq = row_bcast_f64<15>(a[t]); break;
+          }
+          a[q] -= a[t] * lq;
         }
-        const double y = 1.0 / sqrt(piv);
-        if (lane < 15 - t) A[(jj + 1 + lane) * LD + jj] *= y;
-        if (lane == 0) { A[jj * LD + jj] = piv * y; idg[jj] = y; }
-        wave_sync_lds();
-        // rank-1 update of the block's trailing lower triangle
-        const int m = 15 - t, cnt = m * (m + 1) / 2;
-        for (int e = lane; e < cnt; e += 64) {
-          int i, j;
-          tri_index(e, i, j);
-          const int r = jj + 1 + i, s = jj + 1 + j;
-          A[r * LD + s] -= A[r * LD + jj] * A[s * LD + jj];
-        }
-        wave_sync_lds();
+      }
+      if (code) {
+        if (lane == 0) bad = code;
+      } else if (lane < 16) {
+#pragma unroll
+        for (int q = 0; q < 16; ++q)
+          if (q <= s) A[(c + s) * LD + c + q] = a[q];
       }
     }
     __syncthreads();
@@ -179,10 +208,10 @@ __global__ __launch_bounds__(kThreads) void factor_kernel(Geo g, const double* _
       for (int t = 0; t < 16; ++t) x[t] = A[r * LD + c + t];
 #pragma unroll
       for (int t = 0; t < 16; ++t) {
-        double s = x[t];
+        double sum = x[t];
 #pragma unroll
-        for (int q = 0; q < t; ++q) s -= x[q] * A[(c + t) * LD + c + q];
-        x[t] = s * idg[c + t];
+        for (int q = 0; q < t; ++q) sum -= x[q] * A[(c + t) * LD + c + q];
+        x[t] = sum * idg[c + t];
       }
 #pragma unroll
       for (int t = 0; t < 16; ++t) A[r * LD + c + t] = x[t];
@@ -201,15 +230,15 @@ __global__ __launch_bounds__(kThreads) void factor_kernel(Geo g, const double* _
         double acc[4][4] = {};
 #pragma unroll
         for (int t = 0; t < 16; ++t) {
-          double a[4], b[4];
+          double av[4], bv[4];
 #pragma unroll
-          for (int i = 0; i < 4; ++i) a[i] = A[(r0 + i) * LD + c + t];
+          for (int i = 0; i < 4; ++i) av[i] = A[(r0 + i) * LD + c + t];
 #pragma unroll
-          for (int j = 0; j < 4; ++j) b[j] = A[(s0 + j) * LD + c + t];
+          for (int j = 0; j < 4; ++j) bv[j] = A[(s0 + j) * LD + c + t];
 #pragma unroll
           for (int i = 0; i < 4; ++i)
 #pragma unroll
-            for (int j = 0; j < 4; ++j) acc[i][j] += a[i] * b[j];
+            for (int j = 0; j < 4; ++j) acc[i][j] += av[i] * bv[j];
         }
 #pragma unroll
         for (int i = 0; i < 4; ++i)
@@ -220,103 +249,102 @@ __global__ __launch_bounds__(kThreads) void factor_kernel(Geo g, const double* _
     __syncthreads();
   }
 
-  // ---------------- Inverse X = L^{-1} (transposed into the upper triangle) --
+  // ---------------- Inverse X = L^{-1} --------------------------------------
   // 4. Diagonal blocks: lane (k, t) computes column t of X_kk by forward
-  //    substitution and stores X_kk[i][t] (i > t) at A[c + t][c + i].
+  //    substitution and stores X_kk[i][t] (i > t) at A[c + t][c + i] (the
+  //    block's upper half; L_kk is still being read), then the block is
+  //    copied down over L_kk with 1 / L_rr on the diagonal.
   if (tid < 16 * NB) {
     const int k = tid >> 4, t = tid & 15, c = 16 * k;
     double x[16];
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
-      double s = 0.0;
+      double sum = 0.0;
 #pragma unroll
-      for (int q = 0; q < i; ++q) s += A[(c + i) * LD + c + q] * x[q];
-      x[i] = i < t ? 0.0 : (i == t ? idg[c + i] : -idg[c + i] * s);
+      for (int q = 0; q < i; ++q) sum += A[(c + i) * LD + c + q] * x[q];
+      x[i] = i < t ? 0.0 : (i == t ? idg[c + i] : -idg[c + i] * sum);
     }
 #pragma unroll
     for (int i = 1; i < 16; ++i)
       if (i > t) A[(c + t) * LD + c + i] = x[i];
   }
   __syncthreads();
-  // 5. Off-diagonal blocks, diagonal sd = i - j = 1 .. NB-1.
-  //    X_kj[m][b] for k > j, or k == j and m > b, sits at A[16j + b][16k + m].
-  for (int sd = 1; sd < NB; ++sd) {
-    const int nblk = NB - sd;
-    // T_j = sum_{k=j}^{j+sd-1} L_{j+sd,k} X_kj, written into X_{j+sd,j}'s slot;
-    // 4x4 output tiles (a0..a0+3, b0..b0+3), 16 tiles per block.
-    for (int e = tid; e < nblk * 16; e += kThreads) {
-      const int j = e >> 4, a0 = 4 * ((e >> 2) & 3), b0 = 4 * (e & 3);
-      const int i = j + sd;
+  for (int e = tid; e < NB * 256; e += kThreads) {
+    const int c = 16 * (e >> 8), i = (e >> 4) & 15, t = e & 15;
+    if (i > t) A[(c + i) * LD + c + t] = A[(c + t) * LD + c + i];
+    else if (i == t) A[(c + i) * LD + c + i] = idg[c + i];
+  }
+  __syncthreads();
+  // X[r][c] (zero above the diagonal).
+  auto xat = [&](int r, int cc) -> double { return r >= cc ? A[r * LD + cc] : 0.0; };
+  // 5. Recursive doubling. Pair at offset o, halves of h rows:
+  //    T = X22 L21 (into the pair's upper off-diagonal block, free), then
+  //    X21 = -T X11 (over L21). 4x4 output tiles.
+  for (int h = 16; h < D; h *= 2) {
+    const int npairs = D / (2 * h), tiles = (h / 4) * (h / 4);
+    for (int e = tid; e < npairs * tiles; e += kThreads) {
+      const int o = (e / tiles) * 2 * h, tl = e % tiles;
+      const int a0 = 4 * (tl / (h / 4)), b0 = 4 * (tl % (h / 4));
       double acc[4][4] = {};
-      for (int k = j; k < i; ++k) {
-        for (int m = 0; m < 16; ++m) {
-          double l[4], x[4];
+      for (int mm = 0; mm < a0 + 4; ++mm) {  // X22[a][mm] = 0 for mm > a
+        double xv[4], lv[4];
 #pragma unroll
-          for (int p = 0; p < 4; ++p) l[p] = A[(16 * i + a0 + p) * LD + 16 * k + m];
+        for (int p = 0; p < 4; ++p) xv[p] = xat(o + h + a0 + p, o + h + mm);
 #pragma unroll
-          for (int q = 0; q < 4; ++q) {
-            const int bb = b0 + q;
-            double xv;
-            if (k > j) xv = A[(16 * j + bb) * LD + 16 * k + m];
-            else xv = m > bb ? A[(16 * j + bb) * LD + 16 * j + m] : (m == bb ? idg[16 * j + m] : 0.0);
-            x[q] = xv;
-          }
+        for (int q = 0; q < 4; ++q) lv[q] = A[(o + h + mm) * LD + o + b0 + q];
 #pragma unroll
-          for (int p = 0; p < 4; ++p)
+        for (int p = 0; p < 4; ++p)
 #pragma unroll
-            for (int q = 0; q < 4; ++q) acc[p][q] += l[p] * x[q];
-        }
+          for (int q = 0; q < 4; ++q) acc[p][q] += xv[p] * lv[q];
       }
 #pragma unroll
       for (int p = 0; p < 4; ++p)
 #pragma unroll
-        for (int q = 0; q < 4; ++q) A[(16 * j + b0 + q) * LD + 16 * i + a0 + p] = acc[p][q];
+        for (int q = 0; q < 4; ++q) A[(o + b0 + q) * LD + o + h + a0 + p] = acc[p][q];  // T[a][b]
     }
     __syncthreads();
-    // X_{i,j} = -X_ii T_j, one column b per thread (in place: the column of T
-    // is read into registers first).
-    for (int e = tid; e < nblk * 16; e += kThreads) {
-      const int j = e >> 4, b = e & 15, i = j + sd;
-      double tcol[16];
+    for (int e = tid; e < npairs * tiles; e += kThreads) {
+      const int o = (e / tiles) * 2 * h, tl = e % tiles;
+      const int a0 = 4 * (tl / (h / 4)), b0 = 4 * (tl % (h / 4));
+      double acc[4][4] = {};
+      for (int mm = b0; mm < h; ++mm) {  // X11[mm][b] = 0 for mm < b
+        double tv[4], xv[4];
 #pragma unroll
-      for (int m = 0; m < 16; ++m) tcol[m] = A[(16 * j + b) * LD + 16 * i + m];
+        for (int p = 0; p < 4; ++p) tv[p] = A[(o + mm) * LD + o + h + a0 + p];  // T[a][mm]
 #pragma unroll
-      for (int a = 0; a < 16; ++a) {
-        double s = idg[16 * i + a] * tcol[a];
+        for (int q = 0; q < 4; ++q) xv[q] = xat(o + mm, o + b0 + q);
 #pragma unroll
-        for (int m = 0; m < a; ++m) s += A[(16 * i + m) * LD + 16 * i + a] * tcol[m];
-        A[(16 * j + b) * LD + 16 * i + a] = -s;
+        for (int p = 0; p < 4; ++p)
+#pragma unroll
+          for (int q = 0; q < 4; ++q) acc[p][q] += tv[p] * xv[q];
       }
+#pragma unroll
+      for (int p = 0; p < 4; ++p)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) A[(o + h + a0 + p) * LD + o + b0 + q] = -acc[p][q];  // X21
     }
     __syncthreads();
   }
 
-  // L^{-1}[r][c] for r >= c.
-  auto xinv = [&](int r, int c) -> double { return r == c ? idg[r] : A[c * LD + r]; };
+  auto xinv = xat;
 
-  // 1 / lambda_min(A) = ||L^{-1}||_2^2 by power iteration on L^{-T} L^{-1}.
+  // cond(A) <= ||A||_inf ||L^{-1}||_1 ||L^{-1}||_inf (lambda_max <= ||A||_inf,
+  // 1 / lambda_min = ||L^{-1}||_2^2 <= ||L^{-1}||_1 ||L^{-1}||_inf): a bound,
+  // so no ill-conditioned unit escapes the refinement.
   if (may_refine) {
-    if (tid < D) px[tid] = 1.0 + 0.01 * tid;
-    __syncthreads();
-    normalize<D>(px, px, pred);
-    double inv_min = 0.0;
-    for (int it = 0; it < kPowerIters; ++it) {
-      double s = 0.0;  // py = X px
-      for (int b = ppart; b <= prow; b += TPR) s += xinv(prow, b) * px[b];
-#pragma unroll
-      for (int o = 1; o < TPR; o <<= 1) s += __shfl_xor(s, o);
-      if (ppart == 0) py[prow] = s;
-      __syncthreads();
-      double t2 = 0.0;  // X^T py
-      for (int b = prow + ppart; b < D; b += TPR) t2 += xinv(b, prow) * py[b];
-#pragma unroll
-      for (int o = 1; o < TPR; o <<= 1) t2 += __shfl_xor(t2, o);
-      __syncthreads();
-      if (ppart == 0) py[prow] = t2;
-      __syncthreads();
-      inv_min = normalize<D>(px, py, pred);
+    double rs = 0.0, cs = 0.0;  // row prow's and column prow's absolute sums
+    for (int b = ppart; b < D; b += TPR) {
+      rs += fabs(xat(prow, b));
+      cs += fabs(xat(b, prow));
     }
-    if (lam_max * inv_min > kRefineCond) {
+#pragma unroll
+    for (int o = 1; o < TPR; o <<= 1) {
+      rs += __shfl_xor(rs, o);
+      cs += __shfl_xor(cs, o);
+    }
+    const double xinf = block_max(rs);
+    const double x1 = block_max(cs);
+    if (anorm * x1 * xinf > kRefineCond) {
       if (tid == 0) atomicOr(uflags + u, kUnitRefine);
       return;  // pass 1 writes this unit's L^{-1}
     }
