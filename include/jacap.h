@@ -23,13 +23,23 @@
  * of Algorithm 1 as printed (whose weight omits the 1/d of Eq. 8); ridge = 0
  * is the plain statistical leverage score of App. B.1/B.2.
  *
+ * Output-projection variant (cfg->ridge_mode = JACAP_RIDGE_MATRIX): with
+ * u_i = W~ v_i in place of the proxy v_i (Sec. 2.1 defines u_i = W_O v_i;
+ * W~ is the sum of the output-projection column slices of the G query heads
+ * of the KV head, whose outputs the layer adds), Eq. 9 / Eq. 10 in output
+ * space equal, by the push-through identity,
+ *   score_i = w_i v_i^T (R + sum_j w_j v_j v_j^T)^{-1} v_i,  R = (W~^T W~)^{-1},
+ * so the caller supplies the d x d matrices R per (layer, KV head) in
+ * batch->ridge_mat and they replace ridge * I.
+ *
  * Conventions common to every entry point
  * ---------------------------------------
  * - All data pointers are DEVICE pointers on the current HIP device, except
  *   the two descriptor structs and `flags` of jacap_read_status, which are
  *   host pointers read (or written) during the call only.
  * - The caller owns every buffer. The library allocates no memory, keeps no
- *   pointer after returning and holds no global state; all work is enqueued
+ *   pointer after returning and holds no global state (apart from the
+ *   optional timing records of jacap_timing_*); all work is enqueued
  *   asynchronously on `stream` (a hipStream_t; NULL = the null stream).
  *   Calls on different streams are independent if they use distinct
  *   workspaces.
@@ -84,6 +94,11 @@ enum jacap_cov_mode {
   JACAP_COV_FULL = 1  /* Lambda_Q = full d x d covariance (Algorithm 1 input) */
 };
 
+enum jacap_ridge_mode {
+  JACAP_RIDGE_SCALAR = 0, /* A = cfg->ridge * I + M (Eq. 9) */
+  JACAP_RIDGE_MATRIX = 1  /* A = R + M with R from batch->ridge_mat (output-projection variant) */
+};
+
 enum jacap_dtype {
   JACAP_DTYPE_FP32 = 0, /* K, V, Q stored as float32 */
   JACAP_DTYPE_BF16 = 1  /* K, V, Q stored as bfloat16 */
@@ -112,6 +127,7 @@ typedef struct jacap_config {
   float ridge;          /* ridge >= 0 (see the header comment) */
   int32_t cov_mode;     /* enum jacap_cov_mode */
   int32_t dtype;        /* enum jacap_dtype */
+  int32_t ridge_mode;   /* enum jacap_ridge_mode (0 = scalar ridge) */
 } jacap_config;
 
 /* Batch geometry and strides (host struct; seq_offsets is a device pointer). */
@@ -124,6 +140,9 @@ typedef struct jacap_batch {
   int64_t v_stride_layer, v_stride_head, v_stride_token;
   int64_t q_stride_seq, q_stride_layer, q_stride_head, q_stride_pos;
   int64_t out_stride_seq, out_stride_layer, out_stride_head, out_stride_row;
+  const double* ridge_mat;    /* device fp64 [L][H_kv][d][d], row-major, symmetric positive
+                                 definite; read only when cfg->ridge_mode is
+                                 JACAP_RIDGE_MATRIX (then non-null, 8-byte aligned) */
 } jacap_batch;
 
 /* Bytes of device workspace that jacap_score / jacap_select / jacap_evict

@@ -28,6 +28,7 @@ NumPy and are identical on every device.
 from __future__ import annotations
 
 import dataclasses
+import math
 from typing import Optional, Sequence
 
 import numpy as np
@@ -228,3 +229,22 @@ def make_case(spec="tiny", *, device="cpu", root: int = ROOT_SEED,
 
     offsets = torch.tensor(np.concatenate([[0], np.cumsum(lens)]).astype(np.int32), device=dev)
     return Case(workload=wl, q_win=q_all, k=k_all, v=v_all, seq_lens=lens, seq_offsets=offsets)
+
+
+def make_output_projection(spec="tiny", *, d_model: int = 256, device="cpu",
+                           root: int = ROOT_SEED, **overrides) -> torch.Tensor:
+    """Seeded synthetic output projections W_O, one per layer: fp32
+    [L][d_model][H_q * d] with entries N(0, 1/d_model) (a random stand-in for a
+    trained projection; no checkpoint is available)."""
+    wl = _workload(spec)
+    if overrides:
+        wl = dataclasses.replace(wl, **overrides)
+    out = torch.empty((wl.num_layers, d_model, wl.num_q_heads * wl.head_dim),
+                      dtype=torch.float32, device=device)
+    for layer in range(wl.num_layers):
+        ss = np.random.SeedSequence(root, spawn_key=(wl.wid, 1 << 21, layer))
+        gen = torch.Generator(device=device)
+        gen.manual_seed(_torch_seed(ss))
+        out[layer] = torch.randn((d_model, wl.num_q_heads * wl.head_dim), generator=gen,
+                                 device=device) / math.sqrt(d_model)
+    return out

@@ -18,7 +18,13 @@ open (all listed in the design doc):
   queries; App. B.2: diagonal covariance in practice).
 * GQA: the G query heads sharing a KV head are pooled into one sample of
   G*w queries.
-* u_i = v_i (Sec. 3.4 end: the proxy used when W_O is not applied).
+* u_i = v_i (Sec. 3.4 end: the proxy used when W_O is not applied). The
+  output-projection variant u_i = W_O v_i (Sec. 2.1, Sec. 3.4 end) is taken
+  for the G query heads of a KV head together: their outputs are summed by
+  the layer, so u_i = W~ v_i with W~ = sum_g W_O^g (the heads' column slices
+  of the projection). By the push-through identity its Eq. 10 score equals
+  w_i v_i^T (R + sum_j w_j v_j v_j^T)^{-1} v_i with R = (W~^T W~)^{-1}: the
+  d x d ridge matrix R replaces ridge*I (see output_ridge_matrix).
 * TOP-B: order by (fp32 score desc, index asc), NaN lowest, -0 == +0, and
   return the kept indices in ascending order; |C| = min(B, n).
 """
@@ -106,11 +112,36 @@ def importance_weights(alpha: np.ndarray, one_minus_alpha: np.ndarray,
 # Algorithm 1, steps 3-4: capacity matrix (Eq. 9) and leverage score (Eq. 10)
 # ---------------------------------------------------------------------------
 
-def capacity_matrix(U: np.ndarray, w: np.ndarray, ridge: float) -> np.ndarray:
-    """A = ridge * I + sum_j w_j u_j u_j^T over the whole candidate pool (Eq. 9)."""
+def capacity_matrix(U: np.ndarray, w: np.ndarray, ridge) -> np.ndarray:
+    """A = ridge * I + sum_j w_j u_j u_j^T over the whole candidate pool (Eq. 9).
+    ridge may also be a d x d symmetric positive definite matrix R, which then
+    takes the place of ridge * I (the output-projection variant)."""
     U = np.asarray(U, dtype=np.float64)
     d = U.shape[1]
-    return ridge * np.eye(d) + U.T @ (w[:, None] * U)
+    R = np.asarray(ridge, dtype=np.float64)
+    base = R * np.eye(d) if R.ndim == 0 else R
+    return base + U.T @ (w[:, None] * U)
+
+
+def group_output_projection(w_o: np.ndarray, head: int, group: int, d: int) -> np.ndarray:
+    """W~ = sum_g W_O^g over the G query heads g of KV head `head`: W_O^g is the
+    (d_model x d) column slice of the layer's output projection that maps
+    query head g's attention output into the residual stream (Sec. 2.1, o =
+    W_O sum_i alpha_i v_i, per head). w_o is (d_model, H_q * d)."""
+    w_o = np.asarray(w_o, dtype=np.float64)
+    cols = [w_o[:, (head * group + g) * d:(head * group + g + 1) * d] for g in range(group)]
+    return np.sum(cols, axis=0)
+
+
+def output_ridge_matrix(w_tilde: np.ndarray) -> np.ndarray:
+    """R = (W~^T W~)^{-1} for u_i = W~ v_i. With U = W~ V^T, Eq. 10 in output
+    space is w_i v_i^T W~^T (I + W~ M W~^T)^{-1} W~ v_i (M = sum_j w_j v_j v_j^T),
+    and the push-through identity turns W~^T (I + W~ M W~^T)^{-1} W~ into
+    (G^{-1} + M)^{-1} with G = W~^T W~ (full column rank). So the d x d matrix
+    R = G^{-1} replaces ridge * I in Eq. 9."""
+    w_tilde = np.asarray(w_tilde, dtype=np.float64)
+    G = w_tilde.T @ w_tilde
+    return np.linalg.inv(G)
 
 
 def leverage_scores(U: np.ndarray, w: np.ndarray, A: np.ndarray):
@@ -169,10 +200,11 @@ def compact(K: np.ndarray, V: np.ndarray, idx: np.ndarray):
 # One unit (sequence, layer, KV head) end to end
 # ---------------------------------------------------------------------------
 
-def score_unit(q_group, K, V, *, tau: float = 10.0, ridge: float = 1.0,
+def score_unit(q_group, K, V, *, tau: float = 10.0, ridge=1.0,
                cov_mode: str = DIAG) -> dict:
     """Jacap scores of one KV head (Algorithm 1 steps 1-4) with every
-    intermediate, in float64. q_group is (G, w, d) or (N, d); K and V are (n, d)."""
+    intermediate, in float64. q_group is (G, w, d) or (N, d); K and V are (n, d).
+    ridge is a scalar or a d x d SPD matrix (see capacity_matrix)."""
     K = np.asarray(K, dtype=np.float64)
     V = np.asarray(V, dtype=np.float64)
     n, d = K.shape
@@ -181,7 +213,7 @@ def score_unit(q_group, K, V, *, tau: float = 10.0, ridge: float = 1.0,
     out = {"mu": mu, "lam": lam, "n": n, "d": d}
     if n == 0:
         out.update(scores=np.zeros(0), w=np.zeros(0), singular=False,
-                   A=ridge * np.eye(d))
+                   A=capacity_matrix(np.zeros((0, d)), np.zeros(0), ridge))
         return out
     z = centre_logits(K, mu, tau)
     alpha, one_minus = centre_attention(z)

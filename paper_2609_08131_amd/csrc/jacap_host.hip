@@ -24,6 +24,7 @@ jacap_status check_config(const jacap_config* c) {
   if (c->head_dim != 64 && c->head_dim != 128) return JACAP_ERR_UNSUPPORTED;
   if (c->dtype != JACAP_DTYPE_FP32 && c->dtype != JACAP_DTYPE_BF16) return JACAP_ERR_UNSUPPORTED;
   if (c->cov_mode != JACAP_COV_DIAG && c->cov_mode != JACAP_COV_FULL) return JACAP_ERR_UNSUPPORTED;
+  if (c->ridge_mode != JACAP_RIDGE_SCALAR && c->ridge_mode != JACAP_RIDGE_MATRIX) return JACAP_ERR_UNSUPPORTED;
   return JACAP_OK;
 }
 
@@ -41,6 +42,9 @@ jacap_status check_batch(const jacap_config* c, const jacap_batch* b) {
     if (s < 0 || (s % 8) != 0) return JACAP_ERR_INVALID_ARG;
   if (b->k_stride_token < c->head_dim || b->v_stride_token < c->head_dim) return JACAP_ERR_INVALID_ARG;
   if (b->q_stride_pos < c->head_dim || b->out_stride_row < c->head_dim) return JACAP_ERR_INVALID_ARG;
+  if (c->ridge_mode == JACAP_RIDGE_MATRIX &&
+      (!b->ridge_mat || (reinterpret_cast<uintptr_t>(b->ridge_mat) & 7u)))
+    return JACAP_ERR_INVALID_ARG;
   return JACAP_OK;
 }
 
@@ -96,6 +100,7 @@ Geo make_geo(const jacap_config* c, const jacap_batch* b) {
   g.maxn = b->max_seq_len;
   g.T = b->total_tokens;
   g.seq_off = b->seq_offsets;
+  g.ridge_mat = c->ridge_mode == JACAP_RIDGE_MATRIX ? b->ridge_mat : nullptr;
   g.ksl = b->k_stride_layer; g.ksh = b->k_stride_head; g.kst = b->k_stride_token;
   g.vsl = b->v_stride_layer; g.vsh = b->v_stride_head; g.vst = b->v_stride_token;
   g.qss = b->q_stride_seq; g.qsl = b->q_stride_layer; g.qsh = b->q_stride_head; g.qsp = b->q_stride_pos;

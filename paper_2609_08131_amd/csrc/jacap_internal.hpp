@@ -36,6 +36,7 @@ struct Geo {
   int maxn;                     // host-declared max sequence length
   int64_t T;                    // packed tokens per (layer, head)
   const int32_t* seq_off;       // device [B+1]
+  const double* ridge_mat;      // device [L][H][D][D] replacing ridge * I, or null
   int64_t ksl, ksh, kst;
   int64_t vsl, vsh, vst;
   int64_t qss, qsl, qsh, qsp;

@@ -1,4 +1,5 @@
-// Capacity matrix A = ridge I + M (Eq. 9), its Cholesky factor A = L L^T and
+// Capacity matrix A = ridge I + M (Eq. 9) -- or R + M with a caller-supplied
+// SPD matrix R (the output-projection variant) -- its Cholesky factor A = L L^T and
 // the triangular inverse L^{-1}, one workgroup per unit, in fp64 in LDS.
 // ||L^{-1} v||^2 = v^T A^{-1} v is what the leverage score of Eq. 10 needs.
 //
@@ -107,8 +108,16 @@ __global__ __launch_bounds__(kThreads) void factor_kernel(Geo g, const double* _
   }
   if (tid == 0) bad = 0;
   __syncthreads();
+  if (g.ridge_mat) {  // output-projection variant: A = R + M
+    const double* Rm = g.ridge_mat + ((int64_t)un.l * g.H + un.h) * D * D;
+    for (int e = tid; e < D * D; e += kThreads) {
+      const int r = e / D, cc = e % D;
+      if (cc <= r) A[r * LD + cc] += Rm[e];
+    }
+    __syncthreads();
+  }
   for (int a = tid; a < D; a += kThreads) {
-    A[a * LD + a] += ridge;
+    if (!g.ridge_mat) A[a * LD + a] += ridge;
     dg[a] = A[a * LD + a];
     if (!isfinite(dg[a])) atomicOr(&bad, (int)kUnitNonfinite);
   }

@@ -24,6 +24,7 @@ LIB_PATH = os.path.join(_HERE, "libjacap.so")
 
 OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_WORKSPACE, ERR_HIP = range(5)
 COV_DIAG, COV_FULL = 0, 1
+RIDGE_SCALAR, RIDGE_MATRIX = 0, 1   # enum jacap_ridge_mode
 DTYPE_FP32, DTYPE_BF16 = 0, 1
 FLAG_NONFINITE, FLAG_SINGULAR, FLAG_BAD_OFFSETS = 1, 2, 4
 
@@ -49,6 +50,7 @@ class Config(ctypes.Structure):
         ("ridge", ctypes.c_float),
         ("cov_mode", ctypes.c_int32),
         ("dtype", ctypes.c_int32),
+        ("ridge_mode", ctypes.c_int32),
     ]
 
 
@@ -66,6 +68,7 @@ class Batch(ctypes.Structure):
         ("q_stride_head", ctypes.c_int64), ("q_stride_pos", ctypes.c_int64),
         ("out_stride_seq", ctypes.c_int64), ("out_stride_layer", ctypes.c_int64),
         ("out_stride_head", ctypes.c_int64), ("out_stride_row", ctypes.c_int64),
+        ("ridge_mat", ctypes.c_void_p),
     ]
 
 
@@ -138,6 +141,9 @@ class Params:
     temperature: float = 10.0
     ridge: float = 1.0
     cov_mode: int = COV_DIAG
+    # Output-projection variant: device float64 [L][H_kv][d][d] matrices R that
+    # replace ridge * I (see include/jacap.h); None = scalar ridge.
+    ridge_matrix: Optional[torch.Tensor] = None
 
 
 def make_config(q_win: torch.Tensor, k: torch.Tensor, p: Params) -> Config:
@@ -148,7 +154,8 @@ def make_config(q_win: torch.Tensor, k: torch.Tensor, p: Params) -> Config:
     if k.dtype not in _DTYPE_CODE or q_win.dtype != k.dtype:
         raise ValueError("q_win, k, v must share a dtype: float32 or bfloat16")
     return Config(L, H, Hq, d, w, int(p.budget_k), float(p.temperature), float(p.ridge),
-                  int(p.cov_mode), _DTYPE_CODE[k.dtype])
+                  int(p.cov_mode), _DTYPE_CODE[k.dtype],
+                  RIDGE_SCALAR if p.ridge_matrix is None else RIDGE_MATRIX)
 
 
 def make_batch(seq_offsets: torch.Tensor, seq_lens, q_win: torch.Tensor, k: torch.Tensor,
@@ -177,6 +184,15 @@ def make_batch(seq_offsets: torch.Tensor, seq_lens, q_win: torch.Tensor, k: torc
         # dense [B][L][H][budget][d] is filled in by allocate_outputs users
         b.out_stride_row = d
     return b
+
+
+def set_ridge_matrix(b: Batch, r: torch.Tensor, shape) -> None:
+    """Point the batch at the ridge matrices R (device float64 [L][H_kv][d][d])."""
+    L, H, d = shape
+    if r.dtype != torch.float64 or not r.is_cuda or tuple(r.shape) != (L, H, d, d) \
+            or not r.is_contiguous():
+        raise ValueError("ridge_matrix must be a contiguous device float64 [L][H_kv][d][d] tensor")
+    b.ridge_mat = r.data_ptr()
 
 
 def set_out_strides(b: Batch, out: torch.Tensor) -> None:
@@ -259,6 +275,8 @@ def prepare(q_win, k, v, seq_offsets, seq_lens, params: Params) -> Problem:
     k_out = torch.empty((B, L, H, max(kb, 1), d), dtype=k.dtype, device=dev)
     v_out = torch.empty_like(k_out)
     batch = make_batch(seq_offsets, seq_lens, q_win, k, v, out=k_out)
+    if params.ridge_matrix is not None:
+        set_ridge_matrix(batch, params.ridge_matrix, (L, H, d))
     ws = alloc_workspace(cfg, batch, dev)
     return Problem(cfg, batch, scores, idx, k_out[..., :kb, :], v_out[..., :kb, :], ws)
 

@@ -19,9 +19,13 @@ def tol_for(case) -> float:
     return BF16_TOL if case.workload.dtype == "bf16" else FP32_TOL
 
 
-def run_gpu(case, budget, tau=10.0, ridge=1.0, cov_mode=0, stream=None):
+def run_gpu(case, budget, tau=10.0, ridge=1.0, cov_mode=0, stream=None, ridge_matrices=None):
     from paper_2609_08131_amd import jacap
-    p = jacap.Params(budget_k=budget, temperature=tau, ridge=ridge, cov_mode=cov_mode)
+    rm = None
+    if ridge_matrices is not None:
+        rm = torch.as_tensor(np.ascontiguousarray(ridge_matrices), dtype=torch.float64).cuda()
+    p = jacap.Params(budget_k=budget, temperature=tau, ridge=ridge, cov_mode=cov_mode,
+                     ridge_matrix=rm)
     prob = jacap.prepare(case.q_win, case.k, case.v, case.seq_offsets, case.seq_lens, p)
     jacap.run_evict(prob, case.q_win, case.k, case.v, stream)
     flags = jacap.read_status(prob.ws, stream)

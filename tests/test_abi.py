@@ -43,8 +43,9 @@ def test_struct_layout_matches_header():
 int main(void) {
   printf("sizeof_config %zu\nsizeof_batch %zu\n", sizeof(jacap_config), sizeof(jacap_batch));
   F(jacap_config, temperature) F(jacap_config, ridge) F(jacap_config, dtype)
+  F(jacap_config, ridge_mode)
   F(jacap_batch, total_tokens) F(jacap_batch, seq_offsets) F(jacap_batch, k_stride_layer)
-  F(jacap_batch, q_stride_pos) F(jacap_batch, out_stride_row)
+  F(jacap_batch, q_stride_pos) F(jacap_batch, out_stride_row) F(jacap_batch, ridge_mat)
   return 0;
 }
 """
@@ -57,8 +58,9 @@ int main(void) {
     assert int(out["sizeof_config"]) == ctypes.sizeof(jacap.Config)
     assert int(out["sizeof_batch"]) == ctypes.sizeof(jacap.Batch)
     for s, m in (("Config", "temperature"), ("Config", "ridge"), ("Config", "dtype"),
+                 ("Config", "ridge_mode"),
                  ("Batch", "total_tokens"), ("Batch", "seq_offsets"), ("Batch", "k_stride_layer"),
-                 ("Batch", "q_stride_pos"), ("Batch", "out_stride_row")):
+                 ("Batch", "q_stride_pos"), ("Batch", "out_stride_row"), ("Batch", "ridge_mat")):
         assert int(out[m]) == getattr(getattr(jacap, s), m).offset, m
 
 
@@ -103,12 +105,17 @@ def test_workspace_size_and_validation():
         (_cfg(temperature=0.0), jacap.ERR_INVALID_ARG),
         (_cfg(temperature=float("nan")), jacap.ERR_INVALID_ARG),
         (_cfg(ridge=-1.0), jacap.ERR_INVALID_ARG),
+        (_cfg(ridge_mode=2), jacap.ERR_UNSUPPORTED),
     ]
     for cfg, want in bad:
         assert _ws_size(cfg, _batch())[0] == want
     assert _ws_size(_cfg(), _batch(k_stride_token=60))[0] == jacap.ERR_INVALID_ARG
     assert _ws_size(_cfg(), _batch(seq_offsets=0))[0] == jacap.ERR_INVALID_ARG
     assert _ws_size(_cfg(), _batch(num_seqs=0))[0] == jacap.ERR_INVALID_ARG
+    # the ridge-matrix variant needs an 8-byte aligned matrix pointer
+    assert _ws_size(_cfg(ridge_mode=1), _batch())[0] == jacap.ERR_INVALID_ARG
+    assert _ws_size(_cfg(ridge_mode=1), _batch(ridge_mat=0x1004))[0] == jacap.ERR_INVALID_ARG
+    assert _ws_size(_cfg(ridge_mode=1), _batch(ridge_mat=0x1008))[0] == jacap.OK
     assert jacap._lib.jacap_workspace_size(ctypes.byref(_cfg()), ctypes.byref(_batch()), None) == jacap.ERR_INVALID_ARG
 
 

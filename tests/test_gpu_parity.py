@@ -13,6 +13,7 @@ import pytest
 import torch
 
 from jacap_synth import make_case
+from jacap_synth.cases import make_output_projection
 from oracle import jacap_oracle as jo
 
 from helpers import (gpu_unit_idx, gpu_unit_scores, oracle_unit, overlap, run_gpu, score_errors,
@@ -32,17 +33,20 @@ def jacap():
     return j
 
 
-def check_case(case, budget, ridge, mode="diag", units=None, tau=10.0, label="", jacap=None):
+def check_case(case, budget, ridge, mode="diag", units=None, tau=10.0, label="", jacap=None,
+               ridge_matrices=None):
     units = unit_list(case) if units is None else units
     all_units = len(units) == len(unit_list(case))
-    prob, flags = run_gpu(case, budget, tau=tau, ridge=ridge, cov_mode=COV[mode])
+    prob, flags = run_gpu(case, budget, tau=tau, ridge=ridge, cov_mode=COV[mode],
+                          ridge_matrices=ridge_matrices)
     # SINGULAR is legitimate only at ridge 0 (rank-deficient weighted Gram)
     assert flags & ~(2 if ridge == 0.0 else 0) == 0, f"status flags {flags}"
     tol = tol_for(case)
     ref32 = torch.zeros_like(prob.scores, device="cpu")
     worst, overlaps, orc, illcond = 0.0, [], {}, []
     for (b, l, h) in units:
-        o = oracle_unit(case, b, l, h, budget, tau=tau, ridge=ridge, cov_mode=mode)
+        o = oracle_unit(case, b, l, h, budget, tau=tau, cov_mode=mode,
+                        ridge=ridge if ridge_matrices is None else ridge_matrices[l, h])
         orc[(b, l, h)] = o
         g = gpu_unit_scores(case, prob, b, l, h)
         if len(g) and np.isnan(g).any():
@@ -285,3 +289,42 @@ def test_select_large_units_both_paths(jacap):
     lo, hi = token_slice(case, 2)
     want = jo.select_top(s[0, 1, lo:hi], n - 1)
     assert np.array_equal(prob.idx[2, 0, 1].cpu().numpy()[:n - 1], want)
+
+
+# ---------------------------------------------------------------------------
+# Output-projection variant: u_i = W~ v_i through the ridge matrix R
+# ---------------------------------------------------------------------------
+
+def wo_ridge_matrices(case, d_model_factor=4):
+    """R = (W~^T W~)^{-1} per (layer, KV head) from the seeded synthetic W_O,
+    computed by the oracle in fp64 (an input of the GPU call)."""
+    w = case.workload
+    d, G = w.head_dim, w.num_q_heads // w.num_kv_heads
+    wo = make_output_projection(w, d_model=d_model_factor * d).numpy()
+    R = np.empty((w.num_layers, w.num_kv_heads, d, d))
+    for layer in range(w.num_layers):
+        for h in range(w.num_kv_heads):
+            R[layer, h] = jo.output_ridge_matrix(jo.group_output_projection(wo[layer], h, G, d))
+    return R
+
+
+@pytest.mark.parametrize("mode", ["diag", "full"])
+def test_wo_variant_tiny_fp32(jacap, mode):
+    case = make_case("tiny").to("cuda")
+    R = wo_ridge_matrices(case)
+    check_case(case, 64, 1.0, mode, label=f"tiny W_O {mode}", jacap=jacap, ridge_matrices=R)
+
+
+def test_wo_variant_llama_layer_bf16(jacap):
+    case = make_case("llama8b_layer", seq_lens=[4096], device="cuda")
+    R = wo_ridge_matrices(case)
+    check_case(case, 512, 1.0, "diag", label="llama_layer W_O", jacap=jacap, ridge_matrices=R)
+
+
+@pytest.mark.parametrize("dtype,d", [("bf16", 128), ("fp32", 64)])
+def test_wo_variant_ragged(jacap, dtype, d):
+    case = make_case("ragged16", seq_lens=[0, 1, 17, 300, 1000, 4100], num_layers=2,
+                     num_kv_heads=2, num_q_heads=4, window=8, head_dim=d, dtype=dtype).to("cuda")
+    R = wo_ridge_matrices(case)
+    check_case(case, 64, 1.0, "diag", label=f"ragged W_O {dtype} d{d}", jacap=jacap,
+               ridge_matrices=R)

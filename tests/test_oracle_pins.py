@@ -15,6 +15,7 @@ import pytest
 import scipy.linalg
 import scipy.stats
 
+from jacap_synth import make_case
 from oracle import jacap_oracle as jo
 from oracle import theory
 
@@ -443,3 +444,54 @@ def test_select_matches_rank_definition():
 def test_select_decides_on_fp32():
     s64 = np.array([1.0, 1.0 + 1e-12, 0.5])          # equal after fp32 rounding
     assert jo.select_top(jo.to_fp32(s64), 1).tolist() == [0]
+
+
+# ---------------------------------------------------------------------------
+# Output-projection variant (u_i = W_O v_i)
+# ---------------------------------------------------------------------------
+
+def test_wo_group_projection_matches_full_output_projection():
+    """Sec. 2.1: the layer output is W_O applied to the concatenated per-head
+    outputs. When the G heads of a KV group share one attention output y_h,
+    that equals sum_h W~_h y_h with W~_h = group_output_projection(...)."""
+    rng = np.random.default_rng(11)
+    d, H, G, dm = 4, 3, 2, 9
+    w_o = rng.normal(size=(dm, H * G * d))
+    ys = rng.normal(size=(H, d))
+    concat = np.concatenate([ys[h] for h in range(H) for _ in range(G)])
+    full = w_o @ concat
+    via_groups = sum(jo.group_output_projection(w_o, h, G, d) @ ys[h] for h in range(H))
+    np.testing.assert_allclose(via_groups, full, rtol=1e-13, atol=1e-13)
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_wo_push_through_equals_literal_output_space_scores(seed):
+    """Eq. 9 / Eq. 10 evaluated literally in output space (u_i = W~ v_i,
+    A = I + sum_j w_j u_j u_j^T of size d_model) equal the d x d ridge-matrix
+    form with R = (W~^T W~)^{-1}."""
+    rng = np.random.default_rng(100 + seed)
+    d, G, w_len, n, dm = 6, 2, 5, 17, 23
+    q = rng.normal(size=(G, w_len, d)) + rng.normal(size=d)
+    K = rng.normal(size=(n, d))
+    V = rng.normal(size=(n, d))
+    w_tilde = rng.normal(size=(dm, d)) / np.sqrt(dm)
+    R = jo.output_ridge_matrix(w_tilde)
+    o = jo.score_unit(q, K, V, tau=1.0, ridge=R)
+    w = o["w"] * 1e3          # larger weights make the capacity term matter
+    U = V @ w_tilde.T         # rows u_i = W~ v_i
+    A_out = np.eye(dm) + U.T @ (w[:, None] * U)
+    lit = w * np.einsum("ij,ij->i", U, np.linalg.solve(A_out, U.T).T)
+    A_d = jo.capacity_matrix(V, w, R)
+    got, singular = jo.leverage_scores(V, w, A_d)
+    assert not singular
+    np.testing.assert_allclose(got, lit, rtol=1e-10, atol=0)
+
+
+def test_ridge_matrix_lambda_identity_equals_scalar_ridge():
+    """R = ridge * I reproduces the scalar-ridge scores."""
+    case = make_case("tiny", seq_lens=[96], head_dim=64)
+    q, k, v = case.unit_arrays(0, 0, 0)
+    for lam in (1.0, 0.25):
+        a = jo.score_unit(q, k, v, ridge=lam)["scores"]
+        b = jo.score_unit(q, k, v, ridge=lam * np.eye(64))["scores"]
+        np.testing.assert_allclose(b, a, rtol=1e-12, atol=0)
