@@ -132,6 +132,26 @@ __device__ __forceinline__ double importance_weight(float z, float kappa, float 
   return rho * rho * (double)kappa * inv_d;
 }
 
+// DPP lane exchanges inside each 16-lane row (one VALU instruction each):
+// quad swaps (lane ^ 1, lane ^ 2), the half-row mirror (i <-> 7 - i within 8)
+// and the row mirror (i <-> 15 - i).
+constexpr int kDppQuadXor1 = 0xB1;   // quad_perm [1,0,3,2]
+constexpr int kDppQuadXor2 = 0x4E;   // quad_perm [2,3,0,1]
+constexpr int kDppHalfMirror = 0x141;
+constexpr int kDppMirror = 0x140;
+template <int CTRL>
+__device__ __forceinline__ float dpp_f32(float v) {
+  return __builtin_bit_cast(
+      float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL, 0xF, 0xF, true));
+}
+template <int CTRL>
+__device__ __forceinline__ double dpp_f64(double v) {
+  const uint64_t b = __builtin_bit_cast(uint64_t, v);
+  const uint32_t lo = __builtin_amdgcn_update_dpp(0, (int)(uint32_t)b, CTRL, 0xF, 0xF, true);
+  const uint32_t hi = __builtin_amdgcn_update_dpp(0, (int)(uint32_t)(b >> 32), CTRL, 0xF, 0xF, true);
+  return __builtin_bit_cast(double, ((uint64_t)hi << 32) | lo);
+}
+
 // Wave64 butterfly reductions: every lane ends with the same, order-fixed value
 // (IEEE addition is commutative, so partner lanes compute identical sums).
 __device__ __forceinline__ float wave_max(float v) {

@@ -29,6 +29,7 @@ __global__ __launch_bounds__(kThreads, 2) void leverage_mfma_kernel(
   if (base >= un.n) return;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int ch = lane & 15, kg = lane >> 4;
+  const int rl = 2 * (ch >> 3) + ((ch >> 2) & 1);  // token (of 4) whose score this lane ends with
   const int64_t trow = token_row(g, un);
   const int end = min(un.n, base + kLChunkMfma);
 
@@ -64,11 +65,11 @@ __global__ __launch_bounds__(kThreads, 2) void leverage_mfma_kernel(
 #pragma unroll
     for (int kb = 0; kb < NK; ++kb)
       b.a[kb] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(vb + (int64_t)tok * g.vst + 32 * kb + 8 * kg));
-    b.w = wbuf[trow + min(t0 + 4 * kg + (ch & 3), end - 1)];
+    b.w = wbuf[trow + min(t0 + 4 * kg + rl, end - 1)];
     __builtin_amdgcn_sched_barrier(0);  // issue here, ahead of the MFMAs that follow
   };
   auto step = [&](int t0, const Buf& b) {
-    const int tw = t0 + 4 * kg + (ch & 3);
+    const int tw = t0 + 4 * kg + rl;
     const float wt = b.w;
     const bf16x8 (&cur)[NK] = b.a;
     // Output blocks j = 2 jp and 2 jp + 1 share the K-block range kb <= jp:
@@ -89,18 +90,18 @@ __global__ __launch_bounds__(kThreads, 2) void leverage_mfma_kernel(
 #pragma unroll
       for (int r = 0; r < 4; ++r) ss[r] += y0[r] * y0[r] + y1[r] * y1[r];
     }
-    // lane holds Y[token t0 + 4 kg + r][a = 16 j + ch]: reduce over ch.
-#pragma unroll
-    for (int r = 0; r < 4; ++r)
-#pragma unroll
-      for (int o = 1; o < 16; o <<= 1) ss[r] += __shfl_xor(ss[r], o);
-    if (ch < 4 && tw < end) {
-      float sv = ss[0];
-#pragma unroll
-      for (int r = 1; r < 4; ++r)
-        if (ch == r) sv = ss[r];
-      scores[trow + tw] = wt * sv;
-    }
+    // ss[r] is this lane's channel's part of token 4 kg + r; sum over the 16
+    // lanes (channels) of the row by a transposing reduction: the row mirror
+    // (ch <-> 15 - ch) leaves tokens 0, 1 to the lower half and 2, 3 to the
+    // upper, the half-row mirror (ch <-> 7 - ch) one token per lane, and two
+    // quad swaps finish; lane ch then holds token rl.
+    const bool hi8 = ch >= 8, hi4 = (ch & 4) != 0;
+    const float m0 = (hi8 ? ss[2] : ss[0]) + dpp_f32<kDppMirror>(hi8 ? ss[0] : ss[2]);
+    const float m1 = (hi8 ? ss[3] : ss[1]) + dpp_f32<kDppMirror>(hi8 ? ss[1] : ss[3]);
+    float sv = (hi4 ? m1 : m0) + dpp_f32<kDppHalfMirror>(hi4 ? m0 : m1);
+    sv += dpp_f32<kDppQuadXor1>(sv);
+    sv += dpp_f32<kDppQuadXor2>(sv);
+    if ((ch & 3) == 0 && tw < end) scores[trow + tw] = wt * sv;
   };
   constexpr int WSTRIDE = 16 * (kThreads / 64);
   const int t_first = base + wave * 16;

@@ -155,35 +155,20 @@ hipError_t launch_qstats(const Launch& L, const void* q) {
 // ends with the same value. Within a 16-lane row the partners come from DPP
 // (quad swaps, then the half-row and row mirrors: one VALU instruction per
 // level); groups of 32 add one cross-row exchange.
-__device__ __forceinline__ float dpp_f32(float v, int ctrl_sel) {
-  const int x = __builtin_bit_cast(int, v);
-  int r;
-  switch (ctrl_sel) {  // dpp_ctrl must be a constant
-    case 0: r = __builtin_amdgcn_update_dpp(0, x, 0xB1, 0xF, 0xF, true); break;   // quad_perm [1,0,3,2]
-    case 1: r = __builtin_amdgcn_update_dpp(0, x, 0x4E, 0xF, 0xF, true); break;   // quad_perm [2,3,0,1]
-    case 2: r = __builtin_amdgcn_update_dpp(0, x, 0x141, 0xF, 0xF, true); break;  // row_half_mirror
-    default: r = __builtin_amdgcn_update_dpp(0, x, 0x140, 0xF, 0xF, true); break; // row_mirror
-  }
-  return __builtin_bit_cast(float, r);
-}
-__device__ __forceinline__ double dpp_f64(double v, int ctrl_sel) {
-  const uint64_t b = __builtin_bit_cast(uint64_t, v);
-  const float lo = dpp_f32(__builtin_bit_cast(float, (uint32_t)b), ctrl_sel);
-  const float hi = dpp_f32(__builtin_bit_cast(float, (uint32_t)(b >> 32)), ctrl_sel);
-  return __builtin_bit_cast(double, ((uint64_t)__builtin_bit_cast(uint32_t, hi) << 32) |
-                                        __builtin_bit_cast(uint32_t, lo));
-}
 template <int G, typename F>
 __device__ __forceinline__ F group_sum(F v) {
   static_assert(G == 8 || G == 16 || G == 32, "group of 8, 16 or 32 lanes");
-  auto step = [&](int sel) {
-    if constexpr (sizeof(F) == 4) v += dpp_f32(v, sel);
-    else v += dpp_f64(v, sel);
-  };
-  step(0);
-  step(1);
-  step(2);
-  if constexpr (G >= 16) step(3);
+  if constexpr (sizeof(F) == 4) {
+    v += dpp_f32<kDppQuadXor1>(v);
+    v += dpp_f32<kDppQuadXor2>(v);
+    v += dpp_f32<kDppHalfMirror>(v);
+    if constexpr (G >= 16) v += dpp_f32<kDppMirror>(v);
+  } else {
+    v += dpp_f64<kDppQuadXor1>(v);
+    v += dpp_f64<kDppQuadXor2>(v);
+    v += dpp_f64<kDppHalfMirror>(v);
+    if constexpr (G >= 16) v += dpp_f64<kDppMirror>(v);
+  }
   if constexpr (G == 32) v += __shfl_xor(v, 16);
   return v;
 }
