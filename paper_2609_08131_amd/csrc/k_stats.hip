@@ -204,6 +204,7 @@ __global__ __launch_bounds__(kThreads) void kpass_kernel(
     muv[e] = (Acc)mu[(int64_t)u * D + sub * VEC + e];
     lamv[e] = (Acc)lam[(int64_t)u * D + sub * VEC + e];
   }
+  drain_vmem();  // keep these prologue loads out of the loop's wait counts
 
   __shared__ float zsh[kKChunk];
   __shared__ float ksq[kKChunk];
@@ -222,14 +223,25 @@ __global__ __launch_bounds__(kThreads) void kpass_kernel(
   // one: it stages each token row in LDS between barriers).
   constexpr int UNR = FULL ? 1 : 4;
   static_assert(kKChunk % (UNR * TPB) == 0, "chunk must be whole unrolled trips");
-  for (int it0 = 0; it0 < kKChunk; it0 += UNR * TPB) {
-    uint4 raw[UNR];
+  // Rows are loaded one trip ahead (double buffer); every load is
+  // unconditional (past-the-end rows clamped, discarded) so the compiler's
+  // wait counts stay static.
+  auto load_trip = [&](int it0, uint4 (&raw)[UNR]) {
 #pragma unroll
     for (int j = 0; j < UNR; ++j) {
       const int i = base + it0 + j * TPB + wave * TPW + tiw;
-      const int ic = min(i, un.n - 1);  // in bounds; the value is unused when i >= n
+      const int ic = min(i, un.n - 1);
       raw[j] = *reinterpret_cast<const uint4*>(kb + (un.t0 + ic) * g.kst + sub * VEC);
     }
+    __builtin_amdgcn_sched_barrier(0);
+  };
+  uint4 nxt[UNR];
+  load_trip(0, nxt);
+  for (int it0 = 0; it0 < kKChunk; it0 += UNR * TPB) {
+    uint4 raw[UNR];
+#pragma unroll
+    for (int j = 0; j < UNR; ++j) raw[j] = nxt[j];
+    load_trip(min(it0 + UNR * TPB, kKChunk - UNR * TPB), nxt);
 #pragma unroll
     for (int j = 0; j < UNR; ++j) {
       const int tl = it0 + j * TPB + wave * TPW + tiw;
