@@ -32,6 +32,17 @@
  * so the caller supplies the d x d matrices R per (layer, KV head) in
  * batch->ridge_mat and they replace ridge * I.
  *
+ * GQA (the paper is single-head): by default the G query heads of a KV head
+ * are pooled into one window of G*w queries. With cfg->gqa_mode =
+ * JACAP_GQA_PER_HEAD each query head g is scored alone (its own w queries give
+ * its mu_Q, Lambda_Q, weights and capacity matrix) and a token's score is the
+ * mean over the G heads.
+ *
+ * Protected tokens (Algorithm 1 ranks every token; cfg->protect_last = 0 keeps
+ * that): with protect_last = P > 0 the last min(P, n_b) positions of every
+ * sequence are always kept and the rest of the budget is filled by score
+ * from the earlier positions (budget <= P keeps the last `budget` positions).
+ *
  * Conventions common to every entry point
  * ---------------------------------------
  * - All data pointers are DEVICE pointers on the current HIP device, except
@@ -84,7 +95,7 @@ extern "C" {
 typedef enum jacap_status {
   JACAP_OK = 0,
   JACAP_ERR_INVALID_ARG = 1, /* null/misaligned pointer, bad shape/stride/parameter */
-  JACAP_ERR_UNSUPPORTED = 2, /* head_dim not in {64, 128}, or unknown dtype / cov_mode */
+  JACAP_ERR_UNSUPPORTED = 2, /* head_dim not in {64, 128}, or an unknown dtype / mode */
   JACAP_ERR_WORKSPACE = 3,   /* workspace smaller than jacap_workspace_size() */
   JACAP_ERR_HIP = 4          /* a HIP launch or runtime call failed */
 } jacap_status;
@@ -97,6 +108,11 @@ enum jacap_cov_mode {
 enum jacap_ridge_mode {
   JACAP_RIDGE_SCALAR = 0, /* A = cfg->ridge * I + M (Eq. 9) */
   JACAP_RIDGE_MATRIX = 1  /* A = R + M with R from batch->ridge_mat (output-projection variant) */
+};
+
+enum jacap_gqa_mode {
+  JACAP_GQA_POOLED = 0,   /* one sample of G*w window queries per KV head */
+  JACAP_GQA_PER_HEAD = 1  /* score per query head, average over the group */
 };
 
 enum jacap_dtype {
@@ -128,6 +144,8 @@ typedef struct jacap_config {
   int32_t cov_mode;     /* enum jacap_cov_mode */
   int32_t dtype;        /* enum jacap_dtype */
   int32_t ridge_mode;   /* enum jacap_ridge_mode (0 = scalar ridge) */
+  int32_t gqa_mode;     /* enum jacap_gqa_mode (0 = pooled) */
+  int32_t protect_last; /* >= 0: most recent positions of each sequence always kept */
 } jacap_config;
 
 /* Batch geometry and strides (host struct; seq_offsets is a device pointer). */
@@ -163,6 +181,8 @@ jacap_status jacap_score(const jacap_config* cfg, const jacap_batch* batch,
 /* Algorithm 1 step 5 (TOP-B): for each unit keeps min(budget_k, n_b) tokens
  * ordered by (score descending, position ascending), NaN lowest and -0 equal
  * to +0, and writes their positions in ascending order to idx (-1 padding).
+ * With cfg->protect_last = P > 0 the last min(P, n_b) positions are kept
+ * first and the ranking fills the rest from the earlier positions.
  * Bit-exact and deterministic for given scores. */
 jacap_status jacap_select(const jacap_config* cfg, const jacap_batch* batch,
                           const float* scores, int32_t* idx, void* ws, size_t ws_bytes,

@@ -17,7 +17,7 @@ open (all listed in the design doc):
   the observation-window queries (Sec. 3.4 end: estimated from observed
   queries; App. B.2: diagonal covariance in practice).
 * GQA: the G query heads sharing a KV head are pooled into one sample of
-  G*w queries.
+  G*w queries; the per-head alternative scores each head alone and averages.
 * u_i = v_i (Sec. 3.4 end: the proxy used when W_O is not applied). The
   output-projection variant u_i = W_O v_i (Sec. 2.1, Sec. 3.4 end) is taken
   for the G query heads of a KV head together: their outputs are summed by
@@ -26,7 +26,9 @@ open (all listed in the design doc):
   w_i v_i^T (R + sum_j w_j v_j v_j^T)^{-1} v_i with R = (W~^T W~)^{-1}: the
   d x d ridge matrix R replaces ridge*I (see output_ridge_matrix).
 * TOP-B: order by (fp32 score desc, index asc), NaN lowest, -0 == +0, and
-  return the kept indices in ascending order; |C| = min(B, n).
+  return the kept indices in ascending order; |C| = min(B, n). No token is
+  protected by default (Algorithm 1 ranks all); an optional protected tail
+  keeps the most recent positions first.
 """
 
 from __future__ import annotations
@@ -178,12 +180,18 @@ def to_fp32(scores: np.ndarray) -> np.ndarray:
     return np.asarray(scores, dtype=np.float64).astype(np.float32)
 
 
-def select_top(scores32: np.ndarray, budget: int) -> np.ndarray:
+def select_top(scores32: np.ndarray, budget: int, protect_last: int = 0) -> np.ndarray:
     """Indices of the min(budget, n) best tokens by (score desc, index asc), NaN
-    ranked lowest and -0 equal to +0, returned in ascending index order (int32)."""
+    ranked lowest and -0 equal to +0, returned in ascending index order (int32).
+    protect_last = P > 0: the last min(P, budget, n) positions are kept first
+    and the ranking fills the rest of the budget from the earlier positions."""
     s = np.asarray(scores32, dtype=np.float32).astype(np.float64)
     n = s.shape[0]
     b = max(0, min(int(budget), n))
+    p = min(max(int(protect_last), 0), b)
+    if p > 0:
+        head = select_top(s[:n - p], b - p)
+        return np.concatenate([head, np.arange(n - p, n)]).astype(np.int32)
     nan = np.isnan(s)
     key = np.where(nan, 0.0, s) + 0.0        # +0.0 turns -0 into +0
     # lexsort: last key is primary -> NaN flag, then -score, then index.
@@ -226,11 +234,31 @@ def score_unit(q_group, K, V, *, tau: float = 10.0, ridge=1.0,
     return out
 
 
-def evict_unit(q_group, K, V, budget: int, **kw) -> dict:
-    """score_unit, then TOP-B on the fp32 scores and the compacted K', V'."""
-    out = score_unit(q_group, K, V, **kw)
+def score_unit_per_head(q_group, K, V, **kw) -> dict:
+    """Per-query-head GQA reading: each of the G query heads is scored alone
+    (its own w window queries give mu_Q, Lambda_Q, the weights and A), and a
+    token's score is the mean over the heads, summed in head order."""
+    q_group = np.asarray(q_group, dtype=np.float64)
+    if q_group.ndim == 2:
+        q_group = q_group[None]
+    heads = [score_unit(q_group[g:g + 1], K, V, **kw) for g in range(q_group.shape[0])]
+    total = heads[0]["scores"].copy()
+    for h in heads[1:]:
+        total = total + h["scores"]
+    out = dict(heads[0])
+    out.update(scores=total / len(heads), heads=heads,
+               singular=any(h["singular"] for h in heads))
+    return out
+
+
+def evict_unit(q_group, K, V, budget: int, gqa: str = "pooled", protect_last: int = 0,
+               **kw) -> dict:
+    """score_unit (or score_unit_per_head for gqa="per_head"), then TOP-B on
+    the fp32 scores and the compacted K', V'."""
+    scorer = score_unit_per_head if gqa == "per_head" else score_unit
+    out = scorer(q_group, K, V, **kw)
     s32 = to_fp32(out["scores"])
-    idx = select_top(s32, budget)
+    idx = select_top(s32, budget, protect_last)
     Kc, Vc = compact(np.asarray(K), np.asarray(V), idx)
     out.update(scores32=s32, idx=idx, k_out=Kc, v_out=Vc)
     return out

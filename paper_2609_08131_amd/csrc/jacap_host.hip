@@ -25,6 +25,8 @@ jacap_status check_config(const jacap_config* c) {
   if (c->dtype != JACAP_DTYPE_FP32 && c->dtype != JACAP_DTYPE_BF16) return JACAP_ERR_UNSUPPORTED;
   if (c->cov_mode != JACAP_COV_DIAG && c->cov_mode != JACAP_COV_FULL) return JACAP_ERR_UNSUPPORTED;
   if (c->ridge_mode != JACAP_RIDGE_SCALAR && c->ridge_mode != JACAP_RIDGE_MATRIX) return JACAP_ERR_UNSUPPORTED;
+  if (c->gqa_mode != JACAP_GQA_POOLED && c->gqa_mode != JACAP_GQA_PER_HEAD) return JACAP_ERR_UNSUPPORTED;
+  if (c->protect_last < 0) return JACAP_ERR_INVALID_ARG;
   return JACAP_OK;
 }
 
@@ -79,6 +81,8 @@ Workspace layout(const jacap_config* c, const jacap_batch* b) {
   w.kappa = take(4 * LHT);
   w.cstat = take(8 * U * (int64_t)w.kchunks);
   w.wgt = take(4 * LHT);
+  const bool per_head = c->gqa_mode == JACAP_GQA_PER_HEAD && c->num_q_heads > c->num_kv_heads;
+  w.hscore = take(per_head ? 4 * LHT : 4);
   w.gram = take((size_t)(U * (int64_t)w.gchunks * part_bytes));
   w.gram_red = take(8 * U * npair * 256);
   w.linv64 = take(w.mfma ? 8 : 8 * U * D * D);
@@ -138,8 +142,13 @@ jacap_status prepare(const jacap_config* c, const jacap_batch* b, void* ws, size
     JACAP_TRY(expr);                        \
   } while (0)
 
-jacap_status run_score(const Launch& L, const void* q, const void* k, const void* v, float* scores) {
-  JACAP_PHASE(JACAP_PHASE_INIT, launch_init(L));
+// One scoring pass (Algorithm 1 steps 1-4) over every unit. The first pass of
+// a call clears the status words; later passes (per-head GQA) keep the sticky
+// flags and clear only the refinement marks.
+jacap_status score_pass(const Launch& L, const void* q, const void* k, const void* v,
+                        float* scores, bool first) {
+  if (first) JACAP_PHASE(JACAP_PHASE_INIT, launch_init(L));
+  else JACAP_PHASE(JACAP_PHASE_INIT, launch_clear_refine(L));
   JACAP_PHASE(JACAP_PHASE_QSTATS, launch_qstats(L, q));
   JACAP_PHASE(JACAP_PHASE_KPASS, launch_kpass(L, k));
   JACAP_PHASE(JACAP_PHASE_WEIGHTS, launch_softmax_weights(L));
@@ -153,6 +162,27 @@ jacap_status run_score(const Launch& L, const void* q, const void* k, const void
     JACAP_TRY(launch_factor(L, true));
   }
   JACAP_PHASE(JACAP_PHASE_LEVERAGE, launch_leverage(L, v, scores));
+  return JACAP_OK;
+}
+
+jacap_status run_score(const Launch& L, const void* q, const void* k, const void* v, float* scores) {
+  const int G = L.geo.G;
+  if (L.cfg->gqa_mode != JACAP_GQA_PER_HEAD || G == 1) return score_pass(L, q, k, v, scores, true);
+  // Per-head GQA: query head g of every group alone (a geometry with one query
+  // head per KV head, whose head stride skips the group), then the mean.
+  const size_t esize = L.cfg->dtype == JACAP_DTYPE_BF16 ? 2 : 4;
+  float* hs = ws_ptr<float>(L.wsp, L.ws.hscore);
+  for (int g = 0; g < G; ++g) {
+    Launch Lg = L;
+    Lg.geo.G = 1;
+    Lg.geo.Hq = L.geo.H;
+    Lg.geo.qsh = L.geo.qsh * G;
+    const void* qg = static_cast<const char*>(q) + (size_t)g * L.geo.qsh * esize;
+    const jacap_status s = score_pass(Lg, qg, k, v, g == 0 ? scores : hs, g == 0);
+    if (s != JACAP_OK) return s;
+    // scores = (((s_0 + s_1) + s_2) + ...) / G, in fp32, fixed order
+    if (g > 0) JACAP_TRY(launch_accumulate_scores(L, scores, hs, g == G - 1 ? 1.0f / G : 1.0f));
+  }
   return JACAP_OK;
 }
 

@@ -88,6 +88,7 @@ struct Workspace {
   size_t kappa;    // float  [L][H][T]       query response
   size_t cstat;    // float2 [U][kchunks]    per-chunk (max, sum exp)
   size_t wgt;      // float  [L][H][T]       importance weights (Eq. 8)
+  size_t hscore;   // float  [L][H][T]       one query head's scores (per-head GQA mode)
   size_t gram;     // per-chunk partial Grams [U][gchunks][NPAIR*256], fp32 (bf16 path) or fp64
   size_t gram_red; // double [U][NPAIR*256]  reduced Gram, block-lane layout
   size_t linv64;   // double [U][D][D]       L^{-1} (lower, zeros above), fp32-input path
@@ -236,6 +237,8 @@ hipError_t launch_init(const Launch& L);
 hipError_t launch_qstats(const Launch& L, const void* q);
 hipError_t launch_kpass(const Launch& L, const void* k);
 hipError_t launch_softmax_weights(const Launch& L);
+hipError_t launch_clear_refine(const Launch& L);
+hipError_t launch_accumulate_scores(const Launch& L, float* acc, const float* add, float scale);
 hipError_t launch_gram(const Launch& L, const void* v, bool refine);
 hipError_t launch_gram_reduce(const Launch& L, bool refine);
 hipError_t launch_factor(const Launch& L, bool refine);

@@ -161,16 +161,23 @@ __device__ __forceinline__ int lower_bound_lds(const int32_t* a, int cnt, int32_
 }
 
 __global__ __launch_bounds__(kSelThreads) void select_kernel(Geo g, const float* __restrict__ scores,
-                                                             int32_t* __restrict__ idx, int budget) {
+                                                             int32_t* __restrict__ idx, int budget,
+                                                             int protect) {
   __shared__ SelShared sh;
   const int u = blockIdx.x, tid = threadIdx.x;
   const Unit un = decode_unit(g, u);
   int32_t* out = idx + (int64_t)u * budget;
-  const int n = un.n;
-  const int kk = min(budget, n);
+  const int kk_all = min(budget, un.n);
   const float* s = scores + token_row(g, un);
 
-  for (int j = kk + tid; j < budget; j += kSelThreads) out[j] = -1;
+  for (int j = kk_all + tid; j < budget; j += kSelThreads) out[j] = -1;
+  if (kk_all == 0) return;
+  // Protected tail: the last p positions are kept; the ranking fills the
+  // remaining kk slots from positions 0 .. n-1 (n = n_b - p), whose indices
+  // all precede the tail, so the tail simply follows them in idx.
+  const int p = min(protect, kk_all);
+  const int n = un.n - p, kk = kk_all - p;
+  for (int j = tid; j < p; j += kSelThreads) out[kk + j] = n + j;
   if (kk == 0) return;
   if (kk == n) {
     for (int j = tid; j < n; j += kSelThreads) out[j] = j;
@@ -284,7 +291,8 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(Geo g, const float*
 }
 
 hipError_t launch_select(const Launch& L, const float* scores, int32_t* idx) {
-  select_kernel<<<L.geo.U, kSelThreads, 0, L.stream>>>(L.geo, scores, idx, L.cfg->budget_k);
+  select_kernel<<<L.geo.U, kSelThreads, 0, L.stream>>>(L.geo, scores, idx, L.cfg->budget_k,
+                                                       L.cfg->protect_last);
   return hipGetLastError();
 }
 

@@ -2,6 +2,8 @@
 // softmax normaliser (Algorithm 1, first two steps; Sec. 3.4).
 #include <type_traits>
 
+#include <algorithm>
+
 #include "jacap_internal.hpp"
 
 namespace jacap {
@@ -18,6 +20,35 @@ hipError_t launch_init(const Launch& L) {
   const int U = L.geo.U;
   init_kernel<<<(U + kThreads - 1) / kThreads, kThreads, 0, L.stream>>>(
       ws_ptr<uint32_t>(L.wsp, L.ws.status), ws_ptr<uint32_t>(L.wsp, L.ws.uflags), U);
+  return hipGetLastError();
+}
+
+// Clears the refinement marks only (between the per-head passes of one call).
+__global__ void clear_refine_kernel(uint32_t* __restrict__ uflags, int U) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < U) uflags[i] &= ~kUnitRefine;
+}
+
+hipError_t launch_clear_refine(const Launch& L) {
+  const int U = L.geo.U;
+  clear_refine_kernel<<<(U + kThreads - 1) / kThreads, kThreads, 0, L.stream>>>(
+      ws_ptr<uint32_t>(L.wsp, L.ws.uflags), U);
+  return hipGetLastError();
+}
+
+// acc = (acc + add) * scale over the [L][H][T] score array.
+__global__ void accumulate_scores_kernel(float* __restrict__ acc, const float* __restrict__ add,
+                                         int64_t n, float scale) {
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride)
+    acc[i] = (acc[i] + add[i]) * scale;
+}
+
+hipError_t launch_accumulate_scores(const Launch& L, float* acc, const float* add, float scale) {
+  const int64_t n = (int64_t)L.geo.L * L.geo.H * L.geo.T;
+  if (n == 0) return hipSuccess;
+  const int64_t blocks = std::min<int64_t>((n + kThreads - 1) / kThreads, 8192);
+  accumulate_scores_kernel<<<(unsigned)blocks, kThreads, 0, L.stream>>>(acc, add, n, scale);
   return hipGetLastError();
 }
 

@@ -25,6 +25,7 @@ LIB_PATH = os.path.join(_HERE, "libjacap.so")
 OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_WORKSPACE, ERR_HIP = range(5)
 COV_DIAG, COV_FULL = 0, 1
 RIDGE_SCALAR, RIDGE_MATRIX = 0, 1   # enum jacap_ridge_mode
+GQA_POOLED, GQA_PER_HEAD = 0, 1     # enum jacap_gqa_mode
 DTYPE_FP32, DTYPE_BF16 = 0, 1
 FLAG_NONFINITE, FLAG_SINGULAR, FLAG_BAD_OFFSETS = 1, 2, 4
 
@@ -51,6 +52,8 @@ class Config(ctypes.Structure):
         ("cov_mode", ctypes.c_int32),
         ("dtype", ctypes.c_int32),
         ("ridge_mode", ctypes.c_int32),
+        ("gqa_mode", ctypes.c_int32),
+        ("protect_last", ctypes.c_int32),
     ]
 
 
@@ -144,6 +147,8 @@ class Params:
     # Output-projection variant: device float64 [L][H_kv][d][d] matrices R that
     # replace ridge * I (see include/jacap.h); None = scalar ridge.
     ridge_matrix: Optional[torch.Tensor] = None
+    gqa_mode: int = GQA_POOLED
+    protect_last: int = 0       # most recent positions of each sequence always kept
 
 
 def make_config(q_win: torch.Tensor, k: torch.Tensor, p: Params) -> Config:
@@ -155,7 +160,8 @@ def make_config(q_win: torch.Tensor, k: torch.Tensor, p: Params) -> Config:
         raise ValueError("q_win, k, v must share a dtype: float32 or bfloat16")
     return Config(L, H, Hq, d, w, int(p.budget_k), float(p.temperature), float(p.ridge),
                   int(p.cov_mode), _DTYPE_CODE[k.dtype],
-                  RIDGE_SCALAR if p.ridge_matrix is None else RIDGE_MATRIX)
+                  RIDGE_SCALAR if p.ridge_matrix is None else RIDGE_MATRIX,
+                  int(p.gqa_mode), int(p.protect_last))
 
 
 def make_batch(seq_offsets: torch.Tensor, seq_lens, q_win: torch.Tensor, k: torch.Tensor,

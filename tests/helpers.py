@@ -19,13 +19,16 @@ def tol_for(case) -> float:
     return BF16_TOL if case.workload.dtype == "bf16" else FP32_TOL
 
 
-def run_gpu(case, budget, tau=10.0, ridge=1.0, cov_mode=0, stream=None, ridge_matrices=None):
+def run_gpu(case, budget, tau=10.0, ridge=1.0, cov_mode=0, stream=None, ridge_matrices=None,
+            gqa="pooled", protect_last=0):
     from paper_2609_08131_amd import jacap
     rm = None
     if ridge_matrices is not None:
         rm = torch.as_tensor(np.ascontiguousarray(ridge_matrices), dtype=torch.float64).cuda()
     p = jacap.Params(budget_k=budget, temperature=tau, ridge=ridge, cov_mode=cov_mode,
-                     ridge_matrix=rm)
+                     ridge_matrix=rm,
+                     gqa_mode=jacap.GQA_PER_HEAD if gqa == "per_head" else jacap.GQA_POOLED,
+                     protect_last=protect_last)
     prob = jacap.prepare(case.q_win, case.k, case.v, case.seq_offsets, case.seq_lens, p)
     jacap.run_evict(prob, case.q_win, case.k, case.v, stream)
     flags = jacap.read_status(prob.ws, stream)
@@ -49,9 +52,11 @@ def token_slice(case, b):
     return lo, lo + int(case.seq_lens[b])
 
 
-def oracle_unit(case, b, l, h, budget, tau=10.0, ridge=1.0, cov_mode="diag"):
+def oracle_unit(case, b, l, h, budget, tau=10.0, ridge=1.0, cov_mode="diag", gqa="pooled",
+                protect_last=0):
     q, k, v = case.unit_arrays(b, l, h)
-    return jo.evict_unit(q, k, v, budget, tau=tau, ridge=ridge, cov_mode=cov_mode)
+    return jo.evict_unit(q, k, v, budget, tau=tau, ridge=ridge, cov_mode=cov_mode, gqa=gqa,
+                         protect_last=protect_last)
 
 
 def score_errors(gpu: np.ndarray, ref: np.ndarray) -> np.ndarray:

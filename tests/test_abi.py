@@ -43,7 +43,7 @@ def test_struct_layout_matches_header():
 int main(void) {
   printf("sizeof_config %zu\nsizeof_batch %zu\n", sizeof(jacap_config), sizeof(jacap_batch));
   F(jacap_config, temperature) F(jacap_config, ridge) F(jacap_config, dtype)
-  F(jacap_config, ridge_mode)
+  F(jacap_config, ridge_mode) F(jacap_config, gqa_mode) F(jacap_config, protect_last)
   F(jacap_batch, total_tokens) F(jacap_batch, seq_offsets) F(jacap_batch, k_stride_layer)
   F(jacap_batch, q_stride_pos) F(jacap_batch, out_stride_row) F(jacap_batch, ridge_mat)
   return 0;
@@ -58,7 +58,7 @@ int main(void) {
     assert int(out["sizeof_config"]) == ctypes.sizeof(jacap.Config)
     assert int(out["sizeof_batch"]) == ctypes.sizeof(jacap.Batch)
     for s, m in (("Config", "temperature"), ("Config", "ridge"), ("Config", "dtype"),
-                 ("Config", "ridge_mode"),
+                 ("Config", "ridge_mode"), ("Config", "gqa_mode"), ("Config", "protect_last"),
                  ("Batch", "total_tokens"), ("Batch", "seq_offsets"), ("Batch", "k_stride_layer"),
                  ("Batch", "q_stride_pos"), ("Batch", "out_stride_row"), ("Batch", "ridge_mat")):
         assert int(out[m]) == getattr(getattr(jacap, s), m).offset, m
@@ -106,6 +106,8 @@ def test_workspace_size_and_validation():
         (_cfg(temperature=float("nan")), jacap.ERR_INVALID_ARG),
         (_cfg(ridge=-1.0), jacap.ERR_INVALID_ARG),
         (_cfg(ridge_mode=2), jacap.ERR_UNSUPPORTED),
+        (_cfg(gqa_mode=2), jacap.ERR_UNSUPPORTED),
+        (_cfg(protect_last=-1), jacap.ERR_INVALID_ARG),
     ]
     for cfg, want in bad:
         assert _ws_size(cfg, _batch())[0] == want

@@ -34,18 +34,19 @@ def jacap():
 
 
 def check_case(case, budget, ridge, mode="diag", units=None, tau=10.0, label="", jacap=None,
-               ridge_matrices=None):
+               ridge_matrices=None, gqa="pooled", protect_last=0):
     units = unit_list(case) if units is None else units
     all_units = len(units) == len(unit_list(case))
     prob, flags = run_gpu(case, budget, tau=tau, ridge=ridge, cov_mode=COV[mode],
-                          ridge_matrices=ridge_matrices)
+                          ridge_matrices=ridge_matrices, gqa=gqa, protect_last=protect_last)
     # SINGULAR is legitimate only at ridge 0 (rank-deficient weighted Gram)
     assert flags & ~(2 if ridge == 0.0 else 0) == 0, f"status flags {flags}"
     tol = tol_for(case)
     ref32 = torch.zeros_like(prob.scores, device="cpu")
     worst, overlaps, orc, illcond = 0.0, [], {}, []
     for (b, l, h) in units:
-        o = oracle_unit(case, b, l, h, budget, tau=tau, cov_mode=mode,
+        o = oracle_unit(case, b, l, h, budget, tau=tau, cov_mode=mode, gqa=gqa,
+                        protect_last=protect_last,
                         ridge=ridge if ridge_matrices is None else ridge_matrices[l, h])
         orc[(b, l, h)] = o
         g = gpu_unit_scores(case, prob, b, l, h)
@@ -62,8 +63,11 @@ def check_case(case, budget, ridge, mode="diag", units=None, tau=10.0, label="",
             # Error model of fp32 accumulation: the stated tolerance holds while
             # cond(A) <= COND_REF; beyond it the bound grows like cond(A) (the
             # Gram's and L^-1 v's rounding is amplified by the conditioning).
-            ev = np.linalg.eigvalsh(o["A"])
-            cond = np.inf if ev[0] <= 0 else ev[-1] / ev[0]
+            # Per-head GQA: the worst head's A.
+            cond = 0.0
+            for hd in o.get("heads", [o]):
+                ev = np.linalg.eigvalsh(hd["A"])
+                cond = max(cond, np.inf if ev[0] <= 0 else ev[-1] / ev[0])
             cref = COND_REF[case.workload.dtype]
             unit_tol = tol * max(1.0, cond / cref)
             if cond > cref:
@@ -72,7 +76,8 @@ def check_case(case, budget, ridge, mode="diag", units=None, tau=10.0, label="",
                 worst = max(worst, float(err.max()))
             assert err.max() <= unit_tol, (label, (b, l, h), float(err.max()), cond, int(err.argmax()))
         idx = gpu_unit_idx(case, prob, b, l, h, budget)
-        assert np.array_equal(idx, jo.select_top(g.astype(np.float32), budget)), (label, (b, l, h))
+        assert np.array_equal(idx, jo.select_top(g.astype(np.float32), budget, protect_last)), \
+            (label, (b, l, h))
         overlaps.append(overlap(idx, o["idx"]) if len(o["idx"]) else 1.0)
         lo, hi = token_slice(case, b)
         kk = len(idx)
@@ -328,3 +333,29 @@ def test_wo_variant_ragged(jacap, dtype, d):
     R = wo_ridge_matrices(case)
     check_case(case, 64, 1.0, "diag", label=f"ragged W_O {dtype} d{d}", jacap=jacap,
                ridge_matrices=R)
+
+
+# ---------------------------------------------------------------------------
+# Per-query-head GQA scoring and the protected tail
+# ---------------------------------------------------------------------------
+
+def test_per_head_gqa_llama_layer_bf16(jacap):
+    case = make_case("llama8b_layer", seq_lens=[4096], device="cuda")
+    check_case(case, 512, 1.0, "diag", label="llama_layer per-head GQA", jacap=jacap,
+               gqa="per_head")
+
+
+@pytest.mark.parametrize("dtype,d,mode", [("bf16", 128, "diag"), ("fp32", 64, "full")])
+def test_per_head_gqa_ragged(jacap, dtype, d, mode):
+    case = make_case("ragged16", seq_lens=[0, 1, 17, 300, 1000, 4100], num_layers=2,
+                     num_kv_heads=2, num_q_heads=4, window=8, head_dim=d, dtype=dtype).to("cuda")
+    check_case(case, 64, 1.0, mode, label=f"ragged per-head {dtype} d{d}", jacap=jacap,
+               gqa="per_head")
+
+
+@pytest.mark.parametrize("protect", [0, 7, 64, 100])
+def test_protect_last_evict(jacap, protect):
+    case = make_case("ragged16", seq_lens=[0, 5, 64, 300, 9000], num_layers=1, num_kv_heads=2,
+                     num_q_heads=2, window=8, head_dim=64, dtype="bf16").to("cuda")
+    check_case(case, 64, 1.0, "diag", label=f"protect_last {protect}", jacap=jacap,
+               protect_last=protect)

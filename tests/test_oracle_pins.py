@@ -495,3 +495,64 @@ def test_ridge_matrix_lambda_identity_equals_scalar_ridge():
         a = jo.score_unit(q, k, v, ridge=lam)["scores"]
         b = jo.score_unit(q, k, v, ridge=lam * np.eye(64))["scores"]
         np.testing.assert_allclose(b, a, rtol=1e-12, atol=0)
+
+
+# ---------------------------------------------------------------------------
+# Per-query-head GQA and the protected tail
+# ---------------------------------------------------------------------------
+
+def test_per_head_with_one_head_equals_pooled():
+    case = make_case("tiny", seq_lens=[80])
+    q, k, v = case.unit_arrays(0, 0, 0)
+    a = jo.score_unit(q, k, v, ridge=0.5)["scores"]
+    b = jo.score_unit_per_head(q, k, v, ridge=0.5)["scores"]
+    np.testing.assert_array_equal(a, b)
+
+
+@pytest.mark.parametrize("mode", [jo.DIAG, jo.FULL])
+def test_per_head_identical_heads_equals_pooled(mode):
+    """G copies of one head's window give the pooled sample the same mean and
+    1/N covariance as the single head, so both readings coincide; a wrong
+    normalisation of the pooled statistics (e.g. 1/(N-1)) breaks this."""
+    rng = np.random.default_rng(5)
+    d, w, n, G = 8, 6, 40, 3
+    q1 = rng.normal(size=(1, w, d)) + rng.normal(size=d)
+    qG = np.repeat(q1, G, axis=0)
+    K = rng.normal(size=(n, d)) * 2
+    V = rng.normal(size=(n, d))
+    a = jo.score_unit(qG, K, V, tau=1.0, ridge=0.1, cov_mode=mode)["scores"]
+    b = jo.score_unit_per_head(qG, K, V, tau=1.0, ridge=0.1, cov_mode=mode)["scores"]
+    np.testing.assert_allclose(b, a, rtol=1e-12, atol=0)
+
+
+def test_per_head_is_mean_of_single_head_scores():
+    rng = np.random.default_rng(6)
+    d, w, n, G = 8, 5, 30, 4
+    q = rng.normal(size=(G, w, d)) + rng.normal(size=d)
+    K, V = rng.normal(size=(n, d)), rng.normal(size=(n, d))
+    got = jo.score_unit_per_head(q, K, V, tau=1.0)["scores"]
+    each = [jo.score_unit(q[g][None], K, V, tau=1.0)["scores"] for g in range(G)]
+    np.testing.assert_allclose(got, np.mean(each, axis=0), rtol=1e-13, atol=0)
+
+
+@pytest.mark.parametrize("n,budget,p", [(30, 10, 0), (30, 10, 4), (30, 10, 10), (30, 10, 25),
+                                        (30, 40, 5), (12, 12, 3), (1, 1, 1)])
+def test_protect_last_against_definition(n, budget, p):
+    """Kept set = the last min(P, B, n) positions, plus the best of the earlier
+    positions by (score desc, index asc) up to min(B, n) in total."""
+    rng = np.random.default_rng(n * 100 + budget + p)
+    s = rng.integers(0, 4, n).astype(np.float32)
+    s[rng.random(n) < 0.2] = np.nan
+    got = jo.select_top(s, budget, protect_last=p)
+    b = min(budget, n)
+    tail = min(p, b)
+    keep = set(range(n - tail, n))
+    def better(i, j):  # i ranks before j
+        ki = -np.inf if np.isnan(s[i]) else s[i]
+        kj = -np.inf if np.isnan(s[j]) else s[j]
+        return ki > kj or (ki == kj and (i < j))
+    head = [i for i in range(n - tail)]
+    ranked = [i for i in head if sum(better(j, i) for j in head) < b - tail]
+    keep |= set(ranked)
+    assert list(got) == sorted(keep)
+    assert len(got) == b
