@@ -84,6 +84,16 @@ WORKLOADS = {
         num_q_heads=32, head_dim=128, window=32, budget_k=256, dtype="bf16",
         ragged=(16, 4096, 32768), n_heavy=32,
         k_outlier=("uniform", 2.0, 10.0)),
+    # Decoding-stage eviction: a cache holding the reserved budget plus one
+    # re-eviction interval of 128 new tokens, 16 sequences.
+    "decode2k": Workload(
+        name="decode2k", wid=5, num_layers=32, num_kv_heads=8,
+        num_q_heads=32, head_dim=128, window=64, budget_k=2048, dtype="bf16",
+        seq_lens=(2048 + 128,) * 16, n_heavy=32, k_outlier=("uniform", 2.0, 10.0)),
+    "decode16k": Workload(
+        name="decode16k", wid=6, num_layers=32, num_kv_heads=8,
+        num_q_heads=32, head_dim=128, window=64, budget_k=16384, dtype="bf16",
+        seq_lens=(16384 + 128,) * 16, n_heavy=32, k_outlier=("uniform", 2.0, 10.0)),
 }
 BY_ID = {w.wid: w for w in WORKLOADS.values()}
 

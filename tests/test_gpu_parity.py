@@ -359,3 +359,52 @@ def test_protect_last_evict(jacap, protect):
                      num_q_heads=2, window=8, head_dim=64, dtype="bf16").to("cuda")
     check_case(case, 64, 1.0, "diag", label=f"protect_last {protect}", jacap=jacap,
                protect_last=protect)
+
+
+# ---------------------------------------------------------------------------
+# Decoding-stage eviction: evict -> append new tokens -> evict, several rounds
+# ---------------------------------------------------------------------------
+
+def test_decode_rounds_follow_the_oracle_chain(jacap):
+    """A cache of R reserved + D new tokens per sequence is evicted back to R
+    each round; the retained rows plus the next D tokens (and a new window)
+    form the next round's cache. The GPU chain and the oracle's own chain must
+    keep the same positions in every round (the caches then stay identical)."""
+    R, D, B, rounds = 256, 32, 2, 3
+    spec = dict(num_layers=1, num_kv_heads=2, num_q_heads=4, window=8, head_dim=64, dtype="bf16")
+    L, H = spec["num_layers"], spec["num_kv_heads"]
+    first = make_case("ragged16", seq_lens=[R + D] * B, **spec)
+    k_cache, v_cache = first.k.clone(), first.v.clone()        # CPU tensors, packed
+    ok = {(b, l, h): (first.unit_arrays(b, l, h)[1], first.unit_arrays(b, l, h)[2])
+          for b in range(B) for l in range(L) for h in range(H)}
+    q_win = first.q_win
+    offsets = torch.tensor([i * (R + D) for i in range(B + 1)], dtype=torch.int32)
+    for r in range(rounds):
+        print(f"[decode] round {r}", flush=True)
+        p = jacap.Params(budget_k=R)
+        kc, vc, qc = k_cache.cuda(), v_cache.cuda(), q_win.cuda()
+        prob = jacap.prepare(qc, kc, vc, offsets.cuda(), [R + D] * B, p)
+        jacap.run_evict(prob, qc, kc, vc)
+        assert jacap.read_status(prob.ws) == 0
+        torch.cuda.synchronize()
+        nxt = make_case("ragged16", seq_lens=[D] * B, root=260908131 + 1000 + r, **spec)
+        new_k, new_v = [], []
+        for b in range(B):
+            for l in range(L):
+                for h in range(H):
+                    qa = q_win[b, l, h * 2:(h + 1) * 2].to(torch.float64).numpy()
+                    kk, vv = ok[(b, l, h)]
+                    o = jo.evict_unit(qa, kk, vv, R)
+                    got = prob.idx[b, l, h].cpu().numpy()
+                    assert np.array_equal(got, o["idx"]), (r, b, l, h)
+                    _, nk, nv = nxt.unit_arrays(b, l, h)
+                    ok[(b, l, h)] = (np.concatenate([o["k_out"], nk]), np.concatenate([o["v_out"], nv]))
+            new_k.append(torch.cat([prob.k_out[b].cpu(), nxt.k[:, :, b * D:(b + 1) * D]], dim=2))
+            new_v.append(torch.cat([prob.v_out[b].cpu(), nxt.v[:, :, b * D:(b + 1) * D]], dim=2))
+        k_cache = torch.cat(new_k, dim=2).contiguous()
+        v_cache = torch.cat(new_v, dim=2).contiguous()
+        q_win = nxt.q_win
+        # the GPU cache and the oracle cache hold the same rows
+        for (b, l, h), (kk, vv) in ok.items():
+            lo = b * (R + D)
+            np.testing.assert_array_equal(k_cache[l, h, lo:lo + R + D].to(torch.float64).numpy(), kk)
