@@ -262,3 +262,85 @@ def evict_unit(q_group, K, V, budget: int, gqa: str = "pooled", protect_last: in
     Kc, Vc = compact(np.asarray(K), np.asarray(V), idx)
     out.update(scores32=s32, idx=idx, k_out=Kc, v_out=Vc)
     return out
+
+
+# ---------------------------------------------------------------------------
+# Exact greedy log-det selection (a quality comparator for the TOP-B ranking)
+# ---------------------------------------------------------------------------
+
+def greedy_logdet(U: np.ndarray, w: np.ndarray, ridge: float, budget: int,
+                  protect_last: int = 0) -> np.ndarray:
+    """Sequential greedy maximisation of log det(ridge I + sum_{i in C} w_i u_i u_i^T)
+    (App. B.1: the capacity objective Jacap's one-shot scores approximate),
+    with the full-pool Eq. 8 weights. Step t adds the token with the largest
+    gain w_i c_i, c_i = u_i^T A_C^{-1} u_i (its log-det increase is
+    log(1 + w_i c_i)); ties go to the lowest index.
+    A_C^{-1} = I / ridge - sum_t g_t g_t^T, g_t = A^{-1} u_s sqrt(w_s / (1 + w_s c_s))
+    (Sherman-Morrison), so c_i <- c_i - (u_i . g_t)^2.
+    protect_last = P: the last min(P, budget, n) positions are added first, in
+    position order, and the search covers the earlier ones.
+    Returns the chosen indices in the order they were added. Requires ridge > 0."""
+    U = np.asarray(U, dtype=np.float64)
+    w = np.asarray(w, dtype=np.float64)
+    n, d = U.shape
+    k = max(0, min(int(budget), n))
+    p = min(max(int(protect_last), 0), k)
+    nfree = n - p
+    c = (U * U).sum(axis=1) / ridge
+    taken = np.zeros(n, dtype=bool)
+    taken[nfree:] = True            # protected: never candidates of the search
+    G = np.zeros((0, d))
+    order = []
+    for t in range(k):
+        if t < p:
+            s = nfree + t
+        else:
+            gain = np.where(taken, -np.inf, w * c)
+            s = int(np.argmax(gain))             # first maximum: lowest index
+        us = U[s]
+        h = us / ridge - G.T @ (G @ us)
+        g = h * math.sqrt(w[s] / (1.0 + w[s] * c[s]))
+        taken[s] = True
+        order.append(s)
+        c = c - (U @ g) ** 2
+        G = np.vstack([G, g])
+    return np.asarray(order, dtype=np.int64)
+
+
+def greedy_replay(U: np.ndarray, w: np.ndarray, ridge: float, order, protect_last: int = 0):
+    """Follow a given pick order and report, per step, the gain w_s c_s of the
+    token it took and the best gain available then (over the untaken
+    positions before the protected tail; protected steps report their own
+    gain for both). An order is a valid greedy path when every chosen gain
+    equals the best one. Same Sherman-Morrison bookkeeping as greedy_logdet."""
+    U = np.asarray(U, dtype=np.float64)
+    w = np.asarray(w, dtype=np.float64)
+    n, d = U.shape
+    order = [int(s) for s in order]
+    p = min(max(int(protect_last), 0), len(order))
+    nfree = n - p
+    c = (U * U).sum(axis=1) / ridge
+    taken = np.zeros(n, dtype=bool)
+    taken[nfree:] = True
+    G = np.zeros((0, d))
+    chosen, best = [], []
+    for t, s in enumerate(order):
+        gain = w * c
+        chosen.append(gain[s])
+        best.append(gain[s] if t < p else np.where(taken, -np.inf, gain).max())
+        us = U[s]
+        h = us / ridge - G.T @ (G @ us)
+        g = h * math.sqrt(w[s] / (1.0 + w[s] * c[s]))
+        taken[s] = True
+        c = c - (U @ g) ** 2
+        G = np.vstack([G, g])
+    return np.asarray(chosen), np.asarray(best)
+
+
+def logdet_objective(U: np.ndarray, w: np.ndarray, ridge: float, C) -> float:
+    """log det(ridge I + sum_{i in C} w_i u_i u_i^T)."""
+    U = np.asarray(U, dtype=np.float64)
+    C = np.asarray(list(C), dtype=np.int64)
+    A = ridge * np.eye(U.shape[1]) + U[C].T @ (np.asarray(w)[C, None] * U[C])
+    sign, val = np.linalg.slogdet(A)
+    return float(val) if sign > 0 else -math.inf

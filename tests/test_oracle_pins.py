@@ -556,3 +556,79 @@ def test_protect_last_against_definition(n, budget, p):
     keep |= set(ranked)
     assert list(got) == sorted(keep)
     assert len(got) == b
+
+
+# ---------------------------------------------------------------------------
+# Exact greedy log-det selection
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("seed", range(4))
+def test_greedy_logdet_matches_brute_force_greedy(seed):
+    """The rank-one-update greedy equals the plain greedy that re-evaluates
+    log det for every candidate set (slogdet) at every step."""
+    rng = np.random.default_rng(300 + seed)
+    n, d, k, ridge = 11, 4, 6, 0.3
+    U = rng.normal(size=(n, d))
+    w = rng.uniform(0.1, 2.0, n)
+    got = jo.greedy_logdet(U, w, ridge, k)
+    obj = lambda C: jo.logdet_objective(U, w, ridge, C)
+    want = theory.greedy(obj, n, k)
+    assert sorted(got.tolist()) == want
+    # every step's choice is the best marginal gain given the earlier picks
+    for t in range(k):
+        base = obj(got[:t])
+        gains = [obj(list(got[:t]) + [i]) - base if i not in got[:t] else -np.inf for i in range(n)]
+        assert got[t] == int(np.argmax(gains))
+
+
+def test_greedy_first_pick_and_orthogonal_case():
+    """First pick = argmax w_i ||u_i||^2; with orthogonal u_i the gains never
+    interact, so greedy = TOP-B by w_i ||u_i||^2 (= Jacap's ranking, P7)."""
+    rng = np.random.default_rng(9)
+    d = 7
+    U = np.eye(d) * rng.uniform(0.5, 2.0, d)[:, None]
+    w = rng.uniform(0.1, 1.0, d)
+    order = jo.greedy_logdet(U, w, 1.0, 4)
+    x = w * (U * U).sum(axis=1)
+    assert order[0] == int(np.argmax(x))
+    assert sorted(order.tolist()) == sorted(np.argsort(-x)[:4].tolist())
+
+
+@pytest.mark.parametrize("protect", [1, 3])
+def test_greedy_protected_tail_is_forced_then_greedy(protect):
+    """With a protected tail: the tail first, then the plain greedy (brute
+    force over slogdet) over the earlier positions from that starting set."""
+    rng = np.random.default_rng(40 + protect)
+    n, d, k, ridge = 10, 3, 6, 0.5
+    U = rng.normal(size=(n, d))
+    w = rng.uniform(0.1, 2.0, n)
+    got = jo.greedy_logdet(U, w, ridge, k, protect_last=protect)
+    assert got[:protect].tolist() == list(range(n - protect, n))
+    C = list(range(n - protect, n))
+    for _ in range(k - protect):
+        base = jo.logdet_objective(U, w, ridge, C)
+        gains = [jo.logdet_objective(U, w, ridge, C + [i]) - base if i not in C and i < n - protect
+                 else -np.inf for i in range(n)]
+        C.append(int(np.argmax(gains)))
+    assert got.tolist() == C
+
+
+def test_greedy_replay_and_determinant_lemma():
+    """Replay of the greedy order: every chosen gain is the best one, and
+    d log(ridge) + sum log(1 + gain_t) is the log det of the chosen set (matrix
+    determinant lemma); a non-greedy order is caught by the replay."""
+    rng = np.random.default_rng(77)
+    n, d, k, ridge = 40, 5, 12, 0.25
+    U = rng.normal(size=(n, d))
+    w = rng.uniform(0.05, 1.5, n)
+    order = jo.greedy_logdet(U, w, ridge, k)
+    chosen, best = jo.greedy_replay(U, w, ridge, order)
+    np.testing.assert_allclose(chosen, best, rtol=1e-12)
+    total = d * np.log(ridge) + np.log1p(chosen).sum()
+    assert abs(total - jo.logdet_objective(U, w, ridge, order)) < 1e-10
+    # swap the step-3 pick for the runner-up: the replay must flag that step
+    bad = list(order)
+    alt = [i for i in np.argsort(-w * (U * U).sum(1)) if i not in bad[:3]][1]
+    bad[3] = int(alt) if alt != order[3] else int([i for i in range(n) if i not in bad[:4]][0])
+    ch2, be2 = jo.greedy_replay(U, w, ridge, bad[:4])
+    assert ch2[3] < be2[3]
