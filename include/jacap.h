@@ -201,6 +201,40 @@ jacap_status jacap_evict(const jacap_config* cfg, const jacap_batch* batch,
                          int32_t* idx, void* k_out, void* v_out, void* ws, size_t ws_bytes,
                          void* stream);
 
+/* ------------------------------------------------------------------------
+ * Exact greedy log-det selection (App. B.1): the sequential selection that
+ * the one-shot leverage score of Eq. 10 approximates, for comparing the
+ * quality of TOP-B. With the same Eq. 8 weights w_i and u_i = v_i, for each
+ * unit, B = min(budget_k, n_b) times: add the token with the largest gain
+ * w_i u_i^T A_C^{-1} u_i, A_C = ridge I + sum_{j in C} w_j u_j u_j^T (its
+ * log-det increase is log(1 + gain)), ties to the lower position. C starts
+ * empty; with cfg->protect_last = P > 0 it starts with the last min(P, B)
+ * positions (taken first, in position order) and the search covers the rest.
+ *
+ * Outputs (device pointers):
+ *   idx    : int32 [B][L][H_kv][budget_k], the chosen positions ascending,
+ *            -1 padding (the jacap_select layout; jacap_compact accepts it).
+ *   order  : optional (NULL = not written) int32 [B][L][H_kv][budget_k], the
+ *            positions in the order they were added, -1 padding.
+ *   logdet : optional (NULL = not written) double [B][L][H_kv], the objective
+ *            log det(ridge I + sum_{i in C} w_i u_i u_i^T) of the chosen set,
+ *            accumulated as d log(ridge) + sum_t log(1 + gain_t).
+ *
+ * Requirements beyond jacap_score's: cfg->ridge_mode = JACAP_RIDGE_SCALAR
+ * with ridge > 0 (JACAP_ERR_INVALID_ARG for ridge 0: A_0 would be singular),
+ * pooled GQA (cfg->gqa_mode = JACAP_GQA_PER_HEAD with H_q > H_kv and the
+ * matrix ridge give JACAP_ERR_UNSUPPORTED), max_seq_len <= 524288
+ * (JACAP_ERR_UNSUPPORTED), and a workspace of jacap_greedy_workspace_size()
+ * bytes (256-byte aligned). Runs the weight steps of jacap_score (status
+ * flags reset first), then one workgroup per unit; the work is sequential in
+ * the picks, so it takes far longer than jacap_evict. Deterministic. */
+jacap_status jacap_greedy_workspace_size(const jacap_config* cfg, const jacap_batch* batch,
+                                         size_t* bytes);
+
+jacap_status jacap_greedy(const jacap_config* cfg, const jacap_batch* batch, const void* q_win,
+                          const void* k, const void* v, int32_t* idx, int32_t* order,
+                          double* logdet, void* ws, size_t ws_bytes, void* stream);
+
 /* Synchronises `stream` and returns the sticky device flags (enum
  * jacap_flags, OR-ed) written by the last jacap_score / jacap_evict that used
  * this workspace. */
@@ -214,7 +248,7 @@ const char* jacap_status_string(jacap_status s);
  * is needed to use the entry points above).
  *
  * While timing is on, every jacap_score / jacap_select / jacap_compact /
- * jacap_evict call records a HIP event before and after each phase whose bit
+ * jacap_evict / jacap_greedy call records a HIP event before and after each phase whose bit
  * (1u << phase) is set in the mask, on the stream the phase's kernels are
  * launched on; the elapsed time between the two events is that phase's GPU
  * duration. Events are created on the device that is current when the call
@@ -233,7 +267,9 @@ enum jacap_phase {
   JACAP_PHASE_LEVERAGE = 8,    /* leverage scores (Eq. 10) */
   JACAP_PHASE_SELECT = 9,      /* TOP-B selection */
   JACAP_PHASE_COMPACT = 10,    /* K/V compaction */
-  JACAP_NUM_PHASES = 11
+  JACAP_PHASE_GREEDY_INIT = 11, /* greedy selection: initial c_i and block maxima */
+  JACAP_PHASE_GREEDY = 12,     /* greedy selection: the sequential picks */
+  JACAP_NUM_PHASES = 13
 };
 
 /* Clears the accumulated times and starts recording the phases in
@@ -247,7 +283,7 @@ jacap_status jacap_timing_start(uint32_t phase_mask);
  * are cleared. Returns JACAP_ERR_HIP if an event query failed. */
 jacap_status jacap_timing_stop(double* ms, int32_t* calls);
 
-/* Static name of a phase ("gram", "leverage", ...), or "unknown". */
+/* Static name of a phase ("gram", "leverage", "greedy", ...), or "unknown". */
 const char* jacap_phase_name(int32_t phase);
 
 #ifdef __cplusplus

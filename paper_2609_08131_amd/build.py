@@ -31,7 +31,7 @@ CFLAGS = [
 ]
 
 SOURCES = ["jacap_host.hip", "jacap_timing.hip", "k_stats.hip", "k_gram.hip", "k_factor.hip",
-           "k_leverage.hip", "k_select.hip"]
+           "k_leverage.hip", "k_select.hip", "k_greedy.hip"]
 
 
 def _compile(src: str, verbose: bool) -> str:

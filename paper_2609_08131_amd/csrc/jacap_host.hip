@@ -50,7 +50,9 @@ jacap_status check_batch(const jacap_config* c, const jacap_batch* b) {
   return JACAP_OK;
 }
 
-Workspace layout(const jacap_config* c, const jacap_batch* b) {
+// Workspace of jacap_score / _select / _evict, or (greedy) of jacap_greedy,
+// which needs the weight buffers but none of the Gram / factor storage.
+Workspace layout(const jacap_config* c, const jacap_batch* b, bool greedy = false) {
   Workspace w{};
   const int64_t U = (int64_t)b->num_seqs * c->num_layers * c->num_kv_heads;
   const int64_t D = c->head_dim;
@@ -82,6 +84,14 @@ Workspace layout(const jacap_config* c, const jacap_batch* b) {
   w.cstat = take(8 * U * (int64_t)w.kchunks);
   w.wgt = take(4 * LHT);
   const bool per_head = c->gqa_mode == JACAP_GQA_PER_HEAD && c->num_q_heads > c->num_kv_heads;
+  if (greedy) {
+    const int64_t nblk = (maxn + 255) / 256;
+    w.gc = take(8 * LHT);
+    w.gst = take(4 * LHT);
+    w.gent = take(sizeof(GreedyEntry) * U * nblk);
+    w.total = o;
+    return w;
+  }
   w.hscore = take(per_head ? 4 * LHT : 4);
   w.gram = take((size_t)(U * (int64_t)w.gchunks * part_bytes));
   w.gram_red = take(8 * U * npair * 256);
@@ -112,15 +122,28 @@ Geo make_geo(const jacap_config* c, const jacap_batch* b) {
   return g;
 }
 
+// Extra conditions of jacap_greedy (after check_config / check_batch).
+jacap_status check_greedy(const jacap_config* c, const jacap_batch* b) {
+  if (c->ridge_mode != JACAP_RIDGE_SCALAR) return JACAP_ERR_UNSUPPORTED;
+  if (!(c->ridge > 0.0f)) return JACAP_ERR_INVALID_ARG;
+  if (c->gqa_mode == JACAP_GQA_PER_HEAD && c->num_q_heads > c->num_kv_heads) return JACAP_ERR_UNSUPPORTED;
+  if (b->max_seq_len > kGreedyMaxLen) return JACAP_ERR_UNSUPPORTED;
+  return JACAP_OK;
+}
+
 jacap_status prepare(const jacap_config* c, const jacap_batch* b, void* ws, size_t ws_bytes,
-                     void* stream, Launch* L) {
+                     void* stream, Launch* L, bool greedy = false) {
   jacap_status s = check_config(c);
   if (s != JACAP_OK) return s;
   s = check_batch(c, b);
   if (s != JACAP_OK) return s;
+  if (greedy) {
+    s = check_greedy(c, b);
+    if (s != JACAP_OK) return s;
+  }
   L->cfg = c;
   L->geo = make_geo(c, b);
-  L->ws = layout(c, b);
+  L->ws = layout(c, b, greedy);
   L->wsp = static_cast<char*>(ws);
   L->stream = static_cast<hipStream_t>(stream);
   if (ws != nullptr || ws_bytes != 0) {
@@ -264,6 +287,42 @@ jacap_status jacap_evict(const jacap_config* cfg, const jacap_batch* batch, cons
   if (cfg->budget_k == 0) return JACAP_OK;
   JACAP_PHASE(JACAP_PHASE_SELECT, launch_select(L, scores, idx));
   JACAP_PHASE(JACAP_PHASE_COMPACT, launch_compact(L, idx, k, v, k_out, v_out));
+  return JACAP_OK;
+}
+
+jacap_status jacap_greedy_workspace_size(const jacap_config* cfg, const jacap_batch* batch,
+                                         size_t* bytes) {
+  if (!bytes) return JACAP_ERR_INVALID_ARG;
+  jacap_status s = check_config(cfg);
+  if (s != JACAP_OK) return s;
+  s = check_batch(cfg, batch);
+  if (s != JACAP_OK) return s;
+  s = check_greedy(cfg, batch);
+  if (s != JACAP_OK) return s;
+  *bytes = layout(cfg, batch, true).total;
+  return JACAP_OK;
+}
+
+jacap_status jacap_greedy(const jacap_config* cfg, const jacap_batch* batch, const void* q_win,
+                          const void* k, const void* v, int32_t* idx, int32_t* order,
+                          double* logdet, void* ws, size_t ws_bytes, void* stream) {
+  Launch L;
+  if (!ws) return JACAP_ERR_INVALID_ARG;
+  jacap_status s = prepare(cfg, batch, ws, ws_bytes, stream, &L, true);
+  if (s != JACAP_OK) return s;
+  if (!q_win || !k || !v || !aligned16(q_win) || !aligned16(k) || !aligned16(v))
+    return JACAP_ERR_INVALID_ARG;
+  if (cfg->budget_k > 0 && (!idx || !aligned16(idx))) return JACAP_ERR_INVALID_ARG;
+  if (order && !aligned16(order)) return JACAP_ERR_INVALID_ARG;
+  if (logdet && (reinterpret_cast<uintptr_t>(logdet) & 7u)) return JACAP_ERR_INVALID_ARG;
+  JACAP_PHASE(JACAP_PHASE_INIT, launch_init(L));
+  if (batch->total_tokens > 0) {
+    JACAP_PHASE(JACAP_PHASE_QSTATS, launch_qstats(L, q_win));
+    JACAP_PHASE(JACAP_PHASE_KPASS, launch_kpass(L, k));
+    JACAP_PHASE(JACAP_PHASE_WEIGHTS, launch_softmax_weights(L));
+  }
+  if (cfg->budget_k == 0 && !logdet) return JACAP_OK;
+  JACAP_TRY(launch_greedy(L, v, idx, order, logdet));
   return JACAP_OK;
 }
 

@@ -19,6 +19,8 @@ constexpr int kGChunkPrecise = 1024; // tokens per workgroup in the fp64 Gram pa
 constexpr int kLChunkMfma = 4096;    // tokens per workgroup in the MFMA leverage pass
 constexpr int kLChunkPrecise = 1024; // tokens per workgroup in the fp64 leverage pass
 constexpr int kWChunk = 4096;        // tokens per workgroup in the weight pass
+constexpr int kGreedyMaxLen = 524288; // longest sequence the greedy selection takes
+constexpr int kGreedyMaxD = 128;
 
 // Unit flags (per (seq, layer, kv head)); the public flags are the OR of all.
 constexpr uint32_t kUnitNonfinite = JACAP_FLAG_NONFINITE;
@@ -93,9 +95,20 @@ struct Workspace {
   size_t gram_red; // double [U][NPAIR*256]  reduced Gram, block-lane layout
   size_t linv64;   // double [U][D][D]       L^{-1} (lower, zeros above), fp32-input path
   size_t lfrag;    // bf16 [U][NLP][2][64][8] L^{-1} hi/lo MFMA B fragments, bf16 path
+  size_t gc;       // double [L][H][T]       greedy: c_i when last computed
+  size_t gst;      // int32  [L][H][T]       greedy: picks made at that time (-1 = taken)
+  size_t gent;     // GreedyEntry [U][ceil(maxn / 256)]  greedy: best of each 256-position block
   size_t total;
   int kchunks, wchunks, gchunks, gchunk, gparts, lchunks;
   bool mfma;       // bf16 path (MFMA Gram and leverage)
+};
+
+// Best token of one 256-position block in the greedy log-det search.
+struct GreedyEntry {
+  double key;     // w_i c_i (-inf: no candidate left in the block)
+  double c;       // c_i = u_i^T A^{-1} u_i as last computed
+  int32_t pos;    // position in the sequence (INT32_MAX: none)
+  int32_t stamp;  // number of picks when c_i was computed
 };
 
 // ---------------------------------------------------------------------------
@@ -246,6 +259,8 @@ hipError_t launch_leverage(const Launch& L, const void* v, float* scores);
 hipError_t launch_select(const Launch& L, const float* scores, int32_t* idx);
 hipError_t launch_compact(const Launch& L, const int32_t* idx, const void* k, const void* v,
                           void* ko, void* vo);
+hipError_t launch_greedy(const Launch& L, const void* v, int32_t* idx, int32_t* order,
+                         double* logdet);
 
 template <typename T>
 __host__ __device__ __forceinline__ T* ws_ptr(char* base, size_t off) {

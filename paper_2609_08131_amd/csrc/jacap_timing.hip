@@ -97,7 +97,8 @@ jacap_status jacap_timing_stop(double* ms, int32_t* calls) {
 const char* jacap_phase_name(int32_t phase) {
   static const char* names[JACAP_NUM_PHASES] = {"init", "qstats", "kpass", "weights", "gram",
                                                  "gram_reduce", "factor", "refine", "leverage",
-                                                 "select", "compact"};
+                                                 "select", "compact", "greedy_init",
+                                                 "greedy"};
   if (phase < 0 || phase >= JACAP_NUM_PHASES) return "unknown";
   return names[phase];
 }

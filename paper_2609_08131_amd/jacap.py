@@ -90,6 +90,8 @@ def _load() -> ctypes.CDLL:
         "jacap_compact": [C, B, P, P, P, P, P, P],
         "jacap_evict": [C, B, P, P, P, P, P, P, P, P, sz, P],
         "jacap_read_status": [P, P, ctypes.POINTER(ctypes.c_uint32)],
+        "jacap_greedy_workspace_size": [C, B, ctypes.POINTER(sz)],
+        "jacap_greedy": [C, B, P, P, P, P, P, P, P, sz, P],
     }
     for name, args in sigs.items():
         fn = getattr(lib, name)
@@ -109,8 +111,9 @@ def _load() -> ctypes.CDLL:
 _lib = _load()
 EXPORTED = ("jacap_workspace_size", "jacap_score", "jacap_select", "jacap_compact",
             "jacap_evict", "jacap_read_status", "jacap_status_string", "jacap_timing_start",
-            "jacap_timing_stop", "jacap_phase_name")
-NUM_PHASES = 11   # enum jacap_phase
+            "jacap_timing_stop", "jacap_phase_name", "jacap_greedy_workspace_size",
+            "jacap_greedy")
+NUM_PHASES = 13   # enum jacap_phase
 
 
 def status_string(code: int) -> str:
@@ -247,6 +250,20 @@ def evict(cfg, batch, q_win, k, v, scores, idx, k_out, v_out, ws, stream=None) -
         _ptr(idx), _ptr(k_out), _ptr(v_out), _ptr(ws), ws.numel(), _stream(stream)))
 
 
+def greedy_workspace_size(cfg: Config, batch: Batch) -> int:
+    n = ctypes.c_size_t(0)
+    _check("jacap_greedy_workspace_size", _lib.jacap_greedy_workspace_size(
+        ctypes.byref(cfg), ctypes.byref(batch), ctypes.byref(n)))
+    return int(n.value)
+
+
+def greedy(cfg, batch, q_win, k, v, idx, order, logdet, ws, stream=None) -> None:
+    _check("jacap_greedy", _lib.jacap_greedy(
+        ctypes.byref(cfg), ctypes.byref(batch), _ptr(q_win), _ptr(k), _ptr(v), _ptr(idx),
+        _ptr(order), _ptr(logdet), _ptr(ws), ws.numel() if ws is not None else 0,
+        _stream(stream)))
+
+
 def read_status(ws: torch.Tensor, stream=None) -> int:
     f = ctypes.c_uint32(0)
     _check("jacap_read_status", _lib.jacap_read_status(_ptr(ws), _stream(stream), ctypes.byref(f)))
@@ -290,6 +307,38 @@ def prepare(q_win, k, v, seq_offsets, seq_lens, params: Params) -> Problem:
 def run_evict(prob: Problem, q_win, k, v, stream=None) -> None:
     evict(prob.cfg, prob.batch, q_win, k, v, prob.scores, prob.idx, prob.k_out, prob.v_out,
           prob.ws, stream)
+
+
+@dataclasses.dataclass
+class GreedyProblem:
+    """Descriptors, outputs and workspace of jacap_greedy for one batch."""
+
+    cfg: Config
+    batch: Batch
+    idx: torch.Tensor       # int32 [B][L][H][budget], ascending, -1 padding
+    order: torch.Tensor     # int32 [B][L][H][budget], pick order, -1 padding
+    logdet: torch.Tensor    # float64 [B][L][H]
+    ws: torch.Tensor
+
+
+def prepare_greedy(q_win, k, v, seq_offsets, seq_lens, params: Params) -> GreedyProblem:
+    cfg = make_config(q_win, k, params)
+    B = len(seq_lens)
+    L, H, T, d = k.shape
+    dev = k.device
+    kb = max(int(params.budget_k), 0)
+    idx = torch.empty((B, L, H, max(kb, 1)), dtype=torch.int32, device=dev)[..., :kb]
+    order = torch.empty_like(idx)
+    logdet = torch.empty((B, L, H), dtype=torch.float64, device=dev)
+    batch = make_batch(seq_offsets, seq_lens, q_win, k, v)
+    nbytes = greedy_workspace_size(cfg, batch)
+    ws = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=dev)
+    assert ws.data_ptr() % 256 == 0
+    return GreedyProblem(cfg, batch, idx, order, logdet, ws)
+
+
+def run_greedy(prob: GreedyProblem, q_win, k, v, stream=None) -> None:
+    greedy(prob.cfg, prob.batch, q_win, k, v, prob.idx, prob.order, prob.logdet, prob.ws, stream)
 
 
 # ---------------------------------------------------------------------------

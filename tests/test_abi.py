@@ -158,3 +158,36 @@ def test_timing_api_host_side():
     assert lib.jacap_timing_start(1 << jacap.NUM_PHASES) == 1   # JACAP_ERR_INVALID_ARG
     jacap.timing_start(["gram", "leverage"])
     assert jacap.timing_stop() == {}
+
+
+def _greedy_ws_size(cfg, b):
+    n = ctypes.c_size_t(0)
+    return jacap._lib.jacap_greedy_workspace_size(ctypes.byref(cfg), ctypes.byref(b),
+                                                  ctypes.byref(n)), n.value
+
+
+def test_greedy_workspace_and_validation():
+    """jacap_greedy's extra conditions: scalar ridge > 0, pooled GQA, sequences
+    up to 524288 tokens; its workspace holds no Gram/factor storage."""
+    code, n = _greedy_ws_size(_cfg(), _batch())
+    assert code == jacap.OK and n > 0 and n % 256 == 0
+    code, big = _greedy_ws_size(_cfg(dtype=1), _batch(max_seq_len=524288, total_tokens=524288))
+    assert code == jacap.OK
+    assert _greedy_ws_size(_cfg(ridge=0.0), _batch())[0] == jacap.ERR_INVALID_ARG
+    assert _greedy_ws_size(_cfg(ridge_mode=1), _batch(ridge_mat=0x1008))[0] == jacap.ERR_UNSUPPORTED
+    assert _greedy_ws_size(_cfg(gqa_mode=1, num_q_heads=4), _batch())[0] == jacap.ERR_UNSUPPORTED
+    assert _greedy_ws_size(_cfg(gqa_mode=1), _batch())[0] == jacap.OK      # G = 1: same as pooled
+    assert _greedy_ws_size(_cfg(), _batch(max_seq_len=524289, total_tokens=524289))[0] \
+        == jacap.ERR_UNSUPPORTED
+    assert _greedy_ws_size(_cfg(head_dim=96), _batch())[0] == jacap.ERR_UNSUPPORTED
+    P = ctypes.c_void_p
+    good = P(0x100000)
+    cfg, b = _cfg(), _batch()
+    lib = jacap._lib
+    call = lambda *a: lib.jacap_greedy(ctypes.byref(cfg), ctypes.byref(b), *a)
+    assert call(good, good, good, good, None, None, None, n, None) == jacap.ERR_INVALID_ARG  # no ws
+    assert call(good, good, good, good, None, None, good, n - 256, None) == jacap.ERR_WORKSPACE
+    assert call(good, good, good, None, None, None, good, n, None) == jacap.ERR_INVALID_ARG  # no idx
+    assert call(good, good, good, good, P(0x100004), None, good, n, None) == jacap.ERR_INVALID_ARG
+    assert call(good, good, good, good, None, P(0x100004), good, n, None) == jacap.ERR_INVALID_ARG
+    assert call(None, good, good, good, None, None, good, n, None) == jacap.ERR_INVALID_ARG
