@@ -49,6 +49,9 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="time budget of the oracle CPU baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--mode", choices=("evict", "greedy"), default="evict",
+                    help="evict: the Jacap pass (the headline line); greedy: the exact "
+                         "greedy log-det selection (jacap_greedy), a quality comparator")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="first run a plain 1 GiB elementwise copy (torch.neg; the "
                          "reference kernel for scaling rocprofv3 FETCH_SIZE / WRITE_SIZE)")
@@ -62,6 +65,7 @@ PHASE_SOURCES = {
     "qstats": "k_stats.hip", "kpass": "k_stats.hip", "weights": "k_stats.hip",
     "gram": "k_gram.hip", "gram_reduce": "k_gram.hip", "factor": "k_factor.hip",
     "leverage": "k_leverage.hip", "select": "k_select.hip", "compact": "k_select.hip",
+    "greedy_init": "k_greedy.hip", "greedy": "k_greedy.hip",
 }
 
 
@@ -107,7 +111,18 @@ def phase_bytes(phase, case, budget, prob):
         "select": entries * 4 + units * budget * 4,         # scores in; idx out
         "compact": 2 * kept * d * e * 2,                    # K, V rows in and out
         "gram_reduce": None, "factor": units * npair * 256 * 8, "refine": None, "init": None,
+        "greedy_init": entries * (d * e + 4 + 12),          # V rows, w; c, stamp out
+        "greedy": None,
     }.get(phase)
+
+
+def greedy_flops(case, budget):
+    """Least fp64 work of the greedy picks: per pick, A^{-1} u (d^2 FMA) and the
+    rank-one downdate (d^2 FMA), 4 d^2 flops; refreshes of stale bounds add
+    2 d^2 each and are not counted."""
+    w = case.workload
+    picks = sum(min(budget, n) for n in case.seq_lens) * w.num_layers * w.num_kv_heads
+    return 4.0 * w.head_dim ** 2 * picks
 
 
 def ensure_built():
@@ -153,6 +168,63 @@ def cpu_baseline(case, budget, tau, ridge, seconds):
             "entries_per_s": entries_per_s}
 
 
+PEAK_FP64_TFLOPS = 78.6   # MI355X vector fp64
+
+
+def main_greedy(args):
+    """jacap_greedy on the workload: Eq. 8 weights, the initial pass and the
+    sequential greedy picks (one workgroup per unit)."""
+    from jacap_synth import make_case
+    from paper_2609_08131_amd import jacap
+
+    torch.cuda.set_device(0)
+    case = make_case(args.workload, device="cuda")
+    w = case.workload
+    budget = args.budget if args.budget is not None else w.budget_k
+    params = jacap.Params(budget_k=budget, temperature=args.tau, ridge=args.ridge)
+    prob = jacap.prepare_greedy(case.q_win, case.k, case.v, case.seq_offsets, case.seq_lens, params)
+    stream = torch.cuda.current_stream()
+    for _ in range(args.warmup):
+        jacap.run_greedy(prob, case.q_win, case.k, case.v, stream)
+    flags = jacap.read_status(prob.ws, stream)
+    torch.cuda.synchronize()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(args.steps)]
+    jacap.timing_start()
+    for s, e in ev:
+        s.record(stream)
+        jacap.run_greedy(prob, case.q_win, case.k, case.v, stream)
+        e.record(stream)
+    torch.cuda.synchronize()
+    per_phase = {k: ms / n for k, (ms, n) in jacap.timing_stop().items()}
+    times = np.array([s.elapsed_time(e) for s, e in ev])
+    ms = float(times.mean())
+    g_ms = per_phase["greedy"]
+    flops = greedy_flops(case, budget)
+    units = case.num_seqs * w.num_layers * w.num_kv_heads
+    # one workgroup per unit: at most min(units, 256) compute units are busy
+    peak = PEAK_FP64_TFLOPS * min(units, 256) / 256
+    achieved = flops / (g_ms * 1e-3) / 1e12
+    init_bytes = phase_bytes("greedy_init", case, budget, prob)
+    out = {
+        "metric": "cached tokens greedily selected/sec per GPU (exact greedy log-det comparator)",
+        "value": case.total_tokens / (ms * 1e-3), "unit": "tokens/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": w.dtype,
+        "data": "synthetic", "status_flags": flags,
+        "config": {"workload": w.name, "mode": "greedy", "num_seqs": case.num_seqs,
+                   "layers": w.num_layers, "kv_heads": w.num_kv_heads, "head_dim": w.head_dim,
+                   "tokens": case.total_tokens, "budget_k": budget, "ridge": args.ridge},
+        "roofline": {"bound": "alu", "achieved": achieved, "peak": peak, "unit": "TFLOP/s",
+                     "frac": achieved / peak, "traffic": None, "kernel": "greedy",
+                     "kernel_ms": g_ms, "flops_per_launch": flops,
+                     "note": "fp64 work of the picks only; sequential in the picks"},
+        "greedy_init_gbs": init_bytes / (per_phase["greedy_init"] * 1e-3) / 1e9,
+        "phases_ms": {k: round(v, 4) for k, v in per_phase.items()},
+    }
+    print(json.dumps(out), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -160,6 +232,8 @@ def main():
                           "n_gpus": args.gpus}))
         sys.exit(2)
     ensure_built()
+    if args.mode == "greedy":
+        return main_greedy(args)
     from jacap_synth import make_case
     from paper_2609_08131_amd import jacap
 

@@ -128,6 +128,8 @@ __device__ __forceinline__ void load_elems(const T* p, float (&x)[N]) {
   }
 }
 
+}  // namespace
+
 // ---------------------------------------------------------------------------
 // Initial pass: c_i = ||v_i||^2 / ridge (A_0 = ridge I), stamp 0, and each
 // block's best entry. One workgroup per (block of 256 positions, unit); 16
@@ -451,8 +453,6 @@ __global__ __launch_bounds__(kThreads) void greedy_kernel(
   }
   if (logdet_out && tid == 0) logdet_out[u] = (double)D * log(ridge) + logdet;
 }
-
-}  // namespace
 
 hipError_t launch_greedy(const Launch& L, const void* v, int32_t* idx, int32_t* order,
                          double* logdet) {
