@@ -56,7 +56,8 @@
  *   workspaces.
  * - Host-detectable errors (null or misaligned pointers, bad shapes or
  *   strides, unsupported head_dim or dtype, too small a workspace) return an
- *   error code and enqueue nothing. A failed launch returns JACAP_ERR_HIP.
+ *   error code and enqueue nothing. K and V token strides above 2^24
+ *   elements give JACAP_ERR_UNSUPPORTED. A failed launch returns JACAP_ERR_HIP.
  * - Data-dependent problems are reported through sticky device flags in the
  *   workspace (read with jacap_read_status): JACAP_FLAG_NONFINITE when a
  *   query, key or value is NaN/Inf, JACAP_FLAG_SINGULAR when A is not

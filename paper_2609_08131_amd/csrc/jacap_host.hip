@@ -43,6 +43,9 @@ jacap_status check_batch(const jacap_config* c, const jacap_batch* b) {
   for (int64_t s : st)
     if (s < 0 || (s % 8) != 0) return JACAP_ERR_INVALID_ARG;
   if (b->k_stride_token < c->head_dim || b->v_stride_token < c->head_dim) return JACAP_ERR_INVALID_ARG;
+  // The streaming kernels address a step's rows with 32-bit byte offsets.
+  if (b->k_stride_token > kMaxTokenStride || b->v_stride_token > kMaxTokenStride)
+    return JACAP_ERR_UNSUPPORTED;
   if (b->q_stride_pos < c->head_dim || b->out_stride_row < c->head_dim) return JACAP_ERR_INVALID_ARG;
   if (c->ridge_mode == JACAP_RIDGE_MATRIX &&
       (!b->ridge_mat || (reinterpret_cast<uintptr_t>(b->ridge_mat) & 7u)))

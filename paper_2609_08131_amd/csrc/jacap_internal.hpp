@@ -21,6 +21,7 @@ constexpr int kLChunkPrecise = 1024; // tokens per workgroup in the fp64 leverag
 constexpr int kWChunk = 4096;        // tokens per workgroup in the weight pass
 constexpr int kGreedyMaxLen = 524288; // longest sequence the greedy selection takes
 constexpr int kGreedyMaxD = 128;
+constexpr int64_t kMaxTokenStride = int64_t(1) << 24;  // elements between consecutive K / V rows
 
 // Unit flags (per (seq, layer, kv head)); the public flags are the OR of all.
 constexpr uint32_t kUnitNonfinite = JACAP_FLAG_NONFINITE;
@@ -206,6 +207,29 @@ __device__ __forceinline__ void raise_flags(uint32_t* status, uint32_t* uflags, 
                                             uint32_t f) {
   atomicOr(status, f);
   atomicOr(uflags + u, f);
+}
+
+// Raw buffer resource over [base, base + bytes): loads at byte offsets at or
+// past `bytes` return zeros instead of touching memory (the descriptor's
+// range check; stride 0, 32-bit data format). Used to read the rows of one
+// step of a streaming loop without clamping row indices: the range ends at
+// the last row the step may use, and the per-lane offsets stay constant.
+constexpr int kBufferFormat = 0x00020000;
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_range(const void* base, int32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, bytes, kBufferFormat);
+}
+// Bytes of the rows [0, rows) of a row range whose row stride is `stride`
+// bytes and whose rows are `row_bytes` long (0 for rows <= 0). The caller keeps
+// rows * stride below 2^31.
+__device__ __forceinline__ int32_t rows_bytes(int32_t rows, int32_t stride, int32_t row_bytes) {
+  return rows > 0 ? (rows - 1) * stride + row_bytes : 0;
+}
+__device__ __forceinline__ uint4 buffer_load16(__amdgpu_buffer_rsrc_t r, int32_t off) {
+  const auto x = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
+  return uint4{x[0], x[1], x[2], x[3]};
+}
+__device__ __forceinline__ float buffer_load_f32(__amdgpu_buffer_rsrc_t r, int32_t off) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0));
 }
 
 // Waits for every outstanding vector-memory load of this wave. Placed after a

@@ -127,22 +127,34 @@ __device__ __forceinline__ void gram_wave(const GramArgs& ga, uint16_t* tiles, f
 #pragma unroll
   for (int p = 0; p < NP; ++p) acc2[p] = floatx4{0.f, 0.f, 0.f, 0.f};
 
-  // Tokens past the chunk end are loaded from the last token (in bounds) and
-  // get weight 0: x = 0 in their K-slots, so they add exactly nothing.
+  // Each step reads its 32 rows through a buffer range that ends at the
+  // chunk's last row: rows past it (and their weights) load as zeros, so
+  // they add exactly nothing. Per-lane offsets are fixed; only the range's
+  // base moves with the step (scalar arithmetic).
   struct Pre { uint4 v[LOADS]; float w; };
-  auto gload = [&](int st) {
-    Pre buf;
-    const int t0 = ga.base + st * kGramStep;
-    const int last = ga.end - 1;
+  int32_t voff[LOADS];
 #pragma unroll
-    for (int r = 0; r < LOADS; ++r) {
-      const int flat = r * kThreads + tid, tok = flat / OCT, oc = flat % OCT;
-      const int t = min(t0 + tok, last);
-      buf.v[r] = *reinterpret_cast<const uint4*>(ga.vb + (int64_t)t * ga.vst + oc * 8);
-    }
-    const int tw = t0 + W * WPW + (lane & (WPW - 1));
-    const float w = ga.wrow[min(tw, last)];
-    buf.w = tw <= last ? w : 0.f;
+  for (int r = 0; r < LOADS; ++r) {
+    const int flat = r * kThreads + tid, tok = flat / OCT, oc = flat % OCT;
+    voff[r] = tok * (int32_t)ga.vst * 2 + oc * 16;
+  }
+  const int32_t woff = (W * WPW + (lane & (WPW - 1))) * 4;
+  // Steps are loaded strictly in order (0, 1, 2, ...), so the range advances
+  // by one step per call; past the chunk end it is empty.
+  const uint16_t* vnext = ga.vb + (int64_t)ga.base * ga.vst;
+  const float* wnext = ga.wrow + ga.base;
+  int32_t left = ga.end - ga.base;  // rows of the chunk from vnext on
+  const int32_t vstb = (int32_t)ga.vst * 2;
+  auto gload = [&]() {
+    Pre buf;
+    const int32_t rows = min(left, kGramStep);
+    const auto vr = buffer_range(vnext, rows_bytes(rows, vstb, D * 2));
+#pragma unroll
+    for (int r = 0; r < LOADS; ++r) buf.v[r] = buffer_load16(vr, voff[r]);
+    buf.w = buffer_load_f32(buffer_range(wnext, max(rows, 0) * 4), woff);
+    vnext += kGramStep * ga.vst;
+    wnext += kGramStep;
+    left -= kGramStep;
     return buf;
   };
   auto stage = [&](const Pre& buf, uint16_t* tile, float* wt) {
@@ -216,8 +228,23 @@ __device__ __forceinline__ void gram_wave(const GramArgs& ga, uint16_t* tiles, f
 #pragma unroll
         for (int q = 0; q < 4; ++q) { a[i][q] = (uint16_t)lo[q]; a[i][q + 4] = (uint16_t)hi[q]; }
       }
-      if constexpr (HAS_A) column(std::integral_constant<int, JA>{}, std::integral_constant<int, 0>{}, firstc, a, wl);
+      // Column JB (the longer MFMA run) first; the scheduling groups below
+      // then issue column JA's operand split between column JB's MFMAs, so
+      // the VALU work runs while the matrix core is busy.
       if constexpr (HAS_B) column(std::integral_constant<int, JB>{}, std::integral_constant<int, PA>{}, firstc, a, wl);
+      if constexpr (HAS_A) column(std::integral_constant<int, JA>{}, std::integral_constant<int, 0>{}, firstc, a, wl);
+      if constexpr (HAS_A && HAS_B) {
+        constexpr int MB = NT * (JB + 1), MA = NT * (JA + 1);
+        constexpr int SPLIT = 8 * 5;                     // VALU ops of one column's split
+        constexpr int PER = (SPLIT + MB - 1) / MB;
+        __builtin_amdgcn_sched_group_barrier(0x002, SPLIT, 0);   // split of column JB
+#pragma unroll
+        for (int m = 0; m < MB; ++m) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);     // one MFMA of column JB
+          __builtin_amdgcn_sched_group_barrier(0x002, PER, 0);   // part of column JA's split
+        }
+        __builtin_amdgcn_sched_group_barrier(0x008, MA, 0);      // column JA's MFMAs
+      }
     }
   };
   // One step: stage the prefetched data, barrier, prefetch two steps ahead,
@@ -225,13 +252,15 @@ __device__ __forceinline__ void gram_wave(const GramArgs& ga, uint16_t* tiles, f
   auto step = [&](int st, Pre& buf, int half, auto firstc) {
     stage(buf, tiles + half * TILE, wts + half * kGramStep);
     __syncthreads();
-    buf = gload(min(st + 2, ga.nsteps - 1));  // unconditional: static wait counts
+    buf = gload();  // step st + 2 (empty past the chunk end): static wait counts
     __builtin_amdgcn_sched_barrier(0);        // keep the loads ahead of this step's MFMAs
     compute(tiles + half * TILE, wts + half * kGramStep, firstc);
   };
 
   static_assert(kGramFlush == 4, "the step loop below is unrolled by four");
-  Pre b0 = gload(0), b1 = gload(1);
+  Pre b0 = gload();
+  Pre b1 = gload();
+  drain_vmem();  // prologue loads done: the loop's wait counts then stay static
   for (int st = 0; st < ga.nsteps; st += kGramFlush) {
     step(st, b0, 0, std::true_type{});
     step(st + 1, b1, 1, std::false_type{});

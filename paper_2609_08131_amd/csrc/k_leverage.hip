@@ -27,7 +27,7 @@ __global__ __launch_bounds__(kThreads, 2) void leverage_mfma_kernel(
   const Unit un = decode_unit(g, u);
   const int base = chunk * kLChunkMfma;
   if (base >= un.n) return;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int ch = lane & 15, kg = lane >> 4;
   const int rl = 2 * (ch >> 3) + ((ch >> 2) & 1);  // token (of 4) whose score this lane ends with
   const int64_t trow = token_row(g, un);
@@ -52,20 +52,27 @@ __global__ __launch_bounds__(kThreads, 2) void leverage_mfma_kernel(
 
   // A step is 16 tokens (one MFMA row tile). V rows are prefetched two
   // steps ahead into three rotating register buffers (the loop is unrolled
-  // by three so the buffers stay in fixed registers). Every load in the loop
-  // is issued unconditionally (past-the-end rows are clamped and unused): a
-  // load skipped on some path would make the compiler wait for the newest
-  // loads, i.e. drain the prefetch, in every step. MFMAs are issued kb-outer
-  // so that consecutive MFMAs update different output blocks.
+  // by three so the buffers stay in fixed registers). Each step reads its
+  // rows through a buffer range that ends at the chunk's last row: rows past
+  // it load as zeros (and are not stored), so every load is issued
+  // unconditionally with a fixed per-lane offset, and the compiler's wait
+  // counts stay static. MFMAs are issued kb-outer so that consecutive MFMAs
+  // update different output blocks.
   // One prefetched step: the lane's V row pieces and the weight of the token
   // whose score this lane writes.
   struct Buf { bf16x8 a[NK]; float w; };
-  auto load = [&](int t0, Buf& b) {
-    const int tok = min(t0 + ch, end - 1);  // A-operand row of this lane (clamped; result unused)
+  const int32_t vstb = (int32_t)g.vst * 2;
+  int32_t voff[NK];
 #pragma unroll
-    for (int kb = 0; kb < NK; ++kb)
-      b.a[kb] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(vb + (int64_t)tok * g.vst + 32 * kb + 8 * kg));
-    b.w = wbuf[trow + min(t0 + 4 * kg + rl, end - 1)];
+  for (int kb = 0; kb < NK; ++kb) voff[kb] = ch * vstb + (32 * kb + 8 * kg) * 2;
+  const int32_t woff = (4 * kg + rl) * 4;
+  const float* wb = wbuf + trow;
+  auto load = [&](int t0, Buf& b) {
+    const int32_t rows = min(end - t0, 16);
+    const auto vr = buffer_range(vb + (int64_t)t0 * g.vst, rows_bytes(rows, vstb, D * 2));
+#pragma unroll
+    for (int kb = 0; kb < NK; ++kb) b.a[kb] = __builtin_bit_cast(bf16x8, buffer_load16(vr, voff[kb]));
+    b.w = buffer_load_f32(buffer_range(wb + t0, max(rows, 0) * 4), woff);
     __builtin_amdgcn_sched_barrier(0);  // issue here, ahead of the MFMAs that follow
   };
   auto step = [&](int t0, const Buf& b) {

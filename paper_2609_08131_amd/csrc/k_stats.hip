@@ -204,6 +204,45 @@ __device__ __forceinline__ F group_sum(F v) {
   return v;
 }
 
+// Chunk epilogue of the K pass: z and kappa of the chunk (staged in LDS) stored
+// coalesced with one non-finite check, then the chunk's (max z, sum exp(z - max)).
+__device__ __forceinline__ void kpass_epilogue(const Unit& un, int u, int base, int64_t trow,
+                                               const float* zsh, const float* ksq, float* red,
+                                               float* __restrict__ zout,
+                                               float* __restrict__ kout,
+                                               float2* __restrict__ cstat, int kchunks,
+                                               uint32_t* status, uint32_t* uflags, int chunk) {
+  const int tid = threadIdx.x;
+  __syncthreads();
+  bool bad = false;
+  for (int tl = tid; tl < kKChunk; tl += kThreads) {
+    const int i = base + tl;
+    if (i < un.n) {
+      const float z = zsh[tl], kq = ksq[tl];
+      zout[trow + i] = z;
+      kout[trow + i] = kq;
+      bad |= !isfinite(z) || !isfinite(kq);
+    }
+  }
+  if (__any(bad) && (threadIdx.x & 63) == 0) raise_flags(status, uflags, u, kUnitNonfinite);
+  __syncthreads();
+  static_assert(kKChunk % kThreads == 0, "whole logits per thread in the chunk reduction");
+  constexpr int ZPT = kKChunk / kThreads;
+  float zv[ZPT];
+  float mloc = -INFINITY;
+#pragma unroll
+  for (int q = 0; q < ZPT; ++q) {
+    zv[q] = zsh[q * kThreads + tid];
+    mloc = fmaxf(mloc, zv[q]);
+  }
+  const float m = block_combine(wave_max(mloc), red, [](float a, float b) { return fmaxf(a, b); });
+  float ex = 0.0f;
+#pragma unroll
+  for (int q = 0; q < ZPT; ++q) ex += (zv[q] == -INFINITY) ? 0.0f : expf(zv[q] - m);
+  const float s = block_combine(wave_sum(ex), red, [](float a, float b) { return a + b; });
+  if (tid == 0) cstat[(int64_t)u * kchunks + chunk] = make_float2(m, s);
+}
+
 // ---------------------------------------------------------------------------
 // K pass: z_i = k_i . mu / (tau sqrt d) and kappa_i = k_i^T Lambda k_i for a
 // chunk of kKChunk tokens, then the chunk's (max z, sum exp(z - max)).
@@ -309,35 +348,116 @@ __global__ __launch_bounds__(kThreads) void kpass_kernel(
       }
     }
   }
-  // z and kappa of the chunk: coalesced stores, one non-finite check.
-  __syncthreads();
-  bool bad = false;
-  for (int tl = tid; tl < kKChunk; tl += kThreads) {
-    const int i = base + tl;
-    if (i < un.n) {
-      const float z = zsh[tl], kq = ksq[tl];
-      zout[trow + i] = z;
-      kout[trow + i] = kq;
-      bad |= !isfinite(z) || !isfinite(kq);
+  kpass_epilogue(un, u, base, trow, zsh, ksq, red, zout, kout, cstat, kchunks, status, uflags,
+                 chunk);
+}
+
+// K pass for bf16 keys, diagonal Lambda: four lanes per key row, each lane
+// reading D/32 16-byte pieces (the four lanes of a row read 64 contiguous
+// bytes per load), so a row's two sums need two quad DPP levels instead of
+// four row levels per 16-byte load.
+template <int D>
+__global__ __launch_bounds__(kThreads) void kpass_quad_kernel(
+    Geo g, const uint16_t* __restrict__ k, const double* __restrict__ mu,
+    const double* __restrict__ lam, float* __restrict__ zout, float* __restrict__ kout,
+    float2* __restrict__ cstat, int kchunks, double inv_scale, uint32_t* status,
+    uint32_t* uflags) {
+  const int u = blockIdx.y, chunk = blockIdx.x;
+  const Unit un = decode_unit(g, u);
+  const int base = chunk * kKChunk;
+  if (base >= un.n) return;
+
+  constexpr int VEC = 8;                 // bf16 per 16-byte piece
+  constexpr int LPT = 4;                 // lanes per token row
+  constexpr int PIECES = D / (LPT * VEC);
+  constexpr int TPW = 64 / LPT;          // 16 rows per wave per load
+  constexpr int TPB = TPW * (kThreads / 64);
+  constexpr int UNR = 2;                 // rows per lane per loop trip
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int sub = lane % LPT, tiw = lane / LPT;
+
+  // channel of (piece p, element e): p * 32 + sub * 8 + e
+  float muv[PIECES][VEC], lamv[PIECES][VEC];
+#pragma unroll
+  for (int p = 0; p < PIECES; ++p)
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) {
+      muv[p][e] = (float)mu[(int64_t)u * D + p * LPT * VEC + sub * VEC + e];
+      lamv[p][e] = (float)lam[(int64_t)u * D + p * LPT * VEC + sub * VEC + e];
     }
-  }
-  if (__any(bad) && (threadIdx.x & 63) == 0) raise_flags(status, uflags, u, kUnitNonfinite);
-  __syncthreads();
-  static_assert(kKChunk % kThreads == 0, "whole logits per thread in the chunk reduction");
-  constexpr int ZPT = kKChunk / kThreads;
-  float zv[ZPT];
-  float mloc = -INFINITY;
+  drain_vmem();
+
+  __shared__ float zsh[kKChunk];
+  __shared__ float ksq[kKChunk];
+  __shared__ float red[kThreads / 64];
+
+  const uint16_t* kb = k + un.l * g.ksl + un.h * g.ksh + un.t0 * g.kst;
+  const int64_t trow = token_row(g, un);
+  static_assert(kKChunk % (UNR * TPB) == 0, "chunk must be whole unrolled trips");
+
+  // Each load reads the wave's 16 rows through a buffer range that ends at
+  // the unit's last row (rows past it load as zeros and are discarded), with
+  // fixed per-lane offsets.
+  const int32_t kstb = (int32_t)g.kst * 2;
+  int32_t koff[PIECES];
 #pragma unroll
-  for (int q = 0; q < ZPT; ++q) {
-    zv[q] = zsh[q * kThreads + tid];
-    mloc = fmaxf(mloc, zv[q]);
-  }
-  const float m = block_combine(wave_max(mloc), red, [](float a, float b) { return fmaxf(a, b); });
-  float ex = 0.0f;
+  for (int p = 0; p < PIECES; ++p) koff[p] = tiw * kstb + sub * 16 + p * LPT * 16;
+  auto load_trip = [&](int it0, uint4 (&raw)[UNR][PIECES]) {
 #pragma unroll
-  for (int q = 0; q < ZPT; ++q) ex += (zv[q] == -INFINITY) ? 0.0f : expf(zv[q] - m);
-  const float s = block_combine(wave_sum(ex), red, [](float a, float b) { return a + b; });
-  if (tid == 0) cstat[(int64_t)u * kchunks + chunk] = make_float2(m, s);
+    for (int j = 0; j < UNR; ++j) {
+      const int r0 = base + it0 + j * TPB + wave * TPW;  // first row of the wave
+      const int32_t rows = min(un.n - r0, TPW);
+      const auto kr = buffer_range(kb + (int64_t)r0 * g.kst, rows_bytes(rows, kstb, D * 2));
+#pragma unroll
+      for (int p = 0; p < PIECES; ++p) raw[j][p] = buffer_load16(kr, koff[p]);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+  };
+  // Two register buffers, swapped by unrolling the trip loop by two (a copy
+  // between them would make the compiler wait for the prefetched loads).
+  auto process = [&](int it0, const uint4 (&raw)[UNR][PIECES]) {
+#pragma unroll
+    for (int j = 0; j < UNR; ++j) {
+      const int tl = it0 + j * TPB + wave * TPW + tiw;
+      const bool valid = base + tl < un.n;
+      float dot = 0.0f, kap = 0.0f;
+#pragma unroll
+      for (int p = 0; p < PIECES; ++p) {
+        const uint32_t wd[4] = {raw[j][p].x, raw[j][p].y, raw[j][p].z, raw[j][p].w};
+#pragma unroll
+        for (int h = 0; h < 4; ++h) {
+          const float x0 = __uint_as_float(wd[h] << 16);
+          const float x1 = __uint_as_float(wd[h] & 0xFFFF0000u);
+          dot = fmaf(muv[p][2 * h], x0, dot);
+          dot = fmaf(muv[p][2 * h + 1], x1, dot);
+          kap = fmaf(lamv[p][2 * h] * x0, x0, kap);
+          kap = fmaf(lamv[p][2 * h + 1] * x1, x1, kap);
+        }
+      }
+      dot += dpp_f32<kDppQuadXor1>(dot);
+      kap += dpp_f32<kDppQuadXor1>(kap);
+      dot += dpp_f32<kDppQuadXor2>(dot);
+      kap += dpp_f32<kDppQuadXor2>(kap);
+      if (sub == 0) {
+        zsh[tl] = valid ? (float)((double)dot * inv_scale) : -INFINITY;
+        ksq[tl] = kap;
+      }
+    }
+  };
+  constexpr int TRIP = UNR * TPB;
+  static_assert(kKChunk % (2 * TRIP) == 0, "chunk must be whole pairs of trips");
+  uint4 ba[UNR][PIECES], bb[UNR][PIECES];
+  load_trip(0, ba);
+  for (int it0 = 0; it0 < kKChunk; it0 += 2 * TRIP) {
+    load_trip(it0 + TRIP, bb);
+    process(it0, ba);
+    load_trip(min(it0 + 2 * TRIP, kKChunk - TRIP), ba);
+    process(it0 + TRIP, bb);
+  }
+  kpass_epilogue(un, u, base, trow, zsh, ksq, red, zout, kout, cstat, kchunks, status, uflags,
+                 chunk);
 }
 
 template <typename T, int D>
@@ -350,10 +470,17 @@ static void kpass_dispatch(const Launch& L, const void* k, bool full, dim3 grid,
         ws_ptr<float>(L.wsp, L.ws.kappa), ws_ptr<float2>(L.wsp, L.ws.cstat), L.ws.kchunks,
         inv_scale, ws_ptr<uint32_t>(L.wsp, L.ws.status), ws_ptr<uint32_t>(L.wsp, L.ws.uflags));
   };
-  if (full)
+  if (full) {
     args(kpass_kernel<T, D, true>);
-  else
+  } else if constexpr (std::is_same<T, uint16_t>::value) {
+    kpass_quad_kernel<D><<<grid, kThreads, 0, L.stream>>>(
+        g, (const uint16_t*)k, ws_ptr<double>(L.wsp, L.ws.mu), ws_ptr<double>(L.wsp, L.ws.lam),
+        ws_ptr<float>(L.wsp, L.ws.z), ws_ptr<float>(L.wsp, L.ws.kappa),
+        ws_ptr<float2>(L.wsp, L.ws.cstat), L.ws.kchunks, inv_scale,
+        ws_ptr<uint32_t>(L.wsp, L.ws.status), ws_ptr<uint32_t>(L.wsp, L.ws.uflags));
+  } else {
     args(kpass_kernel<T, D, false>);
+  }
 }
 
 hipError_t launch_kpass(const Launch& L, const void* k) {

@@ -3,6 +3,11 @@
   python profile_summary.py stats  <kernel_stats.csv> <out.md> <command...>
       per-kernel calls / average / total time of the library's kernels.
 
+  python profile_summary.py sq <out.md> <command> <pmc_dir>...
+      per-kernel utilisation and stall fractions from `--pmc` runs of SQ
+      counters (first dispatch of each library kernel; any of the counters
+      below that the runs collected).
+
   python profile_summary.py traffic <fetch_dir> <write_dir> <workload> <out.md> <command...>
       HBM bytes per dispatch of each phase's kernel from two `--pmc` runs
       (FETCH_SIZE, then WRITE_SIZE; both in KiB per dispatch), each scaled by
@@ -29,7 +34,7 @@ COPY_BYTES = 1 << 30
 # Kernel of each phase (first match of the demangled name).
 PHASE_KERNELS = {
     "qstats": r"jacap::qstats_kernel",
-    "kpass": r"jacap::kpass_kernel",
+    "kpass": r"jacap::kpass_(quad_)?kernel",
     "weights": r"jacap::softmax_weights_kernel",
     "gram": r"jacap::gram_mfma_kernel<\d+, 2>",
     "leverage": r"jacap::leverage_mfma_kernel",
@@ -51,6 +56,64 @@ def stats(csv_path, out_md, command):
     with open(out_md, "w") as fh:
         fh.write("# rocprofv3 kernel statistics\n\nCommand:\n\n```\n" + command + "\n```\n\n")
         fh.write("\n".join(lines) + "\n")
+
+
+def _first_dispatch_counters(pmc_dirs):
+    """{kernel: {counter: value}} for the first dispatch of each jacap kernel."""
+    vals = defaultdict(dict)
+    for d in pmc_dirs:
+        for f in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
+            first = {}
+            for r in csv.DictReader(open(f)):
+                if "jacap::" not in r["Kernel_Name"]:
+                    continue
+                name = r["Kernel_Name"].split("(")[0].replace("void ", "")
+                did = int(r["Dispatch_Id"])
+                if first.setdefault(name, did) != did:
+                    continue
+                c = r["Counter_Name"]
+                vals[name][c] = vals[name].get(c, 0.0) + float(r["Counter_Value"])
+    return vals
+
+
+def sq(out_md, command, pmc_dirs):
+    """Fractions per kernel. GRBM_GUI_ACTIVE is summed over the 8 XCDs, so
+    GUI/8 is the kernel's cycles; per-SIMD rates divide by 1024 SIMDs, per-CU
+    rates by 256 CUs; wave fractions divide by SQ_WAVE_CYCLES."""
+    vals = _first_dispatch_counters(pmc_dirs)
+    cols = [
+        ("MFMA busy", lambda v, cyc: v["SQ_VALU_MFMA_BUSY_CYCLES"] / (cyc * 1024)),
+        ("VALU active", lambda v, cyc: v["SQ_ACTIVE_INST_VALU"] / (cyc * 256)),
+        ("LDS active", lambda v, cyc: v["SQ_ACTIVE_INST_LDS"] / (cyc * 256)),
+        ("LDS bank conflict", lambda v, cyc: v["SQ_LDS_BANK_CONFLICT"] / v["SQ_LDS_IDX_ACTIVE"]),
+        ("wave: waiting on data", lambda v, cyc: v["SQ_WAIT_ANY"] / v["SQ_WAVE_CYCLES"]),
+        ("wave: ready, not issued", lambda v, cyc: v["SQ_WAIT_INST_ANY"] / v["SQ_WAVE_CYCLES"]),
+        ("wave: issuing", lambda v, cyc: v["SQ_ACTIVE_INST_ANY"] / v["SQ_WAVE_CYCLES"]),
+        ("MFMA-VALU co-exec", lambda v, cyc: v["SQ_VALU_MFMA_COEXEC_CYCLES"] / (cyc * 1024)),
+    ]
+    names = [c for c, f in cols if any(_ok(f, v) for v in vals.values())]
+    lines = ["| kernel | " + " | ".join(names) + " |", "|---|" + "---:|" * len(names)]
+    for k, v in vals.items():
+        cyc = v.get("GRBM_GUI_ACTIVE", 8.0) / 8.0
+        row = []
+        for c, f in cols:
+            if c not in names:
+                continue
+            x = _ok(f, v, cyc)
+            row.append("" if x is None else f"{100 * x:.1f}%")
+        lines.append(f"| `{k}` | " + " | ".join(row) + " |")
+    with open(out_md, "w") as fh:
+        fh.write("# SQ counters per kernel (first dispatch of each)\n\nCommand (one run per "
+                 "counter set):\n\n```\n" + command + "\n```\n\n" + (sq.__doc__ or "")
+                 .replace("\n    ", " ").strip() + "\n\n")
+        fh.write("\n".join(lines) + "\n")
+
+
+def _ok(f, v, cyc=None):
+    try:
+        return f(v, v.get("GRBM_GUI_ACTIVE", 8.0) / 8.0 if cyc is None else cyc)
+    except (KeyError, ZeroDivisionError):
+        return None
 
 
 def _per_dispatch(pmc_dir, counter):
@@ -116,6 +179,8 @@ if __name__ == "__main__":
     mode = sys.argv[1]
     if mode == "stats":
         stats(sys.argv[2], sys.argv[3], " ".join(sys.argv[4:]))
+    elif mode == "sq":
+        sq(sys.argv[2], sys.argv[3], sys.argv[4:])
     elif mode == "traffic":
         traffic(sys.argv[2], sys.argv[3], sys.argv[4], sys.argv[5], " ".join(sys.argv[6:]))
     else:

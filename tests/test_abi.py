@@ -191,3 +191,10 @@ def test_greedy_workspace_and_validation():
     assert call(good, good, good, good, P(0x100004), None, good, n, None) == jacap.ERR_INVALID_ARG
     assert call(good, good, good, good, None, P(0x100004), good, n, None) == jacap.ERR_INVALID_ARG
     assert call(None, good, good, good, None, None, good, n, None) == jacap.ERR_INVALID_ARG
+
+
+def test_token_stride_limit():
+    """K / V token strides above 2^24 elements are not taken (32-bit row offsets)."""
+    assert _ws_size(_cfg(), _batch(k_stride_token=1 << 24))[0] == jacap.OK
+    assert _ws_size(_cfg(), _batch(v_stride_token=(1 << 24) + 8))[0] == jacap.ERR_UNSUPPORTED
+    assert _ws_size(_cfg(), _batch(k_stride_token=(1 << 24) + 8))[0] == jacap.ERR_UNSUPPORTED
