@@ -120,15 +120,16 @@ __device__ uint32_t radix_rank(KeyAt key_at, int cnt, uint32_t rank, SelShared& 
 
 // General path: radix select over the scores, then an ordered emission pass
 // over contiguous per-thread segments.
-__device__ void select_general(const float* s, int n, int kk, int32_t* out, SelShared& sh) {
+template <class KeyAt>
+__device__ void select_general(KeyAt key_at, int n, int kk, int32_t* out, SelShared& sh) {
   const int tid = threadIdx.x;
   uint32_t need;
-  const uint32_t T = radix_rank([&](int i) { return score_key(s[i]); }, n, (uint32_t)kk, sh, need);
+  const uint32_t T = radix_rank(key_at, n, (uint32_t)kk, sh, need);
   const int seg = (n + kSelThreads - 1) / kSelThreads;
   const int lo = min(n, tid * seg), hi = min(n, lo + seg);
   uint32_t cgt = 0, ceq = 0;
   for (int i = lo; i < hi; ++i) {
-    const uint32_t key = score_key(s[i]);
+    const uint32_t key = key_at(i);
     cgt += key > T;
     ceq += key == T;
   }
@@ -136,7 +137,7 @@ __device__ void select_general(const float* s, int n, int kk, int32_t* out, SelS
   uint32_t gt_before = block_exclusive_scan(cgt, sh.scan, tot);
   uint32_t eq_before = block_exclusive_scan(ceq, sh.scan, tot);
   for (int i = lo; i < hi; ++i) {
-    const uint32_t key = score_key(s[i]);
+    const uint32_t key = key_at(i);
     if (key > T) {
       const uint32_t pos = gt_before + min(eq_before, need);
       if (pos < (uint32_t)kk) out[pos] = i;
@@ -160,30 +161,11 @@ __device__ __forceinline__ int lower_bound_lds(const int32_t* a, int cnt, int32_
   return lo;
 }
 
-__global__ __launch_bounds__(kSelThreads) void select_kernel(Geo g, const float* __restrict__ scores,
-                                                             int32_t* __restrict__ idx, int budget,
-                                                             int protect) {
-  __shared__ SelShared sh;
-  const int u = blockIdx.x, tid = threadIdx.x;
-  const Unit un = decode_unit(g, u);
-  int32_t* out = idx + (int64_t)u * budget;
-  const int kk_all = min(budget, un.n);
-  const float* s = scores + token_row(g, un);
-
-  for (int j = kk_all + tid; j < budget; j += kSelThreads) out[j] = -1;
-  if (kk_all == 0) return;
-  // Protected tail: the last p positions are kept; the ranking fills the
-  // remaining kk slots from positions 0 .. n-1 (n = n_b - p), whose indices
-  // all precede the tail, so the tail simply follows them in idx.
-  const int p = min(protect, kk_all);
-  const int n = un.n - p, kk = kk_all - p;
-  for (int j = tid; j < p; j += kSelThreads) out[kk + j] = n + j;
-  if (kk == 0) return;
-  if (kk == n) {
-    for (int j = tid; j < n; j += kSelThreads) out[j] = j;
-    return;
-  }
-
+// TOP-kk of key_at(0 .. n-1) by (key desc, position asc), written to out[0 ..
+// kk) in ascending position order (0 < kk < n).
+template <class KeyAt>
+__device__ void select_unit(KeyAt key_at, int n, int kk, int32_t* out, SelShared& sh) {
+  const int tid = threadIdx.x;
   // Bracket [lo, hi] of T from the sample (the whole unit if it fits the band).
   uint32_t lo = 0u, hi = 0xFFFFFFFFu;
   if (n > kCandCap) {
@@ -193,7 +175,7 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(Geo g, const float*
     const int last_start = (nsb - 1) * q * 64;
     const int S = (nsb - 1) * 64 + min(64, n - last_start);   // valid samples form a prefix
     for (int j = tid; j < S; j += kSelThreads)
-      sh.stage[j] = score_key(s[(j >> 6) * q * 64 + (j & 63)]);
+      sh.stage[j] = key_at((j >> 6) * q * 64 + (j & 63));
     __syncthreads();
     const double ks = (double)kk * (double)S / (double)n;
     const int delta = (int)(4.0 * sqrt(ks)) + 16;
@@ -213,7 +195,7 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(Geo g, const float*
 #pragma unroll
     for (int j = 0; j < kSelPer; ++j) {
       const int p = base + j * kSelThreads + tid;
-      sh.stage[j * kSelThreads + tid] = p < n ? score_key(s[p]) : 0u;
+      sh.stage[j * kSelThreads + tid] = p < n ? key_at(p) : 0u;
     }
     __syncthreads();
     uint32_t k8[kSelPer];
@@ -248,7 +230,7 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(Geo g, const float*
   const bool ok = gcnt < (uint32_t)kk && gcnt + ccnt >= (uint32_t)kk &&
                   gcnt <= (uint32_t)kSureCap && ccnt <= (uint32_t)kCandCap;
   if (!ok) {  // uniform: every thread holds the same counts
-    select_general(s, n, kk, out, sh);
+    select_general(key_at, n, kk, out, sh);
     return;
   }
 
@@ -288,6 +270,50 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(Geo g, const float*
     const int32_t p = kept_c[b];
     out[b + lower_bound_lds(sh.gpos, (int)gcnt, p)] = p;
   }
+}
+
+__global__ __launch_bounds__(kSelThreads) void select_kernel(Geo g, const float* __restrict__ scores,
+                                                             int32_t* __restrict__ idx, int budget,
+                                                             int protect) {
+  __shared__ SelShared sh;
+  const int u = blockIdx.x, tid = threadIdx.x;
+  const Unit un = decode_unit(g, u);
+  int32_t* out = idx + (int64_t)u * budget;
+  const int kk_all = min(budget, un.n);
+  const float* s = scores + token_row(g, un);
+
+  for (int j = kk_all + tid; j < budget; j += kSelThreads) out[j] = -1;
+  if (kk_all == 0) return;
+  // Protected tail: the last p positions are kept; the ranking fills the
+  // remaining kk slots from positions 0 .. n-1 (n = n_b - p), whose indices
+  // all precede the tail, so the tail simply follows them in idx.
+  const int npro = min(protect, kk_all);
+  const int n = un.n - npro, kk = kk_all - npro;
+  for (int j = tid; j < npro; j += kSelThreads) out[kk + j] = n + j;
+  if (kk == 0) return;
+  if (kk == n) {
+    for (int j = tid; j < n; j += kSelThreads) out[j] = j;
+    return;
+  }
+
+  // Keeping more than half: select the n - kk tokens to evict instead (the
+  // last n - kk of the order (key desc, position asc) are the first n - kk of
+  // (~key desc, reversed position asc)), then emit every other position.
+  const int m = n - kk;
+  if (m < kk && m <= kSelChunk) {
+    select_unit([&](int i) { return ~score_key(s[n - 1 - i]); }, n, m, out, sh);
+    __syncthreads();  // out[0 .. m): evicted, as reversed positions ascending
+    uint32_t* ev = sh.stage;
+    for (int j = tid; j < m; j += kSelThreads) ev[j] = (uint32_t)(n - 1 - out[m - 1 - j]);
+    __syncthreads();
+    const int32_t* evs = reinterpret_cast<const int32_t*>(ev);
+    for (int i = tid; i < n; i += kSelThreads) {
+      const int c = lower_bound_lds(evs, m, i);
+      if (c == m || evs[c] != i) out[i - c] = i;
+    }
+    return;
+  }
+  select_unit([&](int i) { return score_key(s[i]); }, n, kk, out, sh);
 }
 
 hipError_t launch_select(const Launch& L, const float* scores, int32_t* idx) {

@@ -224,7 +224,8 @@ def test_select_ties_nan_negzero(jacap):
     case = make_case("ragged16", device="cuda", seq_lens=[1, 33, 1000, 5000], num_layers=1,
                      num_kv_heads=3, num_q_heads=3, head_dim=64, window=2)
     rng = np.random.default_rng(0)
-    for budget in (1, 7, 33, 999, 2048):
+    # 600, 999, 3000, 4990 keep more than half of some units (the complement path)
+    for budget in (1, 7, 33, 600, 999, 2048, 3000, 4990):
         p = jacap.Params(budget_k=budget)
         prob = jacap.prepare(case.q_win, case.k, case.v, case.seq_offsets, case.seq_lens, p)
         s = (rng.integers(0, 6, size=prob.scores.shape).astype(np.float32) * 0.5)
@@ -260,7 +261,8 @@ def test_select_large_units_both_paths(jacap):
         2: lambda n: rng.integers(0, 5, n).astype(np.float64),
         3: lambda n: np.exp(rng.normal(0.0, 3.0, n)),
     }
-    for budget in (1, 1024, 2048, 20000):
+    # 16384 and 125000 keep more than half (selection of the evicted tokens)
+    for budget in (1, 1024, 2048, 16384, 20000, 125000):
         p = jacap.Params(budget_k=budget)
         prob = jacap.prepare(case.q_win, case.k, case.v, case.seq_offsets, case.seq_lens, p)
         s = np.zeros((1, 4, T), np.float32)
