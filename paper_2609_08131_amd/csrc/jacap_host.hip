@@ -65,6 +65,13 @@ Workspace layout(const jacap_config* c, const jacap_batch* b, bool greedy = fals
   w.kchunks = (maxn + kKChunk - 1) / kKChunk;
   w.wchunks = (maxn + kWChunk - 1) / kWChunk;
   w.gchunk = w.mfma ? kGChunkMfma : kGChunkPrecise;
+  // Larger chunks write and re-read fewer partials; the chunk doubles while
+  // the grid keeps kGramMinBlocks blocks and the longest sequence at least 8
+  // chunks (so that its ragged last chunk stays a small share).
+  if (w.mfma)
+    while (w.gchunk < kGChunkMfmaMax && 16 * (int64_t)w.gchunk <= maxn &&
+           U * (int64_t)((maxn + 2 * w.gchunk - 1) / (2 * w.gchunk)) >= kGramMinBlocks)
+      w.gchunk *= 2;
   w.gchunks = (maxn + w.gchunk - 1) / w.gchunk;
   w.gparts = 1;
   const int lchunk = w.mfma ? kLChunkMfma : kLChunkPrecise;

@@ -14,7 +14,9 @@ namespace jacap {
 // ---------------------------------------------------------------------------
 constexpr int kThreads = 256;        // 4 wave64 per workgroup
 constexpr int kKChunk = 1024;        // tokens per workgroup in the K pass
-constexpr int kGChunkMfma = 4096;    // tokens per workgroup in the MFMA Gram pass
+constexpr int kGChunkMfma = 4096;    // tokens per workgroup in the MFMA Gram pass: at least
+constexpr int kGChunkMfmaMax = 16384; // ... and at most (larger chunks: fewer partial Grams)
+constexpr int kGramMinBlocks = 2048;  // the chunk doubles while the grid keeps this many blocks
 constexpr int kGChunkPrecise = 1024; // tokens per workgroup in the fp64 Gram pass
 constexpr int kLChunkMfma = 4096;    // tokens per workgroup in the MFMA leverage pass
 constexpr int kLChunkPrecise = 1024; // tokens per workgroup in the fp64 leverage pass

@@ -287,14 +287,14 @@ __device__ __forceinline__ void gram_wave(const GramArgs& ga, uint16_t* tiles, f
 template <int D, int NT>
 __global__ __launch_bounds__(kThreads, 2) void gram_mfma_kernel(
     Geo g, const uint16_t* __restrict__ v, const float* __restrict__ wbuf,
-    const uint32_t* __restrict__ uflags, float* __restrict__ partials, int gchunks) {
+    const uint32_t* __restrict__ uflags, float* __restrict__ partials, int gchunks, int gchunk) {
   constexpr int NB = D / 16;
   constexpr int NPAIR = NB * (NB + 1) / 2;
   constexpr int TILE = kGramStep * kGramPitch;
   const int u = blockIdx.y, chunk = blockIdx.x;
   if (NT == 3 && !(uflags[u] & kUnitRefine)) return;
   const Unit un = decode_unit(g, u);
-  const int base = chunk * kGChunkMfma;
+  const int base = chunk * gchunk;
   if (base >= un.n) return;
   __shared__ __attribute__((aligned(16))) uint16_t tiles[2 * TILE];
   __shared__ __attribute__((aligned(16))) float wts[2 * kGramStep];
@@ -303,7 +303,7 @@ __global__ __launch_bounds__(kThreads, 2) void gram_mfma_kernel(
   ga.vst = g.vst;
   ga.wrow = wbuf + token_row(g, un);
   ga.base = base;
-  ga.end = min(un.n, base + kGChunkMfma);
+  ga.end = min(un.n, base + gchunk);
   constexpr int SPAN = kGramStep * kGramFlush;
   ga.nsteps = (ga.end - base + SPAN - 1) / SPAN * kGramFlush;
   ga.out = partials + ((int64_t)u * gchunks + chunk) * (NPAIR * 256);
@@ -386,11 +386,11 @@ hipError_t launch_gram(const Launch& L, const void* v, bool refine) {
     float* part = ws_ptr<float>(L.wsp, L.ws.gram);
     const uint16_t* vv = (const uint16_t*)v;
     if (g.D == 128) {
-      if (refine) gram_mfma_kernel<128, 3><<<grid, kThreads, 0, L.stream>>>(g, vv, wb, uf, part, L.ws.gchunks);
-      else gram_mfma_kernel<128, 2><<<grid, kThreads, 0, L.stream>>>(g, vv, wb, uf, part, L.ws.gchunks);
+      if (refine) gram_mfma_kernel<128, 3><<<grid, kThreads, 0, L.stream>>>(g, vv, wb, uf, part, L.ws.gchunks, L.ws.gchunk);
+      else gram_mfma_kernel<128, 2><<<grid, kThreads, 0, L.stream>>>(g, vv, wb, uf, part, L.ws.gchunks, L.ws.gchunk);
     } else {
-      if (refine) gram_mfma_kernel<64, 3><<<grid, kThreads, 0, L.stream>>>(g, vv, wb, uf, part, L.ws.gchunks);
-      else gram_mfma_kernel<64, 2><<<grid, kThreads, 0, L.stream>>>(g, vv, wb, uf, part, L.ws.gchunks);
+      if (refine) gram_mfma_kernel<64, 3><<<grid, kThreads, 0, L.stream>>>(g, vv, wb, uf, part, L.ws.gchunks, L.ws.gchunk);
+      else gram_mfma_kernel<64, 2><<<grid, kThreads, 0, L.stream>>>(g, vv, wb, uf, part, L.ws.gchunks, L.ws.gchunk);
     }
   } else {
     if (refine) return hipSuccess;

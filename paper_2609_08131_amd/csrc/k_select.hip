@@ -35,7 +35,10 @@ __device__ __forceinline__ uint32_t score_key(float f) {
 }
 
 struct SelShared {
-  uint32_t stage[kSelChunk];  // staged chunk keys / sample keys / kept candidate positions
+  // staged chunk keys (one pad word per 8: the per-thread reads of 8
+  // consecutive keys are then bank-conflict free) / sample keys / kept
+  // candidate positions
+  uint32_t stage[kSelChunk + kSelChunk / 8];
   uint32_t ckey[kCandCap];    // candidate keys (position order)
   int32_t cpos[kCandCap];     // candidate positions
   int32_t gpos[kSureCap];     // kept-for-sure positions (position order)
@@ -190,20 +193,30 @@ __device__ void select_unit(KeyAt key_at, int n, int kk, int32_t* out, SelShared
   }
 
   // One ordered pass: kept-for-sure (key > hi) and candidates (lo <= key <= hi).
-  uint32_t gcnt = 0, ccnt = 0;
-  for (int base = 0; base < n; base += kSelChunk) {
+  // Chunks of 8192 keys are loaded coalesced one chunk ahead, staged in LDS,
+  // and read back as 8 consecutive keys per thread.
+  auto pad = [](int e) { return e + (e >> 3); };
+  uint32_t nxt[kSelPer];
+  auto load_chunk = [&](int base) {
 #pragma unroll
     for (int j = 0; j < kSelPer; ++j) {
       const int p = base + j * kSelThreads + tid;
-      sh.stage[j * kSelThreads + tid] = p < n ? key_at(p) : 0u;
+      nxt[j] = p < n ? key_at(p) : 0u;
     }
+  };
+  load_chunk(0);
+  uint32_t gcnt = 0, ccnt = 0;
+  for (int base = 0; base < n; base += kSelChunk) {
+#pragma unroll
+    for (int j = 0; j < kSelPer; ++j) sh.stage[pad(j * kSelThreads + tid)] = nxt[j];
+    if (base + kSelChunk < n) load_chunk(base + kSelChunk);  // uniform
     __syncthreads();
     uint32_t k8[kSelPer];
     uint32_t ng = 0, nc = 0;
 #pragma unroll
     for (int qd = 0; qd < kSelPer; ++qd) {
       const int p = base + kSelPer * tid + qd;
-      k8[qd] = sh.stage[kSelPer * tid + qd];
+      k8[qd] = sh.stage[pad(kSelPer * tid + qd)];
       const bool valid = p < n;
       ng += valid && k8[qd] > hi;
       nc += valid && k8[qd] >= lo && k8[qd] <= hi;
