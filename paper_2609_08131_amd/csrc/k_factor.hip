@@ -35,20 +35,15 @@ namespace jacap {
 // exact three-term split (its two-term error grows like ~1e-8 cond(A)).
 constexpr double kRefineCond = 2e3;
 
-__device__ __forceinline__ double readlane_f64(double v, int lane) {
-  const uint64_t b = __builtin_bit_cast(uint64_t, v);
-  const uint32_t lo = __builtin_amdgcn_readlane((int)(uint32_t)b, lane);
-  const uint32_t hi = __builtin_amdgcn_readlane((int)(uint32_t)(b >> 32), lane);
-  return __builtin_bit_cast(double, ((uint64_t)hi << 32) | lo);
-}
+// Eight waves: two per SIMD, so that one wave's LDS and fp64 latencies
+// overlap the other's work.
+constexpr int kFactorThreads = 512;
 
-// Lane N of each 16-lane row, broadcast to the row (DPP row_newbcast).
+// Lane N of each 16-lane row, broadcast to the row (one 64-bit DPP move,
+// row_newbcast).
 template <int N>
 __device__ __forceinline__ double row_bcast_f64(double v) {
-  const uint64_t b = __builtin_bit_cast(uint64_t, v);
-  const uint32_t lo = __builtin_amdgcn_update_dpp(0, (int)(uint32_t)b, 0x150 + N, 0xF, 0xF, false);
-  const uint32_t hi = __builtin_amdgcn_update_dpp(0, (int)(uint32_t)(b >> 32), 0x150 + N, 0xF, 0xF, false);
-  return __builtin_bit_cast(double, ((uint64_t)hi << 32) | lo);
+  return __builtin_amdgcn_update_dpp(v, v, 0x150 + N, 0xF, 0xF, false);
 }
 
 // 1 / sqrt(x) to full fp64 accuracy: hardware estimate, two Newton steps.
@@ -71,7 +66,7 @@ __device__ __forceinline__ void tri_index(int e, int& i, int& j) {
 // PASS 0: first factorisation (all units). PASS 1: refinement of the units
 // marked kUnitRefine by pass 0 (bf16 path), from their exact-split Gram.
 template <int D, bool FRAGS>
-__global__ __launch_bounds__(kThreads) void factor_kernel(Geo g, const double* __restrict__ red,
+__global__ __launch_bounds__(kFactorThreads) void factor_kernel(Geo g, const double* __restrict__ red,
                                                           double ridge, double piv_rel, int pass,
                                                           double* __restrict__ linv64,
                                                           uint16_t* __restrict__ lfrag,
@@ -90,33 +85,32 @@ __global__ __launch_bounds__(kThreads) void factor_kernel(Geo g, const double* _
   __shared__ double A[D * LD];
   __shared__ double dg[D];   // diagonal of A before factorisation
   __shared__ double idg[D];  // 1 / L_rr
-  __shared__ double red_sh[kThreads / 64];
+  __shared__ double red_sh[kFactorThreads / 64];
   __shared__ int bad;        // 0, or the unit flag that stops the factorisation
 
   // Lower triangle of A = ridge I + M from the upper blocks of M: pass p
   // copies block pair p (uniform), thread tid one entry of it.
   const double* R = red + (int64_t)u * (NPAIR * 256);
-  {
-    int bi = 0, bj = 0;
-    for (int p = 0; p < NPAIR; ++p) {
-      const int ln = tid / 4, r = tid % 4;
-      const int row = bi * 16 + (ln >> 4) * 4 + r;
-      const int col = bj * 16 + (ln & 15);
-      if (row <= col) A[col * LD + row] = R[p * 256 + tid];  // diagonal block: upper half only
-      if (++bj == NB) { ++bi; bj = bi; }
-    }
+  for (int e = tid; e < NPAIR * 256; e += kFactorThreads) {
+    int p = e >> 8, bi = 0;  // block pair p -> block (bi, bj), bi <= bj, row-major
+    while (p >= NB - bi) { p -= NB - bi; ++bi; }
+    const int bj = bi + p;
+    const int ln = (e & 255) / 4, r = e % 4;
+    const int row = bi * 16 + (ln >> 4) * 4 + r;
+    const int col = bj * 16 + (ln & 15);
+    if (row <= col) A[col * LD + row] = R[e];  // diagonal block: upper half only
   }
   if (tid == 0) bad = 0;
   __syncthreads();
   if (g.ridge_mat) {  // output-projection variant: A = R + M
     const double* Rm = g.ridge_mat + ((int64_t)un.l * g.H + un.h) * D * D;
-    for (int e = tid; e < D * D; e += kThreads) {
+    for (int e = tid; e < D * D; e += kFactorThreads) {
       const int r = e / D, cc = e % D;
       if (cc <= r) A[r * LD + cc] += Rm[e];
     }
     __syncthreads();
   }
-  for (int a = tid; a < D; a += kThreads) {
+  for (int a = tid; a < D; a += kFactorThreads) {
     if (!g.ridge_mat) A[a * LD + a] += ridge;
     dg[a] = A[a * LD + a];
     if (!isfinite(dg[a])) atomicOr(&bad, (int)kUnitNonfinite);
@@ -129,10 +123,17 @@ __global__ __launch_bounds__(kThreads) void factor_kernel(Geo g, const double* _
 
   // max over rows of sum_c |A[r][c]| (>= lambda_max(A), A symmetric with its
   // lower triangle stored); TPR threads per row.
-  constexpr int TPR = kThreads / D;
+  constexpr int TPR = kFactorThreads / D;
   const int prow = tid / TPR, ppart = tid % TPR;
   auto block_max = [&](double v) {
-    return block_combine(wave_max_f64(v), red_sh, [](double a, double b) { return fmax(a, b); });
+    v = wave_max_f64(v);
+    __syncthreads();
+    if (lane == 0) red_sh[wave] = v;
+    __syncthreads();
+    double m = red_sh[0];
+#pragma unroll
+    for (int w = 1; w < kFactorThreads / 64; ++w) m = fmax(m, red_sh[w]);
+    return m;
   };
   double anorm = 0.0;
   if (may_refine) {
@@ -158,7 +159,25 @@ __global__ __launch_bounds__(kThreads) void factor_kernel(Geo g, const double* _
       int code = 0;
 #pragma unroll
       for (int t = 0; t < 16; ++t) {
-        const double piv = readlane_f64(a[t], t);  // A[t][t], uniform
+        double piv;  // A[t][t], from lane t of the row
+        switch (t) {
+          case 0: piv = row_bcast_f64<0>(a[t]); break;
+          case 1: piv = row_bcast_f64<1>(a[t]); break;
+          case 2: piv = row_bcast_f64<2>(a[t]); break;
+          case 3: piv = row_bcast_f64<3>(a[t]); break;
+          case 4: piv = row_bcast_f64<4>(a[t]); break;
+          case 5: piv = row_bcast_f64<5>(a[t]); break;
+          case 6: piv = row_bcast_f64<6>(a[t]); break;
+          case 7: piv = row_bcast_f64<7>(a[t]); break;
+          case 8: piv = row_bcast_f64<8>(a[t]); break;
+          case 9: piv = row_bcast_f64<9>(a[t]); break;
+          case 10: piv = row_bcast_f64<10>(a[t]); break;
+          case 11: piv = row_bcast_f64<11>(a[t]); break;
+          case 12: piv = row_bcast_f64<12>(a[t]); break;
+          case 13: piv = row_bcast_f64<13>(a[t]); break;
+          case 14: piv = row_bcast_f64<14>(a[t]); break;
+          default: piv = row_bcast_f64<15>(a[t]); break;
+        }
         // A pivot that has lost all but piv_rel of its diagonal entry is within
         // the rounding noise of the accumulated Gram: A is numerically singular
         // at the path's working precision (rank-deficient M with ridge 0).
@@ -191,7 +210,7 @@ __global__ __launch_bounds__(kThreads) void factor_kernel(Geo g, const double* _
             case 14: lq = row_bcast_f64<14>(a[t]); break;
             default: lq = row_bcast_f64<15>(a[t]); break;
           }
-          a[q] -= a[t] * lq;
+          a[q] = fma(-a[t], lq, a[q]);
         }
       }
       if (code) {
@@ -211,16 +230,18 @@ __global__ __launch_bounds__(kThreads) void factor_kernel(Geo g, const double* _
       return;
     }
     // 2. Panel rows r >= c + 16: L[r, c:c+16] = A[r, c:c+16] L_kk^{-T}.
-    for (int r = c + 16 + tid; r < D; r += kThreads) {
+    for (int r = c + 16 + tid; r < D; r += kFactorThreads) {
       double x[16];
 #pragma unroll
       for (int t = 0; t < 16; ++t) x[t] = A[r * LD + c + t];
 #pragma unroll
       for (int t = 0; t < 16; ++t) {
-        double sum = x[t];
+        // x[t] = (A[r][c+t] - sum_q x[q] L[c+t][c+q]) / L[c+t][c+t]; the sum in
+        // four independent chains (latency, not order, bounds this loop)
+        double sp[4] = {x[t], 0.0, 0.0, 0.0};
 #pragma unroll
-        for (int q = 0; q < t; ++q) sum -= x[q] * A[(c + t) * LD + c + q];
-        x[t] = sum * idg[c + t];
+        for (int q = 0; q < t; ++q) sp[q & 3] = fma(-x[q], A[(c + t) * LD + c + q], sp[q & 3]);
+        x[t] = ((sp[0] + sp[1]) + (sp[2] + sp[3])) * idg[c + t];
       }
 #pragma unroll
       for (int t = 0; t < 16; ++t) A[r * LD + c + t] = x[t];
@@ -232,7 +253,7 @@ __global__ __launch_bounds__(kThreads) void factor_kernel(Geo g, const double* _
     const int m = D - c - 16;
     if (m > 0) {
       const int mt = m / 4, ntile = mt * (mt + 1) / 2;
-      for (int e = tid; e < ntile; e += kThreads) {
+      for (int e = tid; e < ntile; e += kFactorThreads) {
         int ti, tj;
         tri_index(e, ti, tj);
         const int r0 = c + 16 + 4 * ti, s0 = c + 16 + 4 * tj;
@@ -278,7 +299,7 @@ __global__ __launch_bounds__(kThreads) void factor_kernel(Geo g, const double* _
       if (i > t) A[(c + t) * LD + c + i] = x[i];
   }
   __syncthreads();
-  for (int e = tid; e < NB * 256; e += kThreads) {
+  for (int e = tid; e < NB * 256; e += kFactorThreads) {
     const int c = 16 * (e >> 8), i = (e >> 4) & 15, t = e & 15;
     if (i > t) A[(c + i) * LD + c + t] = A[(c + t) * LD + c + i];
     else if (i == t) A[(c + i) * LD + c + i] = idg[c + i];
@@ -291,10 +312,11 @@ __global__ __launch_bounds__(kThreads) void factor_kernel(Geo g, const double* _
   //    X21 = -T X11 (over L21). 4x4 output tiles.
   for (int h = 16; h < D; h *= 2) {
     const int npairs = D / (2 * h), tiles = (h / 4) * (h / 4);
-    for (int e = tid; e < npairs * tiles; e += kThreads) {
+    for (int e = tid; e < npairs * tiles; e += kFactorThreads) {
       const int o = (e / tiles) * 2 * h, tl = e % tiles;
       const int a0 = 4 * (tl / (h / 4)), b0 = 4 * (tl % (h / 4));
       double acc[4][4] = {};
+#pragma unroll 4
       for (int mm = 0; mm < a0 + 4; ++mm) {  // X22[a][mm] = 0 for mm > a
         double xv[4], lv[4];
 #pragma unroll
@@ -312,10 +334,11 @@ __global__ __launch_bounds__(kThreads) void factor_kernel(Geo g, const double* _
         for (int q = 0; q < 4; ++q) A[(o + b0 + q) * LD + o + h + a0 + p] = acc[p][q];  // T[a][b]
     }
     __syncthreads();
-    for (int e = tid; e < npairs * tiles; e += kThreads) {
+    for (int e = tid; e < npairs * tiles; e += kFactorThreads) {
       const int o = (e / tiles) * 2 * h, tl = e % tiles;
       const int a0 = 4 * (tl / (h / 4)), b0 = 4 * (tl % (h / 4));
       double acc[4][4] = {};
+#pragma unroll 4
       for (int mm = b0; mm < h; ++mm) {  // X11[mm][b] = 0 for mm < b
         double tv[4], xv[4];
 #pragma unroll
@@ -362,7 +385,7 @@ __global__ __launch_bounds__(kThreads) void factor_kernel(Geo g, const double* _
   // Store L^{-1}.
   if constexpr (!FRAGS) {
     double* o64 = linv64 + (int64_t)u * D * D;
-    for (int e = tid; e < D * D; e += kThreads) {
+    for (int e = tid; e < D * D; e += kFactorThreads) {
       const int a = e / D, b = e % D;
       o64[e] = (b <= a) ? xinv(a, b) : 0.0;
     }
@@ -371,7 +394,7 @@ __global__ __launch_bounds__(kThreads) void factor_kernel(Geo g, const double* _
     // (b = 32 kb + 8 kg + q): lane (ch, kg) holds 8 bf16; hi then lo.
     constexpr int NLP = (NB / 2) * (NB / 2 + 1);  // lower (j, kb) pairs: sum_j (j/2 + 1)
     uint16_t* out = lfrag + (int64_t)u * NLP * 2 * 64 * 8;
-    for (int e = tid; e < NLP * 64; e += kThreads) {
+    for (int e = tid; e < NLP * 64; e += kFactorThreads) {
       const int qp = e / 64, ln = e % 64, ch = ln & 15, kg = ln >> 4;
       int j = 0, kb = 0, q = qp;
       for (int jj = 0; jj < NB; ++jj) {
@@ -412,11 +435,11 @@ hipError_t launch_factor(const Launch& L, bool refine) {
   // path ~1e-15.
   const double piv_rel = L.ws.mfma ? 1e-4 : 1e-12;
   if (L.ws.mfma) {
-    if (g.D == 128) factor_kernel<128, true><<<g.U, kThreads, 0, L.stream>>>(g, red, ridge, piv_rel, pass, l64, lf, st, uf);
-    else factor_kernel<64, true><<<g.U, kThreads, 0, L.stream>>>(g, red, ridge, piv_rel, pass, l64, lf, st, uf);
+    if (g.D == 128) factor_kernel<128, true><<<g.U, kFactorThreads, 0, L.stream>>>(g, red, ridge, piv_rel, pass, l64, lf, st, uf);
+    else factor_kernel<64, true><<<g.U, kFactorThreads, 0, L.stream>>>(g, red, ridge, piv_rel, pass, l64, lf, st, uf);
   } else {
-    if (g.D == 128) factor_kernel<128, false><<<g.U, kThreads, 0, L.stream>>>(g, red, ridge, piv_rel, pass, l64, lf, st, uf);
-    else factor_kernel<64, false><<<g.U, kThreads, 0, L.stream>>>(g, red, ridge, piv_rel, pass, l64, lf, st, uf);
+    if (g.D == 128) factor_kernel<128, false><<<g.U, kFactorThreads, 0, L.stream>>>(g, red, ridge, piv_rel, pass, l64, lf, st, uf);
+    else factor_kernel<64, false><<<g.U, kFactorThreads, 0, L.stream>>>(g, red, ridge, piv_rel, pass, l64, lf, st, uf);
   }
   return hipGetLastError();
 }
