@@ -54,6 +54,14 @@ __device__ __forceinline__ double rsqrt_f64(double x) {
   return y;
 }
 
+typedef double f64x4 __attribute__((ext_vector_type(4)));
+
+// D += A B on the fp64 MFMA (16x16x4): lane l supplies A[l % 16][l / 16] and
+// B[l / 16][l % 16]; element i of lane l's result is D[4 i + l / 16][l % 16].
+__device__ __forceinline__ f64x4 mfma64(double a, double b, f64x4 acc) {
+  return __builtin_amdgcn_mfma_f64_16x16x4f64(a, b, acc, 0, 0, 0);
+}
+
 // Lower-triangle index e -> (row i, column j), j <= i (row-major over the triangle).
 __device__ __forceinline__ void tri_index(int e, int& i, int& j) {
   int r = (int)((sqrtf(8.0f * (float)e + 1.0f) - 1.0f) * 0.5f);
@@ -247,33 +255,25 @@ __global__ __launch_bounds__(kFactorThreads) void factor_kernel(Geo g, const dou
       for (int t = 0; t < 16; ++t) A[r * LD + c + t] = x[t];
     }
     __syncthreads();
-    // 3. Trailing update A[r][s] -= sum_t L[r][c+t] L[s][c+t], r >= s >= c + 16,
-    //    in 4x4 tiles (diagonal tiles also touch their upper half, which is
-    //    unused until the inverse overwrites it).
-    const int m = D - c - 16;
+    // 3. Trailing update A_IJ -= L_Ik L_Jk^T for the 16x16 blocks I >= J > k,
+    //    one block per wave at a time on the fp64 MFMA (K = 16 in four
+    //    slices). Diagonal blocks also update their upper half, which is
+    //    unused until the inverse overwrites it.
+    const int m = NB - kb - 1;
     if (m > 0) {
-      const int mt = m / 4, ntile = mt * (mt + 1) / 2;
-      for (int e = tid; e < ntile; e += kFactorThreads) {
-        int ti, tj;
-        tri_index(e, ti, tj);
-        const int r0 = c + 16 + 4 * ti, s0 = c + 16 + 4 * tj;
-        double acc[4][4] = {};
+      const int r16 = lane & 15, q4 = lane >> 4;
+      for (int e = wave; e < m * (m + 1) / 2; e += kFactorThreads / 64) {
+        int bi, bj;
+        tri_index(e, bi, bj);
+        const int I = 16 * (kb + 1 + bi), J = 16 * (kb + 1 + bj);
+        f64x4 acc = {0.0, 0.0, 0.0, 0.0};
 #pragma unroll
-        for (int t = 0; t < 16; ++t) {
-          double av[4], bv[4];
-#pragma unroll
-          for (int i = 0; i < 4; ++i) av[i] = A[(r0 + i) * LD + c + t];
-#pragma unroll
-          for (int j = 0; j < 4; ++j) bv[j] = A[(s0 + j) * LD + c + t];
-#pragma unroll
-          for (int i = 0; i < 4; ++i)
-#pragma unroll
-            for (int j = 0; j < 4; ++j) acc[i][j] += av[i] * bv[j];
+        for (int kq = 0; kq < 4; ++kq) {
+          const int t = c + 4 * kq + q4;
+          acc = mfma64(A[(I + r16) * LD + t], A[(J + r16) * LD + t], acc);
         }
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
-#pragma unroll
-          for (int j = 0; j < 4; ++j) A[(r0 + i) * LD + s0 + j] -= acc[i][j];
+        for (int i = 0; i < 4; ++i) A[(I + 4 * i + q4) * LD + J + r16] -= acc[i];
       }
     }
     __syncthreads();
@@ -305,58 +305,52 @@ __global__ __launch_bounds__(kFactorThreads) void factor_kernel(Geo g, const dou
     else if (i == t) A[(c + i) * LD + c + i] = idg[c + i];
   }
   __syncthreads();
-  // X[r][c] (zero above the diagonal).
-  auto xat = [&](int r, int cc) -> double { return r >= cc ? A[r * LD + cc] : 0.0; };
   // 5. Recursive doubling. Pair at offset o, halves of h rows:
   //    T = X22 L21 (into the pair's upper off-diagonal block, free), then
-  //    X21 = -T X11 (over L21). 4x4 output tiles.
-  for (int h = 16; h < D; h *= 2) {
-    const int npairs = D / (2 * h), tiles = (h / 4) * (h / 4);
-    for (int e = tid; e < npairs * tiles; e += kFactorThreads) {
-      const int o = (e / tiles) * 2 * h, tl = e % tiles;
-      const int a0 = 4 * (tl / (h / 4)), b0 = 4 * (tl % (h / 4));
-      double acc[4][4] = {};
-#pragma unroll 4
-      for (int mm = 0; mm < a0 + 4; ++mm) {  // X22[a][mm] = 0 for mm > a
-        double xv[4], lv[4];
+  //    X21 = -T X11 (over L21). 16x16 output blocks, one per wave at a time,
+  //    on the fp64 MFMA; the triangular operands are masked to zero above
+  //    their diagonal.
+  {
+    const int r16 = lane & 15, q4 = lane >> 4;
+    for (int h = 16; h < D; h *= 2) {
+      const int hb = h / 16, nout = (D / (2 * h)) * hb * hb;
+      for (int e = wave; e < nout; e += kFactorThreads / 64) {
+        const int o = (e / (hb * hb)) * 2 * h, ab = (e % (hb * hb)) / hb, bb = e % hb;
+        f64x4 acc = {0.0, 0.0, 0.0, 0.0};
+        for (int mb = 0; mb <= ab; ++mb) {  // X22 block (ab, mb) is zero for mb > ab
 #pragma unroll
-        for (int p = 0; p < 4; ++p) xv[p] = xat(o + h + a0 + p, o + h + mm);
+          for (int kq = 0; kq < 4; ++kq) {
+            const int t = 4 * kq + q4;
+            const double x = (mb < ab || r16 >= t) ? A[(o + h + 16 * ab + r16) * LD + o + h + 16 * mb + t] : 0.0;
+            const double l = A[(o + h + 16 * mb + t) * LD + o + 16 * bb + r16];
+            acc = mfma64(x, l, acc);
+          }
+        }
 #pragma unroll
-        for (int q = 0; q < 4; ++q) lv[q] = A[(o + h + mm) * LD + o + b0 + q];
-#pragma unroll
-        for (int p = 0; p < 4; ++p)
-#pragma unroll
-          for (int q = 0; q < 4; ++q) acc[p][q] += xv[p] * lv[q];
+        for (int i = 0; i < 4; ++i)  // T[a][b] at A[o + b][o + h + a]
+          A[(o + 16 * bb + r16) * LD + o + h + 16 * ab + 4 * i + q4] = acc[i];
       }
+      __syncthreads();
+      for (int e = wave; e < nout; e += kFactorThreads / 64) {
+        const int o = (e / (hb * hb)) * 2 * h, ab = (e % (hb * hb)) / hb, bb = e % hb;
+        f64x4 acc = {0.0, 0.0, 0.0, 0.0};
+        for (int mb = bb; mb < hb; ++mb) {  // X11 block (mb, bb) is zero for mb < bb
 #pragma unroll
-      for (int p = 0; p < 4; ++p)
+          for (int kq = 0; kq < 4; ++kq) {
+            const int t = 4 * kq + q4;
+            const double tv = A[(o + 16 * mb + t) * LD + o + h + 16 * ab + r16];  // T[a][m]
+            const double x = (mb > bb || t >= r16) ? A[(o + 16 * mb + t) * LD + o + 16 * bb + r16] : 0.0;
+            acc = mfma64(tv, x, acc);
+          }
+        }
 #pragma unroll
-        for (int q = 0; q < 4; ++q) A[(o + b0 + q) * LD + o + h + a0 + p] = acc[p][q];  // T[a][b]
-    }
-    __syncthreads();
-    for (int e = tid; e < npairs * tiles; e += kFactorThreads) {
-      const int o = (e / tiles) * 2 * h, tl = e % tiles;
-      const int a0 = 4 * (tl / (h / 4)), b0 = 4 * (tl % (h / 4));
-      double acc[4][4] = {};
-#pragma unroll 4
-      for (int mm = b0; mm < h; ++mm) {  // X11[mm][b] = 0 for mm < b
-        double tv[4], xv[4];
-#pragma unroll
-        for (int p = 0; p < 4; ++p) tv[p] = A[(o + mm) * LD + o + h + a0 + p];  // T[a][mm]
-#pragma unroll
-        for (int q = 0; q < 4; ++q) xv[q] = xat(o + mm, o + b0 + q);
-#pragma unroll
-        for (int p = 0; p < 4; ++p)
-#pragma unroll
-          for (int q = 0; q < 4; ++q) acc[p][q] += tv[p] * xv[q];
+        for (int i = 0; i < 4; ++i) A[(o + h + 16 * ab + 4 * i + q4) * LD + o + 16 * bb + r16] = -acc[i];
       }
-#pragma unroll
-      for (int p = 0; p < 4; ++p)
-#pragma unroll
-        for (int q = 0; q < 4; ++q) A[(o + h + a0 + p) * LD + o + b0 + q] = -acc[p][q];  // X21
+      __syncthreads();
     }
-    __syncthreads();
   }
+  // X[r][c] (zero above the diagonal).
+  auto xat = [&](int r, int cc) -> double { return r >= cc ? A[r * LD + cc] : 0.0; };
 
   auto xinv = xat;
 
