@@ -37,7 +37,7 @@ __device__ __forceinline__ uint32_t score_key(float f) {
 struct SelShared {
   // staged chunk keys (one pad word per 8: the per-thread reads of 8
   // consecutive keys are then bank-conflict free) / sample keys / kept
-  // candidate positions
+  // candidate positions / evicted positions
   uint32_t stage[kSelChunk + kSelChunk / 8];
   uint32_t ckey[kCandCap];    // candidate keys (position order)
   int32_t cpos[kCandCap];     // candidate positions
@@ -47,7 +47,9 @@ struct SelShared {
   uint32_t bc[2];
 };
 
-// Exclusive prefix sum over kSelThreads values (one per thread), fixed order.
+// Exclusive prefix sum over kSelThreads values (one per thread), fixed order:
+// a wave scan, then every thread adds the totals of the waves before its own
+// (broadcast LDS reads, no serial pass).
 __device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t x, uint32_t* sh, uint32_t& total) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   uint32_t incl = x;
@@ -59,18 +61,15 @@ __device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t x, uint32_t* s
   __syncthreads();
   if (lane == 63) sh[wave] = incl;
   __syncthreads();
-  if (tid == 0) {
-    uint32_t run = 0;
-    for (int i = 0; i < kSelThreads / 64; ++i) {
-      const uint32_t t = sh[i];
-      sh[i] = run;
-      run += t;
-    }
-    sh[kSelThreads / 64] = run;
+  uint32_t before = 0, all = 0;
+#pragma unroll
+  for (int w = 0; w < kSelThreads / 64; ++w) {
+    const uint32_t t = sh[w];
+    before += w < wave ? t : 0u;
+    all += t;
   }
-  __syncthreads();
-  total = sh[kSelThreads / 64];
-  return sh[wave] + incl - x;
+  total = all;
+  return before + incl - x;
 }
 
 // Radix select (11 + 11 + 10 bits, MSB first): the key of rank `rank`
@@ -166,8 +165,9 @@ __device__ __forceinline__ int lower_bound_lds(const int32_t* a, int cnt, int32_
 
 // TOP-kk of key_at(0 .. n-1) by (key desc, position asc), written to out[0 ..
 // kk) in ascending position order (0 < kk < n).
-template <class KeyAt>
-__device__ void select_unit(KeyAt key_at, int n, int kk, int32_t* out, SelShared& sh) {
+template <class KeyAt, class RawAt, class Conv>
+__device__ void select_unit(KeyAt key_at, RawAt raw_at, Conv conv, int n, int kk, int32_t* out,
+                            SelShared& sh) {
   const int tid = threadIdx.x;
   // Bracket [lo, hi] of T from the sample (the whole unit if it fits the band).
   uint32_t lo = 0u, hi = 0xFFFFFFFFu;
@@ -193,22 +193,24 @@ __device__ void select_unit(KeyAt key_at, int n, int kk, int32_t* out, SelShared
   }
 
   // One ordered pass: kept-for-sure (key > hi) and candidates (lo <= key <= hi).
-  // Chunks of 8192 keys are loaded coalesced one chunk ahead, staged in LDS,
-  // and read back as 8 consecutive keys per thread.
+  // Chunks of 8192 scores are loaded coalesced one chunk ahead (kept raw until
+  // staged, so that no conversion waits on the loads early), staged in LDS
+  // with a pad word per 8 keys, and read back as 8 consecutive keys per
+  // thread (bank-conflict free); the block scan orders the threads' lists.
   auto pad = [](int e) { return e + (e >> 3); };
-  uint32_t nxt[kSelPer];
+  float nxt[kSelPer];
   auto load_chunk = [&](int base) {
 #pragma unroll
-    for (int j = 0; j < kSelPer; ++j) {
-      const int p = base + j * kSelThreads + tid;
-      nxt[j] = p < n ? key_at(p) : 0u;
-    }
+    for (int j = 0; j < kSelPer; ++j) nxt[j] = raw_at(min(base + j * kSelThreads + tid, n - 1));
   };
   load_chunk(0);
   uint32_t gcnt = 0, ccnt = 0;
   for (int base = 0; base < n; base += kSelChunk) {
 #pragma unroll
-    for (int j = 0; j < kSelPer; ++j) sh.stage[pad(j * kSelThreads + tid)] = nxt[j];
+    for (int j = 0; j < kSelPer; ++j) {
+      const int p = base + j * kSelThreads + tid;
+      sh.stage[pad(j * kSelThreads + tid)] = p < n ? conv(nxt[j]) : 0u;
+    }
     if (base + kSelChunk < n) load_chunk(base + kSelChunk);  // uniform
     __syncthreads();
     uint32_t k8[kSelPer];
@@ -314,7 +316,8 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(Geo g, const float*
   // (~key desc, reversed position asc)), then emit every other position.
   const int m = n - kk;
   if (m < kk && m <= kSelChunk) {
-    select_unit([&](int i) { return ~score_key(s[n - 1 - i]); }, n, m, out, sh);
+    select_unit([&](int i) { return ~score_key(s[n - 1 - i]); }, [&](int i) { return s[n - 1 - i]; },
+                [](float f) { return ~score_key(f); }, n, m, out, sh);
     __syncthreads();  // out[0 .. m): evicted, as reversed positions ascending
     uint32_t* ev = sh.stage;
     for (int j = tid; j < m; j += kSelThreads) ev[j] = (uint32_t)(n - 1 - out[m - 1 - j]);
@@ -326,7 +329,8 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(Geo g, const float*
     }
     return;
   }
-  select_unit([&](int i) { return score_key(s[i]); }, n, kk, out, sh);
+  select_unit([&](int i) { return score_key(s[i]); }, [&](int i) { return s[i]; },
+              [](float f) { return score_key(f); }, n, kk, out, sh);
 }
 
 hipError_t launch_select(const Launch& L, const float* scores, int32_t* idx) {
