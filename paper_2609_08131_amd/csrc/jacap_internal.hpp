@@ -135,20 +135,6 @@ __device__ __forceinline__ float to_f32<float>(float x) { return x; }
 template <>
 __device__ __forceinline__ float to_f32<uint16_t>(uint16_t x) { return bf16_to_f32(x); }
 
-// Importance weight of Eq. 8 from the stored logit z and query response kappa,
-// given the unit's logit max m and softmax normaliser Z:
-//   e = exp(z - m), alpha = e / Z, 1 - alpha = (Z - e) / Z,
-//   w = (alpha (1 - alpha))^2 kappa / d.
-// Shared by the Gram and leverage passes so both see bit-identical weights.
-__device__ __forceinline__ double importance_weight(float z, float kappa, float m, double Z,
-                                                    double inv_d) {
-  double e = exp((double)z - (double)m);
-  double a = e / Z;
-  double oma = (Z - e) / Z;
-  double rho = a * oma;
-  return rho * rho * (double)kappa * inv_d;
-}
-
 // DPP lane exchanges inside each 16-lane row (one VALU instruction each):
 // quad swaps (lane ^ 1, lane ^ 2), the half-row mirror (i <-> 7 - i within 8)
 // and the row mirror (i <-> 15 - i).

@@ -531,8 +531,31 @@ __global__ __launch_bounds__(kThreads) void softmax_weights_kernel(
   if (chunk == 0 && tid == 0) { m_out[u] = m; z_out[u] = s; }
   const int64_t trow = token_row(g, un);
   const int end = min(un.n, base + kWChunk);
-  for (int t = base + tid; t < end; t += kThreads)
-    wout[trow + t] = (float)importance_weight(zbuf[trow + t], kbuf[trow + t], m, s, inv_d);
+  // Eq. 8 per token: e = exp(z - m) from the fp32 exponential of the rounded
+  // difference, corrected to first order by the difference's rounding error
+  // (relative error ~1e-7), alpha = e / Z and 1 - alpha = (Z - e) / Z in fp64.
+  const double invZ = 1.0 / s;
+  auto weight = [&](float z, float kap) {
+    const double dz = (double)z - (double)m;  // exact
+    const float df = (float)dz;
+    const double e = (double)expf(df) * (1.0 + (dz - (double)df));
+    const double rho = (e * invZ) * ((s - e) * invZ);
+    return (float)(rho * rho * (double)kap * inv_d);
+  };
+  constexpr int U4 = 4;
+  static_assert(kWChunk % (U4 * kThreads) == 0, "whole unrolled trips per chunk");
+  for (int t0 = base + tid; t0 < end; t0 += U4 * kThreads) {
+    float z[U4], kq[U4];
+#pragma unroll
+    for (int j = 0; j < U4; ++j) {
+      const int t = min(t0 + j * kThreads, end - 1);
+      z[j] = zbuf[trow + t];
+      kq[j] = kbuf[trow + t];
+    }
+#pragma unroll
+    for (int j = 0; j < U4; ++j)
+      if (t0 + j * kThreads < end) wout[trow + t0 + j * kThreads] = weight(z[j], kq[j]);
+  }
 }
 
 hipError_t launch_softmax_weights(const Launch& L) {
