@@ -203,6 +203,10 @@ __device__ __forceinline__ void raise_flags(uint32_t* status, uint32_t* uflags, 
 // step of a streaming loop without clamping row indices: the range ends at
 // the last row the step may use, and the per-lane offsets stay constant.
 constexpr int kBufferFormat = 0x00020000;
+// Cache policy of a streamed load: non-temporal (no reuse expected). Only for
+// loads whose wave reads whole 128-byte lines: a line read in halves by two
+// loads would be fetched twice.
+constexpr int kPolicyStream = 2;
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_range(const void* base, int32_t bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, bytes, kBufferFormat);
 }
@@ -212,8 +216,9 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_range(const void* base,
 __device__ __forceinline__ int32_t rows_bytes(int32_t rows, int32_t stride, int32_t row_bytes) {
   return rows > 0 ? (rows - 1) * stride + row_bytes : 0;
 }
+template <int POLICY = 0>
 __device__ __forceinline__ uint4 buffer_load16(__amdgpu_buffer_rsrc_t r, int32_t off) {
-  const auto x = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
+  const auto x = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, POLICY);
   return uint4{x[0], x[1], x[2], x[3]};
 }
 __device__ __forceinline__ float buffer_load_f32(__amdgpu_buffer_rsrc_t r, int32_t off) {

@@ -150,7 +150,7 @@ __device__ __forceinline__ void gram_wave(const GramArgs& ga, uint16_t* tiles, f
     const int32_t rows = min(left, kGramStep);
     const auto vr = buffer_range(vnext, rows_bytes(rows, vstb, D * 2));
 #pragma unroll
-    for (int r = 0; r < LOADS; ++r) buf.v[r] = buffer_load16(vr, voff[r]);
+    for (int r = 0; r < LOADS; ++r) buf.v[r] = buffer_load16<kPolicyStream>(vr, voff[r]);  // whole lines
     buf.w = buffer_load_f32(buffer_range(wnext, max(rows, 0) * 4), woff);
     vnext += kGramStep * ga.vst;
     wnext += kGramStep;
