@@ -112,3 +112,18 @@ def test_ragged16():
     _check_sampled(case, prob, budget, 1.0, "ragged16")
     del prob, case
     _free()
+
+
+def test_decode16k():
+    """Decoding-stage eviction at its bench shape: 16 sequences x 32 layers x 8
+    KV heads of 16512 tokens, budget 16384. The budget keeps more than half of
+    every unit, so selection ranks the 128 evictions (the complement path)."""
+    case = make_case("decode16k", device="cuda")
+    budget = case.workload.budget_k
+    prob, flags = run_gpu(case, budget)
+    assert flags == 0, flags
+    _check_all_units_properties(case, prob, budget, 1.0)
+    _check_sampled(case, prob, budget, 1.0, "decode16k")
+    del prob
+    del case
+    _free()

@@ -173,3 +173,32 @@ def test_greedy_vs_leverage_quality_report(jacap, ridge):
     r = np.array(rows)
     print(f"\n[quality] prefill32k ridge {ridge:g} B={budget}: leverage/greedy log-det gain "
           f"min {r[:, 0].min():.4f} mean {r[:, 0].mean():.4f}; set overlap mean {r[:, 1].mean():.3f}")
+
+
+def test_greedy_long128k_full_batch(jacap):
+    """The comparator on the full long128k batch (256 units x 131072 tokens,
+    B = 1024): every unit's output is a valid selection, and one sampled unit's
+    pick order is replayed through the fp64 oracle."""
+    case = make_case("long128k", device="cuda")
+    budget = case.workload.budget_k
+    prob, flags = run_greedy(jacap, case, budget)
+    assert flags == 0, flags
+    n = case.seq_lens[0]
+    idx, order = prob.idx[0], prob.order[0]                # [L][H][B]
+    assert torch.all(idx >= 0) and torch.all(idx < n)
+    assert torch.all(torch.diff(idx, dim=-1) > 0)
+    assert torch.equal(torch.sort(order, dim=-1).values, idx)
+    assert torch.isfinite(prob.logdet).all() and (prob.logdet > 0).all()   # ridge 1: log det > 0
+    l, h = 19, 5
+    q, k, v = case.unit_arrays(0, l, h)
+    w = jo.score_unit(q, k, v)["w"]
+    got = order[l, h].cpu().numpy()
+    chosen, best = jo.greedy_replay(v, w, 1.0, got)
+    rel = (best - chosen) / np.abs(best)
+    assert rel.max() <= GAIN_TOL["bf16"], float(rel.max())
+    ref = jo.greedy_logdet(v, w, 1.0, budget)
+    diff = np.nonzero(ref != got)[0]
+    print(f"\n[greedy] long128k unit (0, {l}, {h}): worst replay gap {rel.max():.2e}; "
+          f"identical prefix {(diff[0] if len(diff) else budget)} of {budget}", flush=True)
+    del prob, case
+    torch.cuda.empty_cache()
