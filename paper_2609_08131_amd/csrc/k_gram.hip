@@ -65,10 +65,10 @@ __device__ __forceinline__ s16x4 lds_read_tr16(const uint16_t* p) {
       (__attribute__((address_space(3))) s16x4*)(p));
 }
 
-// The workgroup walks its chunk in steps of 32 tokens. Each step is loaded
-// with coalesced 16-byte loads (prefetched two steps ahead) and staged in LDS
-// token-major (double-buffered, one barrier per step); the four waves share
-// it. The upper 16x16 block pairs (i <= j) are split between the waves by
+// The workgroup walks its chunk in steps of 32 tokens. Each step is read with
+// 16-byte buffer loads (non-temporal; each wave load covers whole 128-byte
+// lines), prefetched two steps ahead, and staged in LDS token-major
+// (double-buffered, one barrier per step); the four waves share it. The upper 16x16 block pairs (i <= j) are split between the waves by
 // column pairs {w, NB-1-w}, which gives every wave the same number of pairs
 // (9 at d = 128), so no cross-wave reduction is needed.
 //
@@ -247,12 +247,12 @@ __device__ __forceinline__ void gram_wave(const GramArgs& ga, uint16_t* tiles, f
       }
     }
   };
-  // One step: stage the prefetched data, barrier, prefetch two steps ahead,
-  // compute. The two buffers alternate with the step parity.
-  auto step = [&](int st, Pre& buf, int half, auto firstc) {
+  // One step: stage the prefetched data, barrier, prefetch the step two
+  // ahead, compute. The two buffers alternate with the step parity.
+  auto step = [&](Pre& buf, int half, auto firstc) {
     stage(buf, tiles + half * TILE, wts + half * kGramStep);
     __syncthreads();
-    buf = gload();  // step st + 2 (empty past the chunk end): static wait counts
+    buf = gload();  // two steps ahead (empty past the chunk end): static wait counts
     __builtin_amdgcn_sched_barrier(0);        // keep the loads ahead of this step's MFMAs
     compute(tiles + half * TILE, wts + half * kGramStep, firstc);
   };
@@ -262,10 +262,10 @@ __device__ __forceinline__ void gram_wave(const GramArgs& ga, uint16_t* tiles, f
   Pre b1 = gload();
   drain_vmem();  // prologue loads done: the loop's wait counts then stay static
   for (int st = 0; st < ga.nsteps; st += kGramFlush) {
-    step(st, b0, 0, std::true_type{});
-    step(st + 1, b1, 1, std::false_type{});
-    step(st + 2, b0, 0, std::false_type{});
-    step(st + 3, b1, 1, std::false_type{});
+    step(b0, 0, std::true_type{});
+    step(b1, 1, std::false_type{});
+    step(b0, 0, std::false_type{});
+    step(b1, 1, std::false_type{});
 #pragma unroll
     for (int p = 0; p < NP; ++p) acc2[p] = acc2[p] + acc32[p];
   }
