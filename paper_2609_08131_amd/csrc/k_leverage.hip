@@ -52,33 +52,49 @@ __global__ __launch_bounds__(kThreads, 2) void leverage_mfma_kernel(
 
   // A step is 16 tokens (one MFMA row tile). V rows are prefetched two
   // steps ahead into three rotating register buffers (the loop is unrolled
-  // by three so the buffers stay in fixed registers). Each step reads its
-  // rows through a buffer range that ends at the chunk's last row: rows past
-  // it load as zeros (and are not stored), so every load is issued
-  // unconditionally with a fixed per-lane offset, and the compiler's wait
-  // counts stay static. MFMAs are issued kb-outer so that consecutive MFMAs
-  // update different output blocks.
+  // by three so the buffers stay in fixed registers). A step's 16 rows are
+  // read whole: each wave load brings RPL consecutive rows (d / 8 lanes per
+  // row, 1 KB of contiguous lines, non-temporal), through a buffer range
+  // that ends at the chunk's last row (rows past it load as zeros and are not
+  // stored), so every load is unconditional with a fixed per-lane offset and
+  // the compiler's wait counts stay static. The rows then pass through a
+  // wave-private LDS tile into the MFMA operand layout (lane (ch, kg) of
+  // K-block kb: row ch, channels 32 kb + 8 kg .. + 7). MFMAs are issued
+  // kb-outer so that consecutive MFMAs update different output blocks.
   // One prefetched step: the lane's V row pieces and the weight of the token
   // whose score this lane writes.
-  struct Buf { bf16x8 a[NK]; float w; };
+  struct Buf { uint4 a[NK]; float w; };
+  constexpr int PITCH = D * 2 + 16;             // bytes per tile row (the pad spreads the banks)
+  __shared__ __attribute__((aligned(16))) char tiles[kThreads / 64][16 * PITCH];
+  char* tile = tiles[wave];
   const int32_t vstb = (int32_t)g.vst * 2;
+  constexpr int LPR = D / 8;                    // lanes per whole row (16 bytes each)
+  constexpr int RPL = 64 / LPR;                 // rows per wave load
+  static_assert(RPL * NK == 16, "a step's 16 rows in NK whole-row loads");
+  const int rrow = lane / LPR, rpc = lane % LPR;  // row (of RPL) and 16-byte piece of a load
   int32_t voff[NK];
 #pragma unroll
-  for (int kb = 0; kb < NK; ++kb) voff[kb] = ch * vstb + (32 * kb + 8 * kg) * 2;
+  for (int i = 0; i < NK; ++i) voff[i] = (RPL * i + rrow) * vstb + rpc * 16;
   const int32_t woff = (4 * kg + rl) * 4;
   const float* wb = wbuf + trow;
   auto load = [&](int t0, Buf& b) {
     const int32_t rows = min(end - t0, 16);
     const auto vr = buffer_range(vb + (int64_t)t0 * g.vst, rows_bytes(rows, vstb, D * 2));
 #pragma unroll
-    for (int kb = 0; kb < NK; ++kb) b.a[kb] = __builtin_bit_cast(bf16x8, buffer_load16(vr, voff[kb]));
+    for (int i = 0; i < NK; ++i) b.a[i] = buffer_load16<kPolicyStream>(vr, voff[i]);
     b.w = buffer_load_f32(buffer_range(wb + t0, max(rows, 0) * 4), woff);
     __builtin_amdgcn_sched_barrier(0);  // issue here, ahead of the MFMAs that follow
   };
   auto step = [&](int t0, const Buf& b) {
     const int tw = t0 + 4 * kg + rl;
     const float wt = b.w;
-    const bf16x8 (&cur)[NK] = b.a;
+#pragma unroll
+    for (int i = 0; i < NK; ++i)
+      *reinterpret_cast<uint4*>(tile + (RPL * i + rrow) * PITCH + rpc * 16) = b.a[i];
+    bf16x8 cur[NK];
+#pragma unroll
+    for (int kb = 0; kb < NK; ++kb)
+      cur[kb] = *reinterpret_cast<const bf16x8*>(tile + ch * PITCH + kb * 64 + kg * 16);
     // Output blocks j = 2 jp and 2 jp + 1 share the K-block range kb <= jp:
     // their two accumulation chains are interleaved.
     float ss[4] = {0.f, 0.f, 0.f, 0.f};
