@@ -1,8 +1,9 @@
 // Leverage score of Eq. 10: score_i = w_i v_i^T A^{-1} v_i = w_i ||L^{-1} v_i||^2.
 //
 // bf16 inputs: Y = V L^{-T} on MFMA 16x16x32 bf16. The token dimension is the
-// MFMA row dimension, so each lane loads 8 consecutive channels of one token
-// straight from HBM (16 bytes, no transpose). L^{-1} is split into bf16
+// MFMA row dimension. V rows are read whole (each wave load covers complete
+// 128-byte lines, streamed non-temporally) and pass through a small
+// wave-private LDS tile into the operand layout. L^{-1} is split into bf16
 // hi + lo and kept in registers; only the K-blocks with b <= a of the lower
 // triangle are multiplied. The squared row norm is reduced across the 16
 // lanes that share a token.
