@@ -4,6 +4,8 @@
 #include <math.h>
 #include <string.h>
 
+#include <algorithm>
+
 #include "jacap_internal.hpp"
 
 using namespace jacap;
@@ -65,13 +67,17 @@ Workspace layout(const jacap_config* c, const jacap_batch* b, bool greedy = fals
   w.kchunks = (maxn + kKChunk - 1) / kKChunk;
   w.wchunks = (maxn + kWChunk - 1) / kWChunk;
   w.gchunk = w.mfma ? kGChunkMfma : kGChunkPrecise;
-  // Larger chunks write and re-read fewer partials; the chunk doubles while
-  // the grid keeps kGramMinBlocks blocks and the longest sequence at least 8
-  // chunks (so that its ragged last chunk stays a small share).
-  if (w.mfma)
-    while (w.gchunk < kGChunkMfmaMax && 16 * (int64_t)w.gchunk <= maxn &&
-           U * (int64_t)((maxn + 2 * w.gchunk - 1) / (2 * w.gchunk)) >= kGramMinBlocks)
-      w.gchunk *= 2;
+  // Larger chunks write and re-read fewer partials. The longest sequence is
+  // cut into the fewest equal chunks (whole 128-token flush spans) that keep
+  // kGramMinBlocks blocks in the grid and no chunk above kGChunkMfmaMax
+  // tokens; chunks stay at least kGChunkMfma tokens.
+  if (w.mfma && maxn > 0) {
+    const int64_t span = kGramSpan;
+    const int64_t nmin = (kGramMinBlocks + U - 1) / U;
+    const int64_t nch = std::max(nmin, (int64_t)(maxn + kGChunkMfmaMax - 1) / kGChunkMfmaMax);
+    const int64_t per = ((maxn + nch - 1) / nch + span - 1) / span * span;
+    w.gchunk = (int)std::min<int64_t>(std::max<int64_t>(per, kGChunkMfma), kGChunkMfmaMax);
+  }
   w.gchunks = (maxn + w.gchunk - 1) / w.gchunk;
   w.gparts = 1;
   const int lchunk = w.mfma ? kLChunkMfma : kLChunkPrecise;

@@ -16,7 +16,8 @@ constexpr int kThreads = 256;        // 4 wave64 per workgroup
 constexpr int kKChunk = 1024;        // tokens per workgroup in the K pass
 constexpr int kGChunkMfma = 4096;    // tokens per workgroup in the MFMA Gram pass: at least
 constexpr int kGChunkMfmaMax = 16384; // ... and at most (larger chunks: fewer partial Grams)
-constexpr int kGramMinBlocks = 2048;  // the chunk doubles while the grid keeps this many blocks
+constexpr int kGramMinBlocks = 2048;  // chunks are as large as this many blocks in the grid allow
+constexpr int kGramSpan = 128;       // tokens between two flushes of the Gram's short fp32 chains
 constexpr int kGChunkPrecise = 1024; // tokens per workgroup in the fp64 Gram pass
 constexpr int kLChunkMfma = 4096;    // tokens per workgroup in the MFMA leverage pass
 constexpr int kLChunkPrecise = 1024; // tokens per workgroup in the fp64 leverage pass

@@ -86,6 +86,7 @@ __device__ __forceinline__ s16x4 lds_read_tr16(const uint16_t* p) {
 constexpr int kGramStep = 32;
 constexpr int kGramPitch = 144;  // u16 elements per staged token row (288 bytes)
 constexpr int kGramFlush = 4;
+static_assert(kGramStep * kGramFlush == kGramSpan, "flush span");
 
 struct GramArgs {
   const uint16_t* vb;   // V of the unit, at its first token
