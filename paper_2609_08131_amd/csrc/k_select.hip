@@ -340,30 +340,70 @@ hipError_t launch_select(const Launch& L, const float* scores, int32_t* idx) {
 }
 
 // ---------------------------------------------------------------------------
-// Gather: each thread copies one 16-byte piece of a kept K row and V row.
+// Gather: a workgroup copies `rows` consecutive kept rows of one unit; each
+// thread moves one 16-byte piece of UNR rows of K and of V per trip (all
+// loads issued before the stores). STREAM: non-temporal loads and stores, for
+// copies much larger than the caches.
 // ---------------------------------------------------------------------------
-template <int ROWBYTES>
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+template <bool STREAM>
+__device__ __forceinline__ u32x4 copy_load(const char* p) {
+  if constexpr (STREAM) return __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+  else return *reinterpret_cast<const u32x4*>(p);
+}
+
+template <bool STREAM>
+__device__ __forceinline__ void copy_store(char* p, u32x4 x) {
+  if constexpr (STREAM) __builtin_nontemporal_store(x, reinterpret_cast<u32x4*>(p));
+  else *reinterpret_cast<u32x4*>(p) = x;
+}
+
+template <int ROWBYTES, bool STREAM>
 __global__ __launch_bounds__(kThreads) void compact_kernel(Geo g, const int32_t* __restrict__ idx,
-                                                           int budget, int esize,
+                                                           int budget, int rows, int esize,
                                                            const char* __restrict__ k,
                                                            const char* __restrict__ v,
                                                            char* __restrict__ ko,
                                                            char* __restrict__ vo) {
   constexpr int PIECES = ROWBYTES / 16;
+  constexpr int RPT = kThreads / PIECES;  // rows per trip slice
+  constexpr int UNR = 4;
   const int u = blockIdx.y;
-  const int e = blockIdx.x * kThreads + threadIdx.x;
-  const int j = e / PIECES, piece = e % PIECES;
-  if (j >= budget) return;
+  const int j0 = blockIdx.x * rows;
+  const int jend = min(budget, j0 + rows);
+  if (j0 >= jend) return;
   const Unit un = decode_unit(g, u);
-  const int32_t t = idx[(int64_t)u * budget + j];
-  if (t < 0 || t >= un.n) return;  // padding (or a position outside the sequence)
-  const int64_t src_k = ((int64_t)un.l * g.ksl + (int64_t)un.h * g.ksh + (un.t0 + t) * g.kst) * esize;
-  const int64_t src_v = ((int64_t)un.l * g.vsl + (int64_t)un.h * g.vsh + (un.t0 + t) * g.vst) * esize;
-  const int64_t dst = ((int64_t)un.b * g.oss + (int64_t)un.l * g.osl + (int64_t)un.h * g.osh +
-                       (int64_t)j * g.osr) * esize;
-  const int64_t off = piece * 16;
-  *reinterpret_cast<uint4*>(ko + dst + off) = *reinterpret_cast<const uint4*>(k + src_k + off);
-  *reinterpret_cast<uint4*>(vo + dst + off) = *reinterpret_cast<const uint4*>(v + src_v + off);
+  const int rr = threadIdx.x / PIECES, off = (threadIdx.x % PIECES) * 16;
+  const char* kb = k + ((int64_t)un.l * g.ksl + (int64_t)un.h * g.ksh + un.t0 * g.kst) * esize + off;
+  const char* vb = v + ((int64_t)un.l * g.vsl + (int64_t)un.h * g.vsh + un.t0 * g.vst) * esize + off;
+  char* kob = ko + ((int64_t)un.b * g.oss + (int64_t)un.l * g.osl + (int64_t)un.h * g.osh) * esize + off;
+  char* vob = vo + ((int64_t)un.b * g.oss + (int64_t)un.l * g.osl + (int64_t)un.h * g.osh) * esize + off;
+  const int32_t* ix = idx + (int64_t)u * budget;
+  const int64_t kst = g.kst * esize, vst = g.vst * esize, ost = g.osr * esize;
+  for (int jb = j0; jb < jend; jb += UNR * RPT) {
+    int32_t t[UNR];
+#pragma unroll
+    for (int q = 0; q < UNR; ++q) {
+      const int j = jb + q * RPT + rr;
+      t[q] = j < jend ? ix[j] : -1;
+      if (t[q] >= un.n) t[q] = -1;  // a position outside the sequence
+    }
+    u32x4 a[UNR], b[UNR];
+#pragma unroll
+    for (int q = 0; q < UNR; ++q)
+      if (t[q] >= 0) {
+        a[q] = copy_load<STREAM>(kb + t[q] * kst);
+        b[q] = copy_load<STREAM>(vb + t[q] * vst);
+      }
+#pragma unroll
+    for (int q = 0; q < UNR; ++q)
+      if (t[q] >= 0) {
+        const int64_t j = jb + q * RPT + rr;
+        copy_store<STREAM>(kob + j * ost, a[q]);
+        copy_store<STREAM>(vob + j * ost, b[q]);
+      }
+  }
 }
 
 hipError_t launch_compact(const Launch& L, const int32_t* idx, const void* k, const void* v,
@@ -373,16 +413,23 @@ hipError_t launch_compact(const Launch& L, const int32_t* idx, const void* k, co
   if (budget == 0) return hipSuccess;
   const int esize = L.cfg->dtype == JACAP_DTYPE_BF16 ? 2 : 4;
   const int rowbytes = g.D * esize;
-  const int64_t pieces = (int64_t)budget * (rowbytes / 16);
-  const dim3 grid((unsigned)((pieces + kThreads - 1) / kThreads), g.U);
+  // Rows per workgroup: 64 .. 1024, the most that keep >= 8192 workgroups.
+  int rows = 64;
+  while (rows < 1024 && (int64_t)g.U * ((budget + 2 * rows - 1) / (2 * rows)) >= 8192) rows *= 2;
+  const dim3 grid((unsigned)((budget + rows - 1) / rows), g.U);
   auto go = [&](auto kern) {
-    kern<<<grid, kThreads, 0, L.stream>>>(g, idx, budget, esize, (const char*)k, (const char*)v,
-                                          (char*)ko, (char*)vo);
+    kern<<<grid, kThreads, 0, L.stream>>>(g, idx, budget, rows, esize, (const char*)k,
+                                          (const char*)v, (char*)ko, (char*)vo);
   };
-  switch (rowbytes) {
-    case 128: go(compact_kernel<128>); break;
-    case 256: go(compact_kernel<256>); break;
-    case 512: go(compact_kernel<512>); break;
+  // Non-temporal above 1 GiB of kept rows (K and V), far beyond L2 and MALL.
+  const bool stream = 2 * (int64_t)g.U * budget * rowbytes > (int64_t(1) << 30);
+  switch (rowbytes * 2 + (stream ? 1 : 0)) {
+    case 256: go(compact_kernel<128, false>); break;
+    case 257: go(compact_kernel<128, true>); break;
+    case 512: go(compact_kernel<256, false>); break;
+    case 513: go(compact_kernel<256, true>); break;
+    case 1024: go(compact_kernel<512, false>); break;
+    case 1025: go(compact_kernel<512, true>); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
