@@ -4,10 +4,13 @@
 // Selection is exact integer work on order-preserving 32-bit keys of the fp32
 // scores (NaN -> 0, the lowest key; -0 -> +0): the budget-th largest key T,
 // then every token with key > T and the lowest-position tokens with key == T,
-// written in ascending position order. One workgroup per unit.
+// written in ascending position order. One workgroup per unit, in one of two
+// shapes (1024 threads with 8192-entry lists, or 256 threads with 1024-entry
+// lists for batches of many units with small effective budgets).
 //
 // Fast path (sample select): keys of a fixed sample of the unit (up to 128
-// blocks of 64 contiguous tokens, evenly spaced) bracket T between two sample
+// blocks of 64 contiguous tokens, evenly spaced; 32 in the narrow shape)
+// bracket T between two sample
 // order statistics lo <= T <= hi. One ordered pass over the scores then
 // collects, in position order, the tokens with key > hi (kept for sure) and
 // the band lo <= key <= hi (candidates) into LDS; T and the emission are
@@ -16,16 +19,31 @@
 // otherwise the unit takes the general path: a three-pass radix select over
 // the scores (11 + 11 + 10 bits, MSB first) and an ordered emission pass.
 // Both paths give the same, deterministic result.
+#include <algorithm>
+
 #include "jacap_internal.hpp"
+
 
 namespace jacap {
 
-constexpr int kSelThreads = 1024;
-constexpr int kSelPer = 8;                          // tokens per thread per staged chunk
-constexpr int kSelChunk = kSelPer * kSelThreads;    // 8192
-constexpr int kCandCap = 8192;                      // candidate band capacity
-constexpr int kSureCap = 8192;                      // kept-for-sure list capacity
-constexpr int kSampleBlocks = 128;                  // sample: <= 128 blocks of 64 tokens
+// Launch shape of the selection: THREADS per workgroup, CAP entries in each
+// LDS list. The wide shape (one unit per CU) serves few long units; the
+// narrow one fits several workgroups per CU for many units with small
+// effective budgets.
+template <int THREADS, int CAP>
+struct SelCfg {
+  static constexpr int kThreads = THREADS;
+  static constexpr int kPer = 8;                   // tokens per thread per staged chunk
+  static constexpr int kChunk = kPer * THREADS;    // scores per staged chunk
+  static constexpr int kCand = CAP;                // candidate band capacity
+  static constexpr int kSure = CAP;                // kept-for-sure list capacity
+  static constexpr int kSample = kChunk / 64;      // sample: <= kSample blocks of 64 tokens
+};
+using SelWide = SelCfg<1024, 8192>;   // 141 KB of LDS: one workgroup per CU
+using SelNarrow = SelCfg<256, 1024>;  // 29 KB: five per CU
+// Batches of at least this many units take the narrow shape when no unit
+// ranks more than half its list capacity.
+constexpr int kSelNarrowUnits = 1024;
 
 __device__ __forceinline__ uint32_t score_key(float f) {
   if (f != f) return 0u;          // NaN ranks lowest
@@ -34,22 +52,24 @@ __device__ __forceinline__ uint32_t score_key(float f) {
   return (b & 0x80000000u) ? ~b : (b | 0x80000000u);
 }
 
+template <class C>
 struct SelShared {
   // staged chunk keys (one pad word per 8: the per-thread reads of 8
   // consecutive keys are then bank-conflict free) / sample keys / kept
   // candidate positions / evicted positions
-  uint32_t stage[kSelChunk + kSelChunk / 8];
-  uint32_t ckey[kCandCap];    // candidate keys (position order)
-  int32_t cpos[kCandCap];     // candidate positions
-  int32_t gpos[kSureCap];     // kept-for-sure positions (position order)
+  uint32_t stage[C::kChunk + C::kChunk / 8];
+  uint32_t ckey[C::kCand];    // candidate keys (position order)
+  int32_t cpos[C::kCand];     // candidate positions
+  int32_t gpos[C::kSure];     // kept-for-sure positions (position order)
   uint32_t hist[2048];
-  uint32_t scan[kSelThreads / 64 + 1];
+  uint32_t scan[C::kThreads / 64 + 1];
   uint32_t bc[2];
 };
 
-// Exclusive prefix sum over kSelThreads values (one per thread), fixed order:
+// Exclusive prefix sum over C::kThreads values (one per thread), fixed order:
 // a wave scan, then every thread adds the totals of the waves before its own
 // (broadcast LDS reads, no serial pass).
+template <class C>
 __device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t x, uint32_t* sh, uint32_t& total) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   uint32_t incl = x;
@@ -63,7 +83,7 @@ __device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t x, uint32_t* s
   __syncthreads();
   uint32_t before = 0, all = 0;
 #pragma unroll
-  for (int w = 0; w < kSelThreads / 64; ++w) {
+  for (int w = 0; w < C::kThreads / 64; ++w) {
     const uint32_t t = sh[w];
     before += w < wave ? t : 0u;
     all += t;
@@ -75,8 +95,8 @@ __device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t x, uint32_t* s
 // Radix select (11 + 11 + 10 bits, MSB first): the key of rank `rank`
 // (1 = largest, rank <= cnt) among key_at(0 .. cnt-1); `need` = how many keys
 // equal to it fall within the top `rank`.
-template <class KeyAt>
-__device__ uint32_t radix_rank(KeyAt key_at, int cnt, uint32_t rank, SelShared& sh,
+template <class C, class KeyAt>
+__device__ uint32_t radix_rank(KeyAt key_at, int cnt, uint32_t rank, SelShared<C>& sh,
                                uint32_t& need) {
   const int tid = threadIdx.x;
   uint32_t prefix = 0u, pmask = 0u, remaining = rank;
@@ -86,21 +106,21 @@ __device__ uint32_t radix_rank(KeyAt key_at, int cnt, uint32_t rank, SelShared& 
     const int shf = shifts[pass];
     const uint32_t nb = 1u << widths[pass];
     const uint32_t dmask = nb - 1u;
-    for (uint32_t i = tid; i < nb; i += kSelThreads) sh.hist[i] = 0u;
+    for (uint32_t i = tid; i < nb; i += C::kThreads) sh.hist[i] = 0u;
     if (tid == 0) { sh.bc[0] = 0u; sh.bc[1] = 0u; }
     __syncthreads();
-    for (int i = tid; i < cnt; i += kSelThreads) {
+    for (int i = tid; i < cnt; i += C::kThreads) {
       const uint32_t key = key_at(i);
       if ((key & pmask) == prefix) atomicAdd(&sh.hist[(key >> shf) & dmask], 1u);
     }
     __syncthreads();
     // Suffix counts from the top digit down: each thread owns a contiguous run
     // of bins (descending digit order), then a block scan.
-    const uint32_t per = nb / kSelThreads;  // 2 or 1
+    const uint32_t per = nb / C::kThreads;  // bins per thread
     uint32_t local = 0;
     for (uint32_t q = 0; q < per; ++q) local += sh.hist[nb - 1 - (tid * per + q)];
     uint32_t tot;
-    uint32_t above = block_exclusive_scan(local, sh.scan, tot);
+    uint32_t above = block_exclusive_scan<C>(local, sh.scan, tot);
     for (uint32_t q = 0; q < per; ++q) {
       const uint32_t d = nb - 1 - (tid * per + q);
       const uint32_t c = sh.hist[d];
@@ -122,12 +142,12 @@ __device__ uint32_t radix_rank(KeyAt key_at, int cnt, uint32_t rank, SelShared& 
 
 // General path: radix select over the scores, then an ordered emission pass
 // over contiguous per-thread segments.
-template <class KeyAt>
-__device__ void select_general(KeyAt key_at, int n, int kk, int32_t* out, SelShared& sh) {
+template <class C, class KeyAt>
+__device__ void select_general(KeyAt key_at, int n, int kk, int32_t* out, SelShared<C>& sh) {
   const int tid = threadIdx.x;
   uint32_t need;
-  const uint32_t T = radix_rank(key_at, n, (uint32_t)kk, sh, need);
-  const int seg = (n + kSelThreads - 1) / kSelThreads;
+  const uint32_t T = radix_rank<C>(key_at, n, (uint32_t)kk, sh, need);
+  const int seg = (n + C::kThreads - 1) / C::kThreads;
   const int lo = min(n, tid * seg), hi = min(n, lo + seg);
   uint32_t cgt = 0, ceq = 0;
   for (int i = lo; i < hi; ++i) {
@@ -136,8 +156,8 @@ __device__ void select_general(KeyAt key_at, int n, int kk, int32_t* out, SelSha
     ceq += key == T;
   }
   uint32_t tot;
-  uint32_t gt_before = block_exclusive_scan(cgt, sh.scan, tot);
-  uint32_t eq_before = block_exclusive_scan(ceq, sh.scan, tot);
+  uint32_t gt_before = block_exclusive_scan<C>(cgt, sh.scan, tot);
+  uint32_t eq_before = block_exclusive_scan<C>(ceq, sh.scan, tot);
   for (int i = lo; i < hi; ++i) {
     const uint32_t key = key_at(i);
     if (key > T) {
@@ -165,19 +185,21 @@ __device__ __forceinline__ int lower_bound_lds(const int32_t* a, int cnt, int32_
 
 // TOP-kk of key_at(0 .. n-1) by (key desc, position asc), written to out[0 ..
 // kk) in ascending position order (0 < kk < n).
-template <class KeyAt, class RawAt, class Conv>
+template <class C, class KeyAt, class RawAt, class Conv>
 __device__ void select_unit(KeyAt key_at, RawAt raw_at, Conv conv, int n, int kk, int32_t* out,
-                            SelShared& sh) {
+                            SelShared<C>& sh) {
+  static_assert(C::kCand <= C::kChunk + C::kChunk / 8, "kept candidates are merged from stage");
+  static_assert(C::kSample * 64 <= C::kChunk, "the sample is staged in stage");
   const int tid = threadIdx.x;
   // Bracket [lo, hi] of T from the sample (the whole unit if it fits the band).
   uint32_t lo = 0u, hi = 0xFFFFFFFFu;
-  if (n > kCandCap) {
+  if (n > C::kCand) {
     const int nb64 = (n + 63) / 64;
-    const int q = (nb64 + kSampleBlocks - 1) / kSampleBlocks;  // every q-th 64-token block
+    const int q = (nb64 + C::kSample - 1) / C::kSample;  // every q-th 64-token block
     const int nsb = (nb64 + q - 1) / q;
     const int last_start = (nsb - 1) * q * 64;
     const int S = (nsb - 1) * 64 + min(64, n - last_start);   // valid samples form a prefix
-    for (int j = tid; j < S; j += kSelThreads)
+    for (int j = tid; j < S; j += C::kThreads)
       sh.stage[j] = key_at((j >> 6) * q * 64 + (j & 63));
     __syncthreads();
     const double ks = (double)kk * (double)S / (double)n;
@@ -188,8 +210,8 @@ __device__ void select_unit(KeyAt key_at, RawAt raw_at, Conv conv, int n, int kk
     // When the band reaches the top of the sample there is no upper bound:
     // tokens above the sample maximum are candidates too.
     if (kr - delta >= 1)
-      hi = radix_rank([&](int i) { return sh.stage[i]; }, S, (uint32_t)(kr - delta), sh, dummy);
-    lo = radix_rank([&](int i) { return sh.stage[i]; }, S, r_lo, sh, dummy);
+      hi = radix_rank<C>([&](int i) { return sh.stage[i]; }, S, (uint32_t)(kr - delta), sh, dummy);
+    lo = radix_rank<C>([&](int i) { return sh.stage[i]; }, S, r_lo, sh, dummy);
   }
 
   // One ordered pass: kept-for-sure (key > hi) and candidates (lo <= key <= hi).
@@ -198,43 +220,43 @@ __device__ void select_unit(KeyAt key_at, RawAt raw_at, Conv conv, int n, int kk
   // with a pad word per 8 keys, and read back as 8 consecutive keys per
   // thread (bank-conflict free); the block scan orders the threads' lists.
   auto pad = [](int e) { return e + (e >> 3); };
-  float nxt[kSelPer];
+  float nxt[C::kPer];
   auto load_chunk = [&](int base) {
 #pragma unroll
-    for (int j = 0; j < kSelPer; ++j) nxt[j] = raw_at(min(base + j * kSelThreads + tid, n - 1));
+    for (int j = 0; j < C::kPer; ++j) nxt[j] = raw_at(min(base + j * C::kThreads + tid, n - 1));
   };
   load_chunk(0);
   uint32_t gcnt = 0, ccnt = 0;
-  for (int base = 0; base < n; base += kSelChunk) {
+  for (int base = 0; base < n; base += C::kChunk) {
 #pragma unroll
-    for (int j = 0; j < kSelPer; ++j) {
-      const int p = base + j * kSelThreads + tid;
-      sh.stage[pad(j * kSelThreads + tid)] = p < n ? conv(nxt[j]) : 0u;
+    for (int j = 0; j < C::kPer; ++j) {
+      const int p = base + j * C::kThreads + tid;
+      sh.stage[pad(j * C::kThreads + tid)] = p < n ? conv(nxt[j]) : 0u;
     }
-    if (base + kSelChunk < n) load_chunk(base + kSelChunk);  // uniform
+    if (base + C::kChunk < n) load_chunk(base + C::kChunk);  // uniform
     __syncthreads();
-    uint32_t k8[kSelPer];
+    uint32_t k8[C::kPer];
     uint32_t ng = 0, nc = 0;
 #pragma unroll
-    for (int qd = 0; qd < kSelPer; ++qd) {
-      const int p = base + kSelPer * tid + qd;
-      k8[qd] = sh.stage[pad(kSelPer * tid + qd)];
+    for (int qd = 0; qd < C::kPer; ++qd) {
+      const int p = base + C::kPer * tid + qd;
+      k8[qd] = sh.stage[pad(C::kPer * tid + qd)];
       const bool valid = p < n;
       ng += valid && k8[qd] > hi;
       nc += valid && k8[qd] >= lo && k8[qd] <= hi;
     }
     uint32_t tot;
-    const uint32_t off = block_exclusive_scan((ng << 16) | nc, sh.scan, tot);
+    const uint32_t off = block_exclusive_scan<C>((ng << 16) | nc, sh.scan, tot);
     uint32_t go = gcnt + (off >> 16), co = ccnt + (off & 0xFFFFu);
 #pragma unroll
-    for (int qd = 0; qd < kSelPer; ++qd) {
-      const int p = base + kSelPer * tid + qd;
+    for (int qd = 0; qd < C::kPer; ++qd) {
+      const int p = base + C::kPer * tid + qd;
       if (p >= n) continue;
       if (k8[qd] > hi) {
-        if (go < (uint32_t)kSureCap) sh.gpos[go] = p;
+        if (go < (uint32_t)C::kSure) sh.gpos[go] = p;
         ++go;
       } else if (k8[qd] >= lo) {
-        if (co < (uint32_t)kCandCap) { sh.ckey[co] = k8[qd]; sh.cpos[co] = p; }
+        if (co < (uint32_t)C::kCand) { sh.ckey[co] = k8[qd]; sh.cpos[co] = p; }
         ++co;
       }
     }
@@ -243,30 +265,30 @@ __device__ void select_unit(KeyAt key_at, RawAt raw_at, Conv conv, int n, int kk
     __syncthreads();
   }
   const bool ok = gcnt < (uint32_t)kk && gcnt + ccnt >= (uint32_t)kk &&
-                  gcnt <= (uint32_t)kSureCap && ccnt <= (uint32_t)kCandCap;
+                  gcnt <= (uint32_t)C::kSure && ccnt <= (uint32_t)C::kCand;
   if (!ok) {  // uniform: every thread holds the same counts
-    select_general(key_at, n, kk, out, sh);
+    select_general<C>(key_at, n, kk, out, sh);
     return;
   }
 
   // T among the candidates: rank kk - gcnt.
   const uint32_t r = (uint32_t)kk - gcnt;
   uint32_t need;
-  const uint32_t T = radix_rank([&](int i) { return sh.ckey[i]; }, (int)ccnt, r, sh, need);
+  const uint32_t T = radix_rank<C>([&](int i) { return sh.ckey[i]; }, (int)ccnt, r, sh, need);
   // Kept candidates, in position order, into stage[0 .. r).
-  const int per = ((int)ccnt + kSelThreads - 1) / kSelThreads;
+  const int per = ((int)ccnt + C::kThreads - 1) / C::kThreads;
   const int c0 = min((int)ccnt, tid * per), c1 = min((int)ccnt, c0 + per);
   uint32_t ceq = 0;
   for (int i = c0; i < c1; ++i) ceq += sh.ckey[i] == T;
   uint32_t tot;
-  uint32_t eq_before = block_exclusive_scan(ceq, sh.scan, tot);
+  uint32_t eq_before = block_exclusive_scan<C>(ceq, sh.scan, tot);
   uint32_t csel = 0;
   for (int i = c0, e = eq_before; i < c1; ++i) {
     const uint32_t key = sh.ckey[i];
     if (key > T) ++csel;
     else if (key == T) { csel += (uint32_t)e < need; ++e; }
   }
-  uint32_t sel_before = block_exclusive_scan(csel, sh.scan, tot);
+  uint32_t sel_before = block_exclusive_scan<C>(csel, sh.scan, tot);
   for (int i = c0, e = eq_before; i < c1; ++i) {
     const uint32_t key = sh.ckey[i];
     bool keep = false;
@@ -277,37 +299,38 @@ __device__ void select_unit(KeyAt key_at, RawAt raw_at, Conv conv, int n, int kk
   __syncthreads();
   // Merge the two position-ordered lists into out[0 .. kk).
   const int32_t* kept_c = reinterpret_cast<const int32_t*>(sh.stage);
-  for (int a = tid; a < (int)gcnt; a += kSelThreads) {
+  for (int a = tid; a < (int)gcnt; a += C::kThreads) {
     const int32_t p = sh.gpos[a];
     out[a + lower_bound_lds(kept_c, (int)r, p)] = p;
   }
-  for (int b = tid; b < (int)r; b += kSelThreads) {
+  for (int b = tid; b < (int)r; b += C::kThreads) {
     const int32_t p = kept_c[b];
     out[b + lower_bound_lds(sh.gpos, (int)gcnt, p)] = p;
   }
 }
 
-__global__ __launch_bounds__(kSelThreads) void select_kernel(Geo g, const float* __restrict__ scores,
+template <class C>
+__global__ __launch_bounds__(C::kThreads) void select_kernel(Geo g, const float* __restrict__ scores,
                                                              int32_t* __restrict__ idx, int budget,
                                                              int protect) {
-  __shared__ SelShared sh;
+  __shared__ SelShared<C> sh;
   const int u = blockIdx.x, tid = threadIdx.x;
   const Unit un = decode_unit(g, u);
   int32_t* out = idx + (int64_t)u * budget;
   const int kk_all = min(budget, un.n);
   const float* s = scores + token_row(g, un);
 
-  for (int j = kk_all + tid; j < budget; j += kSelThreads) out[j] = -1;
+  for (int j = kk_all + tid; j < budget; j += C::kThreads) out[j] = -1;
   if (kk_all == 0) return;
   // Protected tail: the last p positions are kept; the ranking fills the
   // remaining kk slots from positions 0 .. n-1 (n = n_b - p), whose indices
   // all precede the tail, so the tail simply follows them in idx.
   const int npro = min(protect, kk_all);
   const int n = un.n - npro, kk = kk_all - npro;
-  for (int j = tid; j < npro; j += kSelThreads) out[kk + j] = n + j;
+  for (int j = tid; j < npro; j += C::kThreads) out[kk + j] = n + j;
   if (kk == 0) return;
   if (kk == n) {
-    for (int j = tid; j < n; j += kSelThreads) out[j] = j;
+    for (int j = tid; j < n; j += C::kThreads) out[j] = j;
     return;
   }
 
@@ -315,27 +338,35 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(Geo g, const float*
   // last n - kk of the order (key desc, position asc) are the first n - kk of
   // (~key desc, reversed position asc)), then emit every other position.
   const int m = n - kk;
-  if (m < kk && m <= kSelChunk) {
-    select_unit([&](int i) { return ~score_key(s[n - 1 - i]); }, [&](int i) { return s[n - 1 - i]; },
+  if (m < kk && m <= C::kChunk) {
+    select_unit<C>([&](int i) { return ~score_key(s[n - 1 - i]); }, [&](int i) { return s[n - 1 - i]; },
                 [](float f) { return ~score_key(f); }, n, m, out, sh);
     __syncthreads();  // out[0 .. m): evicted, as reversed positions ascending
     uint32_t* ev = sh.stage;
-    for (int j = tid; j < m; j += kSelThreads) ev[j] = (uint32_t)(n - 1 - out[m - 1 - j]);
+    for (int j = tid; j < m; j += C::kThreads) ev[j] = (uint32_t)(n - 1 - out[m - 1 - j]);
     __syncthreads();
     const int32_t* evs = reinterpret_cast<const int32_t*>(ev);
-    for (int i = tid; i < n; i += kSelThreads) {
+    for (int i = tid; i < n; i += C::kThreads) {
       const int c = lower_bound_lds(evs, m, i);
       if (c == m || evs[c] != i) out[i - c] = i;
     }
     return;
   }
-  select_unit([&](int i) { return score_key(s[i]); }, [&](int i) { return s[i]; },
+  select_unit<C>([&](int i) { return score_key(s[i]); }, [&](int i) { return s[i]; },
               [](float f) { return score_key(f); }, n, kk, out, sh);
 }
 
 hipError_t launch_select(const Launch& L, const float* scores, int32_t* idx) {
-  select_kernel<<<L.geo.U, kSelThreads, 0, L.stream>>>(L.geo, scores, idx, L.cfg->budget_k,
-                                                       L.cfg->protect_last);
+  const Geo& g = L.geo;
+  const int budget = L.cfg->budget_k;
+  // The largest number of tokens any unit ranks: min(B, n - B) at the longest n.
+  const int kmax = std::min(budget, std::max(0, g.maxn - budget));
+  if (g.U >= kSelNarrowUnits && kmax <= SelNarrow::kCand / 2)
+    select_kernel<SelNarrow><<<g.U, SelNarrow::kThreads, 0, L.stream>>>(g, scores, idx, budget,
+                                                                        L.cfg->protect_last);
+  else
+    select_kernel<SelWide><<<g.U, SelWide::kThreads, 0, L.stream>>>(g, scores, idx, budget,
+                                                                    L.cfg->protect_last);
   return hipGetLastError();
 }
 

@@ -298,6 +298,47 @@ def test_select_large_units_both_paths(jacap):
     assert np.array_equal(prob.idx[2, 0, 1].cpu().numpy()[:n - 1], want)
 
 
+@pytest.mark.gpu
+def test_select_many_units_narrow_shape(jacap):
+    """1024 units (4 sequences x 32 layers x 8 KV heads) take the narrow
+    selection shape when no unit ranks more than 512 tokens: spread-out scores
+    (sampled fast path), heavy ties (the band overflows: radix fallback),
+    NaN/-0/inf mixes, budgets keeping more than half (complement path) and a
+    protected tail; a budget ranking more than 512 takes the wide shape. Every
+    unit must equal the oracle's ranking bit for bit."""
+    lens = [1, 700, 3000, 9000]
+    case = make_case("ragged16", device="cuda", seq_lens=lens, num_layers=32, num_kv_heads=8,
+                     num_q_heads=8, head_dim=64, window=2)
+    L, H, T = 32, 8, sum(lens)
+    rng = np.random.default_rng(11)
+    s = np.exp(rng.normal(0.0, 4.0, (L, H, T))).astype(np.float32)
+    s[1::4] = rng.integers(0, 4, (len(range(1, L, 4)), H, T)).astype(np.float32)  # ties
+    mix = s[2::4]
+    mix[rng.random(mix.shape) < 0.1] = np.nan
+    mix[rng.random(mix.shape) < 0.05] = -0.0
+    mix[rng.random(mix.shape) < 0.05] = 0.0
+    mix[rng.random(mix.shape) < 0.01] = np.inf
+    s[2::4] = mix
+    scores = torch.from_numpy(s).cuda()
+    for budget, protect in ((1, 0), (64, 0), (300, 0), (512, 0), (8600, 0), (8999, 0),
+                            (200, 50), (2048, 0)):
+        p = jacap.Params(budget_k=budget, protect_last=protect)
+        prob = jacap.prepare(case.q_win, case.k, case.v, case.seq_offsets, case.seq_lens, p)
+        print(f"[select] 1024 units, budget {budget}, protect {protect}", flush=True)
+        jacap.select(prob.cfg, prob.batch, scores, prob.idx)
+        torch.cuda.synchronize()
+        got_all = prob.idx.cpu().numpy()
+        for b in range(len(lens)):
+            lo, hi = token_slice(case, b)
+            for layer in range(L):
+                for h in range(H):
+                    want = jo.select_top(s[layer, h, lo:hi], budget, protect)
+                    got = got_all[b, layer, h]
+                    assert np.array_equal(got[:len(want)], want), (budget, protect, b, layer, h)
+                    assert np.all(got[len(want):] == -1)
+        del prob
+
+
 # ---------------------------------------------------------------------------
 # Output-projection variant: u_i = W~ v_i through the ridge matrix R
 # ---------------------------------------------------------------------------
