@@ -179,6 +179,24 @@ jacap_status jacap_score(const jacap_config* cfg, const jacap_batch* batch,
                          const void* q_win, const void* k, const void* v, float* scores,
                          void* ws, size_t ws_bytes, void* stream);
 
+/* jacap_score with the literal inputs of Algorithm 1: the query statistics
+ * (mu_Q, Lambda_Q) of every unit are given instead of the observation window.
+ *   mu     : device float64 [U][d], U = num_seqs * num_layers * num_kv_heads
+ *            in unit order (seq, layer, kv head) -- the order of idx;
+ *   lambda : device float64, cfg->cov_mode = JACAP_COV_DIAG: [U][d]
+ *            per-channel variances; JACAP_COV_FULL: [U][d][d] row-major,
+ *            symmetric positive semi-definite (not checked; it enters the
+ *            K pass rounded to float32, as jacap_score's own estimate does).
+ * Both 8-byte aligned, read during the call's kernels only. The batch's Q
+ * strides are ignored; cfg->window must still be >= 1. Per-query-head GQA
+ * (cfg->gqa_mode = JACAP_GQA_PER_HEAD with num_q_heads > num_kv_heads) gives
+ * JACAP_ERR_UNSUPPORTED: the statistics are per unit. A non-finite mu or
+ * lambda entry raises JACAP_FLAG_NONFINITE for its unit. */
+jacap_status jacap_score_from_stats(const jacap_config* cfg, const jacap_batch* batch,
+                                    const double* mu, const double* lambda, const void* k,
+                                    const void* v, float* scores, void* ws, size_t ws_bytes,
+                                    void* stream);
+
 /* Algorithm 1 step 5 (TOP-B): for each unit keeps min(budget_k, n_b) tokens
  * ordered by (score descending, position ascending), NaN lowest and -0 equal
  * to +0, and writes their positions in ascending order to idx (-1 padding).

@@ -213,11 +213,20 @@ def score_unit(q_group, K, V, *, tau: float = 10.0, ridge=1.0,
     """Jacap scores of one KV head (Algorithm 1 steps 1-4) with every
     intermediate, in float64. q_group is (G, w, d) or (N, d); K and V are (n, d).
     ridge is a scalar or a d x d SPD matrix (see capacity_matrix)."""
-    K = np.asarray(K, dtype=np.float64)
-    V = np.asarray(V, dtype=np.float64)
-    n, d = K.shape
     Qs = pool_queries(q_group)
     mu, lam = query_statistics(Qs, cov_mode)
+    return score_unit_from_stats(mu, lam, K, V, tau=tau, ridge=ridge)
+
+
+def score_unit_from_stats(mu, lam, K, V, *, tau: float = 10.0, ridge=1.0) -> dict:
+    """Algorithm 1 steps 1-4 from its literal inputs: the query centre mu_Q and
+    covariance Lambda_Q (a length-d vector of per-channel variances, or a d x d
+    matrix), K and V (n, d). Same outputs as score_unit."""
+    K = np.asarray(K, dtype=np.float64)
+    V = np.asarray(V, dtype=np.float64)
+    mu = np.asarray(mu, dtype=np.float64)
+    lam = np.asarray(lam, dtype=np.float64)
+    n, d = K.shape
     out = {"mu": mu, "lam": lam, "n": n, "d": d}
     if n == 0:
         out.update(scores=np.zeros(0), w=np.zeros(0), singular=False,

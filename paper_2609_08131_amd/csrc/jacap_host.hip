@@ -181,14 +181,17 @@ jacap_status prepare(const jacap_config* c, const jacap_batch* b, void* ws, size
     JACAP_TRY(expr);                        \
   } while (0)
 
-// One scoring pass (Algorithm 1 steps 1-4) over every unit. The first pass of
-// a call clears the status words; later passes (per-head GQA) keep the sticky
-// flags and clear only the refinement marks.
+// One scoring pass (Algorithm 1 steps 1-4) over every unit, from the window
+// queries q, or (mu != nullptr) from caller-supplied statistics. The first
+// pass of a call clears the status words; later passes (per-head GQA) keep
+// the sticky flags and clear only the refinement marks.
 jacap_status score_pass(const Launch& L, const void* q, const void* k, const void* v,
-                        float* scores, bool first) {
+                        float* scores, bool first, const double* mu = nullptr,
+                        const double* lambda = nullptr) {
   if (first) JACAP_PHASE(JACAP_PHASE_INIT, launch_init(L));
   else JACAP_PHASE(JACAP_PHASE_INIT, launch_clear_refine(L));
-  JACAP_PHASE(JACAP_PHASE_QSTATS, launch_qstats(L, q));
+  if (mu) JACAP_PHASE(JACAP_PHASE_QSTATS, launch_stats_in(L, mu, lambda));
+  else JACAP_PHASE(JACAP_PHASE_QSTATS, launch_qstats(L, q));
   JACAP_PHASE(JACAP_PHASE_KPASS, launch_kpass(L, k));
   JACAP_PHASE(JACAP_PHASE_WEIGHTS, launch_softmax_weights(L));
   JACAP_PHASE(JACAP_PHASE_GRAM, launch_gram(L, v, false));
@@ -256,6 +259,28 @@ jacap_status jacap_score(const jacap_config* cfg, const jacap_batch* batch, cons
     return launch_init(L) == hipSuccess ? JACAP_OK : JACAP_ERR_HIP;
   }
   return run_score(L, q_win, k, v, scores);
+}
+
+jacap_status jacap_score_from_stats(const jacap_config* cfg, const jacap_batch* batch,
+                                    const double* mu, const double* lambda, const void* k,
+                                    const void* v, float* scores, void* ws, size_t ws_bytes,
+                                    void* stream) {
+  Launch L;
+  if (!ws) return JACAP_ERR_INVALID_ARG;
+  jacap_status s = prepare(cfg, batch, ws, ws_bytes, stream, &L);
+  if (s != JACAP_OK) return s;
+  if (cfg->gqa_mode == JACAP_GQA_PER_HEAD && cfg->num_q_heads > cfg->num_kv_heads)
+    return JACAP_ERR_UNSUPPORTED;
+  if (!mu || !lambda || (reinterpret_cast<uintptr_t>(mu) & 7u) ||
+      (reinterpret_cast<uintptr_t>(lambda) & 7u))
+    return JACAP_ERR_INVALID_ARG;
+  if (!k || !v || !scores || !aligned16(k) || !aligned16(v) || !aligned16(scores))
+    return JACAP_ERR_INVALID_ARG;
+  if (batch->total_tokens == 0) {
+    TimedPhase tp(L.stream, JACAP_PHASE_INIT);
+    return launch_init(L) == hipSuccess ? JACAP_OK : JACAP_ERR_HIP;
+  }
+  return score_pass(L, nullptr, k, v, scores, true, mu, lambda);
 }
 
 jacap_status jacap_select(const jacap_config* cfg, const jacap_batch* batch, const float* scores,

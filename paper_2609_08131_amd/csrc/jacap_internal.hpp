@@ -266,6 +266,7 @@ struct Launch {
 
 hipError_t launch_init(const Launch& L);
 hipError_t launch_qstats(const Launch& L, const void* q);
+hipError_t launch_stats_in(const Launch& L, const double* mu, const double* lambda);
 hipError_t launch_kpass(const Launch& L, const void* k);
 hipError_t launch_softmax_weights(const Launch& L);
 hipError_t launch_clear_refine(const Launch& L);

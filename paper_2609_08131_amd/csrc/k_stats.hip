@@ -182,6 +182,47 @@ hipError_t launch_qstats(const Launch& L, const void* q) {
   return hipGetLastError();
 }
 
+// ---------------------------------------------------------------------------
+// Caller-supplied (mu_Q, Lambda_Q) (Algorithm 1's inputs) into the places
+// the window statistics take: mu and the diagonal in fp64, the full matrix
+// rounded to fp32 for the K pass. One workgroup per unit.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(kThreads) void stats_in_kernel(Geo g, const double* __restrict__ mu,
+                                                            const double* __restrict__ lambda,
+                                                            int full, double* __restrict__ mu_out,
+                                                            double* __restrict__ lam_out,
+                                                            float* __restrict__ lamfull,
+                                                            uint32_t* status, uint32_t* uflags) {
+  const int u = blockIdx.x, tid = threadIdx.x, D = g.D;
+  const Unit un = decode_unit(g, u);
+  if (tid == 0 && un.n == 0 && !offsets_ok(g, g.seq_off[un.b], g.seq_off[un.b + 1]))
+    atomicOr(status, (uint32_t)JACAP_FLAG_BAD_OFFSETS);
+  bool bad = false;
+  for (int c = tid; c < D; c += kThreads) {
+    const double m = mu[(int64_t)u * D + c];
+    const double l = full ? lambda[((int64_t)u * D + c) * D + c] : lambda[(int64_t)u * D + c];
+    mu_out[(int64_t)u * D + c] = m;
+    lam_out[(int64_t)u * D + c] = l;
+    bad |= !isfinite(m) || !isfinite(l);
+  }
+  if (full)
+    for (int e = tid; e < D * D; e += kThreads) {
+      const double x = lambda[(int64_t)u * D * D + e];
+      lamfull[(int64_t)u * D * D + e] = (float)x;
+      bad |= !isfinite(x);
+    }
+  if (__any(bad) && (tid & 63) == 0) raise_flags(status, uflags, u, kUnitNonfinite);
+}
+
+hipError_t launch_stats_in(const Launch& L, const double* mu, const double* lambda) {
+  const Geo& g = L.geo;
+  stats_in_kernel<<<g.U, kThreads, 0, L.stream>>>(
+      g, mu, lambda, L.cfg->cov_mode == JACAP_COV_FULL, ws_ptr<double>(L.wsp, L.ws.mu),
+      ws_ptr<double>(L.wsp, L.ws.lam), ws_ptr<float>(L.wsp, L.ws.lamfull),
+      ws_ptr<uint32_t>(L.wsp, L.ws.status), ws_ptr<uint32_t>(L.wsp, L.ws.uflags));
+  return hipGetLastError();
+}
+
 // Sum over aligned groups of G lanes (G = 8, 16 or 32); every lane of a group
 // ends with the same value. Within a 16-lane row the partners come from DPP
 // (quad swaps, then the half-row and row mirrors: one VALU instruction per

@@ -86,6 +86,7 @@ def _load() -> ctypes.CDLL:
     sigs = {
         "jacap_workspace_size": [C, B, ctypes.POINTER(sz)],
         "jacap_score": [C, B, P, P, P, P, P, sz, P],
+        "jacap_score_from_stats": [C, B, P, P, P, P, P, P, sz, P],
         "jacap_select": [C, B, P, P, P, sz, P],
         "jacap_compact": [C, B, P, P, P, P, P, P],
         "jacap_evict": [C, B, P, P, P, P, P, P, P, P, sz, P],
@@ -109,10 +110,10 @@ def _load() -> ctypes.CDLL:
 
 
 _lib = _load()
-EXPORTED = ("jacap_workspace_size", "jacap_score", "jacap_select", "jacap_compact",
-            "jacap_evict", "jacap_read_status", "jacap_status_string", "jacap_timing_start",
-            "jacap_timing_stop", "jacap_phase_name", "jacap_greedy_workspace_size",
-            "jacap_greedy")
+EXPORTED = ("jacap_workspace_size", "jacap_score", "jacap_score_from_stats", "jacap_select",
+            "jacap_compact", "jacap_evict", "jacap_read_status", "jacap_status_string",
+            "jacap_timing_start", "jacap_timing_stop", "jacap_phase_name",
+            "jacap_greedy_workspace_size", "jacap_greedy")
 NUM_PHASES = 13   # enum jacap_phase
 
 
@@ -230,6 +231,14 @@ def score(cfg, batch, q_win, k, v, scores, ws, stream=None) -> None:
     _check("jacap_score", _lib.jacap_score(
         ctypes.byref(cfg), ctypes.byref(batch), _ptr(q_win), _ptr(k), _ptr(v), _ptr(scores),
         _ptr(ws), ws.numel() if ws is not None else 0, _stream(stream)))
+
+
+def score_from_stats(cfg, batch, mu, lam, k, v, scores, ws, stream=None) -> None:
+    """jacap_score_from_stats: mu float64 [U][d]; lam float64 [U][d] (DIAG) or
+    [U][d][d] (FULL), U in unit order (seq, layer, kv head)."""
+    _check("jacap_score_from_stats", _lib.jacap_score_from_stats(
+        ctypes.byref(cfg), ctypes.byref(batch), _ptr(mu), _ptr(lam), _ptr(k), _ptr(v),
+        _ptr(scores), _ptr(ws), ws.numel() if ws is not None else 0, _stream(stream)))
 
 
 def select(cfg, batch, scores, idx, ws=None, stream=None) -> None:

@@ -198,3 +198,28 @@ def test_token_stride_limit():
     assert _ws_size(_cfg(), _batch(k_stride_token=1 << 24))[0] == jacap.OK
     assert _ws_size(_cfg(), _batch(v_stride_token=(1 << 24) + 8))[0] == jacap.ERR_UNSUPPORTED
     assert _ws_size(_cfg(), _batch(k_stride_token=(1 << 24) + 8))[0] == jacap.ERR_UNSUPPORTED
+
+
+def test_score_from_stats_validation():
+    """jacap_score_from_stats: statistics pointers non-null and 8-byte aligned,
+    per-query-head GQA (G > 1) unsupported, the usual workspace checks; all
+    rejected before anything is launched."""
+    P = ctypes.c_void_p
+    good = P(0x100000)
+    cfg, b = _cfg(), _batch()
+    code, n = _ws_size(cfg, b)
+    assert code == jacap.OK
+    lib = jacap._lib
+    call = lambda c, *a: lib.jacap_score_from_stats(ctypes.byref(c), ctypes.byref(b), *a)
+    assert call(cfg, None, good, good, good, good, good, n, None) == jacap.ERR_INVALID_ARG
+    assert call(cfg, good, None, good, good, good, good, n, None) == jacap.ERR_INVALID_ARG
+    assert call(cfg, P(0x100004), good, good, good, good, good, n, None) == jacap.ERR_INVALID_ARG
+    assert call(cfg, good, P(0x100004), good, good, good, good, n, None) == jacap.ERR_INVALID_ARG
+    assert call(cfg, good, good, None, good, good, good, n, None) == jacap.ERR_INVALID_ARG
+    assert call(cfg, good, good, good, good, P(0x100008), good, n, None) == jacap.ERR_INVALID_ARG
+    assert call(cfg, good, good, good, good, good, None, n, None) == jacap.ERR_INVALID_ARG
+    assert call(cfg, good, good, good, good, good, good, n - 256, None) == jacap.ERR_WORKSPACE
+    per_head = _cfg(gqa_mode=1, num_q_heads=4)
+    code, n2 = _ws_size(per_head, b)
+    assert code == jacap.OK
+    assert call(per_head, good, good, good, good, good, good, n2, None) == jacap.ERR_UNSUPPORTED

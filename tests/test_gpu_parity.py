@@ -298,6 +298,68 @@ def test_select_large_units_both_paths(jacap):
     assert np.array_equal(prob.idx[2, 0, 1].cpu().numpy()[:n - 1], want)
 
 
+@pytest.mark.parametrize("wl,mode", [("tiny", "diag"), ("tiny", "full"),
+                                     ("llama8b_layer", "diag"), ("llama8b_layer", "full")])
+def test_score_from_stats(jacap, wl, mode):
+    """jacap_score_from_stats (Algorithm 1 with its literal inputs) on
+    statistics no window produced -- a random centre and positive variances,
+    or a random positive semi-definite matrix -- against the oracle's
+    Algorithm 1 from the same statistics, every unit element by element; with
+    the window's own statistics (oracle, fp64) it reproduces jacap_score."""
+    case = make_case(wl, device="cuda")
+    w = case.workload
+    B, L, H, d = case.num_seqs, w.num_layers, w.num_kv_heads, w.head_dim
+    rng = np.random.default_rng(5)
+    mu = rng.normal(size=(B, L, H, d))
+    if mode == "diag":
+        lam = rng.uniform(0.2, 2.0, size=(B, L, H, d))
+    else:
+        G = rng.normal(size=(B, L, H, d, d))
+        lam = G @ np.swapaxes(G, -1, -2) / d
+    p = jacap.Params(budget_k=w.budget_k, cov_mode=COV[mode])
+    prob = jacap.prepare(case.q_win, case.k, case.v, case.seq_offsets, case.seq_lens, p)
+    jacap.score_from_stats(prob.cfg, prob.batch, torch.from_numpy(mu).cuda(),
+                           torch.from_numpy(lam).cuda(), case.k, case.v, prob.scores, prob.ws)
+    assert jacap.read_status(prob.ws) == 0
+    tol = tol_for(case)
+    worst = 0.0
+    for (b, l, h) in unit_list(case):
+        _, k, v = case.unit_arrays(b, l, h)
+        o = jo.score_unit_from_stats(mu[b, l, h], lam[b, l, h], k, v)
+        e = score_errors(gpu_unit_scores(case, prob, b, l, h), o["scores"])
+        worst = max(worst, float(e.max()))
+    assert worst <= tol, (wl, mode, worst)
+    # the window's own statistics: the same scores as jacap_score
+    mu_w = np.empty((B, L, H, d))
+    lam_w = np.empty_like(lam)
+    for (b, l, h) in unit_list(case):
+        q, _, _ = case.unit_arrays(b, l, h)
+        mu_w[b, l, h], lam_w[b, l, h] = jo.query_statistics(jo.pool_queries(q), mode)
+    from_stats = torch.empty_like(prob.scores)
+    jacap.score_from_stats(prob.cfg, prob.batch, torch.from_numpy(mu_w).cuda(),
+                           torch.from_numpy(lam_w).cuda(), case.k, case.v, from_stats, prob.ws)
+    jacap.score(prob.cfg, prob.batch, case.q_win, case.k, case.v, prob.scores, prob.ws)
+    torch.cuda.synchronize()
+    a, c = from_stats.double().cpu().numpy(), prob.scores.double().cpu().numpy()
+    rel = np.abs(a - c) / np.maximum(np.abs(c), 1e-6 * np.abs(c).max())
+    print(f"\n[from_stats] {wl} {mode}: worst error vs oracle {worst:.2e}; "
+          f"vs jacap_score {rel.max():.2e}")
+    assert rel.max() <= tol
+
+
+def test_score_from_stats_nonfinite_flags_unit(jacap):
+    case = make_case("tiny", device="cuda")
+    d = case.workload.head_dim
+    mu = torch.zeros((1, 1, 1, d), dtype=torch.float64, device="cuda")
+    lam = torch.ones((1, 1, 1, d), dtype=torch.float64, device="cuda")
+    lam[..., 3] = float("nan")
+    p = jacap.Params(budget_k=8)
+    prob = jacap.prepare(case.q_win, case.k, case.v, case.seq_offsets, case.seq_lens, p)
+    jacap.score_from_stats(prob.cfg, prob.batch, mu, lam, case.k, case.v, prob.scores, prob.ws)
+    assert jacap.read_status(prob.ws) & jacap.FLAG_NONFINITE
+    assert torch.isnan(prob.scores).all()
+
+
 @pytest.mark.gpu
 def test_select_many_units_narrow_shape(jacap):
     """1024 units (4 sequences x 32 layers x 8 KV heads) take the narrow

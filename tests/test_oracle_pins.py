@@ -342,6 +342,38 @@ def test_p8_permutations_and_scaling():
     assert np.allclose(jo.score_unit(Q, K, 7.5 * V, tau=2.0, ridge=0.0)["scores"], s0, rtol=1e-10)
 
 
+def test_stats_input_form():
+    """Algorithm 1 with its literal inputs (mu_Q, Lambda_Q). A window of 2d
+    queries mu +- sqrt(d lambda_c) e_c has exactly mean mu and 1/N covariance
+    diag(lambda), so scoring it must equal scoring (mu, lambda) directly, in
+    both covariance modes; FULL with a diagonal Lambda equals DIAG; a rotation
+    of K with mu -> R^T mu, Lambda -> R^T Lambda R leaves FULL scores
+    unchanged; Lambda = 0 gives zero scores."""
+    rng = np.random.default_rng(41)
+    n, d = 70, 6
+    K = rng.normal(size=(n, d)) * 1.5
+    V = rng.normal(size=(n, d))
+    mu = rng.normal(size=d)
+    lam = rng.uniform(0.1, 2.0, size=d)
+    window = np.concatenate([mu + np.sqrt(d * lam)[:, None] * np.eye(d),
+                             mu - np.sqrt(d * lam)[:, None] * np.eye(d)])
+    direct = jo.score_unit_from_stats(mu, lam, K, V, tau=1.5, ridge=0.4)["scores"]
+    assert np.allclose(jo.score_unit(window, K, V, tau=1.5, ridge=0.4)["scores"], direct,
+                       rtol=1e-12)
+    assert np.allclose(jo.score_unit(window, K, V, tau=1.5, ridge=0.4, cov_mode="full")["scores"],
+                       direct, rtol=1e-12)
+    assert np.allclose(jo.score_unit_from_stats(mu, np.diag(lam), K, V, tau=1.5,
+                                                ridge=0.4)["scores"], direct, rtol=1e-12)
+    B = rng.normal(size=(d, d))
+    Lam = B @ B.T / d
+    R = _rot(d, 5)
+    full = jo.score_unit_from_stats(mu, Lam, K, V, tau=1.5, ridge=0.4)["scores"]
+    rot = jo.score_unit_from_stats(R.T @ mu, R.T @ Lam @ R, K @ R, V, tau=1.5, ridge=0.4)["scores"]
+    assert np.allclose(full, rot, rtol=1e-10)
+    assert not np.allclose(full, direct, rtol=1e-3)
+    assert np.all(jo.score_unit_from_stats(mu, np.zeros(d), K, V)["scores"] == 0.0)
+
+
 # ---------------------------------------------------------------------------
 # P9 Algorithm 1 literal form, P10 large-ridge limit, FULL kappa
 # ---------------------------------------------------------------------------
