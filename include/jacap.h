@@ -305,6 +305,15 @@ jacap_status jacap_timing_stop(double* ms, int32_t* calls);
 /* Static name of a phase ("gram", "leverage", "greedy", ...), or "unknown". */
 const char* jacap_phase_name(int32_t phase);
 
+/* Streaming-read probe, for measurement tools: the HBM read bandwidth the
+ * streaming kernels can be compared with. Reads the `bytes` bytes at device
+ * pointer `src` once (16-byte loads, whole 128-byte lines per wave
+ * instruction, the non-temporal hint, 1 MiB per workgroup) on `stream`, and
+ * writes nothing except, in the practically impossible case that the XOR of
+ * all words equals 0x9E3779B9, that value to *sink (device, 4 bytes). src
+ * and bytes must be multiples of 16 (else JACAP_ERR_INVALID_ARG). */
+jacap_status jacap_stream_read(const void* src, size_t bytes, uint32_t* sink, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -104,3 +104,46 @@ const char* jacap_phase_name(int32_t phase) {
 }
 
 }  // extern "C"
+
+// ---------------------------------------------------------------------------
+// Streaming-read probe (jacap_stream_read).
+// ---------------------------------------------------------------------------
+namespace jacap {
+namespace {
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+constexpr int64_t kProbeBlockBytes = int64_t(1) << 20;
+
+// Workgroup b reads 16-byte words [b * per, min(n16, (b + 1) * per)), four
+// wave loads of 1 KiB in flight per trip.
+__global__ __launch_bounds__(kThreads) void stream_read_kernel(const u32x4* __restrict__ p,
+                                                               int64_t n16, int64_t per,
+                                                               uint32_t* sink) {
+  const int64_t b0 = (int64_t)blockIdx.x * per, b1 = min(n16, b0 + per);
+  uint32_t acc = 0;
+  for (int64_t i = b0 + threadIdx.x; i < b1; i += 4 * kThreads) {
+    const u32x4 a = __builtin_nontemporal_load(p + i);
+    const u32x4 b = i + kThreads < b1 ? __builtin_nontemporal_load(p + i + kThreads) : a;
+    const u32x4 c = i + 2 * kThreads < b1 ? __builtin_nontemporal_load(p + i + 2 * kThreads) : a;
+    const u32x4 d = i + 3 * kThreads < b1 ? __builtin_nontemporal_load(p + i + 3 * kThreads) : a;
+    acc ^= a.x ^ b.y ^ c.z ^ d.w;
+  }
+  if (acc == 0x9E3779B9u) sink[0] = acc;
+}
+
+}  // namespace
+}  // namespace jacap
+
+extern "C" jacap_status jacap_stream_read(const void* src, size_t bytes, uint32_t* sink,
+                                          void* stream) {
+  using namespace jacap;
+  if (!src || !sink || (reinterpret_cast<uintptr_t>(src) & 15u) || (bytes & 15u))
+    return JACAP_ERR_INVALID_ARG;
+  if (bytes == 0) return JACAP_OK;
+  const int64_t n16 = (int64_t)(bytes / 16), per = kProbeBlockBytes / 16;
+  const int64_t blocks = (n16 + per - 1) / per;
+  if (blocks > INT32_MAX) return JACAP_ERR_INVALID_ARG;
+  stream_read_kernel<<<(unsigned)blocks, kThreads, 0, static_cast<hipStream_t>(stream)>>>(
+      static_cast<const u32x4*>(src), n16, per, sink);
+  return hipGetLastError() == hipSuccess ? JACAP_OK : JACAP_ERR_HIP;
+}

@@ -93,6 +93,7 @@ def _load() -> ctypes.CDLL:
         "jacap_read_status": [P, P, ctypes.POINTER(ctypes.c_uint32)],
         "jacap_greedy_workspace_size": [C, B, ctypes.POINTER(sz)],
         "jacap_greedy": [C, B, P, P, P, P, P, P, P, sz, P],
+        "jacap_stream_read": [P, sz, P, P],
     }
     for name, args in sigs.items():
         fn = getattr(lib, name)
@@ -113,7 +114,7 @@ _lib = _load()
 EXPORTED = ("jacap_workspace_size", "jacap_score", "jacap_score_from_stats", "jacap_select",
             "jacap_compact", "jacap_evict", "jacap_read_status", "jacap_status_string",
             "jacap_timing_start", "jacap_timing_stop", "jacap_phase_name",
-            "jacap_greedy_workspace_size", "jacap_greedy")
+            "jacap_greedy_workspace_size", "jacap_greedy", "jacap_stream_read")
 NUM_PHASES = 13   # enum jacap_phase
 
 
@@ -239,6 +240,14 @@ def score_from_stats(cfg, batch, mu, lam, k, v, scores, ws, stream=None) -> None
     _check("jacap_score_from_stats", _lib.jacap_score_from_stats(
         ctypes.byref(cfg), ctypes.byref(batch), _ptr(mu), _ptr(lam), _ptr(k), _ptr(v),
         _ptr(scores), _ptr(ws), ws.numel() if ws is not None else 0, _stream(stream)))
+
+
+def stream_read(src: torch.Tensor, sink: torch.Tensor, stream=None) -> None:
+    """jacap_stream_read over every byte of the contiguous device tensor src
+    (a measurement probe; sink: a device tensor of at least 4 bytes)."""
+    assert src.is_contiguous()
+    _check("jacap_stream_read", _lib.jacap_stream_read(
+        _ptr(src), src.numel() * src.element_size(), _ptr(sink), _stream(stream)))
 
 
 def select(cfg, batch, scores, idx, ws=None, stream=None) -> None:

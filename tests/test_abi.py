@@ -223,3 +223,14 @@ def test_score_from_stats_validation():
     code, n2 = _ws_size(per_head, b)
     assert code == jacap.OK
     assert call(per_head, good, good, good, good, good, good, n2, None) == jacap.ERR_UNSUPPORTED
+
+
+def test_stream_read_validation():
+    """The read probe takes 16-byte aligned pointers and sizes only."""
+    P = ctypes.c_void_p
+    f = jacap._lib.jacap_stream_read
+    assert f(None, 1024, P(0x2000), None) == jacap.ERR_INVALID_ARG
+    assert f(P(0x100008), 1024, P(0x2000), None) == jacap.ERR_INVALID_ARG
+    assert f(P(0x100000), 1000, P(0x2000), None) == jacap.ERR_INVALID_ARG
+    assert f(P(0x100000), 1024, None, None) == jacap.ERR_INVALID_ARG
+    assert f(P(0x100000), 0, P(0x2000), None) == jacap.OK   # nothing to read: no launch

@@ -360,6 +360,16 @@ def test_score_from_stats_nonfinite_flags_unit(jacap):
     assert torch.isnan(prob.scores).all()
 
 
+def test_stream_read_probe(jacap):
+    """The measurement probe reads a buffer with a ragged last workgroup and
+    leaves the sink alone (its XOR is not the sentinel)."""
+    x = torch.arange((3 << 20) // 4 + 64, dtype=torch.int32, device="cuda")
+    sink = torch.zeros(4, dtype=torch.int32, device="cuda")
+    jacap.stream_read(x, sink)
+    torch.cuda.synchronize()
+    assert int(sink[0]) == 0
+
+
 @pytest.mark.gpu
 def test_select_many_units_narrow_shape(jacap):
     """1024 units (4 sequences x 32 layers x 8 KV heads) take the narrow
