@@ -8,7 +8,7 @@ the HIP path.
 It follows Algorithm 1 (Jacap) of Sec. 3.4 and the equations it is built from
 (centre attention, Eq. 8 importance weight, Eq. 9 capacity matrix, Eq. 10
 leverage score), step by step, in float64. Readings of points the paper leaves
-open (all listed in the design doc):
+open:
 
 * ridge: A = ridge*I + sum_j w_j u_j u_j^T with w_j from Eq. 8. ridge=1 is
   Eq. 9; ridge=1/d reproduces Algorithm 1 literally (it drops the 1/d_k of

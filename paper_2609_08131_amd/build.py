@@ -22,7 +22,8 @@ LIB = os.path.join(HERE, "libjacap.so")
 
 ARCH = "gfx950"
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
-# Packed fp32 VALU ops are disabled ("Build flags").
+# Packed fp32 VALU ops (v_pk_*_f32) are disabled: every fp32 operation is
+# issued as a scalar VALU instruction.
 CFLAGS = [
     "-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",

@@ -22,8 +22,10 @@ from helpers import (gpu_unit_idx, gpu_unit_scores, oracle_unit, overlap, run_gp
 pytestmark = pytest.mark.gpu
 
 COV = {"diag": 0, "full": 1}
-# Condition number up to which the stated tolerance applies unscaled (see the design doc,
-# "Error model"): bf16 inputs with fp32-accumulated Gram and leverage products.
+# Condition number up to which the stated tolerance applies unscaled: with bf16
+# inputs the fp32-accumulated Gram and leverage products carry rounding errors
+# that A^{-1} amplifies by up to cond(A); above it the tolerance scales with
+# cond(A) / COND_REF.
 COND_REF = {"bf16": 1e5, "fp32": 1e12}
 
 
