@@ -57,7 +57,8 @@
  * - Host-detectable errors (null or misaligned pointers, bad shapes or
  *   strides, unsupported head_dim or dtype, too small a workspace) return an
  *   error code and enqueue nothing. K and V token strides above 2^24
- *   elements give JACAP_ERR_UNSUPPORTED. A failed launch returns JACAP_ERR_HIP.
+ *   elements, and batches with units x ceil(max_seq_len / 1024) above 2^31 - 1,
+ *   give JACAP_ERR_UNSUPPORTED. A failed launch returns JACAP_ERR_HIP.
  * - Data-dependent problems are reported through sticky device flags in the
  *   workspace (read with jacap_read_status): JACAP_FLAG_NONFINITE when a
  *   query, key or value is NaN/Inf, JACAP_FLAG_SINGULAR when A is not

@@ -37,6 +37,11 @@ jacap_status check_batch(const jacap_config* c, const jacap_batch* b) {
   if (b->num_seqs < 1 || b->max_seq_len < 0 || b->total_tokens < 0) return JACAP_ERR_INVALID_ARG;
   if ((int64_t)b->num_seqs * c->num_layers * c->num_kv_heads > 65535) return JACAP_ERR_UNSUPPORTED;
   if (b->total_tokens > (int64_t)INT32_MAX) return JACAP_ERR_UNSUPPORTED;
+  // The streaming kernels run one-dimensional grids of units x chunks (chunks
+  // of at least 1024 tokens).
+  if ((int64_t)b->num_seqs * c->num_layers * c->num_kv_heads * ((b->max_seq_len + 1023) / 1024) >
+      (int64_t)INT32_MAX)
+    return JACAP_ERR_UNSUPPORTED;
   const int64_t st[] = {b->k_stride_layer, b->k_stride_head, b->k_stride_token,
                         b->v_stride_layer, b->v_stride_head, b->v_stride_token,
                         b->q_stride_seq, b->q_stride_layer, b->q_stride_head, b->q_stride_pos,

@@ -292,7 +292,8 @@ __global__ __launch_bounds__(kThreads, 2) void gram_mfma_kernel(
   constexpr int NB = D / 16;
   constexpr int NPAIR = NB * (NB + 1) / 2;
   constexpr int TILE = kGramStep * kGramPitch;
-  const int u = blockIdx.y, chunk = blockIdx.x;
+  // chunk-major block order: every unit's first chunk, then the second ...
+  const int u = blockIdx.x % g.U, chunk = blockIdx.x / g.U;
   if (NT == 3 && !(uflags[u] & kUnitRefine)) return;
   const Unit un = decode_unit(g, u);
   const int base = chunk * gchunk;
@@ -325,7 +326,8 @@ __global__ __launch_bounds__(kThreads) void gram_precise_kernel(
   constexpr int R = D / 16;
   constexpr int NB = D / 16;
   constexpr int NPAIR = NB * (NB + 1) / 2;
-  const int u = blockIdx.y, chunk = blockIdx.x;
+  // chunk-major block order: every unit's first chunk, then the second ...
+  const int u = blockIdx.x % g.U, chunk = blockIdx.x / g.U;
   const Unit un = decode_unit(g, u);
   const int base = chunk * kGChunkPrecise;
   if (base >= un.n) return;
@@ -380,7 +382,7 @@ __global__ __launch_bounds__(kThreads) void gram_precise_kernel(
 
 hipError_t launch_gram(const Launch& L, const void* v, bool refine) {
   const Geo& g = L.geo;
-  const dim3 grid(L.ws.gchunks, g.U);
+  const dim3 grid((unsigned)((int64_t)L.ws.gchunks * g.U));
   const float* wb = ws_ptr<float>(L.wsp, L.ws.wgt);
   const uint32_t* uf = ws_ptr<uint32_t>(L.wsp, L.ws.uflags);
   if (L.ws.mfma) {

@@ -24,7 +24,8 @@ __global__ __launch_bounds__(kThreads, 2) void leverage_mfma_kernel(
   constexpr int NB = D / 16;                    // output blocks of 16 channels (a)
   constexpr int NK = D / 32;                    // K blocks of 32 channels (b)
   constexpr int NLP = (NB / 2) * (NB / 2 + 1);  // lower (j, kb) block pairs
-  const int u = blockIdx.y, chunk = blockIdx.x;
+  // chunk-major block order: every unit's first chunk, then the second ...
+  const int u = blockIdx.x % g.U, chunk = blockIdx.x / g.U;
   const Unit un = decode_unit(g, u);
   const int base = chunk * kLChunkMfma;
   if (base >= un.n) return;
@@ -153,7 +154,8 @@ __global__ __launch_bounds__(kThreads) void leverage_precise_kernel(
   constexpr int LD = D + 1;
   constexpr int TPT = 8;                 // threads per token
   constexpr int TOK = kThreads / TPT;    // tokens per tile
-  const int u = blockIdx.y, chunk = blockIdx.x;
+  // chunk-major block order: every unit's first chunk, then the second ...
+  const int u = blockIdx.x % g.U, chunk = blockIdx.x / g.U;
   const Unit un = decode_unit(g, u);
   const int base = chunk * kLChunkPrecise;
   if (base >= un.n) return;
@@ -194,7 +196,7 @@ __global__ __launch_bounds__(kThreads) void leverage_precise_kernel(
 
 hipError_t launch_leverage(const Launch& L, const void* v, float* scores) {
   const Geo& g = L.geo;
-  const dim3 grid(L.ws.lchunks, g.U);
+  const dim3 grid((unsigned)((int64_t)L.ws.lchunks * g.U));
   const float* wb = ws_ptr<float>(L.wsp, L.ws.wgt);
   const uint32_t* uf = ws_ptr<uint32_t>(L.wsp, L.ws.uflags);
   if (L.ws.mfma) {

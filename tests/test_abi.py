@@ -193,6 +193,14 @@ def test_greedy_workspace_and_validation():
     assert call(None, good, good, good, None, None, good, n, None) == jacap.ERR_INVALID_ARG
 
 
+def test_grid_size_limit():
+    """Units x ceil(max_seq_len / 1024) must fit a one-dimensional grid."""
+    assert _ws_size(_cfg(), _batch(num_seqs=65535, max_seq_len=32768, total_tokens=1 << 20))[0] \
+        == jacap.OK
+    assert _ws_size(_cfg(), _batch(num_seqs=65535, max_seq_len=1 << 26, total_tokens=1 << 26))[0] \
+        == jacap.ERR_UNSUPPORTED
+
+
 def test_token_stride_limit():
     """K / V token strides above 2^24 elements are not taken (32-bit row offsets)."""
     assert _ws_size(_cfg(), _batch(k_stride_token=1 << 24))[0] == jacap.OK
