@@ -197,7 +197,7 @@ jacap_status score_pass(const Launch& L, const void* q, const void* k, const voi
   else JACAP_PHASE(JACAP_PHASE_INIT, launch_clear_refine(L));
   if (mu) JACAP_PHASE(JACAP_PHASE_QSTATS, launch_stats_in(L, mu, lambda));
   else JACAP_PHASE(JACAP_PHASE_QSTATS, launch_qstats(L, q));
-  JACAP_PHASE(JACAP_PHASE_KPASS, launch_kpass(L, k));
+  JACAP_PHASE(JACAP_PHASE_KPASS, launch_kpass(L, k, mu ? nullptr : q));
   JACAP_PHASE(JACAP_PHASE_WEIGHTS, launch_softmax_weights(L));
   JACAP_PHASE(JACAP_PHASE_GRAM, launch_gram(L, v, false));
   JACAP_PHASE(JACAP_PHASE_GRAM_REDUCE, launch_gram_reduce(L, false));
@@ -364,7 +364,7 @@ jacap_status jacap_greedy(const jacap_config* cfg, const jacap_batch* batch, con
   JACAP_PHASE(JACAP_PHASE_INIT, launch_init(L));
   if (batch->total_tokens > 0) {
     JACAP_PHASE(JACAP_PHASE_QSTATS, launch_qstats(L, q_win));
-    JACAP_PHASE(JACAP_PHASE_KPASS, launch_kpass(L, k));
+    JACAP_PHASE(JACAP_PHASE_KPASS, launch_kpass(L, k, q_win));
     JACAP_PHASE(JACAP_PHASE_WEIGHTS, launch_softmax_weights(L));
   }
   if (cfg->budget_k == 0 && !logdet) return JACAP_OK;

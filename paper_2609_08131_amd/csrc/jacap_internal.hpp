@@ -14,6 +14,7 @@ namespace jacap {
 // ---------------------------------------------------------------------------
 constexpr int kThreads = 256;        // 4 wave64 per workgroup
 constexpr int kKChunk = 1024;        // tokens per workgroup in the K pass
+constexpr int kFullMaxQ = 256;       // window queries the FULL-covariance MFMA K pass stages
 constexpr int kGChunkMfma = 4096;    // tokens per workgroup in the MFMA Gram pass: at least
 constexpr int kGChunkMfmaMax = 16384; // ... and at most (larger chunks: fewer partial Grams)
 constexpr int kGramMinBlocks = 2048;  // chunks are as large as this many blocks in the grid allow
@@ -267,7 +268,7 @@ struct Launch {
 hipError_t launch_init(const Launch& L);
 hipError_t launch_qstats(const Launch& L, const void* q);
 hipError_t launch_stats_in(const Launch& L, const double* mu, const double* lambda);
-hipError_t launch_kpass(const Launch& L, const void* k);
+hipError_t launch_kpass(const Launch& L, const void* k, const void* q);
 hipError_t launch_softmax_weights(const Launch& L);
 hipError_t launch_clear_refine(const Launch& L);
 hipError_t launch_accumulate_scores(const Launch& L, float* acc, const float* add, float scale);

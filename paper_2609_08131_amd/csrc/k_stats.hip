@@ -501,6 +501,173 @@ __global__ __launch_bounds__(kThreads) void kpass_quad_kernel(
                  chunk);
 }
 
+// ---------------------------------------------------------------------------
+// K pass for bf16 keys with the FULL window covariance, on the MFMA: the tile
+// L = K Q^T of a chunk's tokens against the unit's N_s window queries (both
+// exact in bf16, fp32 accumulation), kappa_i = the 1/N_s variance of row i of
+// L, which equals k_i^T Lambda_Q k_i. The variance is accumulated about
+// c_i = mu . k_i (from the VALU, also giving z_i), so no large mean is
+// subtracted: kappa = mean((l - c)^2) - (mean(l) - c)^2, the second term
+// being rounding-sized. The window (N_s <= kFullMaxQ rows) is staged in LDS;
+// each wave takes 16-token tiles of the chunk, four per pass.
+// ---------------------------------------------------------------------------
+typedef __bf16 kbf16x8 __attribute__((ext_vector_type(8)));
+typedef float kfloatx4 __attribute__((ext_vector_type(4)));
+
+// Sum over each 16-lane row; every lane of the row ends with the sum.
+__device__ __forceinline__ float row_sum16_f32(float v) {
+  v += dpp_f32<kDppQuadXor1>(v);
+  v += dpp_f32<kDppQuadXor2>(v);
+  v += dpp_f32<kDppHalfMirror>(v);
+  v += dpp_f32<kDppMirror>(v);
+  return v;
+}
+
+template <int D>
+__global__ __launch_bounds__(kThreads, 2) void kpass_full_mfma_kernel(
+    Geo g, const uint16_t* __restrict__ k, const uint16_t* __restrict__ q,
+    const double* __restrict__ mu, float* __restrict__ zout, float* __restrict__ kout,
+    float2* __restrict__ cstat, int kchunks, double inv_scale, uint32_t* status,
+    uint32_t* uflags) {
+  constexpr int NK = D / 32;            // K-blocks of 32 channels
+  constexpr int QP = D + 8;             // u16 per staged query row (16 rows hit distinct banks)
+  constexpr int TT = 4;                 // 16-token tiles per wave pass
+  constexpr int WT = kKChunk / (kThreads / 64);  // tokens per wave per chunk
+  static_assert(WT % (2 * 16 * TT) == 0, "whole pairs of passes per wave");
+  const int u = blockIdx.y, chunk = blockIdx.x;
+  const Unit un = decode_unit(g, u);
+  const int base = chunk * kKChunk;
+  if (base >= un.n) return;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int ch = lane & 15, kg = lane >> 4;
+  const int Ns = g.G * g.w, nqt = (Ns + 15) / 16;
+
+  __shared__ __attribute__((aligned(16))) uint16_t qsh[kFullMaxQ * QP];
+  __shared__ float zsh[kKChunk];
+  __shared__ float ksq[kKChunk];
+  __shared__ float red[kThreads / 64];
+
+  // The pooled window: row r = gq * w + p (query head gq of the group,
+  // position p); rows N_s .. 16 nqt - 1 are zero and masked below.
+  const uint16_t* qb = q + un.b * g.qss + un.l * g.qsl + (int64_t)un.h * g.G * g.qsh;
+  for (int e = tid; e < nqt * 16 * (D / 8); e += kThreads) {
+    const int r = e / (D / 8), pc = e % (D / 8);
+    uint4 x = make_uint4(0u, 0u, 0u, 0u);
+    if (r < Ns) {
+      const int gq = r / g.w, p = r - gq * g.w;
+      x = *reinterpret_cast<const uint4*>(qb + gq * g.qsh + p * g.qsp + pc * 8);
+    }
+    *reinterpret_cast<uint4*>(qsh + r * QP + pc * 8) = x;
+  }
+  // mu on this lane's A-operand channels 32 kb + 8 kg + j
+  float muv[NK][8];
+#pragma unroll
+  for (int kb = 0; kb < NK; ++kb)
+#pragma unroll
+    for (int j = 0; j < 8; ++j) muv[kb][j] = (float)mu[(int64_t)u * D + 32 * kb + 8 * kg + j];
+  drain_vmem();
+  __syncthreads();
+
+  const uint16_t* kbase = k + un.l * g.ksl + un.h * g.ksh + un.t0 * g.kst;
+  const int64_t trow = token_row(g, un);
+  const int32_t kstb = (int32_t)g.kst * 2;
+  // A fragments of a pass: tile tt, token 16 tt + ch, channels 32 kb + 8 kg ..
+  // + 7 (16-byte loads through ranges ending at the unit's last row: rows past
+  // it read as zeros and are discarded).
+  struct Pass { uint4 a[TT][NK]; };
+  // One range per 16-row tile keeps the byte offsets below 16 rows.
+  auto load = [&](int t0, Pass& ps) {
+#pragma unroll
+    for (int tt = 0; tt < TT; ++tt) {
+      const int r0 = base + t0 + 16 * tt;
+      const auto kr = buffer_range(kbase + (int64_t)r0 * g.kst, rows_bytes(min(un.n - r0, 16), kstb, D * 2));
+#pragma unroll
+      for (int kb = 0; kb < NK; ++kb)
+        ps.a[tt][kb] = buffer_load16(kr, ch * kstb + (32 * kb + 8 * kg) * 2);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+  };
+  auto compute = [&](int t0, const Pass& ps) {
+    // c = mu . k for token 16 tt + ch: the lane's 32 channels, then the 4
+    // lanes (kg) of the token
+    float c[TT];
+#pragma unroll
+    for (int tt = 0; tt < TT; ++tt) {
+      float d = 0.0f;
+#pragma unroll
+      for (int kb = 0; kb < NK; ++kb) {
+        const uint32_t wd[4] = {ps.a[tt][kb].x, ps.a[tt][kb].y, ps.a[tt][kb].z, ps.a[tt][kb].w};
+#pragma unroll
+        for (int h = 0; h < 4; ++h) {
+          d = fmaf(muv[kb][2 * h], __uint_as_float(wd[h] << 16), d);
+          d = fmaf(muv[kb][2 * h + 1], __uint_as_float(wd[h] & 0xFFFF0000u), d);
+        }
+      }
+      d += __shfl_xor(d, 16);
+      d += __shfl_xor(d, 32);
+      c[tt] = d;
+    }
+    // the shift of output element (token 4 kg + r of tile tt, query ch)
+    float cs[TT][4];
+#pragma unroll
+    for (int tt = 0; tt < TT; ++tt)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) cs[tt][r] = __shfl(c[tt], 4 * kg + r);
+    float s1[TT][4], s2[TT][4];
+#pragma unroll
+    for (int tt = 0; tt < TT; ++tt)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) { s1[tt][r] = 0.0f; s2[tt][r] = 0.0f; }
+    for (int qt = 0; qt < nqt; ++qt) {
+      kfloatx4 acc[TT];
+#pragma unroll
+      for (int tt = 0; tt < TT; ++tt) acc[tt] = kfloatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int kb = 0; kb < NK; ++kb) {
+        const kbf16x8 b = *reinterpret_cast<const kbf16x8*>(qsh + (qt * 16 + ch) * QP + 32 * kb + 8 * kg);
+#pragma unroll
+        for (int tt = 0; tt < TT; ++tt)
+          acc[tt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+              __builtin_bit_cast(kbf16x8, ps.a[tt][kb]), b, acc[tt], 0, 0, 0);
+      }
+      const float m = (qt * 16 + ch < Ns) ? 1.0f : 0.0f;  // padding queries add nothing
+#pragma unroll
+      for (int tt = 0; tt < TT; ++tt)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const float e = (acc[tt][r] - cs[tt][r]) * m;
+          s1[tt][r] += e;
+          s2[tt][r] = fmaf(e, e, s2[tt][r]);
+        }
+    }
+    const float invn = 1.0f / (float)Ns;
+#pragma unroll
+    for (int tt = 0; tt < TT; ++tt)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const float a1 = row_sum16_f32(s1[tt][r]) * invn;
+        const float a2 = row_sum16_f32(s2[tt][r]) * invn;
+        const int tl = t0 + 16 * tt + 4 * kg + r;  // chunk-local token
+        if (ch == 0) {
+          ksq[tl] = fmaxf(a2 - a1 * a1, 0.0f);
+          zsh[tl] = base + tl < un.n ? (float)((double)cs[tt][r] * inv_scale) : -INFINITY;
+        }
+      }
+  };
+  Pass pa, pb;
+  const int w0 = wave * WT;
+  load(w0, pa);
+  for (int p0 = 0; p0 < WT; p0 += 2 * 16 * TT) {
+    load(w0 + p0 + 16 * TT, pb);
+    compute(w0 + p0, pa);
+    load(min(w0 + p0 + 2 * 16 * TT, w0 + WT - 16 * TT), pa);
+    compute(w0 + p0 + 16 * TT, pb);
+  }
+  kpass_epilogue(un, u, base, trow, zsh, ksq, red, zout, kout, cstat, kchunks, status, uflags,
+                 chunk);
+}
+
 template <typename T, int D>
 static void kpass_dispatch(const Launch& L, const void* k, bool full, dim3 grid, double inv_scale) {
   const Geo& g = L.geo;
@@ -524,12 +691,24 @@ static void kpass_dispatch(const Launch& L, const void* k, bool full, dim3 grid,
   }
 }
 
-hipError_t launch_kpass(const Launch& L, const void* k) {
+hipError_t launch_kpass(const Launch& L, const void* k, const void* q) {
   const Geo& g = L.geo;
   const bool full = L.cfg->cov_mode == JACAP_COV_FULL;
   const double inv_scale = 1.0 / ((double)L.cfg->temperature * sqrt((double)g.D));
   const dim3 grid(L.ws.kchunks, g.U);
   const bool bf = L.cfg->dtype == JACAP_DTYPE_BF16;
+  if (full && bf && q && g.G * g.w <= kFullMaxQ) {  // window queries at hand: the MFMA tile
+    auto go = [&](auto kern) {
+      kern<<<grid, kThreads, 0, L.stream>>>(
+          g, (const uint16_t*)k, (const uint16_t*)q, ws_ptr<double>(L.wsp, L.ws.mu),
+          ws_ptr<float>(L.wsp, L.ws.z), ws_ptr<float>(L.wsp, L.ws.kappa),
+          ws_ptr<float2>(L.wsp, L.ws.cstat), L.ws.kchunks, inv_scale,
+          ws_ptr<uint32_t>(L.wsp, L.ws.status), ws_ptr<uint32_t>(L.wsp, L.ws.uflags));
+    };
+    if (g.D == 128) go(kpass_full_mfma_kernel<128>);
+    else go(kpass_full_mfma_kernel<64>);
+    return hipGetLastError();
+  }
   if (g.D == 128) {
     if (bf) kpass_dispatch<uint16_t, 128>(L, k, full, grid, inv_scale);
     else kpass_dispatch<float, 128>(L, k, full, grid, inv_scale);

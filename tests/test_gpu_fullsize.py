@@ -59,10 +59,10 @@ def _sample_units(case, count=3):
     return out
 
 
-def _check_sampled(case, prob, budget, ridge, label):
+def _check_sampled(case, prob, budget, ridge, label, mode="diag"):
     worst, ovs = 0.0, []
     for (b, l, h) in _sample_units(case):
-        o = oracle_unit(case, b, l, h, budget, ridge=ridge)
+        o = oracle_unit(case, b, l, h, budget, ridge=ridge, cov_mode=mode)
         g = gpu_unit_scores(case, prob, b, l, h)
         err = score_errors(g, o["scores"])
         worst = max(worst, float(err.max()))
@@ -111,6 +111,21 @@ def test_ragged16():
     _check_all_units_properties(case, prob, budget, 1.0)
     _check_sampled(case, prob, budget, 1.0, "ragged16")
     del prob, case
+    _free()
+
+
+@pytest.mark.parametrize("wl", ["prefill32k", "long128k"])
+def test_full_covariance_fullsize(wl):
+    """FULL covariance at full size (N_s = 128 and 256 pooled window queries):
+    the MFMA K pass, sampled units against the oracle, properties on all."""
+    case = make_case(wl, device="cuda")
+    budget = case.workload.budget_k
+    prob, flags = run_gpu(case, budget, cov_mode=1)
+    assert flags == 0, flags
+    _check_all_units_properties(case, prob, budget, 1.0)
+    _check_sampled(case, prob, budget, 1.0, f"{wl} full", mode="full")
+    del prob
+    del case
     _free()
 
 

@@ -144,6 +144,18 @@ def test_llama_layer_bf16_full(jacap, ridge):
 # Ragged batches, both dtypes and head sizes, chunk boundaries and empty seqs
 # ---------------------------------------------------------------------------
 
+@pytest.mark.parametrize("d,heads,window", [(64, 3, 7), (128, 4, 64), (128, 4, 80)])
+def test_full_covariance_window_shapes_bf16(jacap, d, heads, window):
+    """FULL covariance with bf16 keys: the MFMA K pass stages the pooled
+    window in LDS -- N_s = 21 (a partial 16-query tile, d = 64), N_s = 256 (the
+    largest it takes) -- and N_s = 320 takes the VALU path; ragged lengths
+    with partial 64-token passes and an empty sequence."""
+    case = make_case("ragged16", device="cuda", seq_lens=(0, 1, 17, 300, 1500), num_layers=1,
+                     num_kv_heads=2, num_q_heads=2 * heads, window=window, head_dim=d,
+                     dtype="bf16")
+    check_case(case, 64, 1.0, "full", label=f"full d={d} N_s={heads * window}", jacap=jacap)
+
+
 @pytest.mark.parametrize("dtype,d", [("bf16", 128), ("bf16", 64), ("fp32", 64), ("fp32", 128)])
 def test_ragged_small(jacap, dtype, d):
     lens = [0, 1, 17, 255, 256, 257, 1000, 8193]
