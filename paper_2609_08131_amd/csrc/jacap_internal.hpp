@@ -269,6 +269,13 @@ hipError_t launch_init(const Launch& L);
 hipError_t launch_qstats(const Launch& L, const void* q);
 hipError_t launch_stats_in(const Launch& L, const double* mu, const double* lambda);
 hipError_t launch_kpass(const Launch& L, const void* k, const void* q);
+// FULL covariance with bf16 keys and the window queries at hand (q != null):
+// the K pass takes the MFMA tile of the queries, and the d x d Lambda is not
+// formed.
+inline bool full_kpass_on_mfma(const Launch& L, const void* q) {
+  return L.cfg->cov_mode == JACAP_COV_FULL && L.cfg->dtype == JACAP_DTYPE_BF16 && q != nullptr &&
+         L.geo.G * L.geo.w <= kFullMaxQ;
+}
 hipError_t launch_softmax_weights(const Launch& L);
 hipError_t launch_clear_refine(const Launch& L);
 hipError_t launch_accumulate_scores(const Launch& L, float* acc, const float* add, float scale);

@@ -161,7 +161,7 @@ __global__ __launch_bounds__(kThreads) void qstats_kernel(Geo g, const T* __rest
 
 hipError_t launch_qstats(const Launch& L, const void* q) {
   const Geo& g = L.geo;
-  const int full = L.cfg->cov_mode == JACAP_COV_FULL;
+  const int full = L.cfg->cov_mode == JACAP_COV_FULL && !full_kpass_on_mfma(L, q);
   double* mu = ws_ptr<double>(L.wsp, L.ws.mu);
   double* lam = ws_ptr<double>(L.wsp, L.ws.lam);
   float* lf = ws_ptr<float>(L.wsp, L.ws.lamfull);
@@ -697,7 +697,7 @@ hipError_t launch_kpass(const Launch& L, const void* k, const void* q) {
   const double inv_scale = 1.0 / ((double)L.cfg->temperature * sqrt((double)g.D));
   const dim3 grid(L.ws.kchunks, g.U);
   const bool bf = L.cfg->dtype == JACAP_DTYPE_BF16;
-  if (full && bf && q && g.G * g.w <= kFullMaxQ) {  // window queries at hand: the MFMA tile
+  if (full_kpass_on_mfma(L, q)) {  // window queries at hand: the MFMA tile
     auto go = [&](auto kern) {
       kern<<<grid, kThreads, 0, L.stream>>>(
           g, (const uint16_t*)k, (const uint16_t*)q, ws_ptr<double>(L.wsp, L.ws.mu),
