@@ -509,7 +509,8 @@ __global__ __launch_bounds__(kThreads) void kpass_quad_kernel(
 // c_i = mu . k_i (from the VALU, also giving z_i), so no large mean is
 // subtracted: kappa = mean((l - c)^2) - (mean(l) - c)^2, the second term
 // being rounding-sized. The window (N_s <= kFullMaxQ rows) is staged in LDS;
-// each wave takes 16-token tiles of the chunk, four per pass.
+// each wave takes 16-token tiles of the chunk, two per pass (rows loaded one
+// pass ahead), and reads the query fragments one 16-query tile ahead.
 // ---------------------------------------------------------------------------
 typedef __bf16 kbf16x8 __attribute__((ext_vector_type(8)));
 typedef float kfloatx4 __attribute__((ext_vector_type(4)));
@@ -531,7 +532,7 @@ __global__ __launch_bounds__(kThreads, 2) void kpass_full_mfma_kernel(
     uint32_t* uflags) {
   constexpr int NK = D / 32;            // K-blocks of 32 channels
   constexpr int QP = D + 8;             // u16 per staged query row (16 rows hit distinct banks)
-  constexpr int TT = 4;                 // 16-token tiles per wave pass
+  constexpr int TT = 2;                 // 16-token tiles per wave pass
   constexpr int WT = kKChunk / (kThreads / 64);  // tokens per wave per chunk
   static_assert(WT % (2 * 16 * TT) == 0, "whole pairs of passes per wave");
   const int u = blockIdx.y, chunk = blockIdx.x;
@@ -619,28 +620,43 @@ __global__ __launch_bounds__(kThreads, 2) void kpass_full_mfma_kernel(
     for (int tt = 0; tt < TT; ++tt)
 #pragma unroll
       for (int r = 0; r < 4; ++r) { s1[tt][r] = 0.0f; s2[tt][r] = 0.0f; }
-    for (int qt = 0; qt < nqt; ++qt) {
+    // B fragments (query tile qt, K-block kb) are read one tile ahead.
+    auto bload = [&](int qt, kbf16x8 (&b)[NK]) {
+#pragma unroll
+      for (int kb = 0; kb < NK; ++kb)
+        b[kb] = *reinterpret_cast<const kbf16x8*>(qsh + (qt * 16 + ch) * QP + 32 * kb + 8 * kg);
+    };
+    kbf16x8 bcur[NK], bnxt[NK];
+    bload(0, bcur);
+    auto qtile = [&](int qt, auto maskc) {
+      constexpr bool MASK = decltype(maskc)::value;
+      if (!MASK) bload(qt + 1, bnxt);
       kfloatx4 acc[TT];
 #pragma unroll
       for (int tt = 0; tt < TT; ++tt) acc[tt] = kfloatx4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int kb = 0; kb < NK; ++kb) {
-        const kbf16x8 b = *reinterpret_cast<const kbf16x8*>(qsh + (qt * 16 + ch) * QP + 32 * kb + 8 * kg);
 #pragma unroll
         for (int tt = 0; tt < TT; ++tt)
           acc[tt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-              __builtin_bit_cast(kbf16x8, ps.a[tt][kb]), b, acc[tt], 0, 0, 0);
+              __builtin_bit_cast(kbf16x8, ps.a[tt][kb]), bcur[kb], acc[tt], 0, 0, 0);
       }
-      const float m = (qt * 16 + ch < Ns) ? 1.0f : 0.0f;  // padding queries add nothing
+      // the last tile's padding queries (rows >= N_s) add nothing
+      const float m = (!MASK || qt * 16 + ch < Ns) ? 1.0f : 0.0f;
 #pragma unroll
       for (int tt = 0; tt < TT; ++tt)
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          const float e = (acc[tt][r] - cs[tt][r]) * m;
+          const float e = MASK ? (acc[tt][r] - cs[tt][r]) * m : acc[tt][r] - cs[tt][r];
           s1[tt][r] += e;
           s2[tt][r] = fmaf(e, e, s2[tt][r]);
         }
-    }
+      if (!MASK)
+#pragma unroll
+        for (int kb = 0; kb < NK; ++kb) bcur[kb] = bnxt[kb];
+    };
+    for (int qt = 0; qt < nqt - 1; ++qt) qtile(qt, std::false_type{});
+    qtile(nqt - 1, std::true_type{});
     const float invn = 1.0f / (float)Ns;
 #pragma unroll
     for (int tt = 0; tt < TT; ++tt)
