@@ -48,6 +48,8 @@ def parse():
     ap.add_argument("--tau", type=float, default=10.0)
     ap.add_argument("--cov", choices=("diag", "full"), default="diag",
                     help="query covariance: per-channel variances (default) or the full matrix")
+    ap.add_argument("--gqa", choices=("pooled", "per_head"), default="pooled",
+                    help="GQA reading: the group's queries pooled (default) or each head alone")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="time budget of the oracle CPU baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -134,7 +136,7 @@ def ensure_built():
         build.build()
 
 
-def cpu_baseline(case, budget, tau, ridge, seconds, cov="diag"):
+def cpu_baseline(case, budget, tau, ridge, seconds, cov="diag", gqa="pooled"):
     """Time the fp64 oracle on as many units (sequence, layer, KV head) of the
     same workload as fit in `seconds`; scale to full-model tokens/s."""
     from oracle import jacap_oracle as jo
@@ -155,7 +157,7 @@ def cpu_baseline(case, budget, tau, ridge, seconds, cov="diag"):
         b, l, h = units[i]
         q, k, v = case.unit_arrays(b, l, h)          # host copy, not timed
         t0 = time.perf_counter()
-        jo.evict_unit(q, k, v, budget, tau=tau, ridge=ridge, cov_mode=cov)
+        jo.evict_unit(q, k, v, budget, tau=tau, ridge=ridge, cov_mode=cov, gqa=gqa)
         t_total += time.perf_counter() - t0
         done_tokens += k.shape[0]
         done_units += 1
@@ -271,7 +273,9 @@ def main():
     w = case.workload
     budget = args.budget if args.budget is not None else w.budget_k
     params = jacap.Params(budget_k=budget, temperature=args.tau, ridge=args.ridge,
-                          cov_mode={"diag": jacap.COV_DIAG, "full": jacap.COV_FULL}[args.cov])
+                          cov_mode={"diag": jacap.COV_DIAG, "full": jacap.COV_FULL}[args.cov],
+                          gqa_mode={"pooled": jacap.GQA_POOLED,
+                                    "per_head": jacap.GQA_PER_HEAD}[args.gqa])
     prob = jacap.prepare(case.q_win, case.k, case.v, case.seq_offsets, case.seq_lens, params)
     stream = torch.cuda.current_stream()
     torch.cuda.synchronize()
@@ -345,7 +349,7 @@ def main():
             "workload": w.name, "num_seqs": case.num_seqs, "layers": w.num_layers,
             "kv_heads": w.num_kv_heads, "q_heads": w.num_q_heads, "head_dim": d,
             "tokens": case.total_tokens, "window": w.window, "budget_k": budget,
-            "tau": args.tau, "ridge": args.ridge, "cov_mode": args.cov,
+            "tau": args.tau, "ridge": args.ridge, "cov_mode": args.cov, "gqa": args.gqa,
         },
         "roofline": {
             "bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
@@ -362,7 +366,7 @@ def main():
         "step_hbm_gbs": step_bytes / (ms * 1e-3) / 1e9,
     }
     if not args.no_cpu_baseline:
-        cb = cpu_baseline(case, budget, args.tau, args.ridge, args.cpu_seconds, args.cov)
+        cb = cpu_baseline(case, budget, args.tau, args.ridge, args.cpu_seconds, args.cov, args.gqa)
         cb["gpu_speedup"] = tokens_per_s / cb["value"]
         out["cpu_baseline"] = cb
     print(json.dumps(out), flush=True)
