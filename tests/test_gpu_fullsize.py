@@ -142,3 +142,54 @@ def test_decode16k():
     del prob
     del case
     _free()
+
+
+def test_single_unit_of_two_million_tokens():
+    """The largest single unit exercised: 2^21 tokens (512 Gram chunks reduced
+    in order, multi-million-token offsets, selection over 2M scores), every
+    score against the oracle and the selection exact on the GPU's scores."""
+    n = 1 << 21
+    case = make_case("long128k", device="cuda", seq_lens=(n,), num_layers=1, num_kv_heads=1,
+                     num_q_heads=4)
+    budget = 4096
+    print(f"[fullsize] single unit n={n}", flush=True)
+    prob, flags = run_gpu(case, budget)
+    assert flags == 0, flags
+    o = oracle_unit(case, 0, 0, 0, budget)
+    g = gpu_unit_scores(case, prob, 0, 0, 0)
+    err = score_errors(g, o["scores"])
+    idx = gpu_unit_idx(case, prob, 0, 0, 0, budget)
+    assert np.array_equal(idx, jo.select_top(g.astype(np.float32), budget))
+    sel = torch.as_tensor(idx.astype(np.int64), device="cuda")
+    assert torch.equal(prob.k_out[0, 0, 0], case.k[0, 0, sel])
+    assert torch.equal(prob.v_out[0, 0, 0], case.v[0, 0, sel])
+    print(f"[fullsize] n={n}: worst rel err {err.max():.3e}; overlap with oracle selection "
+          f"{overlap(idx, o['idx']):.4f}", flush=True)
+    assert err.max() <= BF16_TOL
+    del prob, case
+    _free()
+
+
+def test_greedy_at_its_length_limit():
+    """jacap_greedy on one unit of 524288 tokens (its limit): a valid selection
+    whose pick order replays through the fp64 oracle as greedy."""
+    from paper_2609_08131_amd import jacap
+    n = 524288
+    case = make_case("long128k", device="cuda", seq_lens=(n,), num_layers=1, num_kv_heads=1,
+                     num_q_heads=4)
+    budget = 48
+    p = jacap.Params(budget_k=budget)
+    prob = jacap.prepare_greedy(case.q_win, case.k, case.v, case.seq_offsets, case.seq_lens, p)
+    jacap.run_greedy(prob, case.q_win, case.k, case.v)
+    assert jacap.read_status(prob.ws) == 0
+    order = prob.order[0, 0, 0].cpu().numpy()
+    assert len(set(order.tolist())) == budget and order.min() >= 0 and order.max() < n
+    assert np.array_equal(prob.idx[0, 0, 0].cpu().numpy(), np.sort(order))
+    q, k, v = case.unit_arrays(0, 0, 0)
+    w = jo.score_unit(q, k, v)["w"]
+    chosen, best = jo.greedy_replay(v, w, 1.0, order)
+    rel = (best - chosen) / np.abs(best)
+    print(f"[greedy] n={n}: worst replay gap {rel.max():.2e}", flush=True)
+    assert rel.max() <= 1e-4
+    del prob, case
+    _free()
