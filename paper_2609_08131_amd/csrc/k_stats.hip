@@ -505,10 +505,11 @@ __global__ __launch_bounds__(kThreads) void kpass_quad_kernel(
 // K pass for bf16 keys with the FULL window covariance, on the MFMA: the tile
 // L = K Q^T of a chunk's tokens against the unit's N_s window queries (both
 // exact in bf16, fp32 accumulation), kappa_i = the 1/N_s variance of row i of
-// L, which equals k_i^T Lambda_Q k_i. The variance is accumulated about
-// c_i = mu . k_i (from the VALU, also giving z_i), so no large mean is
-// subtracted: kappa = mean((l - c)^2) - (mean(l) - c)^2, the second term
-// being rounding-sized. The window (N_s <= kFullMaxQ rows) is staged in LDS;
+// L, which equals k_i^T Lambda_Q k_i. It is taken about c_i = mu . k_i (from
+// the VALU, also giving z_i): each MFMA chain starts from -c_i, so it yields
+// l - c directly, and kappa = mean((l - c)^2), without the large mean ever
+// being subtracted; the omitted (mean(l) - c)^2 is rounding-sized. The
+// window (N_s <= kFullMaxQ rows) is staged in LDS;
 // each wave takes 16-token tiles of the chunk, two per pass (rows loaded one
 // pass ahead), and reads the query fragments one 16-query tile ahead.
 // ---------------------------------------------------------------------------
@@ -531,7 +532,7 @@ __global__ __launch_bounds__(kThreads, 2) void kpass_full_mfma_kernel(
     float2* __restrict__ cstat, int kchunks, double inv_scale, uint32_t* status,
     uint32_t* uflags) {
   constexpr int NK = D / 32;            // K-blocks of 32 channels
-  constexpr int QP = D + 8;             // u16 per staged query row (16 rows hit distinct banks)
+  constexpr int QP = D + 8;             // u16 per staged query row
   constexpr int TT = 2;                 // 16-token tiles per wave pass
   constexpr int WT = kKChunk / (kThreads / 64);  // tokens per wave per chunk
   static_assert(WT % (2 * 16 * TT) == 0, "whole pairs of passes per wave");
@@ -609,17 +610,18 @@ __global__ __launch_bounds__(kThreads, 2) void kpass_full_mfma_kernel(
       d += __shfl_xor(d, 32);
       c[tt] = d;
     }
-    // the shift of output element (token 4 kg + r of tile tt, query ch)
-    float cs[TT][4];
+    // the shift of output element (token 4 kg + r of tile tt, query ch),
+    // negated: the MFMA chain starts from it, so it ends with l - c
+    kfloatx4 negc[TT];
 #pragma unroll
     for (int tt = 0; tt < TT; ++tt)
 #pragma unroll
-      for (int r = 0; r < 4; ++r) cs[tt][r] = __shfl(c[tt], 4 * kg + r);
-    float s1[TT][4], s2[TT][4];
+      for (int r = 0; r < 4; ++r) negc[tt][r] = -__shfl(c[tt], 4 * kg + r);
+    float s2[TT][4];
 #pragma unroll
     for (int tt = 0; tt < TT; ++tt)
 #pragma unroll
-      for (int r = 0; r < 4; ++r) { s1[tt][r] = 0.0f; s2[tt][r] = 0.0f; }
+      for (int r = 0; r < 4; ++r) s2[tt][r] = 0.0f;
     // B fragments (query tile qt, K-block kb) are read one tile ahead.
     auto bload = [&](int qt, kbf16x8 (&b)[NK]) {
 #pragma unroll
@@ -633,13 +635,12 @@ __global__ __launch_bounds__(kThreads, 2) void kpass_full_mfma_kernel(
       if (!MASK) bload(qt + 1, bnxt);
       kfloatx4 acc[TT];
 #pragma unroll
-      for (int tt = 0; tt < TT; ++tt) acc[tt] = kfloatx4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
       for (int kb = 0; kb < NK; ++kb) {
 #pragma unroll
         for (int tt = 0; tt < TT; ++tt)
           acc[tt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-              __builtin_bit_cast(kbf16x8, ps.a[tt][kb]), bcur[kb], acc[tt], 0, 0, 0);
+              __builtin_bit_cast(kbf16x8, ps.a[tt][kb]), bcur[kb], kb == 0 ? negc[tt] : acc[tt],
+              0, 0, 0);
       }
       // the last tile's padding queries (rows >= N_s) add nothing
       const float m = (!MASK || qt * 16 + ch < Ns) ? 1.0f : 0.0f;
@@ -647,8 +648,7 @@ __global__ __launch_bounds__(kThreads, 2) void kpass_full_mfma_kernel(
       for (int tt = 0; tt < TT; ++tt)
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          const float e = MASK ? (acc[tt][r] - cs[tt][r]) * m : acc[tt][r] - cs[tt][r];
-          s1[tt][r] += e;
+          const float e = MASK ? acc[tt][r] * m : acc[tt][r];
           s2[tt][r] = fmaf(e, e, s2[tt][r]);
         }
       if (!MASK)
@@ -657,17 +657,19 @@ __global__ __launch_bounds__(kThreads, 2) void kpass_full_mfma_kernel(
     };
     for (int qt = 0; qt < nqt - 1; ++qt) qtile(qt, std::false_type{});
     qtile(nqt - 1, std::true_type{});
+    // kappa = mean((l - c)^2); the omitted (mean(l) - c)^2 is the square of
+    // a rounding difference (c and the mean of l are the same dot product
+    // summed in two orders). One window query: exactly zero.
     const float invn = 1.0f / (float)Ns;
 #pragma unroll
     for (int tt = 0; tt < TT; ++tt)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const float a1 = row_sum16_f32(s1[tt][r]) * invn;
-        const float a2 = row_sum16_f32(s2[tt][r]) * invn;
+        const float a2 = Ns > 1 ? row_sum16_f32(s2[tt][r]) * invn : 0.0f;
         const int tl = t0 + 16 * tt + 4 * kg + r;  // chunk-local token
         if (ch == 0) {
-          ksq[tl] = fmaxf(a2 - a1 * a1, 0.0f);
-          zsh[tl] = base + tl < un.n ? (float)((double)cs[tt][r] * inv_scale) : -INFINITY;
+          ksq[tl] = a2;
+          zsh[tl] = base + tl < un.n ? (float)((double)(-negc[tt][r]) * inv_scale) : -INFINITY;
         }
       }
   };
