@@ -23,6 +23,7 @@ from __future__ import annotations
 import argparse
 import hashlib
 import json
+import re
 import os
 import sys
 import time
@@ -65,21 +66,80 @@ def parse():
 COPY_BYTES = 1 << 30
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic.json")
 # Source files whose kernels each phase launches (a change voids recorded counters).
+# Source file, kernel (the DIAG bf16 one on long128k) and launch function of
+# each phase.
 PHASE_SOURCES = {
-    "qstats": "k_stats.hip", "kpass": "k_stats.hip", "weights": "k_stats.hip",
-    "gram": "k_gram.hip", "gram_reduce": "k_gram.hip", "factor": "k_factor.hip",
-    "leverage": "k_leverage.hip", "select": "k_select.hip", "compact": "k_select.hip",
-    "greedy_init": "k_greedy.hip", "greedy": "k_greedy.hip",
+    "qstats": ("k_stats.hip", "qstats_kernel", "launch_qstats"),
+    "kpass": ("k_stats.hip", "kpass_quad_kernel", "launch_kpass"),
+    "weights": ("k_stats.hip", "softmax_weights_kernel", "launch_softmax_weights"),
+    "gram": ("k_gram.hip", "gram_mfma_kernel", "launch_gram"),
+    "gram_reduce": ("k_gram.hip", "gram_reduce_kernel", "launch_gram_reduce"),
+    "factor": ("k_factor.hip", "factor_kernel", "launch_factor"),
+    "leverage": ("k_leverage.hip", "leverage_mfma_kernel", "launch_leverage"),
+    "select": ("k_select.hip", "select_kernel", "launch_select"),
+    "compact": ("k_select.hip", "compact_kernel", "launch_compact"),
+    "greedy_init": ("k_greedy.hip", "greedy_init_kernel", "launch_greedy"),
+    "greedy": ("k_greedy.hip", "greedy_kernel", "launch_greedy"),
 }
 
 
+def _top_level_functions(text):
+    """{name: source text} of the function definitions at namespace scope of
+    a HIP source file (with their template line), by brace matching."""
+    # comments and string literals blanked, offsets kept
+    text = re.sub(r"//[^\n]*|/\*.*?\*/|\"(?:\\.|[^\"\\])*\"",
+                  lambda m: re.sub(r"[^\n]", " ", m.group(0)), text, flags=re.S)
+    out, i, n = {}, 0, len(text)
+    while i < n:
+        ch = text[i]
+        if ch == "{":
+            start = max(text.rfind(";", 0, i), text.rfind("}", 0, i), text.rfind("{", 0, i)) + 1
+            head = "\n".join(l for l in text[start:i].split("\n")
+                             if not l.lstrip().startswith("#")).strip()
+            if re.match(r"(namespace\b|extern\s+\S+$)", head):
+                i += 1  # namespace scope: its contents are scanned in place
+                continue
+            j, d = i, 0
+            while j < n:
+                d += text[j] == "{"
+                d -= text[j] == "}"
+                if d == 0:
+                    break
+                j += 1
+            m = re.search(r"(\w+)\s*\((?:[^()]|\([^()]*\))*\)[^()]*$", head)
+            if m and not re.match(r"(struct|class|union|enum)\b", head.split("\n")[-1].strip()):
+                out[m.group(1)] = out.get(m.group(1), "") + text[start:j + 1]
+            i = j + 1
+            continue
+        i += 1
+    return out
+
+
 def source_sha(phase):
-    f = PHASE_SOURCES.get(phase)
-    if f is None:
+    """Hash of what the phase's kernel and launch come from: the shared
+    internal header, the workspace layout (chunk sizes), the launch function,
+    and the kernel's own definition with, transitively, the file's functions
+    it names (edits elsewhere in the file leave it unchanged)."""
+    entry = PHASE_SOURCES.get(phase)
+    if entry is None:
         return None
-    path = os.path.join(ROOT, "paper_2609_08131_amd", "csrc", f)
-    with open(path, "rb") as fh:
-        return hashlib.sha256(fh.read()).hexdigest()[:16]
+    fname, kernel, launch = entry
+    csrc = os.path.join(ROOT, "paper_2609_08131_amd", "csrc")
+    with open(os.path.join(csrc, fname)) as fh:
+        funcs = _top_level_functions(fh.read())
+    with open(os.path.join(csrc, "jacap_host.hip")) as fh:
+        host = _top_level_functions(fh.read())
+    with open(os.path.join(csrc, "jacap_internal.hpp")) as fh:
+        parts = [fh.read(), host.get("layout", ""), funcs.get(launch, "")]
+    seen, todo = set(), [kernel]
+    while todo:
+        name = todo.pop()
+        if name in seen or name not in funcs:
+            continue
+        seen.add(name)
+        parts.append(funcs[name])
+        todo.extend(f for f in funcs if f not in seen and re.search(r"\b%s\b" % f, funcs[name]))
+    return hashlib.sha256("\n".join(parts).encode()).hexdigest()[:16]
 
 
 def recorded_traffic(phase, workload):
