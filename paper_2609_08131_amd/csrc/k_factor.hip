@@ -96,17 +96,34 @@ __global__ __launch_bounds__(kFactorThreads) void factor_kernel(Geo g, const dou
   __shared__ double red_sh[kFactorThreads / 64];
   __shared__ int bad;        // 0, or the unit flag that stops the factorisation
 
-  // Lower triangle of A = ridge I + M from the upper blocks of M: pass p
-  // copies block pair p (uniform), thread tid one entry of it.
+  // Lower triangle of A = ridge I + M from the upper blocks of M. Entries
+  // (2 e', 2 e' + 1) share a block pair and a lane: each thread loads its
+  // pairs first (all loads in flight), then places them.
   const double* R = red + (int64_t)u * (NPAIR * 256);
-  for (int e = tid; e < NPAIR * 256; e += kFactorThreads) {
-    int p = e >> 8, bi = 0;  // block pair p -> block (bi, bj), bi <= bj, row-major
-    while (p >= NB - bi) { p -= NB - bi; ++bi; }
-    const int bj = bi + p;
-    const int ln = (e & 255) / 4, r = e % 4;
-    const int row = bi * 16 + (ln >> 4) * 4 + r;
-    const int col = bj * 16 + (ln & 15);
-    if (row <= col) A[col * LD + row] = R[e];  // diagonal block: upper half only
+  constexpr int NE2 = NPAIR * 128;  // entry pairs
+  constexpr int PER = (NE2 + kFactorThreads - 1) / kFactorThreads;
+  double2 rv[PER];
+#pragma unroll
+  for (int k = 0; k < PER; ++k) {
+    const int e2 = tid + k * kFactorThreads;
+    if (e2 < NE2) rv[k] = reinterpret_cast<const double2*>(R)[e2];
+  }
+#pragma unroll
+  for (int k = 0; k < PER; ++k) {
+    const int e2 = tid + k * kFactorThreads;
+    if (e2 < NE2) {
+      const int e = 2 * e2;
+      int p = e >> 8, bi = 0;  // block pair p -> block (bi, bj), bi <= bj, row-major
+#pragma unroll
+      for (int q = 0; q < NB; ++q)
+        if (p >= NB - bi) { p -= NB - bi; ++bi; }
+      const int bj = bi + p;
+      const int ln = (e & 255) / 4, r = e % 4;  // r even: entries r and r + 1 of lane ln
+      const int row = bi * 16 + (ln >> 4) * 4 + r;
+      const int col = bj * 16 + (ln & 15);
+      if (row <= col) A[col * LD + row] = rv[k].x;  // diagonal block: upper half only
+      if (row + 1 <= col) A[col * LD + row + 1] = rv[k].y;
+    }
   }
   if (tid == 0) bad = 0;
   __syncthreads();
