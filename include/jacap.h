@@ -57,8 +57,9 @@
  * - Host-detectable errors (null or misaligned pointers, bad shapes or
  *   strides, unsupported head_dim or dtype, too small a workspace) return an
  *   error code and enqueue nothing. K and V token strides above 2^24
- *   elements, and batches with units x ceil(max_seq_len / 1024) above 2^31 - 1,
- *   give JACAP_ERR_UNSUPPORTED. A failed launch returns JACAP_ERR_HIP.
+ *   elements, and batches with units x ceil(max_seq_len / 1024) above 2^31 - 1
+ *   (units x G with per-query-head GQA, plus a padding of 8 G), give
+ *   JACAP_ERR_UNSUPPORTED. A failed launch returns JACAP_ERR_HIP.
  * - Data-dependent problems are reported through sticky device flags in the
  *   workspace (read with jacap_read_status): JACAP_FLAG_NONFINITE when a
  *   query, key or value is NaN/Inf, JACAP_FLAG_SINGULAR when A is not
@@ -168,7 +169,10 @@ typedef struct jacap_batch {
 /* Bytes of device workspace that jacap_score / jacap_select / jacap_evict
  * need for this configuration and batch (an upper bound that depends only on
  * the host fields). Returns JACAP_ERR_INVALID_ARG / _UNSUPPORTED for an
- * invalid configuration. Workspace base pointers must be 256-byte aligned. */
+ * invalid configuration. Workspace base pointers must be 256-byte aligned.
+ * Per-query-head GQA scores every query head as a unit of its own, so its
+ * per-unit and per-token storage is G times the pooled one (about 16 G bytes
+ * per cached token and KV head). */
 jacap_status jacap_workspace_size(const jacap_config* cfg, const jacap_batch* batch,
                                   size_t* bytes);
 

@@ -32,15 +32,24 @@ jacap_status check_config(const jacap_config* c) {
   return JACAP_OK;
 }
 
+// Query heads scored apart per KV head: the group size with per-head GQA, else 1.
+int64_t scored_heads(const jacap_config* c) {
+  return c->gqa_mode == JACAP_GQA_PER_HEAD && c->num_q_heads > c->num_kv_heads
+             ? c->num_q_heads / c->num_kv_heads
+             : 1;
+}
+
 jacap_status check_batch(const jacap_config* c, const jacap_batch* b) {
   if (!b || !b->seq_offsets) return JACAP_ERR_INVALID_ARG;
   if (b->num_seqs < 1 || b->max_seq_len < 0 || b->total_tokens < 0) return JACAP_ERR_INVALID_ARG;
   if ((int64_t)b->num_seqs * c->num_layers * c->num_kv_heads > 65535) return JACAP_ERR_UNSUPPORTED;
   if (b->total_tokens > (int64_t)INT32_MAX) return JACAP_ERR_UNSUPPORTED;
   // The streaming kernels run one-dimensional grids of units x chunks (chunks
-  // of at least 1024 tokens).
-  if ((int64_t)b->num_seqs * c->num_layers * c->num_kv_heads * ((b->max_seq_len + 1023) / 1024) >
-      (int64_t)INT32_MAX)
+  // of at least 1024 tokens; per-head GQA scores every query head as a unit
+  // and pads the grid by fewer than 8 units per head).
+  const int64_t vh = scored_heads(c);
+  if ((int64_t)b->num_seqs * c->num_layers * c->num_kv_heads * vh * ((b->max_seq_len + 1023) / 1024) +
+          8 * vh > (int64_t)INT32_MAX)
     return JACAP_ERR_UNSUPPORTED;
   const int64_t st[] = {b->k_stride_layer, b->k_stride_head, b->k_stride_token,
                         b->v_stride_layer, b->v_stride_head, b->v_stride_token,
@@ -64,9 +73,11 @@ jacap_status check_batch(const jacap_config* c, const jacap_batch* b) {
 // which needs the weight buffers but none of the Gram / factor storage.
 Workspace layout(const jacap_config* c, const jacap_batch* b, bool greedy = false) {
   Workspace w{};
-  const int64_t U = (int64_t)b->num_seqs * c->num_layers * c->num_kv_heads;
+  // Units and per-token rows: one per query head with per-head GQA.
+  const int64_t V = greedy ? 1 : scored_heads(c);
+  const int64_t U = (int64_t)b->num_seqs * c->num_layers * c->num_kv_heads * V;
   const int64_t D = c->head_dim;
-  const int64_t LHT = (int64_t)c->num_layers * c->num_kv_heads * b->total_tokens;
+  const int64_t LHT = (int64_t)c->num_layers * c->num_kv_heads * b->total_tokens * V;
   const int maxn = b->max_seq_len;
   w.mfma = c->dtype == JACAP_DTYPE_BF16;
   w.kchunks = (maxn + kKChunk - 1) / kKChunk;
@@ -104,7 +115,6 @@ Workspace layout(const jacap_config* c, const jacap_batch* b, bool greedy = fals
   w.kappa = take(4 * LHT);
   w.cstat = take(8 * U * (int64_t)w.kchunks);
   w.wgt = take(4 * LHT);
-  const bool per_head = c->gqa_mode == JACAP_GQA_PER_HEAD && c->num_q_heads > c->num_kv_heads;
   if (greedy) {
     const int64_t nblk = (maxn + 255) / 256;
     w.gc = take(8 * LHT);
@@ -113,7 +123,7 @@ Workspace layout(const jacap_config* c, const jacap_batch* b, bool greedy = fals
     w.total = o;
     return w;
   }
-  w.hscore = take(per_head ? 4 * LHT : 4);
+  w.hscore = take(V > 1 ? 4 * LHT : 4);
   w.gram = take((size_t)(U * (int64_t)w.gchunks * part_bytes));
   w.gram_red = take(8 * U * npair * 256);
   w.linv64 = take(w.mfma ? 8 : 8 * U * D * D);
@@ -132,6 +142,7 @@ Geo make_geo(const jacap_config* c, const jacap_batch* b) {
   g.w = c->window;
   g.B = b->num_seqs;
   g.U = b->num_seqs * c->num_layers * c->num_kv_heads;
+  g.V = 1;
   g.maxn = b->max_seq_len;
   g.T = b->total_tokens;
   g.seq_off = b->seq_offsets;
@@ -187,14 +198,11 @@ jacap_status prepare(const jacap_config* c, const jacap_batch* b, void* ws, size
   } while (0)
 
 // One scoring pass (Algorithm 1 steps 1-4) over every unit, from the window
-// queries q, or (mu != nullptr) from caller-supplied statistics. The first
-// pass of a call clears the status words; later passes (per-head GQA) keep
-// the sticky flags and clear only the refinement marks.
+// queries q, or (mu != nullptr) from caller-supplied statistics.
 jacap_status score_pass(const Launch& L, const void* q, const void* k, const void* v,
-                        float* scores, bool first, const double* mu = nullptr,
+                        float* scores, const double* mu = nullptr,
                         const double* lambda = nullptr) {
-  if (first) JACAP_PHASE(JACAP_PHASE_INIT, launch_init(L));
-  else JACAP_PHASE(JACAP_PHASE_INIT, launch_clear_refine(L));
+  JACAP_PHASE(JACAP_PHASE_INIT, launch_init(L));
   if (mu) JACAP_PHASE(JACAP_PHASE_QSTATS, launch_stats_in(L, mu, lambda));
   else JACAP_PHASE(JACAP_PHASE_QSTATS, launch_qstats(L, q));
   JACAP_PHASE(JACAP_PHASE_KPASS, launch_kpass(L, k, mu ? nullptr : q));
@@ -214,22 +222,18 @@ jacap_status score_pass(const Launch& L, const void* q, const void* k, const voi
 
 jacap_status run_score(const Launch& L, const void* q, const void* k, const void* v, float* scores) {
   const int G = L.geo.G;
-  if (L.cfg->gqa_mode != JACAP_GQA_PER_HEAD || G == 1) return score_pass(L, q, k, v, scores, true);
-  // Per-head GQA: query head g of every group alone (a geometry with one query
-  // head per KV head, whose head stride skips the group), then the mean.
-  const size_t esize = L.cfg->dtype == JACAP_DTYPE_BF16 ? 2 : 4;
+  if (scored_heads(L.cfg) == 1) return score_pass(L, q, k, v, scores);
+  // Per-head GQA: every query head of a group is a unit of its own (own
+  // statistics, weights and A; the G units of a KV head read its K and V rows
+  // together), then the mean of the G score rows.
+  Launch Lv = L;
+  Lv.geo.V = G;
+  Lv.geo.G = 1;
+  Lv.geo.U = L.geo.U * G;
   float* hs = ws_ptr<float>(L.wsp, L.ws.hscore);
-  for (int g = 0; g < G; ++g) {
-    Launch Lg = L;
-    Lg.geo.G = 1;
-    Lg.geo.Hq = L.geo.H;
-    Lg.geo.qsh = L.geo.qsh * G;
-    const void* qg = static_cast<const char*>(q) + (size_t)g * L.geo.qsh * esize;
-    const jacap_status s = score_pass(Lg, qg, k, v, g == 0 ? scores : hs, g == 0);
-    if (s != JACAP_OK) return s;
-    // scores = (((s_0 + s_1) + s_2) + ...) / G, in fp32, fixed order
-    if (g > 0) JACAP_TRY(launch_accumulate_scores(L, scores, hs, g == G - 1 ? 1.0f / G : 1.0f));
-  }
+  const jacap_status s = score_pass(Lv, q, k, v, hs);
+  if (s != JACAP_OK) return s;
+  JACAP_TRY(launch_head_mean(L, hs, scores));
   return JACAP_OK;
 }
 
@@ -285,7 +289,7 @@ jacap_status jacap_score_from_stats(const jacap_config* cfg, const jacap_batch* 
     TimedPhase tp(L.stream, JACAP_PHASE_INIT);
     return launch_init(L) == hipSuccess ? JACAP_OK : JACAP_ERR_HIP;
   }
-  return score_pass(L, nullptr, k, v, scores, true, mu, lambda);
+  return score_pass(L, nullptr, k, v, scores, mu, lambda);
 }
 
 jacap_status jacap_select(const jacap_config* cfg, const jacap_batch* batch, const float* scores,

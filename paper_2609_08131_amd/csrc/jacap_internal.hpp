@@ -39,7 +39,8 @@ constexpr uint32_t kUnitFailed = kUnitNonfinite | kUnitSingular;
 // Geometry passed by value to every kernel
 // ---------------------------------------------------------------------------
 struct Geo {
-  int L, H, Hq, G, D, w, B, U;  // U = B * L * H units
+  int L, H, Hq, G, D, w, B, U;  // U = B * L * H * V units
+  int V;                        // query heads scored apart per KV head (1: the group pooled)
   int maxn;                     // host-declared max sequence length
   int64_t T;                    // packed tokens per (layer, head)
   const int32_t* seq_off;       // device [B+1]
@@ -51,7 +52,8 @@ struct Geo {
 };
 
 struct Unit {
-  int b, l, h;
+  int b, l, h;  // sequence, layer, KV head
+  int s;        // query head within the group, when the V heads are scored apart
   int64_t t0;  // first packed token of the sequence
   int n;       // tokens of the sequence
 };
@@ -65,9 +67,11 @@ __device__ __forceinline__ bool offsets_ok(const Geo& g, int32_t a, int32_t e) {
 
 __device__ __forceinline__ Unit decode_unit(const Geo& g, int u) {
   Unit r;
-  r.h = u % g.H;
-  r.l = (u / g.H) % g.L;
-  r.b = u / (g.H * g.L);
+  r.s = u % g.V;
+  const int uk = u / g.V;
+  r.h = uk % g.H;
+  r.l = (uk / g.H) % g.L;
+  r.b = uk / (g.H * g.L);
   const int32_t a = g.seq_off[r.b];
   const int32_t e = g.seq_off[r.b + 1];
   r.t0 = a;
@@ -75,9 +79,44 @@ __device__ __forceinline__ Unit decode_unit(const Geo& g, int u) {
   return r;
 }
 
-// Offset of per-token arrays laid out like the scores: [L][H][T].
+// Offset of per-token arrays laid out like the scores: [L][H][V][T].
 __device__ __forceinline__ int64_t token_row(const Geo& g, const Unit& un) {
-  return ((int64_t)un.l * g.H + un.h) * g.T + un.t0;
+  return (((int64_t)un.l * g.H + un.h) * g.V + un.s) * g.T + un.t0;
+}
+
+// Workgroup -> (unit, chunk) of the passes that cut units into chunks, over
+// a one-dimensional grid of chunked_grid() workgroups. The base order of the
+// (KV unit, chunk) pairs is chunk-major (every unit's first chunk, then the
+// second ...) or unit-major. With the query heads of a group scored apart
+// (V > 1) the V units of one KV head read the same K or V rows: the V
+// workgroups of a pair are placed 8 apart in dispatch order, so that they
+// land on the same XCD (workgroups go to the 8 XCDs in turn) at about the same
+// time, and every read after the first hits that XCD's L2. False for the
+// padding past the last pair.
+template <bool CHUNK_MAJOR>
+__device__ __forceinline__ bool grid_unit_chunk(const Geo& g, int nchunks, int& u, int& chunk) {
+  int p = blockIdx.x, s = 0;
+  if (g.V > 1) {
+    const int r = p % (8 * g.V);
+    s = r >> 3;
+    p = p / (8 * g.V) * 8 + (r & 7);
+  }
+  const int nk = g.U / g.V;
+  int uk;
+  if (CHUNK_MAJOR) {
+    uk = p % nk;
+    chunk = p / nk;
+  } else {
+    uk = p / nchunks;
+    chunk = p % nchunks;
+  }
+  u = uk * g.V + s;
+  return uk < nk && chunk < nchunks;
+}
+
+inline int64_t chunked_grid(const Geo& g, int nchunks) {
+  const int64_t pairs = (int64_t)nchunks * (g.U / g.V);
+  return g.V == 1 ? pairs : (pairs + 7) / 8 * 8 * g.V;
 }
 
 // ---------------------------------------------------------------------------
@@ -209,6 +248,9 @@ constexpr int kBufferFormat = 0x00020000;
 // loads whose wave reads whole 128-byte lines: a line read in halves by two
 // loads would be fetched twice.
 constexpr int kPolicyStream = 2;
+// Cache policy of loads whose lines other workgroups of the XCD read next (the
+// query-head units of one KV head): the default, so that they stay in L2.
+constexpr int kPolicyShared = 0;
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_range(const void* base, int32_t bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, bytes, kBufferFormat);
 }
@@ -277,8 +319,7 @@ inline bool full_kpass_on_mfma(const Launch& L, const void* q) {
          L.geo.G * L.geo.w <= kFullMaxQ;
 }
 hipError_t launch_softmax_weights(const Launch& L);
-hipError_t launch_clear_refine(const Launch& L);
-hipError_t launch_accumulate_scores(const Launch& L, float* acc, const float* add, float scale);
+hipError_t launch_head_mean(const Launch& L, const float* hs, float* scores);
 hipError_t launch_gram(const Launch& L, const void* v, bool refine);
 hipError_t launch_gram_reduce(const Launch& L, bool refine);
 hipError_t launch_factor(const Launch& L, bool refine);

@@ -97,7 +97,7 @@ struct GramArgs {
 };
 
 // Whole chunk for wave W: it owns columns JA = W and JB = NB-1-W (if distinct).
-template <int D, int W, int NT>
+template <int D, int W, int NT, int POL>
 __device__ __forceinline__ void gram_wave(const GramArgs& ga, uint16_t* tiles, float* wts) {
   constexpr int NB = D / 16;
   constexpr int OCT = D / 8;                            // 16-byte pieces per token row
@@ -151,7 +151,7 @@ __device__ __forceinline__ void gram_wave(const GramArgs& ga, uint16_t* tiles, f
     const int32_t rows = min(left, kGramStep);
     const auto vr = buffer_range(vnext, rows_bytes(rows, vstb, D * 2));
 #pragma unroll
-    for (int r = 0; r < LOADS; ++r) buf.v[r] = buffer_load16<kPolicyStream>(vr, voff[r]);  // whole lines
+    for (int r = 0; r < LOADS; ++r) buf.v[r] = buffer_load16<POL>(vr, voff[r]);  // whole lines
     buf.w = buffer_load_f32(buffer_range(wnext, max(rows, 0) * 4), woff);
     vnext += kGramStep * ga.vst;
     wnext += kGramStep;
@@ -285,15 +285,17 @@ __device__ __forceinline__ void gram_wave(const GramArgs& ga, uint16_t* tiles, f
 
 // NT = 2: first pass over every unit. NT = 3: refinement pass over the units
 // the factor kernel marked (kUnitRefine), which rewrites their partials.
-template <int D, int NT>
+// POL: cache policy of the V loads (streamed, or kept in L2 for the other
+// query-head units of the same KV head).
+template <int D, int NT, int POL>
 __global__ __launch_bounds__(kThreads, 2) void gram_mfma_kernel(
     Geo g, const uint16_t* __restrict__ v, const float* __restrict__ wbuf,
     const uint32_t* __restrict__ uflags, float* __restrict__ partials, int gchunks, int gchunk) {
   constexpr int NB = D / 16;
   constexpr int NPAIR = NB * (NB + 1) / 2;
   constexpr int TILE = kGramStep * kGramPitch;
-  // chunk-major block order: every unit's first chunk, then the second ...
-  const int u = blockIdx.x % g.U, chunk = blockIdx.x / g.U;
+  int u, chunk;
+  if (!grid_unit_chunk<true>(g, gchunks, u, chunk)) return;
   if (NT == 3 && !(uflags[u] & kUnitRefine)) return;
   const Unit un = decode_unit(g, u);
   const int base = chunk * gchunk;
@@ -310,10 +312,10 @@ __global__ __launch_bounds__(kThreads, 2) void gram_mfma_kernel(
   ga.nsteps = (ga.end - base + SPAN - 1) / SPAN * kGramFlush;
   ga.out = partials + ((int64_t)u * gchunks + chunk) * (NPAIR * 256);
   switch (threadIdx.x >> 6) {
-    case 0: gram_wave<D, 0, NT>(ga, tiles, wts); break;
-    case 1: gram_wave<D, 1, NT>(ga, tiles, wts); break;
-    case 2: gram_wave<D, 2, NT>(ga, tiles, wts); break;
-    default: gram_wave<D, 3, NT>(ga, tiles, wts); break;
+    case 0: gram_wave<D, 0, NT, POL>(ga, tiles, wts); break;
+    case 1: gram_wave<D, 1, NT, POL>(ga, tiles, wts); break;
+    case 2: gram_wave<D, 2, NT, POL>(ga, tiles, wts); break;
+    default: gram_wave<D, 3, NT, POL>(ga, tiles, wts); break;
   }
 }
 
@@ -326,8 +328,8 @@ __global__ __launch_bounds__(kThreads) void gram_precise_kernel(
   constexpr int R = D / 16;
   constexpr int NB = D / 16;
   constexpr int NPAIR = NB * (NB + 1) / 2;
-  // chunk-major block order: every unit's first chunk, then the second ...
-  const int u = blockIdx.x % g.U, chunk = blockIdx.x / g.U;
+  int u, chunk;
+  if (!grid_unit_chunk<true>(g, gchunks, u, chunk)) return;
   const Unit un = decode_unit(g, u);
   const int base = chunk * kGChunkPrecise;
   if (base >= un.n) return;
@@ -382,18 +384,24 @@ __global__ __launch_bounds__(kThreads) void gram_precise_kernel(
 
 hipError_t launch_gram(const Launch& L, const void* v, bool refine) {
   const Geo& g = L.geo;
-  const dim3 grid((unsigned)((int64_t)L.ws.gchunks * g.U));
+  const dim3 grid((unsigned)chunked_grid(g, L.ws.gchunks));
   const float* wb = ws_ptr<float>(L.wsp, L.ws.wgt);
   const uint32_t* uf = ws_ptr<uint32_t>(L.wsp, L.ws.uflags);
   if (L.ws.mfma) {
     float* part = ws_ptr<float>(L.wsp, L.ws.gram);
     const uint16_t* vv = (const uint16_t*)v;
+    auto go = [&](auto kern) {
+      kern<<<grid, kThreads, 0, L.stream>>>(g, vv, wb, uf, part, L.ws.gchunks, L.ws.gchunk);
+    };
+    // The refinement pass is rare and always streams.
     if (g.D == 128) {
-      if (refine) gram_mfma_kernel<128, 3><<<grid, kThreads, 0, L.stream>>>(g, vv, wb, uf, part, L.ws.gchunks, L.ws.gchunk);
-      else gram_mfma_kernel<128, 2><<<grid, kThreads, 0, L.stream>>>(g, vv, wb, uf, part, L.ws.gchunks, L.ws.gchunk);
+      if (refine) go(gram_mfma_kernel<128, 3, kPolicyStream>);
+      else if (g.V > 1) go(gram_mfma_kernel<128, 2, kPolicyShared>);
+      else go(gram_mfma_kernel<128, 2, kPolicyStream>);
     } else {
-      if (refine) gram_mfma_kernel<64, 3><<<grid, kThreads, 0, L.stream>>>(g, vv, wb, uf, part, L.ws.gchunks, L.ws.gchunk);
-      else gram_mfma_kernel<64, 2><<<grid, kThreads, 0, L.stream>>>(g, vv, wb, uf, part, L.ws.gchunks, L.ws.gchunk);
+      if (refine) go(gram_mfma_kernel<64, 3, kPolicyStream>);
+      else if (g.V > 1) go(gram_mfma_kernel<64, 2, kPolicyShared>);
+      else go(gram_mfma_kernel<64, 2, kPolicyStream>);
     }
   } else {
     if (refine) return hipSuccess;
@@ -408,7 +416,7 @@ hipError_t launch_gram(const Launch& L, const void* v, bool refine) {
 
 // ---------------------------------------------------------------------------
 // Reduce the per-chunk partials of each unit, entry by entry, in chunk order
-// (fp64). grid = (NPAIR, U): one 16x16 block pair per workgroup.
+// (fp64). grid = (U, NPAIR): one 16x16 block pair per workgroup.
 // ---------------------------------------------------------------------------
 template <typename P, int D>
 __global__ __launch_bounds__(kThreads) void gram_reduce_kernel(Geo g, const P* __restrict__ partials,
@@ -417,7 +425,7 @@ __global__ __launch_bounds__(kThreads) void gram_reduce_kernel(Geo g, const P* _
                                                                int refine, double* __restrict__ red) {
   constexpr int NB = D / 16;
   constexpr int NPAIR = NB * (NB + 1) / 2;
-  const int p = blockIdx.x, u = blockIdx.y;
+  const int u = blockIdx.x, p = blockIdx.y;
   if (refine && !(uflags[u] & kUnitRefine)) return;
   const Unit un = decode_unit(g, u);
   const int nch = (un.n + gchunk - 1) / gchunk;
@@ -434,7 +442,7 @@ hipError_t launch_gram_reduce(const Launch& L, bool refine) {
   const uint32_t* uf = ws_ptr<uint32_t>(L.wsp, L.ws.uflags);
   const int rf = refine ? 1 : 0;
   const int NB = g.D / 16, npair = NB * (NB + 1) / 2;
-  const dim3 grid(npair, g.U);
+  const dim3 grid(g.U, npair);
   double* red = ws_ptr<double>(L.wsp, L.ws.gram_red);
   if (L.ws.mfma) {
     const float* part = ws_ptr<float>(L.wsp, L.ws.gram);

@@ -16,16 +16,18 @@ namespace jacap {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float floatx4 __attribute__((ext_vector_type(4)));
 
-template <int D>
+// POL: cache policy of the V loads (streamed, or kept in L2 for the other
+// query-head units of the same KV head).
+template <int D, int POL>
 __global__ __launch_bounds__(kThreads, 2) void leverage_mfma_kernel(
     Geo g, const uint16_t* __restrict__ v, const float* __restrict__ wbuf,
     const uint16_t* __restrict__ lfrag, const uint32_t* __restrict__ uflags,
-    float* __restrict__ scores) {
+    float* __restrict__ scores, int lchunks) {
   constexpr int NB = D / 16;                    // output blocks of 16 channels (a)
   constexpr int NK = D / 32;                    // K blocks of 32 channels (b)
   constexpr int NLP = (NB / 2) * (NB / 2 + 1);  // lower (j, kb) block pairs
-  // chunk-major block order: every unit's first chunk, then the second ...
-  const int u = blockIdx.x % g.U, chunk = blockIdx.x / g.U;
+  int u, chunk;
+  if (!grid_unit_chunk<true>(g, lchunks, u, chunk)) return;
   const Unit un = decode_unit(g, u);
   const int base = chunk * kLChunkMfma;
   if (base >= un.n) return;
@@ -83,7 +85,7 @@ __global__ __launch_bounds__(kThreads, 2) void leverage_mfma_kernel(
     const int32_t rows = min(end - t0, 16);
     const auto vr = buffer_range(vb + (int64_t)t0 * g.vst, rows_bytes(rows, vstb, D * 2));
 #pragma unroll
-    for (int i = 0; i < NK; ++i) b.a[i] = buffer_load16<kPolicyStream>(vr, voff[i]);
+    for (int i = 0; i < NK; ++i) b.a[i] = buffer_load16<POL>(vr, voff[i]);
     b.w = buffer_load_f32(buffer_range(wb + t0, max(rows, 0) * 4), woff);
     __builtin_amdgcn_sched_barrier(0);  // issue here, ahead of the MFMAs that follow
   };
@@ -150,12 +152,12 @@ template <int D>
 __global__ __launch_bounds__(kThreads) void leverage_precise_kernel(
     Geo g, const float* __restrict__ v, const float* __restrict__ wbuf,
     const double* __restrict__ linv64, const uint32_t* __restrict__ uflags,
-    float* __restrict__ scores) {
+    float* __restrict__ scores, int lchunks) {
   constexpr int LD = D + 1;
   constexpr int TPT = 8;                 // threads per token
   constexpr int TOK = kThreads / TPT;    // tokens per tile
-  // chunk-major block order: every unit's first chunk, then the second ...
-  const int u = blockIdx.x % g.U, chunk = blockIdx.x / g.U;
+  int u, chunk;
+  if (!grid_unit_chunk<true>(g, lchunks, u, chunk)) return;
   const Unit un = decode_unit(g, u);
   const int base = chunk * kLChunkPrecise;
   if (base >= un.n) return;
@@ -196,21 +198,27 @@ __global__ __launch_bounds__(kThreads) void leverage_precise_kernel(
 
 hipError_t launch_leverage(const Launch& L, const void* v, float* scores) {
   const Geo& g = L.geo;
-  const dim3 grid((unsigned)((int64_t)L.ws.lchunks * g.U));
+  const dim3 grid((unsigned)chunked_grid(g, L.ws.lchunks));
   const float* wb = ws_ptr<float>(L.wsp, L.ws.wgt);
   const uint32_t* uf = ws_ptr<uint32_t>(L.wsp, L.ws.uflags);
   if (L.ws.mfma) {
     const uint16_t* lf = ws_ptr<uint16_t>(L.wsp, L.ws.lfrag);
-    if (g.D == 128)
-      leverage_mfma_kernel<128><<<grid, kThreads, 0, L.stream>>>(g, (const uint16_t*)v, wb, lf, uf, scores);
-    else
-      leverage_mfma_kernel<64><<<grid, kThreads, 0, L.stream>>>(g, (const uint16_t*)v, wb, lf, uf, scores);
+    auto go = [&](auto kern) {
+      kern<<<grid, kThreads, 0, L.stream>>>(g, (const uint16_t*)v, wb, lf, uf, scores, L.ws.lchunks);
+    };
+    if (g.D == 128) {
+      if (g.V > 1) go(leverage_mfma_kernel<128, kPolicyShared>);
+      else go(leverage_mfma_kernel<128, kPolicyStream>);
+    } else {
+      if (g.V > 1) go(leverage_mfma_kernel<64, kPolicyShared>);
+      else go(leverage_mfma_kernel<64, kPolicyStream>);
+    }
   } else {
     const double* l64 = ws_ptr<double>(L.wsp, L.ws.linv64);
     if (g.D == 128)
-      leverage_precise_kernel<128><<<grid, kThreads, 0, L.stream>>>(g, (const float*)v, wb, l64, uf, scores);
+      leverage_precise_kernel<128><<<grid, kThreads, 0, L.stream>>>(g, (const float*)v, wb, l64, uf, scores, L.ws.lchunks);
     else
-      leverage_precise_kernel<64><<<grid, kThreads, 0, L.stream>>>(g, (const float*)v, wb, l64, uf, scores);
+      leverage_precise_kernel<64><<<grid, kThreads, 0, L.stream>>>(g, (const float*)v, wb, l64, uf, scores, L.ws.lchunks);
   }
   return hipGetLastError();
 }

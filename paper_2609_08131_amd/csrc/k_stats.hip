@@ -23,32 +23,29 @@ hipError_t launch_init(const Launch& L) {
   return hipGetLastError();
 }
 
-// Clears the refinement marks only (between the per-head passes of one call).
-__global__ void clear_refine_kernel(uint32_t* __restrict__ uflags, int U) {
-  const int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < U) uflags[i] &= ~kUnitRefine;
-}
-
-hipError_t launch_clear_refine(const Launch& L) {
-  const int U = L.geo.U;
-  clear_refine_kernel<<<(U + kThreads - 1) / kThreads, kThreads, 0, L.stream>>>(
-      ws_ptr<uint32_t>(L.wsp, L.ws.uflags), U);
-  return hipGetLastError();
-}
-
-// acc = (acc + add) * scale over the [L][H][T] score array.
-__global__ void accumulate_scores_kernel(float* __restrict__ acc, const float* __restrict__ add,
-                                         int64_t n, float scale) {
+// Per-head GQA (the paper is single-head; each query head of a group is scored
+// alone and a token's score is the mean over the group):
+// scores[l][h][t] = (((s_0 + s_1) + s_2) + ... + s_{G-1}) / G in fp32, in head
+// order, from the per-head rows hs[l][h][g][t].
+__global__ void head_mean_kernel(const float* __restrict__ hs, float* __restrict__ out, int64_t T,
+                                 int G, float inv) {
+  const float* src = hs + (int64_t)blockIdx.y * G * T;
+  float* dst = out + (int64_t)blockIdx.y * T;
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride)
-    acc[i] = (acc[i] + add[i]) * scale;
+  for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < T; t += stride) {
+    float acc = src[t];
+    for (int g = 1; g < G; ++g) acc += src[(int64_t)g * T + t];
+    dst[t] = acc * inv;
+  }
 }
 
-hipError_t launch_accumulate_scores(const Launch& L, float* acc, const float* add, float scale) {
-  const int64_t n = (int64_t)L.geo.L * L.geo.H * L.geo.T;
-  if (n == 0) return hipSuccess;
-  const int64_t blocks = std::min<int64_t>((n + kThreads - 1) / kThreads, 8192);
-  accumulate_scores_kernel<<<(unsigned)blocks, kThreads, 0, L.stream>>>(acc, add, n, scale);
+hipError_t launch_head_mean(const Launch& L, const float* hs, float* scores) {
+  const Geo& g = L.geo;
+  const int lh = g.L * g.H;
+  if (g.T == 0 || lh == 0) return hipSuccess;
+  const int64_t xb = std::min<int64_t>((g.T + kThreads - 1) / kThreads, std::max(1, 8192 / lh));
+  head_mean_kernel<<<dim3((unsigned)xb, lh), kThreads, 0, L.stream>>>(hs, scores, g.T, g.G,
+                                                                      1.0f / (float)g.G);
   return hipGetLastError();
 }
 
@@ -69,7 +66,7 @@ __global__ __launch_bounds__(kThreads) void qstats_kernel(Geo g, const T* __rest
       !offsets_ok(g, g.seq_off[un.b], g.seq_off[un.b + 1]))
     atomicOr(status, (uint32_t)JACAP_FLAG_BAD_OFFSETS);
   const int Ns = g.G * g.w;
-  const T* qb = q + un.b * g.qss + un.l * g.qsl + (int64_t)un.h * g.G * g.qsh;
+  const T* qb = q + un.b * g.qss + un.l * g.qsl + (int64_t)(un.h * g.V + un.s) * g.G * g.qsh;
   // Thread (cl, rp): 16-byte piece cl of rows rp, rp + RP, ...; partial sums
   // are combined over rp in a fixed order through LDS (fp64).
   constexpr int VEC = 16 / sizeof(T);
@@ -295,7 +292,8 @@ __global__ __launch_bounds__(kThreads) void kpass_kernel(
     const float* __restrict__ lamfull, float* __restrict__ zout, float* __restrict__ kout,
     float2* __restrict__ cstat, int kchunks, double inv_scale, uint32_t* status,
     uint32_t* uflags) {
-  const int u = blockIdx.y, chunk = blockIdx.x;
+  int u, chunk;
+  if (!grid_unit_chunk<false>(g, kchunks, u, chunk)) return;
   const Unit un = decode_unit(g, u);
   const int base = chunk * kKChunk;
   if (base >= un.n) return;
@@ -403,7 +401,8 @@ __global__ __launch_bounds__(kThreads) void kpass_quad_kernel(
     const double* __restrict__ lam, float* __restrict__ zout, float* __restrict__ kout,
     float2* __restrict__ cstat, int kchunks, double inv_scale, uint32_t* status,
     uint32_t* uflags) {
-  const int u = blockIdx.y, chunk = blockIdx.x;
+  int u, chunk;
+  if (!grid_unit_chunk<false>(g, kchunks, u, chunk)) return;
   const Unit un = decode_unit(g, u);
   const int base = chunk * kKChunk;
   if (base >= un.n) return;
@@ -536,7 +535,8 @@ __global__ __launch_bounds__(kThreads, 2) void kpass_full_mfma_kernel(
   constexpr int TT = 2;                 // 16-token tiles per wave pass
   constexpr int WT = kKChunk / (kThreads / 64);  // tokens per wave per chunk
   static_assert(WT % (2 * 16 * TT) == 0, "whole pairs of passes per wave");
-  const int u = blockIdx.y, chunk = blockIdx.x;
+  int u, chunk;
+  if (!grid_unit_chunk<false>(g, kchunks, u, chunk)) return;
   const Unit un = decode_unit(g, u);
   const int base = chunk * kKChunk;
   if (base >= un.n) return;
@@ -552,7 +552,7 @@ __global__ __launch_bounds__(kThreads, 2) void kpass_full_mfma_kernel(
 
   // The pooled window: row r = gq * w + p (query head gq of the group,
   // position p); rows N_s .. 16 nqt - 1 are zero and masked below.
-  const uint16_t* qb = q + un.b * g.qss + un.l * g.qsl + (int64_t)un.h * g.G * g.qsh;
+  const uint16_t* qb = q + un.b * g.qss + un.l * g.qsl + (int64_t)(un.h * g.V + un.s) * g.G * g.qsh;
   for (int e = tid; e < nqt * 16 * (D / 8); e += kThreads) {
     const int r = e / (D / 8), pc = e % (D / 8);
     uint4 x = make_uint4(0u, 0u, 0u, 0u);
@@ -713,7 +713,7 @@ hipError_t launch_kpass(const Launch& L, const void* k, const void* q) {
   const Geo& g = L.geo;
   const bool full = L.cfg->cov_mode == JACAP_COV_FULL;
   const double inv_scale = 1.0 / ((double)L.cfg->temperature * sqrt((double)g.D));
-  const dim3 grid(L.ws.kchunks, g.U);
+  const dim3 grid((unsigned)chunked_grid(g, L.ws.kchunks));
   const bool bf = L.cfg->dtype == JACAP_DTYPE_BF16;
   if (full_kpass_on_mfma(L, q)) {  // window queries at hand: the MFMA tile
     auto go = [&](auto kern) {
@@ -741,14 +741,16 @@ hipError_t launch_kpass(const Launch& L, const void* k, const void* q) {
 // Global softmax normaliser per unit, m = max_c m_c and
 // Z = sum_c Z_c exp(m_c - m) (fp64, fixed order), then the Eq. 8 importance
 // weight of every token of the block's chunk (fp64, stored as fp32).
-// grid = (wchunks, U). Every block of a unit merges the chunk statistics in the
-// same order, so all of them use bit-identical (m, Z); block 0 stores them.
+// wchunks blocks per unit. Every block of a unit merges the chunk statistics
+// in the same order, so all of them use bit-identical (m, Z); block 0 stores them.
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(kThreads) void softmax_weights_kernel(
     Geo g, const float2* __restrict__ cstat, int kchunks, const float* __restrict__ zbuf,
-    const float* __restrict__ kbuf, double inv_d, float* __restrict__ m_out,
+    const float* __restrict__ kbuf, double inv_d, int wchunks, float* __restrict__ m_out,
     double* __restrict__ z_out, float* __restrict__ wout) {
-  const int u = blockIdx.y, chunk = blockIdx.x, tid = threadIdx.x;
+  int u, chunk;
+  if (!grid_unit_chunk<false>(g, wchunks, u, chunk)) return;
+  const int tid = threadIdx.x;
   const Unit un = decode_unit(g, u);
   __shared__ float redf[kThreads / 64];
   __shared__ double redd[kThreads / 64];
@@ -797,10 +799,12 @@ __global__ __launch_bounds__(kThreads) void softmax_weights_kernel(
 }
 
 hipError_t launch_softmax_weights(const Launch& L) {
-  const dim3 grid(L.ws.wchunks > 0 ? L.ws.wchunks : 1, L.geo.U);
+  const int wchunks = L.ws.wchunks > 0 ? L.ws.wchunks : 1;
+  const dim3 grid((unsigned)chunked_grid(L.geo, wchunks));
   softmax_weights_kernel<<<grid, kThreads, 0, L.stream>>>(
       L.geo, ws_ptr<float2>(L.wsp, L.ws.cstat), L.ws.kchunks, ws_ptr<float>(L.wsp, L.ws.z),
-      ws_ptr<float>(L.wsp, L.ws.kappa), 1.0 / (double)L.geo.D, ws_ptr<float>(L.wsp, L.ws.smax_m),
+      ws_ptr<float>(L.wsp, L.ws.kappa), 1.0 / (double)L.geo.D, wchunks,
+      ws_ptr<float>(L.wsp, L.ws.smax_m),
       ws_ptr<double>(L.wsp, L.ws.smax_z), ws_ptr<float>(L.wsp, L.ws.wgt));
   return hipGetLastError();
 }

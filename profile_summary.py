@@ -8,13 +8,14 @@
       counters (first dispatch of each library kernel; any of the counters
       below that the runs collected).
 
-  python profile_summary.py traffic <fetch_dir> <write_dir> <workload> <out.md> <command...>
+  python profile_summary.py traffic|traffic-summary <fetch_dir> <write_dir> <workload> <out.md> <command...>
       HBM bytes per dispatch of each phase's kernel from two `--pmc` runs
       (FETCH_SIZE, then WRITE_SIZE; both in KiB per dispatch), each scaled by
       what the same counter reads for the plain 1 GiB copy that
       `bench.py --copy-calibration` runs first (a torch `neg` kernel: reads
       1 GiB, writes 1 GiB). Updates profiles/hbm_traffic.json, which bench.py
-      reads for roofline.traffic while the kernel source is unchanged.
+      reads for roofline.traffic while the kernel source is unchanged
+      (traffic-summary: the summary only, profiles/hbm_traffic.json untouched).
 """
 
 from __future__ import annotations
@@ -36,7 +37,7 @@ PHASE_KERNELS = {
     "qstats": r"jacap::qstats_kernel",
     "kpass": r"jacap::kpass_(quad_)?kernel",
     "weights": r"jacap::softmax_weights_kernel",
-    "gram": r"jacap::gram_mfma_kernel<\d+, 2>",
+    "gram": r"jacap::gram_mfma_kernel<\d+, 2, \d+>",
     "leverage": r"jacap::leverage_mfma_kernel",
     "select": r"jacap::select_kernel",
     "compact": r"jacap::compact_kernel",
@@ -70,9 +71,12 @@ def stats(csv_path, out_md, command):
 
 
 def _first_dispatch_counters(pmc_dirs):
-    """{kernel: {counter: value}} for the first dispatch of each jacap kernel."""
+    """{kernel: {counter: value}} for the first dispatch of each jacap kernel.
+    Rows of one run are summed (one per XCD or instance); a counter that
+    several runs collected (GRBM_GUI_ACTIVE) is taken from the first."""
     vals = defaultdict(dict)
     for d in pmc_dirs:
+        run = defaultdict(dict)
         for f in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
             first = {}
             for r in csv.DictReader(open(f)):
@@ -83,7 +87,10 @@ def _first_dispatch_counters(pmc_dirs):
                 if first.setdefault(name, did) != did:
                     continue
                 c = r["Counter_Name"]
-                vals[name][c] = vals[name].get(c, 0.0) + float(r["Counter_Value"])
+                run[name][c] = run[name].get(c, 0.0) + float(r["Counter_Value"])
+        for name, cs in run.items():
+            for c, v in cs.items():
+                vals[name].setdefault(c, v)
     return vals
 
 
@@ -101,6 +108,7 @@ def sq(out_md, command, pmc_dirs):
         ("wave: ready, not issued", lambda v, cyc: v["SQ_WAIT_INST_ANY"] / v["SQ_WAVE_CYCLES"]),
         ("wave: issuing", lambda v, cyc: v["SQ_ACTIVE_INST_ANY"] / v["SQ_WAVE_CYCLES"]),
         ("MFMA-VALU co-exec", lambda v, cyc: v["SQ_VALU_MFMA_COEXEC_CYCLES"] / (cyc * 1024)),
+        ("L2 hit", lambda v, cyc: v["TCC_HIT_sum"] / (v["TCC_HIT_sum"] + v["TCC_MISS_sum"])),
     ]
     names = [c for c, f in cols if any(_ok(f, v) for v in vals.values())]
     lines = ["| kernel | " + " | ".join(names) + " |", "|---|" + "---:|" * len(names)]
@@ -144,7 +152,9 @@ def _per_dispatch(pmc_dir, counter):
     return [(names[k], vals[k]) for k in sorted(vals)]
 
 
-def traffic(fetch_dir, write_dir, workload, out_md, command):
+def traffic(fetch_dir, write_dir, workload, out_md, command, record=True):
+    """record=False writes the summary only (a workload other than the one
+    bench.py's default line reports)."""
     import bench  # for source_sha (bench does not touch the GPU on import)
 
     fetch = _per_dispatch(fetch_dir, "FETCH_SIZE")
@@ -177,8 +187,9 @@ def traffic(fetch_dir, write_dir, workload, out_md, command):
                       "hbm_bytes_per_launch": fb + wb, "dispatches": len(fv),
                       "fetch_scale": cf, "write_scale": cw}
         lines.append(f"| {phase} | `{pat}` | {len(fv)} | {f_kib:.0f} | {w_kib:.0f} | {fb + wb:.4g} |")
-    with open(bench.TRAFFIC_FILE, "w") as fh:
-        json.dump(rec, fh, indent=1, sort_keys=True)
+    if record:
+        with open(bench.TRAFFIC_FILE, "w") as fh:
+            json.dump(rec, fh, indent=1, sort_keys=True)
     with open(out_md, "w") as fh:
         fh.write(f"# HBM traffic per dispatch ({workload})\n\nCommand:\n\n```\n{command}\n```\n\n")
         fh.write(f"Calibration: a 1 GiB copy ({cf_name.split('(')[0][:80]}) reads "
@@ -192,7 +203,8 @@ if __name__ == "__main__":
         stats(sys.argv[2], sys.argv[3], " ".join(sys.argv[4:]))
     elif mode == "sq":
         sq(sys.argv[2], sys.argv[3], sys.argv[4:])
-    elif mode == "traffic":
-        traffic(sys.argv[2], sys.argv[3], sys.argv[4], sys.argv[5], " ".join(sys.argv[6:]))
+    elif mode in ("traffic", "traffic-summary"):
+        traffic(sys.argv[2], sys.argv[3], sys.argv[4], sys.argv[5], " ".join(sys.argv[6:]),
+                record=mode == "traffic")
     else:
         raise SystemExit(__doc__)

@@ -199,6 +199,21 @@ def test_grid_size_limit():
         == jacap.OK
     assert _ws_size(_cfg(), _batch(num_seqs=65535, max_seq_len=1 << 26, total_tokens=1 << 26))[0] \
         == jacap.ERR_UNSUPPORTED
+    # per-query-head GQA scores G units per KV unit: the same batch that fits
+    # pooled (65535 x 16384 chunks) does not at G = 4
+    big = dict(num_seqs=65535, max_seq_len=1 << 24, total_tokens=1 << 24)
+    assert _ws_size(_cfg(num_q_heads=4), _batch(**big))[0] == jacap.OK
+    assert _ws_size(_cfg(num_q_heads=4, gqa_mode=1), _batch(**big))[0] == jacap.ERR_UNSUPPORTED
+
+
+def test_per_head_workspace_scales_with_the_group():
+    """Per-query-head GQA keeps per-unit and per-token storage for every query
+    head: its workspace is larger than the pooled one by about G times the
+    per-token arrays."""
+    b = _batch(max_seq_len=20000, total_tokens=20000)
+    _, pooled = _ws_size(_cfg(dtype=1, num_q_heads=4), b)
+    _, per_head = _ws_size(_cfg(dtype=1, num_q_heads=4, gqa_mode=1), b)
+    assert per_head > pooled + 3 * 3 * 4 * 20000
 
 
 def test_token_stride_limit():

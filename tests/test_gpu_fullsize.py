@@ -59,10 +59,10 @@ def _sample_units(case, count=3):
     return out
 
 
-def _check_sampled(case, prob, budget, ridge, label, mode="diag"):
+def _check_sampled(case, prob, budget, ridge, label, mode="diag", gqa="pooled"):
     worst, ovs = 0.0, []
     for (b, l, h) in _sample_units(case):
-        o = oracle_unit(case, b, l, h, budget, ridge=ridge, cov_mode=mode)
+        o = oracle_unit(case, b, l, h, budget, ridge=ridge, cov_mode=mode, gqa=gqa)
         g = gpu_unit_scores(case, prob, b, l, h)
         err = score_errors(g, o["scores"])
         worst = max(worst, float(err.max()))
@@ -110,6 +110,19 @@ def test_ragged16():
     assert flags == 0
     _check_all_units_properties(case, prob, budget, 1.0)
     _check_sampled(case, prob, budget, 1.0, "ragged16")
+    del prob, case
+    _free()
+
+
+def test_per_head_gqa_long128k():
+    """Per-head GQA at full size: the G = 4 query heads of every KV head scored
+    as units of their own in one launch, sampled units against the oracle."""
+    case = make_case("long128k", device="cuda")
+    budget = case.workload.budget_k
+    prob, flags = run_gpu(case, budget, ridge=1.0, gqa="per_head")
+    assert flags == 0
+    _check_all_units_properties(case, prob, budget, 1.0)
+    _check_sampled(case, prob, budget, 1.0, "long128k per-head", gqa="per_head")
     del prob, case
     _free()
 

@@ -474,12 +474,19 @@ def test_per_head_gqa_llama_layer_bf16(jacap):
                gqa="per_head")
 
 
-@pytest.mark.parametrize("dtype,d,mode", [("bf16", 128, "diag"), ("fp32", 64, "full")])
-def test_per_head_gqa_ragged(jacap, dtype, d, mode):
+@pytest.mark.parametrize("dtype,d,mode,hq,hkv", [("bf16", 128, "diag", 4, 2),
+                                                 ("fp32", 64, "full", 4, 2),
+                                                 ("bf16", 128, "full", 4, 2),
+                                                 ("bf16", 64, "diag", 6, 2),
+                                                 ("bf16", 128, "diag", 8, 1)])
+def test_per_head_gqa_ragged(jacap, dtype, d, mode, hq, hkv):
+    """Every query head scored as a unit of its own in one pass (groups of 2, 3
+    and 8 heads; the grid's padding past the last (unit, chunk) pair)."""
     case = make_case("ragged16", seq_lens=[0, 1, 17, 300, 1000, 4100], num_layers=2,
-                     num_kv_heads=2, num_q_heads=4, window=8, head_dim=d, dtype=dtype).to("cuda")
-    check_case(case, 64, 1.0, mode, label=f"ragged per-head {dtype} d{d}", jacap=jacap,
-               gqa="per_head")
+                     num_kv_heads=hkv, num_q_heads=hq, window=8, head_dim=d,
+                     dtype=dtype).to("cuda")
+    check_case(case, 64, 1.0, mode, label=f"ragged per-head {dtype} d{d} G{hq // hkv}",
+               jacap=jacap, gqa="per_head")
 
 
 @pytest.mark.parametrize("protect", [0, 7, 64, 100])
