@@ -198,15 +198,18 @@ __device__ __forceinline__ void gram_wave(const GramArgs& ga, uint16_t* tiles, f
         for (int t = 0; t < NT; ++t) xt[t][q] = h[t];
       }
     }
-    // term-outer order (smallest term first): consecutive MFMAs write
-    // different accumulators
+    // term-outer order, so that consecutive MFMAs write different
+    // accumulators. The two-term split issues the high term first: its
+    // MFMAs need only the rounded products, and the residual term's VALU
+    // work runs under them.
 #pragma unroll
-    for (int t = 0; t < NT; ++t) {
+    for (int tt = 0; tt < NT; ++tt) {
+      const int t = NT == 2 ? 1 - tt : tt;
       const bf16x8 c = __builtin_bit_cast(bf16x8, xt[t]);
 #pragma unroll
       for (int i = 0; i <= J; ++i) {
         const bf16x8 ai = __builtin_bit_cast(bf16x8, a[i]);
-        if (FIRST && t == 0)
+        if (FIRST && tt == 0)
           acc32[PBASE + i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ai, c, floatx4{0.f, 0.f, 0.f, 0.f}, 0, 0, 0);
         else
           acc32[PBASE + i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ai, c, acc32[PBASE + i], 0, 0, 0);
@@ -234,7 +237,28 @@ __device__ __forceinline__ void gram_wave(const GramArgs& ga, uint16_t* tiles, f
       // the VALU work runs while the matrix core is busy.
       if constexpr (HAS_B) column(std::integral_constant<int, JB>{}, std::integral_constant<int, PA>{}, firstc, a, wl);
       if constexpr (HAS_A) column(std::integral_constant<int, JA>{}, std::integral_constant<int, 0>{}, firstc, a, wl);
-      if constexpr (HAS_A && HAS_B) {
+      if constexpr (HAS_A && HAS_B && NT == 2) {
+        // Column JB's high term (products and their packed rounding), then
+        // its high-term MFMAs with the residual term's VALU work between
+        // them, then its residual-term MFMAs with column JA's split between
+        // them, then column JA's MFMAs.
+        constexpr int NBK = JB + 1, MA = NT * (JA + 1);
+        constexpr int HALF = 8 * 5 / 2;                  // VALU ops of one term of a column
+        constexpr int PER1 = (HALF + NBK - 1) / NBK;
+        constexpr int PER2 = (2 * HALF + NBK - 1) / NBK;
+        __builtin_amdgcn_sched_group_barrier(0x002, HALF, 0);    // JB: high term
+#pragma unroll
+        for (int m = 0; m < NBK; ++m) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);     // JB high-term MFMA
+          __builtin_amdgcn_sched_group_barrier(0x002, PER1, 0);  // part of JB's residual
+        }
+#pragma unroll
+        for (int m = 0; m < NBK; ++m) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);     // JB residual-term MFMA
+          __builtin_amdgcn_sched_group_barrier(0x002, PER2, 0);  // part of column JA's split
+        }
+        __builtin_amdgcn_sched_group_barrier(0x008, MA, 0);      // column JA's MFMAs
+      } else if constexpr (HAS_A && HAS_B) {
         constexpr int MB = NT * (JB + 1), MA = NT * (JA + 1);
         constexpr int SPLIT = 8 * 5;                     // VALU ops of one column's split
         constexpr int PER = (SPLIT + MB - 1) / MB;
