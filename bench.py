@@ -57,6 +57,9 @@ def parse():
     ap.add_argument("--mode", choices=("evict", "greedy"), default="evict",
                     help="evict: the Jacap pass (the headline line); greedy: the exact "
                          "greedy log-det selection (jacap_greedy), a quality comparator")
+    ap.add_argument("--inplace", action="store_true",
+                    help="evicted-slot lists instead of the compacted cache "
+                         "(jacap_evict_slots: a decoding round whose cache is refilled in place)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="first run a plain 1 GiB elementwise copy (torch.neg; the "
                          "reference kernel for scaling rocprofv3 FETCH_SIZE / WRITE_SIZE)")
@@ -338,6 +341,11 @@ def main():
                                     "per_head": jacap.GQA_PER_HEAD}[args.gqa])
     prob = jacap.prepare(case.q_win, case.k, case.v, case.seq_offsets, case.seq_lens, params)
     stream = torch.cuda.current_stream()
+    if args.inplace:
+        slots = jacap.alloc_slots(prob, case.seq_lens)
+        run = lambda: jacap.run_evict_slots(prob, slots, case.q_win, case.k, case.v, stream)
+    else:
+        run = lambda: jacap.run_evict(prob, case.q_win, case.k, case.v, stream)
     torch.cuda.synchronize()
 
     if args.copy_calibration:
@@ -348,14 +356,14 @@ def main():
         del src, dst
 
     for _ in range(args.warmup):
-        jacap.run_evict(prob, case.q_win, case.k, case.v, stream)
+        run()
     flags = jacap.read_status(prob.ws, stream)
     torch.cuda.synchronize()
 
     # Which phase dominates: two untimed steps with every phase recorded.
     jacap.timing_start()
     for _ in range(2):
-        jacap.run_evict(prob, case.q_win, case.k, case.v, stream)
+        run()
     per_phase = {k: ms / n for k, (ms, n) in jacap.timing_stop().items()}
     dominant = max(per_phase, key=per_phase.get)
 
@@ -367,7 +375,7 @@ def main():
     t_wall = time.perf_counter()
     for s, e in ev:
         s.record(stream)
-        jacap.run_evict(prob, case.q_win, case.k, case.v, stream)
+        run()
         e.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t_wall
@@ -410,6 +418,7 @@ def main():
             "kv_heads": w.num_kv_heads, "q_heads": w.num_q_heads, "head_dim": d,
             "tokens": case.total_tokens, "window": w.window, "budget_k": budget,
             "tau": args.tau, "ridge": args.ridge, "cov_mode": args.cov, "gqa": args.gqa,
+            "inplace": args.inplace,
         },
         "roofline": {
             "bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",

@@ -166,7 +166,8 @@ typedef struct jacap_batch {
                                  JACAP_RIDGE_MATRIX (then non-null, 8-byte aligned) */
 } jacap_batch;
 
-/* Bytes of device workspace that jacap_score / jacap_select / jacap_evict
+/* Bytes of device workspace that jacap_score / jacap_select / jacap_evict /
+ * jacap_select_evicted / jacap_evict_slots
  * need for this configuration and batch (an upper bound that depends only on
  * the host fields). Returns JACAP_ERR_INVALID_ARG / _UNSUPPORTED for an
  * invalid configuration. Workspace base pointers must be 256-byte aligned.
@@ -224,6 +225,31 @@ jacap_status jacap_evict(const jacap_config* cfg, const jacap_batch* batch,
                          const void* q_win, const void* k, const void* v, float* scores,
                          int32_t* idx, void* k_out, void* v_out, void* ws, size_t ws_bytes,
                          void* stream);
+
+/* The complement of jacap_select, for caches refilled in place during
+ * decoding (the periodic re-eviction of the decoding-stage setting, Sec. 4.3):
+ * for each unit, the positions of the n_b - min(budget_k, n_b) tokens that
+ * TOP-B evicts (the same kept set as jacap_select, protect_last included),
+ * in ascending order, written to slots[u][0 ..) with -1 in the rest. A caller
+ * overwrites those cache rows with its next tokens instead of compacting the
+ * kept ones: the positions then no longer follow arrival order, and the ties
+ * of the ranking resolve by slot. budget_k = 0 evicts every position.
+ *   slots    : int32 [B][L][H_kv][slot_cap], 16-byte aligned, owned by the
+ *              caller; slot_cap >= max(0, max_seq_len - budget_k), else
+ *              JACAP_ERR_INVALID_ARG.
+ *   ws       : required (jacap_workspace_size() bytes): the kept positions are
+ *              staged in it. */
+jacap_status jacap_select_evicted(const jacap_config* cfg, const jacap_batch* batch,
+                                  const float* scores, int32_t* slots, int32_t slot_cap, void* ws,
+                                  size_t ws_bytes, void* stream);
+
+/* jacap_score and jacap_select_evicted enqueued as one launch sequence on
+ * `stream`: one decoding-stage eviction round without the copy of the kept
+ * rows. */
+jacap_status jacap_evict_slots(const jacap_config* cfg, const jacap_batch* batch,
+                               const void* q_win, const void* k, const void* v, float* scores,
+                               int32_t* slots, int32_t slot_cap, void* ws, size_t ws_bytes,
+                               void* stream);
 
 /* ------------------------------------------------------------------------
  * Exact greedy log-det selection (App. B.1): the sequential selection that

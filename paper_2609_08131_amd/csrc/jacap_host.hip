@@ -124,6 +124,7 @@ Workspace layout(const jacap_config* c, const jacap_batch* b, bool greedy = fals
     return w;
   }
   w.hscore = take(V > 1 ? 4 * LHT : 4);
+  w.kept = take(4 * (int64_t)b->num_seqs * c->num_layers * c->num_kv_heads * std::max(c->budget_k, 1));
   w.gram = take((size_t)(U * (int64_t)w.gchunks * part_bytes));
   w.gram_red = take(8 * U * npair * 256);
   w.linv64 = take(w.mfma ? 8 : 8 * U * D * D);
@@ -237,6 +238,14 @@ jacap_status run_score(const Launch& L, const void* q, const void* k, const void
   return JACAP_OK;
 }
 
+// The evicted-slot lists: int32 [B][L][H][slot_cap], room for every eviction.
+bool slots_ok(const jacap_config* c, const jacap_batch* b, const float* scores,
+              const int32_t* slots, int32_t slot_cap) {
+  if (!slots || !aligned16(slots) || (!scores && b->total_tokens > 0)) return false;
+  if (scores && !aligned16(scores)) return false;
+  return slot_cap >= 0 && slot_cap >= b->max_seq_len - c->budget_k;
+}
+
 bool score_ptrs_ok(const void* q, const void* k, const void* v, const float* scores) {
   return q && k && v && scores && aligned16(q) && aligned16(k) && aligned16(v) && aligned16(scores);
 }
@@ -304,6 +313,18 @@ jacap_status jacap_select(const jacap_config* cfg, const jacap_batch* batch, con
   return launch_select(L, scores, idx) == hipSuccess ? JACAP_OK : JACAP_ERR_HIP;
 }
 
+jacap_status jacap_select_evicted(const jacap_config* cfg, const jacap_batch* batch,
+                                  const float* scores, int32_t* slots, int32_t slot_cap, void* ws,
+                                  size_t ws_bytes, void* stream) {
+  Launch L;
+  if (!ws) return JACAP_ERR_INVALID_ARG;
+  jacap_status s = prepare(cfg, batch, ws, ws_bytes, stream, &L);
+  if (s != JACAP_OK) return s;
+  if (!slots_ok(cfg, batch, scores, slots, slot_cap)) return JACAP_ERR_INVALID_ARG;
+  TimedPhase tp(L.stream, JACAP_PHASE_SELECT);
+  return launch_select_evicted(L, scores, slots, slot_cap) == hipSuccess ? JACAP_OK : JACAP_ERR_HIP;
+}
+
 jacap_status jacap_compact(const jacap_config* cfg, const jacap_batch* batch, const int32_t* idx,
                            const void* k, const void* v, void* k_out, void* v_out, void* stream) {
   Launch L;
@@ -337,6 +358,25 @@ jacap_status jacap_evict(const jacap_config* cfg, const jacap_batch* batch, cons
   if (cfg->budget_k == 0) return JACAP_OK;
   JACAP_PHASE(JACAP_PHASE_SELECT, launch_select(L, scores, idx));
   JACAP_PHASE(JACAP_PHASE_COMPACT, launch_compact(L, idx, k, v, k_out, v_out));
+  return JACAP_OK;
+}
+
+jacap_status jacap_evict_slots(const jacap_config* cfg, const jacap_batch* batch, const void* q_win,
+                               const void* k, const void* v, float* scores, int32_t* slots,
+                               int32_t slot_cap, void* ws, size_t ws_bytes, void* stream) {
+  Launch L;
+  if (!ws) return JACAP_ERR_INVALID_ARG;
+  jacap_status s = prepare(cfg, batch, ws, ws_bytes, stream, &L);
+  if (s != JACAP_OK) return s;
+  if (!score_ptrs_ok(q_win, k, v, scores)) return JACAP_ERR_INVALID_ARG;
+  if (!slots_ok(cfg, batch, scores, slots, slot_cap)) return JACAP_ERR_INVALID_ARG;
+  if (batch->total_tokens > 0) {
+    s = run_score(L, q_win, k, v, scores);
+    if (s != JACAP_OK) return s;
+  } else {
+    JACAP_PHASE(JACAP_PHASE_INIT, launch_init(L));
+  }
+  JACAP_PHASE(JACAP_PHASE_SELECT, launch_select_evicted(L, scores, slots, slot_cap));
   return JACAP_OK;
 }
 

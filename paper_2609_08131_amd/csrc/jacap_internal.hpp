@@ -134,7 +134,8 @@ struct Workspace {
   size_t kappa;    // float  [L][H][T]       query response
   size_t cstat;    // float2 [U][kchunks]    per-chunk (max, sum exp)
   size_t wgt;      // float  [L][H][T]       importance weights (Eq. 8)
-  size_t hscore;   // float  [L][H][T]       one query head's scores (per-head GQA mode)
+  size_t hscore;   // float  [L][H][G][T]    per-query-head scores (per-head GQA mode)
+  size_t kept;     // int32  [B][L][H][budget] kept positions, staged by jacap_select_evicted
   size_t gram;     // per-chunk partial Grams [U][gchunks][NPAIR*256], fp32 (bf16 path) or fp64
   size_t gram_red; // double [U][NPAIR*256]  reduced Gram, block-lane layout
   size_t linv64;   // double [U][D][D]       L^{-1} (lower, zeros above), fp32-input path
@@ -325,6 +326,7 @@ hipError_t launch_gram_reduce(const Launch& L, bool refine);
 hipError_t launch_factor(const Launch& L, bool refine);
 hipError_t launch_leverage(const Launch& L, const void* v, float* scores);
 hipError_t launch_select(const Launch& L, const float* scores, int32_t* idx);
+hipError_t launch_select_evicted(const Launch& L, const float* scores, int32_t* slots, int cap);
 hipError_t launch_compact(const Launch& L, const int32_t* idx, const void* k, const void* v,
                           void* ko, void* vo);
 hipError_t launch_greedy(const Launch& L, const void* v, int32_t* idx, int32_t* order,

@@ -1,4 +1,5 @@
-// TOP-B selection (Algorithm 1, last step) and the retained-cache gather
+// TOP-B selection (Algorithm 1, last step), its complement (the evicted
+// positions, for caches refilled in place) and the retained-cache gather
 // Z_C = {(k_i, v_i)}_{i in C} (Sec. 3.1).
 //
 // Selection is exact integer work on order-preserving 32-bit keys of the fp32
@@ -367,6 +368,41 @@ hipError_t launch_select(const Launch& L, const float* scores, int32_t* idx) {
   else
     select_kernel<SelWide><<<g.U, SelWide::kThreads, 0, L.stream>>>(g, scores, idx, budget,
                                                                     L.cfg->protect_last);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Evicted slots: the positions of each unit that the selection does not keep,
+// ascending, then -1 up to the list's capacity. The kept positions come
+// ascending from select_kernel; the evicted ones are the gaps between them:
+// the gap before kept entry j (after entry j - 1) holds positions whose rank
+// among the evicted ones is their index minus j. Thread t takes the gaps
+// j = t, t + kThreads, ... (coalesced reads of the kept list).
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(kThreads) void evicted_kernel(Geo g, const int32_t* __restrict__ kept,
+                                                           int budget, int32_t* __restrict__ slots,
+                                                           int cap) {
+  const int u = blockIdx.x, tid = threadIdx.x;
+  const Unit un = decode_unit(g, u);
+  const int n = un.n, kk = min(budget, n), ne = n - kk;
+  const int32_t* kp = kept + (int64_t)u * budget;
+  int32_t* out = slots + (int64_t)u * cap;
+  for (int j = ne + tid; j < cap; j += kThreads) out[j] = -1;
+  for (int j = tid; j <= kk; j += kThreads) {
+    const int a = j == 0 ? 0 : kp[j - 1] + 1;
+    const int b = j == kk ? n : kp[j];
+    for (int i = max(a, j); i < b && i - j < ne; ++i) out[i - j] = i;  // i - j >= 0 always
+  }
+}
+
+hipError_t launch_select_evicted(const Launch& L, const float* scores, int32_t* slots, int cap) {
+  const int budget = L.cfg->budget_k;
+  int32_t* kept = ws_ptr<int32_t>(L.wsp, L.ws.kept);
+  if (budget > 0) {
+    const hipError_t e = launch_select(L, scores, kept);
+    if (e != hipSuccess) return e;
+  }
+  evicted_kernel<<<L.geo.U, kThreads, 0, L.stream>>>(L.geo, kept, budget, slots, cap);
   return hipGetLastError();
 }
 

@@ -90,6 +90,8 @@ def _load() -> ctypes.CDLL:
         "jacap_select": [C, B, P, P, P, sz, P],
         "jacap_compact": [C, B, P, P, P, P, P, P],
         "jacap_evict": [C, B, P, P, P, P, P, P, P, P, sz, P],
+        "jacap_select_evicted": [C, B, P, P, ctypes.c_int32, P, sz, P],
+        "jacap_evict_slots": [C, B, P, P, P, P, P, ctypes.c_int32, P, sz, P],
         "jacap_read_status": [P, P, ctypes.POINTER(ctypes.c_uint32)],
         "jacap_greedy_workspace_size": [C, B, ctypes.POINTER(sz)],
         "jacap_greedy": [C, B, P, P, P, P, P, P, P, sz, P],
@@ -114,7 +116,8 @@ _lib = _load()
 EXPORTED = ("jacap_workspace_size", "jacap_score", "jacap_score_from_stats", "jacap_select",
             "jacap_compact", "jacap_evict", "jacap_read_status", "jacap_status_string",
             "jacap_timing_start", "jacap_timing_stop", "jacap_phase_name",
-            "jacap_greedy_workspace_size", "jacap_greedy", "jacap_stream_read")
+            "jacap_greedy_workspace_size", "jacap_greedy", "jacap_stream_read",
+            "jacap_select_evicted", "jacap_evict_slots")
 NUM_PHASES = 13   # enum jacap_phase
 
 
@@ -268,6 +271,19 @@ def evict(cfg, batch, q_win, k, v, scores, idx, k_out, v_out, ws, stream=None) -
         _ptr(idx), _ptr(k_out), _ptr(v_out), _ptr(ws), ws.numel(), _stream(stream)))
 
 
+def select_evicted(cfg, batch, scores, slots, ws, stream=None) -> None:
+    """slots: int32 [B][L][H][slot_cap] (the last dimension is the capacity)."""
+    _check("jacap_select_evicted", _lib.jacap_select_evicted(
+        ctypes.byref(cfg), ctypes.byref(batch), _ptr(scores), _ptr(slots),
+        int(slots.shape[-1]), _ptr(ws), ws.numel(), _stream(stream)))
+
+
+def evict_slots(cfg, batch, q_win, k, v, scores, slots, ws, stream=None) -> None:
+    _check("jacap_evict_slots", _lib.jacap_evict_slots(
+        ctypes.byref(cfg), ctypes.byref(batch), _ptr(q_win), _ptr(k), _ptr(v), _ptr(scores),
+        _ptr(slots), int(slots.shape[-1]), _ptr(ws), ws.numel(), _stream(stream)))
+
+
 def greedy_workspace_size(cfg: Config, batch: Batch) -> int:
     n = ctypes.c_size_t(0)
     _check("jacap_greedy_workspace_size", _lib.jacap_greedy_workspace_size(
@@ -325,6 +341,17 @@ def prepare(q_win, k, v, seq_offsets, seq_lens, params: Params) -> Problem:
 def run_evict(prob: Problem, q_win, k, v, stream=None) -> None:
     evict(prob.cfg, prob.batch, q_win, k, v, prob.scores, prob.idx, prob.k_out, prob.v_out,
           prob.ws, stream)
+
+
+def alloc_slots(prob: Problem, seq_lens) -> torch.Tensor:
+    """int32 [B][L][H][max(0, max_seq_len - budget)] for select_evicted / evict_slots."""
+    B, L, H = prob.idx.shape[:3]
+    cap = max(0, int(prob.batch.max_seq_len) - int(prob.cfg.budget_k))
+    return torch.empty((B, L, H, max(cap, 1)), dtype=torch.int32, device=prob.scores.device)
+
+
+def run_evict_slots(prob: Problem, slots, q_win, k, v, stream=None) -> None:
+    evict_slots(prob.cfg, prob.batch, q_win, k, v, prob.scores, slots, prob.ws, stream)
 
 
 @dataclasses.dataclass

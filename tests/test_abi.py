@@ -141,6 +141,30 @@ def test_entry_points_reject_bad_pointers_before_launch():
     assert lib.jacap_read_status(good, None, None) == jacap.ERR_INVALID_ARG
 
 
+def test_evicted_slot_entry_points_reject_bad_arguments():
+    """jacap_select_evicted / jacap_evict_slots: the slot lists must hold every
+    eviction (slot_cap >= max_seq_len - budget_k), be 16-byte aligned, and a
+    workspace is required; all checked before anything is enqueued."""
+    cfg, b = _cfg(budget_k=8), _batch()          # max_seq_len 100: 92 evictions at most
+    _, n = _ws_size(cfg, b)
+    P, I = ctypes.c_void_p, ctypes.c_int32
+    lib = jacap._lib
+    good = P(0x100000)
+    sel = lambda scores, slots, cap, ws, c=cfg: lib.jacap_select_evicted(
+        ctypes.byref(c), ctypes.byref(b), scores, slots, I(cap), ws, _ws_size(c, b)[1], None)
+    assert sel(good, good, 91, good) == jacap.ERR_INVALID_ARG
+    assert sel(good, None, 92, good) == jacap.ERR_INVALID_ARG
+    assert sel(good, P(0x100004), 92, good) == jacap.ERR_INVALID_ARG
+    assert sel(None, good, 92, good) == jacap.ERR_INVALID_ARG
+    assert sel(good, good, 92, None) == jacap.ERR_INVALID_ARG
+    assert sel(good, good, -1, good, _cfg(budget_k=200)) == jacap.ERR_INVALID_ARG
+    ev = lambda q, slots, cap: lib.jacap_evict_slots(
+        ctypes.byref(cfg), ctypes.byref(b), q, good, good, good, slots, I(cap), good, n, None)
+    assert ev(good, good, 91) == jacap.ERR_INVALID_ARG
+    assert ev(None, good, 92) == jacap.ERR_INVALID_ARG
+    assert ev(good, P(0x100008), 92) == jacap.ERR_INVALID_ARG
+
+
 def test_status_strings():
     for code, name in ((0, "JACAP_OK"), (1, "JACAP_ERR_INVALID_ARG"), (2, "JACAP_ERR_UNSUPPORTED"),
                        (3, "JACAP_ERR_WORKSPACE"), (4, "JACAP_ERR_HIP"), (99, "JACAP_ERR_UNKNOWN")):

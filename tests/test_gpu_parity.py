@@ -425,6 +425,94 @@ def test_select_many_units_narrow_shape(jacap):
         del prob
 
 
+def test_select_evicted_is_the_complement(jacap):
+    """jacap_select_evicted lists, per unit and ascending, exactly the positions
+    that the oracle's ranking does not keep (ties, NaN, -0 and inf mixes; both
+    selection shapes; budgets from 0 to beyond the longest sequence; a
+    protected tail); -1 fills the rest of each list."""
+    lens = [1, 700, 3000, 9000]
+    case = make_case("ragged16", device="cuda", seq_lens=lens, num_layers=32, num_kv_heads=8,
+                     num_q_heads=8, head_dim=64, window=2)
+    L, H, T = 32, 8, sum(lens)
+    rng = np.random.default_rng(12)
+    s = np.exp(rng.normal(0.0, 4.0, (L, H, T))).astype(np.float32)
+    s[1::4] = rng.integers(0, 4, (len(range(1, L, 4)), H, T)).astype(np.float32)  # ties
+    mix = s[2::4]
+    mix[rng.random(mix.shape) < 0.1] = np.nan
+    mix[rng.random(mix.shape) < 0.05] = -0.0
+    mix[rng.random(mix.shape) < 0.01] = np.inf
+    s[2::4] = mix
+    scores = torch.from_numpy(s).cuda()
+    for budget, protect in ((0, 0), (1, 0), (300, 0), (512, 0), (2048, 0), (8600, 0),
+                            (8999, 0), (9000, 0), (12000, 0), (200, 50), (8900, 3000)):
+        p = jacap.Params(budget_k=budget, protect_last=protect)
+        prob = jacap.prepare(case.q_win, case.k, case.v, case.seq_offsets, case.seq_lens, p)
+        slots = jacap.alloc_slots(prob, lens)
+        slots.fill_(-7)
+        print(f"[select_evicted] 1024 units, budget {budget}, protect {protect}", flush=True)
+        jacap.select_evicted(prob.cfg, prob.batch, scores, slots, prob.ws)
+        torch.cuda.synchronize()
+        got_all = slots.cpu().numpy()
+        for b in range(len(lens)):
+            lo, hi = token_slice(case, b)
+            for layer in range(L):
+                for h in range(H):
+                    kept = jo.select_top(s[layer, h, lo:hi], budget, protect) if budget else []
+                    want = np.setdiff1d(np.arange(hi - lo), kept)
+                    got = got_all[b, layer, h]
+                    assert np.array_equal(got[:len(want)], want), (budget, protect, b, layer, h)
+                    assert np.all(got[len(want):] == -1)
+        del prob, slots
+
+
+def test_decode_rounds_refill_evicted_slots_in_place(jacap):
+    """jacap_evict_slots: each round writes the next D tokens into the D slots
+    it evicts (ascending slots, tokens in arrival order) instead of compacting
+    the kept rows. The oracle runs the same chain with its own selections: the
+    same slots in every round, hence the same caches."""
+    R, D, B, rounds = 256, 32, 2, 3
+    spec = dict(num_layers=1, num_kv_heads=2, num_q_heads=4, window=8, head_dim=64, dtype="bf16")
+    L, H = spec["num_layers"], spec["num_kv_heads"]
+    first = make_case("ragged16", seq_lens=[R + D] * B, **spec)
+    k_cache, v_cache = first.k.clone().cuda(), first.v.clone().cuda()
+    ok = {(b, l, h): (first.unit_arrays(b, l, h)[1].copy(), first.unit_arrays(b, l, h)[2].copy())
+          for b in range(B) for l in range(L) for h in range(H)}
+    q_win = first.q_win
+    offsets = torch.tensor([i * (R + D) for i in range(B + 1)], dtype=torch.int32).cuda()
+    for r in range(rounds):
+        print(f"[decode in place] round {r}", flush=True)
+        qc = q_win.cuda()
+        prob = jacap.prepare(qc, k_cache, v_cache, offsets, [R + D] * B, jacap.Params(budget_k=R))
+        slots = jacap.alloc_slots(prob, [R + D] * B)
+        assert slots.shape[-1] == D
+        jacap.run_evict_slots(prob, slots, qc, k_cache, v_cache)
+        assert jacap.read_status(prob.ws) == 0
+        torch.cuda.synchronize()
+        nxt = make_case("ragged16", seq_lens=[D] * B, root=260908131 + 2000 + r, **spec)
+        got_all = slots.cpu().numpy()
+        for b in range(B):
+            for l in range(L):
+                for h in range(H):
+                    qa = q_win[b, l, h * 2:(h + 1) * 2].to(torch.float64).numpy()
+                    kk, vv = ok[(b, l, h)]
+                    o = jo.evict_unit(qa, kk, vv, R)
+                    want = np.setdiff1d(np.arange(R + D), o["idx"])
+                    assert np.array_equal(got_all[b, l, h], want), (r, b, l, h)
+                    _, nk, nv = nxt.unit_arrays(b, l, h)
+                    kk, vv = kk.copy(), vv.copy()
+                    kk[want], vv[want] = nk, nv
+                    ok[(b, l, h)] = (kk, vv)
+                    rows = torch.as_tensor(want + b * (R + D), device="cuda")
+                    k_cache[l, h, rows] = nxt.k[l, h, b * D:(b + 1) * D].cuda()
+                    v_cache[l, h, rows] = nxt.v[l, h, b * D:(b + 1) * D].cuda()
+        q_win = nxt.q_win
+        for (b, l, h), (kk, vv) in ok.items():
+            lo = b * (R + D)
+            np.testing.assert_array_equal(k_cache[l, h, lo:lo + R + D].double().cpu().numpy(), kk)
+            np.testing.assert_array_equal(v_cache[l, h, lo:lo + R + D].double().cpu().numpy(), vv)
+        del prob, slots
+
+
 # ---------------------------------------------------------------------------
 # Output-projection variant: u_i = W~ v_i through the ridge matrix R
 # ---------------------------------------------------------------------------
