@@ -82,12 +82,18 @@ def centre_logits(K: np.ndarray, mu: np.ndarray, tau: float) -> np.ndarray:
 def centre_attention(z: np.ndarray):
     """bar-alpha = softmax(z) over every cached token, and 1 - bar-alpha.
 
-    1 - bar-alpha_i is formed as (Z - e_i) / Z, the mass of the other tokens,
-    so that it does not cancel when bar-alpha_i approaches 1."""
+    1 - bar-alpha_i is the softmax mass of the other tokens, sum_{j != i} e_j / Z.
+    Formed as Z - e_i it cancels for a token that holds most of the mass (at
+    most one token holds more than half), so for that token the other tokens'
+    terms are summed directly."""
     m = z.max()
     e = np.exp(z - m)
     Z = e.sum()
-    return e / Z, (Z - e) / Z
+    rest = Z - e
+    i = int(np.argmax(e))
+    if e[i] > 0.5 * Z:
+        rest[i] = np.delete(e, i).sum()
+    return e / Z, rest / Z
 
 
 # ---------------------------------------------------------------------------

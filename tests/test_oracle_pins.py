@@ -188,8 +188,14 @@ def test_p4_sensitivity_peak_and_saturation():
     K[7] = 400.0 * np.eye(d)[0]
     V = rng.normal(size=(n, d))
     out = jo.score_unit(Q, K, V, tau=1.0, ridge=1e-3)
-    assert out["alpha"][7] > 0.999
-    assert out["w"][7] < 1e-3 * np.median(out["w"][out["w"] > 0]) or out["scores"][7] < np.median(out["scores"])
+    a7, r7 = out["alpha"][7], out["one_minus_alpha"][7]
+    assert a7 > 0.999
+    # the other tokens' mass is tiny but not zero, and the key's sensitivity
+    # rho = alpha (1 - alpha) -- hence its weight -- is a vanishing fraction of
+    # what the same key would get at peak sensitivity (rho = 1/4 at alpha = 1/2)
+    assert 0.0 < r7 < 1e-3
+    assert a7 * r7 < 1e-3 * 0.25
+    assert out["w"][7] < 1e-6 * out["kappa"][7] / (16 * d)
 
 
 # ---------------------------------------------------------------------------
@@ -664,3 +670,24 @@ def test_greedy_replay_and_determinant_lemma():
     bad[3] = int(alt) if alt != order[3] else int([i for i in range(n) if i not in bad[:4]][0])
     ch2, be2 = jo.greedy_replay(U, w, ridge, bad[:4])
     assert ch2[3] < be2[3]
+
+
+def test_other_token_mass_of_a_dominant_token():
+    """1 - bar-alpha_i, the factor of the sensitivity rho_i of Eq. 8, is the
+    softmax mass of the other tokens. For a token that holds nearly all of it
+    (here 1 - bar-alpha ~ 1e-13) the oracle's value must match exact rational
+    arithmetic on the same fp64 exponentials to fp64 precision; formed as
+    Z - e_i it would be off by ~1e-3."""
+    from fractions import Fraction
+    rng = np.random.default_rng(5)
+    z = np.concatenate([rng.normal(10.0, 1.0, 12), [40.0], rng.normal(10.0, 1.0, 30)])
+    alpha, one_minus = jo.centre_attention(z)
+    e = np.exp(z - z.max())
+    E = [Fraction(float(x)) for x in e]
+    Zx = sum(E)
+    assert one_minus[12] < 1e-11
+    for i in (0, 5, 12, 42):
+        exact_a = float(E[i] / Zx)
+        exact_r = float((Zx - E[i]) / Zx)
+        assert abs(alpha[i] - exact_a) <= 1e-14 * exact_a
+        assert abs(one_minus[i] - exact_r) <= 1e-14 * exact_r
