@@ -243,7 +243,11 @@ __device__ __forceinline__ F group_sum(F v) {
 }
 
 // Chunk epilogue of the K pass: z and kappa of the chunk (staged in LDS) stored
-// coalesced with one non-finite check, then the chunk's (max z, sum exp(z - max)).
+// coalesced with one non-finite check, then the chunk's (max z, rest), rest =
+// sum of exp(z - max) over every token but the first one holding the max (whose
+// term is exactly 1). Kept apart from that 1, the rest keeps its own relative
+// precision when one token dominates the softmax, which 1 - alpha of that
+// token needs (it is the rest of Z over Z).
 __device__ __forceinline__ void kpass_epilogue(const Unit& un, int u, int base, int64_t trow,
                                                const float* zsh, const float* ksq, float* red,
                                                float* __restrict__ zout,
@@ -274,9 +278,16 @@ __device__ __forceinline__ void kpass_epilogue(const Unit& un, int u, int base, 
     mloc = fmaxf(mloc, zv[q]);
   }
   const float m = block_combine(wave_max(mloc), red, [](float a, float b) { return fmaxf(a, b); });
+  int first = kKChunk;
+#pragma unroll
+  for (int q = ZPT - 1; q >= 0; --q)
+    if (zv[q] == m) first = q * kThreads + tid;
+  __shared__ int redi[kThreads / 64];
+  first = block_combine(wave_min(first), redi, [](int a, int b) { return min(a, b); });
   float ex = 0.0f;
 #pragma unroll
-  for (int q = 0; q < ZPT; ++q) ex += (zv[q] == -INFINITY) ? 0.0f : expf(zv[q] - m);
+  for (int q = 0; q < ZPT; ++q)
+    ex += (zv[q] == -INFINITY || q * kThreads + tid == first) ? 0.0f : expf(zv[q] - m);
   const float s = block_combine(wave_sum(ex), red, [](float a, float b) { return a + b; });
   if (tid == 0) cstat[(int64_t)u * kchunks + chunk] = make_float2(m, s);
 }
@@ -753,6 +764,7 @@ __global__ __launch_bounds__(kThreads) void softmax_weights_kernel(
   const int tid = threadIdx.x;
   const Unit un = decode_unit(g, u);
   __shared__ float redf[kThreads / 64];
+  __shared__ int redi[kThreads / 64];
   __shared__ double redd[kThreads / 64];
   if (un.n == 0) {
     if (chunk == 0 && tid == 0) { m_out[u] = 0.0f; z_out[u] = 1.0; }
@@ -765,21 +777,31 @@ __global__ __launch_bounds__(kThreads) void softmax_weights_kernel(
   float m = -INFINITY;
   for (int c = tid; c < nch; c += kThreads) m = fmaxf(m, cs[c].x);
   m = block_combine(wave_max(m), redf, [](float a, float b) { return fmaxf(a, b); });
-  double s = 0.0;
-  for (int c = tid; c < nch; c += kThreads) s += (double)cs[c].y * exp((double)cs[c].x - (double)m);
-  s = block_combine(wave_sum(s), redd, [](double a, double b) { return a + b; });
+  // The first chunk holding the maximum: its rest is the rest of Z; every
+  // other chunk adds its whole sum, (1 + rest) exp(m_c - m).
+  int cmax = nch;
+  for (int c = tid; c < nch; c += kThreads)
+    if (cs[c].x == m) cmax = min(cmax, c);
+  cmax = block_combine(wave_min(cmax), redi, [](int a, int b) { return min(a, b); });
+  double rest = 0.0;
+  for (int c = tid; c < nch; c += kThreads)
+    rest += c == cmax ? (double)cs[c].y
+                      : (1.0 + (double)cs[c].y) * exp((double)cs[c].x - (double)m);
+  rest = block_combine(wave_sum(rest), redd, [](double a, double b) { return a + b; });
+  const double s = 1.0 + rest;  // Z
   if (chunk == 0 && tid == 0) { m_out[u] = m; z_out[u] = s; }
   const int64_t trow = token_row(g, un);
   const int end = min(un.n, base + kWChunk);
   // Eq. 8 per token: e = exp(z - m) from the fp32 exponential of the rounded
   // difference, corrected to first order by the difference's rounding error
-  // (relative error ~1e-7), alpha = e / Z and 1 - alpha = (Z - e) / Z in fp64.
+  // (relative error ~1e-7), alpha = e / Z and 1 - alpha = (Z - e) / Z in fp64,
+  // with Z - e = (1 - e) + rest (exact for the maximum, where e = 1).
   const double invZ = 1.0 / s;
   auto weight = [&](float z, float kap) {
     const double dz = (double)z - (double)m;  // exact
     const float df = (float)dz;
     const double e = (double)expf(df) * (1.0 + (dz - (double)df));
-    const double rho = (e * invZ) * ((s - e) * invZ);
+    const double rho = (e * invZ) * (((1.0 - e) + rest) * invZ);
     return (float)(rho * rho * (double)kap * inv_d);
   };
   constexpr int U4 = 4;

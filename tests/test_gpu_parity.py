@@ -513,6 +513,50 @@ def test_decode_rounds_refill_evicted_slots_in_place(jacap):
         del prob, slots
 
 
+@pytest.mark.parametrize("gqa", ["pooled", "per_head"])
+def test_dominant_token_keeps_its_weight(jacap, gqa):
+    """At tau = 1 the planted sink takes nearly all of the centre softmax
+    (1 - alpha ~ 1e-11): its weight rests on the rest of Z, which the chunk
+    statistics keep apart from the maximum's own term (summed into it in fp32,
+    it would vanish and the sink's score with it)."""
+    case = make_case("ragged16", seq_lens=[256, 1025], num_layers=2, num_kv_heads=2,
+                     num_q_heads=8, window=4, head_dim=64, dtype="bf16").to("cuda")
+    check_case(case, 64, 1.0, "diag", tau=1.0, label=f"dominant token {gqa}", jacap=jacap,
+               gqa=gqa)
+
+
+def _sweep_specs(count=16):
+    """Seeded random configurations across the supported envelope: head_dim,
+    dtype, covariance, GQA group and mode, ridge, temperature, window (one
+    query included), ragged lengths around the tile sizes (empty and one-token
+    sequences included), budgets from 0 past every length, protected tails."""
+    rng = np.random.default_rng(2609)
+    lens_pool = [0, 1, 2, 15, 16, 17, 63, 255, 256, 257, 1000, 1025, 3000]
+    specs = []
+    for i in range(count):
+        specs.append(dict(
+            i=i, d=int(rng.choice([64, 128])), dtype=str(rng.choice(["bf16", "fp32"])),
+            mode=str(rng.choice(["diag", "full"])), hkv=int(rng.choice([1, 2])),
+            G=int(rng.choice([1, 2, 4])), gqa=str(rng.choice(["pooled", "per_head"])),
+            ridge=float(rng.choice([1.0, 0.0078125, 0.05])), tau=float(rng.choice([1.0, 10.0])),
+            window=int(rng.choice([1, 4, 8])),
+            lens=[int(x) for x in rng.choice(lens_pool, int(rng.integers(1, 5)))],
+            budget=int(rng.choice([0, 1, 16, 64, 300, 5000])),
+            protect=int(rng.choice([0, 0, 3, 40]))))
+    return specs
+
+
+@pytest.mark.parametrize("spec", _sweep_specs(), ids=lambda s: f"sweep{s['i']}")
+def test_random_configuration_sweep(jacap, spec):
+    s = spec
+    print(f"\n[sweep] {s}", flush=True)
+    case = make_case("ragged16", seq_lens=s["lens"], num_layers=2, num_kv_heads=s["hkv"],
+                     num_q_heads=s["hkv"] * s["G"], window=s["window"], head_dim=s["d"],
+                     dtype=s["dtype"]).to("cuda")
+    check_case(case, s["budget"], s["ridge"], s["mode"], tau=s["tau"], label=f"sweep{s['i']}",
+               jacap=jacap, gqa=s["gqa"], protect_last=s["protect"])
+
+
 # ---------------------------------------------------------------------------
 # Output-projection variant: u_i = W~ v_i through the ridge matrix R
 # ---------------------------------------------------------------------------
