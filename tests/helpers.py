@@ -59,13 +59,20 @@ def oracle_unit(case, b, l, h, budget, tau=10.0, ridge=1.0, cov_mode="diag", gqa
                          protect_last=protect_last)
 
 
+# Scores are returned in fp32: below its normal range (2^-126) they carry an
+# absolute resolution, not a relative one, so that is the comparison's scale
+# there (units whose centre softmax is saturated to ~1e-30 and beyond).
+FP32_NORMAL_MIN = float(np.finfo(np.float32).tiny)
+
+
 def score_errors(gpu: np.ndarray, ref: np.ndarray) -> np.ndarray:
-    """Floored relative error |g - o| / max(|o|, FLOOR * max|o|)."""
+    """Floored relative error |g - o| / max(|o|, FLOOR * max|o|, 2^-126)."""
     ref = np.asarray(ref, np.float64)
     gpu = np.asarray(gpu, np.float64)
     if ref.size == 0:
         return np.zeros(0)
     denom = np.maximum(np.abs(ref), FLOOR * np.max(np.abs(ref)))
+    denom = np.maximum(denom, FP32_NORMAL_MIN)
     denom = np.where(denom > 0, denom, 1.0)
     return np.abs(gpu - ref) / denom
 
