@@ -111,6 +111,7 @@ Workspace layout(const jacap_config* c, const jacap_batch* b, bool greedy = fals
   w.lamfull = take(c->cov_mode == JACAP_COV_FULL ? 4 * U * D * D : 4);
   w.smax_m = take(4 * U);
   w.smax_z = take(8 * U);
+  w.wscale = take(8 * U);
   w.z = take(4 * LHT);
   w.kappa = take(4 * LHT);
   w.cstat = take(8 * U * (int64_t)w.kchunks);

@@ -23,6 +23,10 @@ constexpr int kGChunkPrecise = 1024; // tokens per workgroup in the fp64 Gram pa
 constexpr int kLChunkMfma = 4096;    // tokens per workgroup in the MFMA leverage pass
 constexpr int kLChunkPrecise = 1024; // tokens per workgroup in the fp64 leverage pass
 constexpr int kWChunk = 4096;        // tokens per workgroup in the weight pass
+// The K pass sums a chunk's exp(z - max) terms (all but the max's own) as
+// exp(z - max + kRestShift) in fp32, so that they stay normal down to
+// z - max ~ -150 (a sharply peaked softmax at small temperature).
+constexpr float kRestShift = 64.0f;
 constexpr int kGreedyMaxLen = 524288; // longest sequence the greedy selection takes
 constexpr int kGreedyMaxD = 128;
 constexpr int64_t kMaxTokenStride = int64_t(1) << 24;  // elements between consecutive K / V rows
@@ -130,6 +134,7 @@ struct Workspace {
   size_t lamfull;  // float  [U][D][D]       (full covariance, FULL mode only)
   size_t smax_m;   // float  [U]             global logit max
   size_t smax_z;   // double [U]             global sum of exp(z - m)
+  size_t wscale;   // double [U]             power of two by which the stored weights are scaled
   size_t z;        // float  [L][H][T]       centre logits
   size_t kappa;    // float  [L][H][T]       query response
   size_t cstat;    // float2 [U][kchunks]    per-chunk (max, sum exp)

@@ -75,7 +75,9 @@ __device__ __forceinline__ void tri_index(int e, int& i, int& j) {
 // marked kUnitRefine by pass 0 (bf16 path), from their exact-split Gram.
 template <int D, bool FRAGS>
 __global__ __launch_bounds__(kFactorThreads) void factor_kernel(Geo g, const double* __restrict__ red,
-                                                          double ridge, double piv_rel, int pass,
+                                                          double ridge,
+                                                          const double* __restrict__ wscale,
+                                                          double piv_rel, int pass,
                                                           double* __restrict__ linv64,
                                                           uint16_t* __restrict__ lfrag,
                                                           uint32_t* status, uint32_t* uflags) {
@@ -127,16 +129,20 @@ __global__ __launch_bounds__(kFactorThreads) void factor_kernel(Geo g, const dou
   }
   if (tid == 0) bad = 0;
   __syncthreads();
+  // The weights of a saturated softmax are stored times a power of two (the
+  // weight pass's scale); the ridge term takes the same factor, so that A is
+  // the capacity matrix times it and every score is unchanged.
+  const double sc = wscale[u];
   if (g.ridge_mat) {  // output-projection variant: A = R + M
     const double* Rm = g.ridge_mat + ((int64_t)un.l * g.H + un.h) * D * D;
     for (int e = tid; e < D * D; e += kFactorThreads) {
       const int r = e / D, cc = e % D;
-      if (cc <= r) A[r * LD + cc] += Rm[e];
+      if (cc <= r) A[r * LD + cc] += Rm[e] * sc;
     }
     __syncthreads();
   }
   for (int a = tid; a < D; a += kFactorThreads) {
-    if (!g.ridge_mat) A[a * LD + a] += ridge;
+    if (!g.ridge_mat) A[a * LD + a] += ridge * sc;
     dg[a] = A[a * LD + a];
     if (!isfinite(dg[a])) atomicOr(&bad, (int)kUnitNonfinite);
   }
@@ -446,11 +452,11 @@ hipError_t launch_factor(const Launch& L, bool refine) {
   // path ~1e-15.
   const double piv_rel = L.ws.mfma ? 1e-4 : 1e-12;
   if (L.ws.mfma) {
-    if (g.D == 128) factor_kernel<128, true><<<g.U, kFactorThreads, 0, L.stream>>>(g, red, ridge, piv_rel, pass, l64, lf, st, uf);
-    else factor_kernel<64, true><<<g.U, kFactorThreads, 0, L.stream>>>(g, red, ridge, piv_rel, pass, l64, lf, st, uf);
+    if (g.D == 128) factor_kernel<128, true><<<g.U, kFactorThreads, 0, L.stream>>>(g, red, ridge, ws_ptr<double>(L.wsp, L.ws.wscale), piv_rel, pass, l64, lf, st, uf);
+    else factor_kernel<64, true><<<g.U, kFactorThreads, 0, L.stream>>>(g, red, ridge, ws_ptr<double>(L.wsp, L.ws.wscale), piv_rel, pass, l64, lf, st, uf);
   } else {
-    if (g.D == 128) factor_kernel<128, false><<<g.U, kFactorThreads, 0, L.stream>>>(g, red, ridge, piv_rel, pass, l64, lf, st, uf);
-    else factor_kernel<64, false><<<g.U, kFactorThreads, 0, L.stream>>>(g, red, ridge, piv_rel, pass, l64, lf, st, uf);
+    if (g.D == 128) factor_kernel<128, false><<<g.U, kFactorThreads, 0, L.stream>>>(g, red, ridge, ws_ptr<double>(L.wsp, L.ws.wscale), piv_rel, pass, l64, lf, st, uf);
+    else factor_kernel<64, false><<<g.U, kFactorThreads, 0, L.stream>>>(g, red, ridge, ws_ptr<double>(L.wsp, L.ws.wscale), piv_rel, pass, l64, lf, st, uf);
   }
   return hipGetLastError();
 }

@@ -137,7 +137,8 @@ __device__ __forceinline__ void load_elems(const T* p, float (&x)[N]) {
 // ---------------------------------------------------------------------------
 template <int D, typename T>
 __global__ __launch_bounds__(kThreads) void greedy_init_kernel(
-    Geo g, const T* __restrict__ v, const float* __restrict__ wgt, float ridge, int budget,
+    Geo g, const T* __restrict__ v, const float* __restrict__ wgt, float ridge,
+    const double* __restrict__ wscale, int budget,
     int protect, double* __restrict__ gc, int32_t* __restrict__ gst,
     GreedyEntry* __restrict__ entries, int nblk_max) {
   constexpr int EPL = D / 16;
@@ -170,7 +171,7 @@ __global__ __launch_bounds__(kThreads) void greedy_init_kernel(
     if (rl == it) mine = s;
   }
   const int i = i0 + wave * 64 + rl * 4 + row;
-  const double c = mine / (double)ridge;
+  const double c = mine / ((double)ridge * wscale[u]);  // the stored weights' scale
   double key = -__builtin_inf();
   int pos = INT32_MAX;
   if (i < un.n) {
@@ -217,7 +218,8 @@ struct GreedyShared {
 
 template <int D, typename T>
 __global__ __launch_bounds__(kThreads) void greedy_kernel(
-    Geo g, const T* __restrict__ v, const float* __restrict__ wgt, float ridge_f, int budget,
+    Geo g, const T* __restrict__ v, const float* __restrict__ wgt, float ridge_f,
+    const double* __restrict__ wscale, int budget,
     int protect, double* __restrict__ gc, int32_t* __restrict__ gst,
     const GreedyEntry* __restrict__ entries, int nblk_max, int32_t* __restrict__ idx_out,
     int32_t* __restrict__ order_out, double* __restrict__ logdet_out) {
@@ -235,7 +237,8 @@ __global__ __launch_bounds__(kThreads) void greedy_kernel(
   const int nblk = (n + kGBlock - 1) / kGBlock, words = (n + 31) / 32;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int r = tid / TPR, q = tid % TPR;
-  const double ridge = ridge_f;
+  // A_0 = ridge I times the stored weights' scale (gains are unchanged by it)
+  const double ridge = (double)ridge_f * wscale[u];
   const T* vb = v + (int64_t)un.l * g.vsl + (int64_t)un.h * g.vsh + un.t0 * g.vst;
   const int64_t trow = token_row(g, un);
 
@@ -451,7 +454,7 @@ __global__ __launch_bounds__(kThreads) void greedy_kernel(
     out[j] = -1;
     if (order) order[j] = -1;
   }
-  if (logdet_out && tid == 0) logdet_out[u] = (double)D * log(ridge) + logdet;
+  if (logdet_out && tid == 0) logdet_out[u] = (double)D * log((double)ridge_f) + logdet;
 }
 
 hipError_t launch_greedy(const Launch& L, const void* v, int32_t* idx, int32_t* order,
@@ -464,6 +467,7 @@ hipError_t launch_greedy(const Launch& L, const void* v, int32_t* idx, int32_t* 
   int32_t* gst = ws_ptr<int32_t>(L.wsp, L.ws.gst);
   GreedyEntry* ent = ws_ptr<GreedyEntry>(L.wsp, L.ws.gent);
   const float ridge = L.cfg->ridge;
+  const double* wsc = ws_ptr<double>(L.wsp, L.ws.wscale);
   const int protect = L.cfg->protect_last;
   const bool bf16 = L.cfg->dtype == JACAP_DTYPE_BF16;
   {
@@ -471,8 +475,8 @@ hipError_t launch_greedy(const Launch& L, const void* v, int32_t* idx, int32_t* 
     if (nblk_max > 0) {
       const dim3 grid(nblk_max, g.U);
       auto go = [&](auto kern, auto vp) {
-        kern<<<grid, kThreads, 0, L.stream>>>(g, vp, wb, ridge, budget, protect, gc, gst, ent,
-                                              nblk_max);
+        kern<<<grid, kThreads, 0, L.stream>>>(g, vp, wb, ridge, wsc, budget, protect, gc, gst,
+                                              ent, nblk_max);
       };
       if (bf16) {
         if (g.D == 128) go(greedy_init_kernel<128, uint16_t>, (const uint16_t*)v);
@@ -487,7 +491,7 @@ hipError_t launch_greedy(const Launch& L, const void* v, int32_t* idx, int32_t* 
   }
   TimedPhase tp(L.stream, JACAP_PHASE_GREEDY);
   auto go = [&](auto kern, auto vp) {
-    kern<<<g.U, kThreads, 0, L.stream>>>(g, vp, wb, ridge, budget, protect, gc, gst, ent,
+    kern<<<g.U, kThreads, 0, L.stream>>>(g, vp, wb, ridge, wsc, budget, protect, gc, gst, ent,
                                          nblk_max, idx, order, logdet);
   };
   if (bf16) {

@@ -244,10 +244,11 @@ __device__ __forceinline__ F group_sum(F v) {
 
 // Chunk epilogue of the K pass: z and kappa of the chunk (staged in LDS) stored
 // coalesced with one non-finite check, then the chunk's (max z, rest), rest =
-// sum of exp(z - max) over every token but the first one holding the max (whose
-// term is exactly 1). Kept apart from that 1, the rest keeps its own relative
-// precision when one token dominates the softmax, which 1 - alpha of that
-// token needs (it is the rest of Z over Z).
+// sum of exp(z - max + kRestShift) over every token but the first one holding
+// the max (whose term is exactly 1). Kept apart from that 1, the rest keeps its
+// own relative precision when one token dominates the softmax, which
+// 1 - alpha of that token needs (it is the rest of Z over Z); the shift keeps
+// its terms out of fp32's subnormal range.
 __device__ __forceinline__ void kpass_epilogue(const Unit& un, int u, int base, int64_t trow,
                                                const float* zsh, const float* ksq, float* red,
                                                float* __restrict__ zout,
@@ -287,7 +288,8 @@ __device__ __forceinline__ void kpass_epilogue(const Unit& un, int u, int base, 
   float ex = 0.0f;
 #pragma unroll
   for (int q = 0; q < ZPT; ++q)
-    ex += (zv[q] == -INFINITY || q * kThreads + tid == first) ? 0.0f : expf(zv[q] - m);
+    ex += (zv[q] == -INFINITY || q * kThreads + tid == first) ? 0.0f
+                                                               : expf(zv[q] - m + kRestShift);
   const float s = block_combine(wave_sum(ex), red, [](float a, float b) { return a + b; });
   if (tid == 0) cstat[(int64_t)u * kchunks + chunk] = make_float2(m, s);
 }
@@ -758,7 +760,7 @@ hipError_t launch_kpass(const Launch& L, const void* k, const void* q) {
 __global__ __launch_bounds__(kThreads) void softmax_weights_kernel(
     Geo g, const float2* __restrict__ cstat, int kchunks, const float* __restrict__ zbuf,
     const float* __restrict__ kbuf, double inv_d, int wchunks, float* __restrict__ m_out,
-    double* __restrict__ z_out, float* __restrict__ wout) {
+    double* __restrict__ z_out, double* __restrict__ scale_out, float* __restrict__ wout) {
   int u, chunk;
   if (!grid_unit_chunk<false>(g, wchunks, u, chunk)) return;
   const int tid = threadIdx.x;
@@ -767,7 +769,7 @@ __global__ __launch_bounds__(kThreads) void softmax_weights_kernel(
   __shared__ int redi[kThreads / 64];
   __shared__ double redd[kThreads / 64];
   if (un.n == 0) {
-    if (chunk == 0 && tid == 0) { m_out[u] = 0.0f; z_out[u] = 1.0; }
+    if (chunk == 0 && tid == 0) { m_out[u] = 0.0f; z_out[u] = 1.0; scale_out[u] = 1.0; }
     return;
   }
   const int base = chunk * kWChunk;
@@ -784,12 +786,21 @@ __global__ __launch_bounds__(kThreads) void softmax_weights_kernel(
     if (cs[c].x == m) cmax = min(cmax, c);
   cmax = block_combine(wave_min(cmax), redi, [](int a, int b) { return min(a, b); });
   double rest = 0.0;
-  for (int c = tid; c < nch; c += kThreads)
-    rest += c == cmax ? (double)cs[c].y
-                      : (1.0 + (double)cs[c].y) * exp((double)cs[c].x - (double)m);
+  for (int c = tid; c < nch; c += kThreads) {
+    const double dm = (double)cs[c].x - (double)m;
+    rest += (c == cmax ? 0.0 : exp(dm)) + (double)cs[c].y * exp(dm - (double)kRestShift);
+  }
   rest = block_combine(wave_sum(rest), redd, [](double a, double b) { return a + b; });
   const double s = 1.0 + rest;  // Z
-  if (chunk == 0 && tid == 0) { m_out[u] = m; z_out[u] = s; }
+  // Every rho_i = alpha_i (1 - alpha_i) is at most min(1/4, rest / Z). When
+  // that bound is tiny (a saturated softmax) the weights are stored times a
+  // power of two that lifts its square to [1, 4), so that they stay inside
+  // fp32's range; the ridge (or R) is scaled by the same power of two in the
+  // factorisation, which leaves every score w_i v_i^T A^{-1} v_i unchanged.
+  const double rho_max = fmin(0.25, rest / s);
+  const double wscale = rho_max > 0.0 && rho_max < 0x1p-20 ? ldexp(1.0, -2 * ilogb(rho_max)) : 1.0;
+  if (chunk == 0 && tid == 0) { m_out[u] = m; z_out[u] = s; scale_out[u] = wscale; }
+  const double wfac = wscale * inv_d;
   const int64_t trow = token_row(g, un);
   const int end = min(un.n, base + kWChunk);
   // Eq. 8 per token: e = exp(z - m) from the fp32 exponential of the rounded
@@ -800,9 +811,10 @@ __global__ __launch_bounds__(kThreads) void softmax_weights_kernel(
   auto weight = [&](float z, float kap) {
     const double dz = (double)z - (double)m;  // exact
     const float df = (float)dz;
-    const double e = (double)expf(df) * (1.0 + (dz - (double)df));
+    // far below the maximum the fp32 exponential would be subnormal
+    const double e = df > -80.0f ? (double)expf(df) * (1.0 + (dz - (double)df)) : exp(dz);
     const double rho = (e * invZ) * (((1.0 - e) + rest) * invZ);
-    return (float)(rho * rho * (double)kap * inv_d);
+    return (float)(rho * rho * (double)kap * wfac);
   };
   constexpr int U4 = 4;
   static_assert(kWChunk % (U4 * kThreads) == 0, "whole unrolled trips per chunk");
@@ -827,7 +839,8 @@ hipError_t launch_softmax_weights(const Launch& L) {
       L.geo, ws_ptr<float2>(L.wsp, L.ws.cstat), L.ws.kchunks, ws_ptr<float>(L.wsp, L.ws.z),
       ws_ptr<float>(L.wsp, L.ws.kappa), 1.0 / (double)L.geo.D, wchunks,
       ws_ptr<float>(L.wsp, L.ws.smax_m),
-      ws_ptr<double>(L.wsp, L.ws.smax_z), ws_ptr<float>(L.wsp, L.ws.wgt));
+      ws_ptr<double>(L.wsp, L.ws.smax_z), ws_ptr<double>(L.wsp, L.ws.wscale),
+      ws_ptr<float>(L.wsp, L.ws.wgt));
   return hipGetLastError();
 }
 

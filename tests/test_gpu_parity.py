@@ -525,6 +525,19 @@ def test_dominant_token_keeps_its_weight(jacap, gqa):
                gqa=gqa)
 
 
+@pytest.mark.parametrize("dtype,d", [("bf16", 128), ("bf16", 64)])
+def test_saturated_softmax_at_ridge_zero(jacap, dtype, d):
+    """tau = 0.5: the centre softmax is saturated (1 - alpha of the sink and the
+    other tokens' alpha near 1e-35), so the Eq. 8 weights fall far below fp32's
+    range. At ridge 0 the leverage scores do not depend on the weights' common
+    scale and stay O(1); the weight pass stores the weights times a power of
+    two (the factorisation scales the ridge alike), so they must still match."""
+    case = make_case("ragged16", seq_lens=[300, 4097], num_layers=1, num_kv_heads=2,
+                     num_q_heads=4, window=16, head_dim=d, dtype=dtype).to("cuda")
+    check_case(case, 64, 0.0, "diag", tau=0.5, label=f"saturated ridge 0 {dtype}",
+               jacap=jacap)
+
+
 def _sweep_specs(count=16):
     """Seeded random configurations across the supported envelope: head_dim,
     dtype, covariance, GQA group and mode, ridge, temperature, window (one
@@ -572,6 +585,42 @@ def wo_ridge_matrices(case, d_model_factor=4):
         for h in range(w.num_kv_heads):
             R[layer, h] = jo.output_ridge_matrix(jo.group_output_projection(wo[layer], h, G, d))
     return R
+
+
+def _sweep2_specs(count=16):
+    """A second seeded sweep, toward the edges: ridge 0 and the output-projection
+    ridge matrices, temperatures 0.5 to 30, pooled windows up to 512 queries
+    (the FULL MFMA K pass and the VALU one past 256), groups of 8, lengths at
+    the K-pass, Gram and leverage chunk boundaries, budgets at those lengths."""
+    rng = np.random.default_rng(8131)
+    lens_pool = [0, 1, 1023, 1024, 1025, 2047, 4095, 4096, 4097, 6000]
+    specs = []
+    for i in range(count):
+        specs.append(dict(
+            i=i, d=int(rng.choice([64, 128])), dtype=str(rng.choice(["bf16", "fp32"])),
+            mode=str(rng.choice(["diag", "full"])), hkv=int(rng.choice([1, 2])),
+            G=int(rng.choice([1, 2, 4, 8])), gqa=str(rng.choice(["pooled", "per_head"])),
+            ridge=str(rng.choice(["0", "1", "0.25", "wo"])),
+            tau=float(rng.choice([0.5, 3.0, 10.0, 30.0])),
+            window=int(rng.choice([1, 2, 16, 32, 64])),
+            lens=[int(x) for x in rng.choice(lens_pool, int(rng.integers(1, 4)))],
+            budget=int(rng.choice([0, 2, 100, 1023, 1024, 4096, 1 << 20])),
+            protect=int(rng.choice([0, 1, 64]))))
+    return specs
+
+
+@pytest.mark.parametrize("spec", _sweep2_specs(), ids=lambda s: f"edge{s['i']}")
+def test_random_configuration_sweep_edges(jacap, spec):
+    s = spec
+    print(f"\n[sweep edges] {s}", flush=True)
+    case = make_case("ragged16", seq_lens=s["lens"], num_layers=1, num_kv_heads=s["hkv"],
+                     num_q_heads=s["hkv"] * s["G"], window=s["window"], head_dim=s["d"],
+                     dtype=s["dtype"]).to("cuda")
+    R = wo_ridge_matrices(case) if s["ridge"] == "wo" else None
+    ridge = 1.0 if s["ridge"] == "wo" else float(s["ridge"])
+    check_case(case, s["budget"], ridge, s["mode"], tau=s["tau"], label=f"edge{s['i']}",
+               jacap=jacap, gqa=s["gqa"], protect_last=s["protect"], ridge_matrices=R)
+
 
 
 @pytest.mark.parametrize("mode", ["diag", "full"])
