@@ -609,6 +609,38 @@ def _sweep2_specs(count=16):
     return specs
 
 
+def _sweep3_specs(count=8):
+    """A third seeded sweep over long units on the bf16 MFMA path: lengths
+    around 8192, 16384 and 32768 (several K-pass, Gram and leverage chunks,
+    ragged tails), both covariances and GQA modes, ridge 1, 0 and R."""
+    rng = np.random.default_rng(20260908)
+    lens_pool = [8191, 8192, 8193, 16385, 20000, 33000]
+    specs = []
+    for i in range(count):
+        specs.append(dict(
+            i=i, d=int(rng.choice([64, 128, 128])), dtype="bf16",
+            mode=str(rng.choice(["diag", "full"])), hkv=int(rng.choice([1, 2])),
+            G=int(rng.choice([1, 4])), gqa=str(rng.choice(["pooled", "per_head"])),
+            ridge=str(rng.choice(["0", "1", "wo"])), tau=float(rng.choice([1.0, 10.0])),
+            window=int(rng.choice([8, 32])),
+            lens=[int(x) for x in rng.choice(lens_pool, int(rng.integers(1, 3)))],
+            budget=int(rng.choice([256, 4096, 20000])), protect=int(rng.choice([0, 128]))))
+    return specs
+
+
+@pytest.mark.parametrize("spec", _sweep3_specs(), ids=lambda s: f"long{s['i']}")
+def test_random_configuration_sweep_long_units(jacap, spec):
+    s = spec
+    print(f"\n[sweep long] {s}", flush=True)
+    case = make_case("ragged16", seq_lens=s["lens"], num_layers=1, num_kv_heads=s["hkv"],
+                     num_q_heads=s["hkv"] * s["G"], window=s["window"], head_dim=s["d"],
+                     dtype=s["dtype"]).to("cuda")
+    R = wo_ridge_matrices(case) if s["ridge"] == "wo" else None
+    ridge = 1.0 if s["ridge"] == "wo" else float(s["ridge"])
+    check_case(case, s["budget"], ridge, s["mode"], tau=s["tau"], label=f"long{s['i']}",
+               jacap=jacap, gqa=s["gqa"], protect_last=s["protect"], ridge_matrices=R)
+
+
 @pytest.mark.parametrize("spec", _sweep2_specs(), ids=lambda s: f"edge{s['i']}")
 def test_random_configuration_sweep_edges(jacap, spec):
     s = spec
