@@ -47,9 +47,9 @@ def run_greedy(jacap, case, budget, ridge=1.0, tau=10.0, protect_last=0, cov_mod
 
 
 def check_greedy(jacap, case, budget, ridge=1.0, units=None, protect_last=0, label="",
-                 cov_mode="diag"):
+                 cov_mode="diag", tau=10.0):
     units = unit_list(case) if units is None else units
-    prob, flags = run_greedy(jacap, case, budget, ridge=ridge, protect_last=protect_last,
+    prob, flags = run_greedy(jacap, case, budget, ridge=ridge, tau=tau, protect_last=protect_last,
                              cov_mode={"diag": 0, "full": 1}[cov_mode])
     assert flags == 0, flags
     tol = GAIN_TOL[case.workload.dtype]
@@ -60,7 +60,7 @@ def check_greedy(jacap, case, budget, ridge=1.0, units=None, protect_last=0, lab
         kk = min(budget, n)
         pp = min(protect_last, kk)
         q, k, v = case.unit_arrays(b, l, h)
-        o = jo.score_unit(q, k, v, ridge=ridge32, cov_mode=cov_mode)
+        o = jo.score_unit(q, k, v, tau=tau, ridge=ridge32, cov_mode=cov_mode)
         w = o["w"] if n else np.zeros(0)
         order = prob.order[b, l, h].cpu().numpy()
         idx = prob.idx[b, l, h].cpu().numpy()
@@ -114,6 +114,16 @@ def test_greedy_ragged_protected(jacap, protect):
     case = make_case("ragged16", device="cuda", seq_lens=(700, 1, 1300),
                      num_layers=1, num_kv_heads=2, head_dim=64, dtype="fp32")
     check_greedy(jacap, case, 96, ridge=0.5, protect_last=protect, label=f"ragged protect {protect}")
+
+
+@pytest.mark.parametrize("dtype,d", [("bf16", 128), ("fp32", 64)])
+def test_greedy_saturated_softmax(jacap, dtype, d):
+    """tau = 0.5: the Eq. 8 weights (~1e-70) lie far outside fp32; they are
+    stored times a per-unit power of two and A_0 = ridge I takes the same
+    factor, so the gains w_i c_i, the picks and the log det are unchanged."""
+    case = make_case("ragged16", device="cuda", seq_lens=(300, 2100), num_layers=1,
+                     num_kv_heads=2, num_q_heads=4, window=16, head_dim=d, dtype=dtype)
+    check_greedy(jacap, case, 64, ridge=1.0, tau=0.5, label=f"saturated {dtype}")
 
 
 def test_greedy_budget_edges(jacap):
