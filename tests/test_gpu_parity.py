@@ -538,6 +538,54 @@ def test_saturated_softmax_at_ridge_zero(jacap, dtype, d):
                jacap=jacap)
 
 
+@pytest.mark.parametrize("dtype,d,mode,gqa", [("bf16", 128, "diag", "pooled"),
+                                              ("bf16", 128, "full", "per_head"),
+                                              ("fp32", 64, "full", "pooled")])
+def test_token_major_and_padded_layouts(jacap, dtype, d, mode, gqa):
+    """The batch strides take other layouts than the default: K and V stored
+    token-major ([L][T][H][d], viewed as [L][H][T][d]) and window queries with a
+    padded row pitch (d + 8). Addressing only changes, so scores, selection and
+    compaction must be bit-identical to the contiguous layout's."""
+    case = make_case("ragged16", seq_lens=[0, 17, 300, 4100], num_layers=2, num_kv_heads=2,
+                     num_q_heads=4, window=8, head_dim=d, dtype=dtype).to("cuda")
+    p = jacap.Params(budget_k=64, cov_mode=COV[mode], protect_last=3,
+                     gqa_mode=jacap.GQA_PER_HEAD if gqa == "per_head" else jacap.GQA_POOLED)
+    ref = jacap.prepare(case.q_win, case.k, case.v, case.seq_offsets, case.seq_lens, p)
+    jacap.run_evict(ref, case.q_win, case.k, case.v)
+    k_tm = case.k.permute(0, 2, 1, 3).contiguous().permute(0, 2, 1, 3)
+    v_tm = case.v.permute(0, 2, 1, 3).contiguous().permute(0, 2, 1, 3)
+    qpad = torch.zeros(case.q_win.shape[:-1] + (d + 8,), dtype=case.q_win.dtype, device="cuda")
+    qpad[..., :d] = case.q_win
+    q_p = qpad[..., :d]
+    assert k_tm.stride(2) == 2 * d and q_p.stride(3) == d + 8
+    alt = jacap.prepare(q_p, k_tm, v_tm, case.seq_offsets, case.seq_lens, p)
+    print(f"\n[layout] {dtype} d{d} {mode} {gqa}: token-major K/V, query pitch {d + 8}",
+          flush=True)
+    jacap.run_evict(alt, q_p, k_tm, v_tm)
+    assert jacap.read_status(ref.ws) == 0 and jacap.read_status(alt.ws) == 0
+    torch.cuda.synchronize()
+    for b in range(len(case.seq_lens)):
+        lo, hi = token_slice(case, b)
+        assert torch.equal(alt.scores[:, :, lo:hi], ref.scores[:, :, lo:hi]), b
+        kk = min(64, case.seq_lens[b])
+        assert torch.equal(alt.k_out[b, :, :, :kk], ref.k_out[b, :, :, :kk]), b
+        assert torch.equal(alt.v_out[b, :, :, :kk], ref.v_out[b, :, :, :kk]), b
+    assert torch.equal(alt.idx, ref.idx)
+    # retained rows written with a padded row pitch as well
+    B, L, H = alt.idx.shape[:3]
+    pad_k = torch.full((B, L, H, 64, d + 8), -3.0, dtype=case.k.dtype, device="cuda")
+    pad_v = torch.full_like(pad_k, -3.0)
+    k_o, v_o = pad_k[..., :d], pad_v[..., :d]
+    jacap.set_out_strides(alt.batch, k_o)
+    jacap.evict(alt.cfg, alt.batch, q_p, k_tm, v_tm, alt.scores, alt.idx, k_o, v_o, alt.ws)
+    torch.cuda.synchronize()
+    for b in range(len(case.seq_lens)):
+        kk = min(64, case.seq_lens[b])
+        assert torch.equal(k_o[b, :, :, :kk], ref.k_out[b, :, :, :kk]), b
+        assert torch.equal(v_o[b, :, :, :kk], ref.v_out[b, :, :, :kk]), b
+    assert torch.all(pad_k[..., d:] == -3.0) and torch.all(pad_v[..., d:] == -3.0)
+
+
 def _sweep_specs(count=16):
     """Seeded random configurations across the supported envelope: head_dim,
     dtype, covariance, GQA group and mode, ridge, temperature, window (one
