@@ -105,3 +105,43 @@ def test_greedy_replays_from_a_graph(jacap):
         for t, r in zip((prob.idx, prob.order, prob.logdet), ref):
             torch.testing.assert_close(t, r, rtol=0, atol=0, equal_nan=True)
     del g
+
+
+def test_concurrent_streams_with_distinct_workspaces(jacap):
+    """Calls on different streams are independent when their workspaces are
+    distinct: two eviction problems (different budgets, GQA modes and
+    protected tails) launched back to back on two streams give the results of
+    running them one after the other."""
+    case = make_case("ragged16", seq_lens=[17, 300, 4100], num_layers=2, num_kv_heads=2,
+                     num_q_heads=4, window=8, head_dim=128, dtype="bf16").to("cuda")
+    params = [jacap.Params(budget_k=64), jacap.Params(budget_k=200, protect_last=7,
+                                                       gqa_mode=jacap.GQA_PER_HEAD)]
+    probs = [jacap.prepare(case.q_win, case.k, case.v, case.seq_offsets, case.seq_lens, p)
+             for p in params]
+    for prob in probs:                       # one after the other, default stream
+        jacap.run_evict(prob, case.q_win, case.k, case.v)
+    torch.cuda.synchronize()
+    ref = [(pr.scores.clone(), pr.idx.clone(), pr.k_out.clone()) for pr in probs]
+    for pr in probs:
+        pr.scores.fill_(-7.0)
+        pr.idx.fill_(-7)
+        pr.k_out.fill_(-7.0)
+    torch.cuda.synchronize()
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    for rep in range(3):
+        print(f"\n[streams] concurrent run {rep}", flush=True)
+        for st in streams:
+            st.wait_stream(torch.cuda.current_stream())
+        for pr, st in zip(probs, streams):
+            jacap.run_evict(pr, case.q_win, case.k, case.v, st)
+        for st in streams:
+            torch.cuda.current_stream().wait_stream(st)
+        torch.cuda.synchronize()
+        for pr, st, (s_ref, i_ref, k_ref) in zip(probs, streams, ref):
+            assert jacap.read_status(pr.ws, st) == 0
+            for b in range(len(case.seq_lens)):
+                lo, hi = token_slice(case, b)
+                assert torch.equal(pr.scores[:, :, lo:hi], s_ref[:, :, lo:hi])
+                kk = min(pr.cfg.budget_k, case.seq_lens[b])
+                assert torch.equal(pr.k_out[b, :, :, :kk], k_ref[b, :, :, :kk])
+            assert torch.equal(pr.idx, i_ref)
