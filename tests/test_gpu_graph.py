@@ -1,4 +1,4 @@
-"""HIP graph capture of the eviction path.
+"""HIP graph capture of the eviction path, and concurrent calls on two streams.
 
 jacap_evict only enqueues kernels on the caller's stream (no allocation, no
 memset node, no host synchronisation; the per-unit flags are cleared by a
