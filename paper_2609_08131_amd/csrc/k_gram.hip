@@ -66,7 +66,8 @@ __device__ __forceinline__ s16x4 lds_read_tr16(const uint16_t* p) {
 }
 
 // The workgroup walks its chunk in steps of 32 tokens. Each step is read with
-// 16-byte buffer loads (non-temporal; each wave load covers whole 128-byte
+// 16-byte buffer loads (non-temporal, or cached when the query-head units of
+// a KV head share them; each wave load covers whole 128-byte
 // lines), prefetched two steps ahead, and staged in LDS token-major
 // (double-buffered, one barrier per step); the four waves share it. The upper 16x16 block pairs (i <= j) are split between the waves by
 // column pairs {w, NB-1-w}, which gives every wave the same number of pairs

@@ -2,7 +2,7 @@
 //
 // bf16 inputs: Y = V L^{-T} on MFMA 16x16x32 bf16. The token dimension is the
 // MFMA row dimension. V rows are read whole (each wave load covers complete
-// 128-byte lines, streamed non-temporally) and pass through a small
+// 128-byte lines, streamed non-temporally, or cached for per-head GQA) and pass through a small
 // wave-private LDS tile into the operand layout. L^{-1} is split into bf16
 // hi + lo and kept in registers; only the K-blocks with b <= a of the lower
 // triangle are multiplied. The squared row norm is reduced across the 16
@@ -58,7 +58,7 @@ __global__ __launch_bounds__(kThreads, 2) void leverage_mfma_kernel(
   // steps ahead into three rotating register buffers (the loop is unrolled
   // by three so the buffers stay in fixed registers). A step's 16 rows are
   // read whole: each wave load brings RPL consecutive rows (d / 8 lanes per
-  // row, 1 KB of contiguous lines, non-temporal), through a buffer range
+  // row, 1 KB of contiguous lines, cache policy), through a buffer range
   // that ends at the chunk's last row (rows past it load as zeros and are not
   // stored), so every load is unconditional with a fixed per-lane offset and
   // the compiler's wait counts stay static. The rows then pass through a
