@@ -145,3 +145,37 @@ def test_concurrent_streams_with_distinct_workspaces(jacap):
                 kk = min(pr.cfg.budget_k, case.seq_lens[b])
                 assert torch.equal(pr.k_out[b, :, :, :kk], k_ref[b, :, :, :kk])
             assert torch.equal(pr.idx, i_ref)
+
+
+def test_evict_slots_replays_from_a_graph(jacap):
+    """The in-place decoding round (jacap_evict_slots) captured in a graph
+    replays the eager evicted-slot lists and scores bit for bit."""
+    case = make_case("ragged16", seq_lens=[288, 288, 100], num_layers=2, num_kv_heads=2,
+                     num_q_heads=4, window=8, head_dim=64, dtype="bf16").to("cuda")
+    p = jacap.Params(budget_k=256, gqa_mode=jacap.GQA_PER_HEAD)
+    prob = jacap.prepare(case.q_win, case.k, case.v, case.seq_offsets, case.seq_lens, p)
+    slots = jacap.alloc_slots(prob, case.seq_lens)
+    jacap.run_evict_slots(prob, slots, case.q_win, case.k, case.v)
+    assert jacap.read_status(prob.ws) == 0
+    torch.cuda.synchronize()
+    ref_s, ref_sl = prob.scores.clone(), slots.clone()
+    g = torch.cuda.CUDAGraph()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        with torch.cuda.graph(g, stream=side):
+            jacap.run_evict_slots(prob, slots, case.q_win, case.k, case.v)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    for rep in range(3):
+        prob.scores.fill_(-7.0)
+        slots.fill_(-7)
+        torch.cuda.synchronize()
+        print(f"\n[graph] evict_slots: replay {rep}", flush=True)
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(slots, ref_sl)
+        for b in range(len(case.seq_lens)):
+            lo, hi = token_slice(case, b)
+            assert torch.equal(prob.scores[:, :, lo:hi], ref_s[:, :, lo:hi])
+    del g
