@@ -54,6 +54,9 @@
  *   asynchronously on `stream` (a hipStream_t; NULL = the null stream).
  *   Calls on different streams are independent if they use distinct
  *   workspaces.
+ * - A batch without tokens (total_tokens = 0) is a no-op that still writes
+ *   the padding of the outputs (idx, slots: -1); its K, V, query and score
+ *   pointers may then be null (empty arrays), as may k_out / v_out.
  * - Host-detectable errors (null or misaligned pointers, bad shapes or
  *   strides, unsupported head_dim or dtype, too small a workspace) return an
  *   error code and enqueue nothing. K and V token strides above 2^24

@@ -247,8 +247,15 @@ bool slots_ok(const jacap_config* c, const jacap_batch* b, const float* scores,
   return slot_cap >= 0 && slot_cap >= b->max_seq_len - c->budget_k;
 }
 
-bool score_ptrs_ok(const void* q, const void* k, const void* v, const float* scores) {
-  return q && k && v && scores && aligned16(q) && aligned16(k) && aligned16(v) && aligned16(scores);
+// A data pointer: 16-byte aligned, and non-null unless the batch holds no
+// tokens (the arrays are then empty and nothing reads them).
+bool data_ptr_ok(const void* p, const jacap_batch* b) {
+  return p ? aligned16(p) : b->total_tokens == 0;
+}
+
+bool score_ptrs_ok(const jacap_batch* b, const void* q, const void* k, const void* v,
+                   const float* scores) {
+  return data_ptr_ok(q, b) && data_ptr_ok(k, b) && data_ptr_ok(v, b) && data_ptr_ok(scores, b);
 }
 
 }  // namespace
@@ -272,7 +279,7 @@ jacap_status jacap_score(const jacap_config* cfg, const jacap_batch* batch, cons
   if (!ws) return JACAP_ERR_INVALID_ARG;
   jacap_status s = prepare(cfg, batch, ws, ws_bytes, stream, &L);
   if (s != JACAP_OK) return s;
-  if (!score_ptrs_ok(q_win, k, v, scores)) return JACAP_ERR_INVALID_ARG;
+  if (!score_ptrs_ok(batch, q_win, k, v, scores)) return JACAP_ERR_INVALID_ARG;
   if (batch->total_tokens == 0) {
     TimedPhase tp(L.stream, JACAP_PHASE_INIT);
     return launch_init(L) == hipSuccess ? JACAP_OK : JACAP_ERR_HIP;
@@ -293,7 +300,7 @@ jacap_status jacap_score_from_stats(const jacap_config* cfg, const jacap_batch* 
   if (!mu || !lambda || (reinterpret_cast<uintptr_t>(mu) & 7u) ||
       (reinterpret_cast<uintptr_t>(lambda) & 7u))
     return JACAP_ERR_INVALID_ARG;
-  if (!k || !v || !scores || !aligned16(k) || !aligned16(v) || !aligned16(scores))
+  if (!data_ptr_ok(k, batch) || !data_ptr_ok(v, batch) || !data_ptr_ok(scores, batch))
     return JACAP_ERR_INVALID_ARG;
   if (batch->total_tokens == 0) {
     TimedPhase tp(L.stream, JACAP_PHASE_INIT);
@@ -345,10 +352,10 @@ jacap_status jacap_evict(const jacap_config* cfg, const jacap_batch* batch, cons
   if (!ws) return JACAP_ERR_INVALID_ARG;
   jacap_status s = prepare(cfg, batch, ws, ws_bytes, stream, &L);
   if (s != JACAP_OK) return s;
-  if (!score_ptrs_ok(q_win, k, v, scores)) return JACAP_ERR_INVALID_ARG;
+  if (!score_ptrs_ok(batch, q_win, k, v, scores)) return JACAP_ERR_INVALID_ARG;
   if (cfg->budget_k > 0) {
-    if (!idx || !k_out || !v_out) return JACAP_ERR_INVALID_ARG;
-    if (!aligned16(idx) || !aligned16(k_out) || !aligned16(v_out)) return JACAP_ERR_INVALID_ARG;
+    if (!idx || !aligned16(idx)) return JACAP_ERR_INVALID_ARG;
+    if (!data_ptr_ok(k_out, batch) || !data_ptr_ok(v_out, batch)) return JACAP_ERR_INVALID_ARG;
   }
   if (batch->total_tokens > 0) {
     s = run_score(L, q_win, k, v, scores);
@@ -369,7 +376,7 @@ jacap_status jacap_evict_slots(const jacap_config* cfg, const jacap_batch* batch
   if (!ws) return JACAP_ERR_INVALID_ARG;
   jacap_status s = prepare(cfg, batch, ws, ws_bytes, stream, &L);
   if (s != JACAP_OK) return s;
-  if (!score_ptrs_ok(q_win, k, v, scores)) return JACAP_ERR_INVALID_ARG;
+  if (!score_ptrs_ok(batch, q_win, k, v, scores)) return JACAP_ERR_INVALID_ARG;
   if (!slots_ok(cfg, batch, scores, slots, slot_cap)) return JACAP_ERR_INVALID_ARG;
   if (batch->total_tokens > 0) {
     s = run_score(L, q_win, k, v, scores);
@@ -401,7 +408,7 @@ jacap_status jacap_greedy(const jacap_config* cfg, const jacap_batch* batch, con
   if (!ws) return JACAP_ERR_INVALID_ARG;
   jacap_status s = prepare(cfg, batch, ws, ws_bytes, stream, &L, true);
   if (s != JACAP_OK) return s;
-  if (!q_win || !k || !v || !aligned16(q_win) || !aligned16(k) || !aligned16(v))
+  if (!data_ptr_ok(q_win, batch) || !data_ptr_ok(k, batch) || !data_ptr_ok(v, batch))
     return JACAP_ERR_INVALID_ARG;
   if (cfg->budget_k > 0 && (!idx || !aligned16(idx))) return JACAP_ERR_INVALID_ARG;
   if (order && !aligned16(order)) return JACAP_ERR_INVALID_ARG;

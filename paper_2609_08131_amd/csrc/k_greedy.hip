@@ -238,7 +238,7 @@ __global__ __launch_bounds__(kThreads) void greedy_kernel(
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int r = tid / TPR, q = tid % TPR;
   // A_0 = ridge I times the stored weights' scale (gains are unchanged by it)
-  const double ridge = (double)ridge_f * wscale[u];
+  const double ridge = (double)ridge_f * (n > 0 ? wscale[u] : 1.0);
   const T* vb = v + (int64_t)un.l * g.vsl + (int64_t)un.h * g.vsh + un.t0 * g.vst;
   const int64_t trow = token_row(g, un);
 

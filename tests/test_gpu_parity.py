@@ -586,12 +586,43 @@ def test_token_major_and_padded_layouts(jacap, dtype, d, mode, gqa):
     assert torch.all(pad_k[..., d:] == -3.0) and torch.all(pad_v[..., d:] == -3.0)
 
 
-def _sweep_specs(count=16):
+@pytest.mark.parametrize("gqa", ["pooled", "per_head"])
+def test_batch_without_tokens_is_a_no_op(jacap, gqa):
+    """Every sequence empty: the K, V and score arrays have no elements (their
+    tensors hold null data pointers), which the entry points accept; the
+    selections are all padding and the greedy log det is d log(ridge)."""
+    case = make_case("ragged16", seq_lens=[0, 0], num_layers=2, num_kv_heads=2, num_q_heads=4,
+                     window=8, head_dim=64, dtype="bf16").to("cuda")
+    assert case.k.numel() == 0
+    p = jacap.Params(budget_k=16, ridge=0.5,
+                     gqa_mode=jacap.GQA_PER_HEAD if gqa == "per_head" else jacap.GQA_POOLED)
+    prob = jacap.prepare(case.q_win, case.k, case.v, case.seq_offsets, case.seq_lens, p)
+    prob.idx.fill_(7)
+    jacap.run_evict(prob, case.q_win, case.k, case.v)
+    jacap.score(prob.cfg, prob.batch, case.q_win, case.k, case.v, prob.scores, prob.ws)
+    slots = jacap.alloc_slots(prob, case.seq_lens)
+    slots.fill_(7)
+    jacap.run_evict_slots(prob, slots, case.q_win, case.k, case.v)
+    assert jacap.read_status(prob.ws) == 0
+    torch.cuda.synchronize()
+    assert torch.all(prob.idx == -1) and torch.all(slots == -1)
+    if gqa == "pooled":
+        g = jacap.prepare_greedy(case.q_win, case.k, case.v, case.seq_offsets, case.seq_lens, p)
+        jacap.run_greedy(g, case.q_win, case.k, case.v)
+        assert jacap.read_status(g.ws) == 0
+        torch.cuda.synchronize()
+        assert torch.all(g.idx == -1) and torch.all(g.order == -1)
+        want = 64 * np.log(float(np.float32(0.5)))   # fp64 log of the fp32 ridge
+        assert torch.allclose(g.logdet.cpu(), torch.full_like(g.logdet.cpu(), float(want)),
+                              rtol=1e-12, atol=0)
+
+
+def _sweep_specs(count=16, seed=2609):
     """Seeded random configurations across the supported envelope: head_dim,
     dtype, covariance, GQA group and mode, ridge, temperature, window (one
     query included), ragged lengths around the tile sizes (empty and one-token
     sequences included), budgets from 0 past every length, protected tails."""
-    rng = np.random.default_rng(2609)
+    rng = np.random.default_rng(seed)
     lens_pool = [0, 1, 2, 15, 16, 17, 63, 255, 256, 257, 1000, 1025, 3000]
     specs = []
     for i in range(count):
@@ -607,7 +638,9 @@ def _sweep_specs(count=16):
     return specs
 
 
-@pytest.mark.parametrize("spec", _sweep_specs(), ids=lambda s: f"sweep{s['i']}")
+@pytest.mark.parametrize("spec", _sweep_specs() + [dict(sp, i=100 + sp["i"]) for sp in
+                                                    _sweep_specs(seed=131)],
+                         ids=lambda s: f"sweep{s['i']}")
 def test_random_configuration_sweep(jacap, spec):
     s = spec
     print(f"\n[sweep] {s}", flush=True)
