@@ -638,8 +638,9 @@ def _sweep_specs(count=16, seed=2609):
     return specs
 
 
-@pytest.mark.parametrize("spec", _sweep_specs() + [dict(sp, i=100 + sp["i"]) for sp in
-                                                    _sweep_specs(seed=131)],
+@pytest.mark.parametrize("spec", _sweep_specs() + [dict(sp, i=100 * (r + 1) + sp["i"])
+                                                   for r, sd in enumerate((131, 977))
+                                                   for sp in _sweep_specs(seed=sd)],
                          ids=lambda s: f"sweep{s['i']}")
 def test_random_configuration_sweep(jacap, spec):
     s = spec
