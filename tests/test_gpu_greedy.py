@@ -212,3 +212,27 @@ def test_greedy_long128k_full_batch(jacap):
           f"identical prefix {(diff[0] if len(diff) else budget)} of {budget}", flush=True)
     del prob, case
     torch.cuda.empty_cache()
+
+
+def _greedy_sweep_specs(count=8):
+    """Seeded random configurations of the greedy comparator: head_dim, dtype,
+    covariance, ridge > 0, temperature, ragged lengths around its 256-position
+    blocks, budgets from 0 past every length, protected tails."""
+    rng = np.random.default_rng(41)
+    pool = [0, 1, 255, 256, 257, 700, 1500]
+    return [dict(i=i, d=int(rng.choice([64, 128])), dtype=str(rng.choice(["bf16", "fp32"])),
+                 mode=str(rng.choice(["diag", "full"])), ridge=float(rng.choice([1.0, 0.05, 2.0 ** -10])),
+                 tau=float(rng.choice([1.0, 10.0])),
+                 lens=[int(x) for x in rng.choice(pool, int(rng.integers(1, 4)))],
+                 budget=int(rng.choice([0, 1, 40, 300, 2000])), protect=int(rng.choice([0, 0, 9])))
+            for i in range(count)]
+
+
+@pytest.mark.parametrize("spec", _greedy_sweep_specs(), ids=lambda s: f"gsweep{s['i']}")
+def test_greedy_configuration_sweep(jacap, spec):
+    s = spec
+    print(f"\n[greedy sweep] {s}", flush=True)
+    case = make_case("ragged16", device="cuda", seq_lens=s["lens"], num_layers=1,
+                     num_kv_heads=2, num_q_heads=4, window=8, head_dim=s["d"], dtype=s["dtype"])
+    check_greedy(jacap, case, s["budget"], ridge=s["ridge"], protect_last=s["protect"],
+                 cov_mode=s["mode"], tau=s["tau"], label=f"gsweep{s['i']}")
