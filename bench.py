@@ -14,7 +14,9 @@ Prints one JSON line:
                timed region; "traffic" is its measured HBM bytes per launch
                (rocprofv3 FETCH_SIZE + WRITE_SIZE, scaled by a plain copy of
                known size) when the recorded counters match the current
-               kernel source, else null
+               kernel source, else null. roofline.pass is the whole pass:
+               K and V bytes read once per step / ms_per_step against the
+               same peak (also the top-level step_frac)
   cpu_baseline the fp64 oracle timed on this host on a bounded sample
 """
 
@@ -427,12 +429,17 @@ def main():
             "alg_bytes_per_launch": dom_bytes,
             "traffic_over_alg": traffic / dom_bytes if traffic and dom_bytes else None,
             "frac_of_probe": achieved / probe_gbs if achieved else None,
+            "pass": {"achieved": step_bytes / (ms * 1e-3) / 1e9, "peak": PEAK_HBM_GBS,
+                     "frac": step_bytes / (ms * 1e-3) / 1e9 / PEAK_HBM_GBS,
+                     "bytes_per_step": step_bytes,
+                     "note": "score+select+compact pass: K and V bytes read once / step time"},
         },
         "read_probe": {"gbs": probe_gbs, "bytes": probe_bytes,
                        "kind": "jacap_stream_read over the K cache: non-temporal 16-byte "
                                "loads, whole lines per wave instruction, 1 MiB per workgroup"},
         "phases_ms": {k: round(v, 4) for k, v in per_phase.items()},
         "step_hbm_gbs": step_bytes / (ms * 1e-3) / 1e9,
+        "step_frac": step_bytes / (ms * 1e-3) / 1e9 / PEAK_HBM_GBS,
     }
     if not args.no_cpu_baseline:
         cb = cpu_baseline(case, budget, args.tau, args.ridge, args.cpu_seconds, args.cov, args.gqa)

@@ -24,7 +24,7 @@
  * is the plain statistical leverage score of App. B.1/B.2.
  *
  * Output-projection variant (cfg->ridge_mode = JACAP_RIDGE_MATRIX): with
- * u_i = W~ v_i in place of the proxy v_i (Sec. 2.1 defines u_i = W_O v_i;
+ * u_i = W~ v_i in place of the proxy v_i (Sec. 3.1, Preliminary, defines u_i = W_O v_i;
  * W~ is the sum of the output-projection column slices of the G query heads
  * of the KV head, whose outputs the layer adds), Eq. 9 / Eq. 10 in output
  * space equal, by the push-through identity,
@@ -128,11 +128,15 @@ enum jacap_dtype {
 
 enum jacap_flags {
   JACAP_FLAG_NONFINITE = 1u << 0, /* a NaN/Inf input reached a unit's statistics */
-  JACAP_FLAG_SINGULAR = 1u << 1,  /* A = ridge I + M numerically singular: a Cholesky
-                                     pivot fell below 1e-4 (bf16 inputs, fp32-accumulated
-                                     Gram) or 1e-12 (fp32 inputs, fp64 Gram) of its
-                                     diagonal entry; in practice ridge 0 with a
-                                     rank-deficient weighted Gram */
+  JACAP_FLAG_SINGULAR = 1u << 1,  /* A = ridge I + M numerically singular at the score
+                                     tolerance: the fp64 Cholesky factorisation of the
+                                     fp64-accumulated A met a pivot at or below 1e-10
+                                     (bf16 inputs) / 1e-8 (fp32 inputs) of its diagonal
+                                     entry, so cond(A) > 1e10 / 1e8 and fp64 rounding
+                                     alone moves the scores by more than the 1e-3 / 1e-5
+                                     tolerance; in practice ridge 0 with a rank-deficient
+                                     weighted Gram (fewer tokens than d) or weights of a
+                                     saturated softmax spanning tens of decades */
   JACAP_FLAG_BAD_OFFSETS = 1u << 2 /* a sequence's offsets contradict max_seq_len /
                                       total_tokens; it was treated as empty */
 };
@@ -183,7 +187,12 @@ jacap_status jacap_workspace_size(const jacap_config* cfg, const jacap_batch* ba
 /* Algorithm 1 steps 1-4 (centre attention, Eq. 8 weights, Eq. 9 capacity
  * matrix, Eq. 10 leverage scores) for every unit: writes scores[L][H_kv][T]
  * (float32). q_win, k, v are in cfg->dtype. Resets the workspace status
- * flags first. */
+ * flags first. Precision: with bf16 inputs A is accumulated in fp32 from
+ * exact bf16 products of a two-term split of w_i v_i, and the leverage
+ * products use a two-term bf16 L^{-1}; a unit whose capacity matrix the fp64
+ * factorisation finds ill-conditioned (a bound on cond(A) above 2e3, or a
+ * pivot below 1e-4 of its diagonal entry) is recomputed in fp64 throughout
+ * (Gram, Cholesky, L^{-1} v). fp32 inputs take the fp64 path for every unit. */
 jacap_status jacap_score(const jacap_config* cfg, const jacap_batch* batch,
                          const void* q_win, const void* k, const void* v, float* scores,
                          void* ws, size_t ws_bytes, void* stream);
@@ -310,7 +319,7 @@ const char* jacap_status_string(jacap_status s);
  * ------------------------------------------------------------------------ */
 enum jacap_phase {
   JACAP_PHASE_INIT = 0,        /* status/flag reset */
-  JACAP_PHASE_QSTATS = 1,      /* window statistics mu, Lambda (Eq. 6-7) */
+  JACAP_PHASE_QSTATS = 1,      /* window statistics mu, Lambda (Sec. 3.3, local query model) */
   JACAP_PHASE_KPASS = 2,       /* centre logits and query response per token */
   JACAP_PHASE_WEIGHTS = 3,     /* softmax normaliser and Eq. 8 weights */
   JACAP_PHASE_GRAM = 4,        /* weighted Gram partials (Eq. 9) */

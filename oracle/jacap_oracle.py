@@ -19,7 +19,7 @@ open:
 * GQA: the G query heads sharing a KV head are pooled into one sample of
   G*w queries; the per-head alternative scores each head alone and averages.
 * u_i = v_i (Sec. 3.4 end: the proxy used when W_O is not applied). The
-  output-projection variant u_i = W_O v_i (Sec. 2.1, Sec. 3.4 end) is taken
+  output-projection variant u_i = W_O v_i (Sec. 3.1, Preliminary; Sec. 3.4 end) is taken
   for the G query heads of a KV head together: their outputs are summed by
   the layer, so u_i = W~ v_i with W~ = sum_g W_O^g (the heads' column slices
   of the projection). By the push-through identity its Eq. 10 score equals
@@ -134,7 +134,7 @@ def capacity_matrix(U: np.ndarray, w: np.ndarray, ridge) -> np.ndarray:
 def group_output_projection(w_o: np.ndarray, head: int, group: int, d: int) -> np.ndarray:
     """W~ = sum_g W_O^g over the G query heads g of KV head `head`: W_O^g is the
     (d_model x d) column slice of the layer's output projection that maps
-    query head g's attention output into the residual stream (Sec. 2.1, o =
+    query head g's attention output into the residual stream (Sec. 3.1, Preliminary: o =
     W_O sum_i alpha_i v_i, per head). w_o is (d_model, H_q * d)."""
     w_o = np.asarray(w_o, dtype=np.float64)
     cols = [w_o[:, (head * group + g) * d:(head * group + g + 1) * d] for g in range(group)]

@@ -98,10 +98,25 @@ Workspace layout(const jacap_config* c, const jacap_batch* b, bool greedy = fals
   w.gparts = 1;
   const int lchunk = w.mfma ? kLChunkMfma : kLChunkPrecise;
   w.lchunks = (maxn + lchunk - 1) / lchunk;
+  // The fp64 Gram pass (every unit of fp32 keys; the units of bf16 keys that
+  // need it): about kPrecisePartials partials per batch, so that its buffer
+  // stays bounded at any unit count, and no chunk below kGChunkPrecise tokens
+  // (whole 32-token steps).
+  {
+    const int64_t want = std::max<int64_t>(1, kPrecisePartials / std::max<int64_t>(U, 1));
+    const int64_t most = std::max<int64_t>(1, (maxn + kGChunkPrecise - 1) / kGChunkPrecise);
+    const int64_t np = std::min(want, most);
+    const int64_t per = std::max<int64_t>(kGChunkPrecise, ((maxn + np - 1) / np + 31) / 32 * 32);
+    w.pchunk = (int)per;
+    w.pchunks = maxn > 0 ? (int)((maxn + per - 1) / per) : 0;
+  }
+  const int plchunk = w.mfma ? kLChunkRefine : kLChunkPrecise;
+  w.plchunks = (maxn + plchunk - 1) / plchunk;
   const int64_t NB = D / 16;
   const int64_t npair = NB * (NB + 1) / 2;
   const int64_t nlp = (NB / 2) * (NB / 2 + 1);
-  const int64_t part_bytes = npair * 256 * (w.mfma ? 4 : 8);
+  const int64_t mfma_part_bytes = w.mfma ? U * (int64_t)w.gchunks * npair * 256 * 4 : 0;
+  const int64_t fp64_part_bytes = U * (int64_t)w.pchunks * npair * 256 * 8;
   size_t o = 0;
   auto take = [&](size_t bytes) { size_t r = o; o = align256(o + bytes); return r; };
   w.status = take(4);
@@ -126,9 +141,8 @@ Workspace layout(const jacap_config* c, const jacap_batch* b, bool greedy = fals
   }
   w.hscore = take(V > 1 ? 4 * LHT : 4);
   w.kept = take(4 * (int64_t)b->num_seqs * c->num_layers * c->num_kv_heads * std::max(c->budget_k, 1));
-  w.gram = take((size_t)(U * (int64_t)w.gchunks * part_bytes));
+  w.gram = take((size_t)std::max(mfma_part_bytes, fp64_part_bytes));
   w.gram_red = take(8 * U * npair * 256);
-  w.linv64 = take(w.mfma ? 8 : 8 * U * D * D);
   w.lfrag = take(w.mfma ? 2 * U * nlp * 2 * 64 * 8 : 8);
   w.total = o;
   return w;
@@ -195,7 +209,7 @@ jacap_status prepare(const jacap_config* c, const jacap_batch* b, void* ws, size
 // Runs `expr` inside a timed scope of phase `ph`.
 #define JACAP_PHASE(ph, expr)               \
   do {                                      \
-    TimedPhase tp_(L.stream, (ph));         \
+    TimedPhase tp_(L.stream, (ph), L.timed); \
     JACAP_TRY(expr);                        \
   } while (0)
 
@@ -212,11 +226,12 @@ jacap_status score_pass(const Launch& L, const void* q, const void* k, const voi
   JACAP_PHASE(JACAP_PHASE_GRAM, launch_gram(L, v, false));
   JACAP_PHASE(JACAP_PHASE_GRAM_REDUCE, launch_gram_reduce(L, false));
   JACAP_PHASE(JACAP_PHASE_FACTOR, launch_factor(L, false));
-  if (L.ws.mfma) {  // recompute the Gram of ill-conditioned units with the exact split
-    TimedPhase tp(L.stream, JACAP_PHASE_REFINE);
+  if (L.ws.mfma) {  // the units marked by the factorisation, again in fp64
+    TimedPhase tp(L.stream, JACAP_PHASE_REFINE, L.timed);
     JACAP_TRY(launch_gram(L, v, true));
     JACAP_TRY(launch_gram_reduce(L, true));
     JACAP_TRY(launch_factor(L, true));
+    JACAP_TRY(launch_leverage_precise(L, v, scores));
   }
   JACAP_PHASE(JACAP_PHASE_LEVERAGE, launch_leverage(L, v, scores));
   return JACAP_OK;
@@ -259,6 +274,41 @@ bool score_ptrs_ok(const jacap_batch* b, const void* q, const void* k, const voi
 }
 
 }  // namespace
+
+namespace jacap {
+
+jacap_status prepare_launch(const jacap_config* c, const jacap_batch* b, void* ws, size_t ws_bytes,
+                            void* stream, Launch* L) {
+  return prepare(c, b, ws, ws_bytes, stream, L);
+}
+
+jacap_status check_evict_ptrs(const jacap_config* c, const jacap_batch* b, const void* q,
+                              const void* k, const void* v, const float* scores,
+                              const int32_t* idx, const void* k_out, const void* v_out) {
+  if (!score_ptrs_ok(b, q, k, v, scores)) return JACAP_ERR_INVALID_ARG;
+  if (c->budget_k > 0) {
+    if (!idx || !aligned16(idx)) return JACAP_ERR_INVALID_ARG;
+    if (!data_ptr_ok(k_out, b) || !data_ptr_ok(v_out, b)) return JACAP_ERR_INVALID_ARG;
+  }
+  return JACAP_OK;
+}
+
+// Scoring, selection and compaction of a prepared problem, on L.stream.
+jacap_status evict_prepared(const Launch& L, const void* q, const void* k, const void* v,
+                            float* scores, int32_t* idx, void* k_out, void* v_out) {
+  if (L.geo.T > 0) {
+    const jacap_status s = run_score(L, q, k, v, scores);
+    if (s != JACAP_OK) return s;
+  } else {
+    JACAP_PHASE(JACAP_PHASE_INIT, launch_init(L));
+  }
+  if (L.cfg->budget_k == 0) return JACAP_OK;
+  JACAP_PHASE(JACAP_PHASE_SELECT, launch_select(L, scores, idx));
+  JACAP_PHASE(JACAP_PHASE_COMPACT, launch_compact(L, idx, k, v, k_out, v_out));
+  return JACAP_OK;
+}
+
+}  // namespace jacap
 
 extern "C" {
 
@@ -339,8 +389,10 @@ jacap_status jacap_compact(const jacap_config* cfg, const jacap_batch* batch, co
   jacap_status s = prepare(cfg, batch, nullptr, 0, stream, &L);
   if (s != JACAP_OK) return s;
   if (cfg->budget_k == 0) return JACAP_OK;
-  if (!idx || !k || !v || !k_out || !v_out) return JACAP_ERR_INVALID_ARG;
-  if (!aligned16(k) || !aligned16(v) || !aligned16(k_out) || !aligned16(v_out)) return JACAP_ERR_INVALID_ARG;
+  if (!idx || !aligned16(idx)) return JACAP_ERR_INVALID_ARG;
+  if (!data_ptr_ok(k, batch) || !data_ptr_ok(v, batch) || !data_ptr_ok(k_out, batch) ||
+      !data_ptr_ok(v_out, batch))
+    return JACAP_ERR_INVALID_ARG;
   TimedPhase tp(L.stream, JACAP_PHASE_COMPACT);
   return launch_compact(L, idx, k, v, k_out, v_out) == hipSuccess ? JACAP_OK : JACAP_ERR_HIP;
 }
@@ -352,21 +404,9 @@ jacap_status jacap_evict(const jacap_config* cfg, const jacap_batch* batch, cons
   if (!ws) return JACAP_ERR_INVALID_ARG;
   jacap_status s = prepare(cfg, batch, ws, ws_bytes, stream, &L);
   if (s != JACAP_OK) return s;
-  if (!score_ptrs_ok(batch, q_win, k, v, scores)) return JACAP_ERR_INVALID_ARG;
-  if (cfg->budget_k > 0) {
-    if (!idx || !aligned16(idx)) return JACAP_ERR_INVALID_ARG;
-    if (!data_ptr_ok(k_out, batch) || !data_ptr_ok(v_out, batch)) return JACAP_ERR_INVALID_ARG;
-  }
-  if (batch->total_tokens > 0) {
-    s = run_score(L, q_win, k, v, scores);
-    if (s != JACAP_OK) return s;
-  } else {
-    JACAP_PHASE(JACAP_PHASE_INIT, launch_init(L));
-  }
-  if (cfg->budget_k == 0) return JACAP_OK;
-  JACAP_PHASE(JACAP_PHASE_SELECT, launch_select(L, scores, idx));
-  JACAP_PHASE(JACAP_PHASE_COMPACT, launch_compact(L, idx, k, v, k_out, v_out));
-  return JACAP_OK;
+  s = jacap::check_evict_ptrs(cfg, batch, q_win, k, v, scores, idx, k_out, v_out);
+  if (s != JACAP_OK) return s;
+  return jacap::evict_prepared(L, q_win, k, v, scores, idx, k_out, v_out);
 }
 
 jacap_status jacap_evict_slots(const jacap_config* cfg, const jacap_batch* batch, const void* q_win,

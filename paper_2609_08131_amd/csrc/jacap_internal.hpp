@@ -19,9 +19,11 @@ constexpr int kGChunkMfma = 4096;    // tokens per workgroup in the MFMA Gram pa
 constexpr int kGChunkMfmaMax = 16384; // ... and at most (larger chunks: fewer partial Grams)
 constexpr int kGramMinBlocks = 2048;  // chunks are as large as this many blocks in the grid allow
 constexpr int kGramSpan = 128;       // tokens between two flushes of the Gram's short fp32 chains
-constexpr int kGChunkPrecise = 1024; // tokens per workgroup in the fp64 Gram pass
+constexpr int kGChunkPrecise = 1024; // tokens per workgroup in the fp64 Gram pass: at least
+constexpr int kPrecisePartials = 256;  // fp64 Gram partials per batch the chunking aims at
 constexpr int kLChunkMfma = 4096;    // tokens per workgroup in the MFMA leverage pass
-constexpr int kLChunkPrecise = 1024; // tokens per workgroup in the fp64 leverage pass
+constexpr int kLChunkPrecise = 1024; // tokens per workgroup in the fp64 leverage pass (fp32 keys)
+constexpr int kLChunkRefine = 4096;  // ... and over the bf16 units that take the fp64 path
 constexpr int kWChunk = 4096;        // tokens per workgroup in the weight pass
 // The K pass sums a chunk's exp(z - max) terms (all but the max's own) as
 // exp(z - max + kRestShift) in fp32, so that they stay normal down to
@@ -34,8 +36,10 @@ constexpr int64_t kMaxTokenStride = int64_t(1) << 24;  // elements between conse
 // Unit flags (per (seq, layer, kv head)); the public flags are the OR of all.
 constexpr uint32_t kUnitNonfinite = JACAP_FLAG_NONFINITE;
 constexpr uint32_t kUnitSingular = JACAP_FLAG_SINGULAR;
-// Internal: the unit's capacity matrix is ill-conditioned enough that its Gram
-// is recomputed with the exact three-term split (bf16 path only).
+// Internal (bf16 path only): the unit's capacity matrix is ill-conditioned
+// enough (or one of its pivots small enough) that the fp32-accumulated Gram
+// and the bf16 leverage products could miss the score tolerance; its Gram,
+// factor and leverage scores are recomputed in fp64.
 constexpr uint32_t kUnitRefine = 1u << 8;
 constexpr uint32_t kUnitFailed = kUnitNonfinite | kUnitSingular;
 
@@ -141,15 +145,18 @@ struct Workspace {
   size_t wgt;      // float  [L][H][T]       importance weights (Eq. 8)
   size_t hscore;   // float  [L][H][G][T]    per-query-head scores (per-head GQA mode)
   size_t kept;     // int32  [B][L][H][budget] kept positions, staged by jacap_select_evicted
-  size_t gram;     // per-chunk partial Grams [U][gchunks][NPAIR*256], fp32 (bf16 path) or fp64
-  size_t gram_red; // double [U][NPAIR*256]  reduced Gram, block-lane layout
-  size_t linv64;   // double [U][D][D]       L^{-1} (lower, zeros above), fp32-input path
+  size_t gram;     // per-chunk partial Grams: [U][gchunks][NPAIR*256] fp32 (bf16 MFMA pass)
+                   // or [U][pchunks][NPAIR*256] fp64 (fp64 pass); one buffer for both
+  size_t gram_red; // double [U][NPAIR*256]  reduced Gram, block-lane layout; after an fp64
+                   // factorisation, L^{-1} in the lower-block layout (see k_factor.hip)
   size_t lfrag;    // bf16 [U][NLP][2][64][8] L^{-1} hi/lo MFMA B fragments, bf16 path
   size_t gc;       // double [L][H][T]       greedy: c_i when last computed
   size_t gst;      // int32  [L][H][T]       greedy: picks made at that time (-1 = taken)
   size_t gent;     // GreedyEntry [U][ceil(maxn / 256)]  greedy: best of each 256-position block
   size_t total;
   int kchunks, wchunks, gchunks, gchunk, gparts, lchunks;
+  int pchunks, pchunk;  // chunks of the fp64 Gram pass
+  int plchunks;         // chunks of the fp64 leverage pass
   bool mfma;       // bf16 path (MFMA Gram and leverage)
 };
 
@@ -296,7 +303,8 @@ __device__ __forceinline__ void drain_vmem() {
 // ---------------------------------------------------------------------------
 class TimedPhase {
  public:
-  TimedPhase(hipStream_t stream, int phase);
+  // enabled = false: never records (no event is created), whatever the mask.
+  TimedPhase(hipStream_t stream, int phase, bool enabled = true);
   ~TimedPhase();
   TimedPhase(const TimedPhase&) = delete;
   TimedPhase& operator=(const TimedPhase&) = delete;
@@ -314,6 +322,7 @@ struct Launch {
   const jacap_config* cfg;
   Geo geo;
   Workspace ws;
+  bool timed = true;  // phases may be recorded by the timing API
   char* wsp;  // workspace base
   hipStream_t stream;
 };
@@ -335,12 +344,24 @@ hipError_t launch_gram(const Launch& L, const void* v, bool refine);
 hipError_t launch_gram_reduce(const Launch& L, bool refine);
 hipError_t launch_factor(const Launch& L, bool refine);
 hipError_t launch_leverage(const Launch& L, const void* v, float* scores);
+hipError_t launch_leverage_precise(const Launch& L, const void* v, float* scores);
 hipError_t launch_select(const Launch& L, const float* scores, int32_t* idx);
 hipError_t launch_select_evicted(const Launch& L, const float* scores, int32_t* slots, int cap);
 hipError_t launch_compact(const Launch& L, const int32_t* idx, const void* k, const void* v,
                           void* ko, void* vo);
 hipError_t launch_greedy(const Launch& L, const void* v, int32_t* idx, int32_t* order,
                          double* logdet);
+
+// Host side of the entry points (jacap_host.hip): validation of the
+// descriptors and workspace, and the launch sequence of jacap_evict once the
+// problem is prepared.
+jacap_status prepare_launch(const jacap_config* c, const jacap_batch* b, void* ws, size_t ws_bytes,
+                            void* stream, Launch* L);
+jacap_status check_evict_ptrs(const jacap_config* c, const jacap_batch* b, const void* q,
+                              const void* k, const void* v, const float* scores,
+                              const int32_t* idx, const void* k_out, const void* v_out);
+jacap_status evict_prepared(const Launch& L, const void* q, const void* k, const void* v,
+                            float* scores, int32_t* idx, void* k_out, void* v_out);
 
 template <typename T>
 __host__ __device__ __forceinline__ T* ws_ptr(char* base, size_t off) {

@@ -30,7 +30,8 @@ hipEvent_t take_event() {
 
 }  // namespace
 
-TimedPhase::TimedPhase(hipStream_t stream, int phase) : stream_(stream), phase_(phase) {
+TimedPhase::TimedPhase(hipStream_t stream, int phase, bool enabled) : stream_(stream), phase_(phase) {
+  if (!enabled) return;
   std::lock_guard<std::mutex> lk(g_mu);
   if (!(g_mask & (1u << phase))) return;
   begin_ = take_event();

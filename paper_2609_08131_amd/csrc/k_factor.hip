@@ -4,10 +4,15 @@
 // ||L^{-1} v||^2 = v^T A^{-1} v is what the leverage score of Eq. 10 needs.
 //
 // Input: the reduced Gram in block-lane layout (upper 16x16 blocks, see
-// k_gram.hip). Output: L^{-1} in fp64 (fp32-input path), or, for the bf16
-// MFMA leverage pass, L^{-1} rounded to fp32 and split into bf16 hi + lo
-// terms, stored directly in the per-lane B-fragment order of the
-// 16x16x32 MFMA (only the K-blocks that touch the lower triangle).
+// k_gram.hip). Output, after the first factorisation of an fp32-accumulated
+// Gram (bf16 inputs): L^{-1} rounded to fp32 and split into bf16 hi + lo
+// terms, stored directly in the per-lane B-fragment order of the 16x16x32
+// MFMA (only the K-blocks that touch the lower triangle). After a
+// factorisation of an fp64 Gram (fp32 inputs; the bf16 units marked for the
+// fp64 path): L^{-1} in fp64, written over the unit's reduced Gram in the
+// lower-block layout -- block pair p = pair_index(i, j), i <= j, holds the
+// 16x16 block X[16 j + r][16 i + c] at p * 256 + 16 r + c (zero above the
+// diagonal of a diagonal block).
 //
 // Blocked algorithm on 16x16 blocks (the sequential chain is what bounds a
 // single workgroup, so the work between barriers is made as wide as possible):
@@ -31,9 +36,21 @@
 
 namespace jacap {
 
-// cond(A) bound above which the bf16 path recomputes the unit's Gram with the
-// exact three-term split (its two-term error grows like ~1e-8 cond(A)).
+// cond(A) bound above which the bf16 path recomputes the unit in fp64: the
+// fp32-accumulated two-term Gram and the two-term L^{-1} products carry errors
+// that A^{-1} amplifies by up to cond(A) (~1e-8 cond(A) in the scores).
 constexpr double kRefineCond = 2e3;
+// Smallest pivot, relative to its diagonal entry, taken as positive. On the
+// fp32-accumulated Gram a smaller one sends the unit to the fp64 path. On an
+// fp64 Gram it means A is numerically singular at the score tolerance: a
+// pivot ratio r implies cond(A) >= 1 / r, and fp64 rounding (any evaluation
+// order, ~1e-14 relative in A) then moves the scores by about 5e-15 / r, so
+// below 1e-13 / tol (1e-10 for the 1e-3 of bf16 inputs, 1e-8 for the 1e-5 of
+// fp32 inputs) the scores are not determined to the tolerance -- at ridge 0,
+// a rank-deficient M or a saturated softmax's weights spanning 1e30.
+constexpr double kPivRelRefine = 1e-4;
+constexpr double kPivRelSingularBf16 = 1e-10;
+constexpr double kPivRelSingularFp32 = 1e-8;
 
 // Eight waves: two per SIMD, so that one wave's LDS and fp64 latencies
 // overlap the other's work.
@@ -71,14 +88,13 @@ __device__ __forceinline__ void tri_index(int e, int& i, int& j) {
   j = e - r * (r + 1) / 2;
 }
 
-// PASS 0: first factorisation (all units). PASS 1: refinement of the units
-// marked kUnitRefine by pass 0 (bf16 path), from their exact-split Gram.
+// PASS 0: first factorisation (all units). PASS 1: the units marked
+// kUnitRefine by pass 0 (bf16 path), from their fp64 Gram. FRAGS: bf16 inputs.
 template <int D, bool FRAGS>
-__global__ __launch_bounds__(kFactorThreads) void factor_kernel(Geo g, const double* __restrict__ red,
+__global__ __launch_bounds__(kFactorThreads) void factor_kernel(Geo g, double* __restrict__ red,
                                                           double ridge,
                                                           const double* __restrict__ wscale,
-                                                          double piv_rel, int pass,
-                                                          double* __restrict__ linv64,
+                                                          int pass,
                                                           uint16_t* __restrict__ lfrag,
                                                           uint32_t* status, uint32_t* uflags) {
   constexpr int LD = D + 1;
@@ -88,9 +104,11 @@ __global__ __launch_bounds__(kFactorThreads) void factor_kernel(Geo g, const dou
   if (pass == 1 && !(uflags[u] & kUnitRefine)) return;
   const Unit un = decode_unit(g, u);
   if (un.n == 0) return;
-  // The two-term bf16 Gram may be refined later; singularity is decided on
-  // the exact one (pass 1) or on the fp64 one (fp32 inputs).
+  // The fp32-accumulated Gram of bf16 inputs may be redone in fp64 later;
+  // singularity is decided on an fp64 Gram only (pass 1, or fp32 inputs).
   const bool may_refine = FRAGS && pass == 0;
+  const double piv_rel =
+      may_refine ? kPivRelRefine : (FRAGS ? kPivRelSingularBf16 : kPivRelSingularFp32);
 
   __shared__ double A[D * LD];
   __shared__ double dg[D];   // diagonal of A before factorisation
@@ -400,11 +418,15 @@ __global__ __launch_bounds__(kFactorThreads) void factor_kernel(Geo g, const dou
   }
 
   // Store L^{-1}.
-  if constexpr (!FRAGS) {
-    double* o64 = linv64 + (int64_t)u * D * D;
-    for (int e = tid; e < D * D; e += kFactorThreads) {
-      const int a = e / D, b = e % D;
-      o64[e] = (b <= a) ? xinv(a, b) : 0.0;
+  if (!may_refine) {  // fp64, over the reduced Gram (already in LDS)
+    double* o64 = red + (int64_t)u * (NPAIR * 256);
+    for (int e = tid; e < NPAIR * 256; e += kFactorThreads) {
+      int p = e >> 8, bi = 0;  // block pair p -> (bi, bj), bi <= bj
+#pragma unroll
+      for (int q = 0; q < NB; ++q)
+        if (p >= NB - bi) { p -= NB - bi; ++bi; }
+      const int bj = bi + p;
+      o64[e] = xinv(16 * bj + ((e >> 4) & 15), 16 * bi + (e & 15));
     }
   } else {
     // B fragment of output block j (a = 16 j + ch) and K block kb
@@ -442,21 +464,18 @@ hipError_t launch_factor(const Launch& L, bool refine) {
   if (refine && !L.ws.mfma) return hipSuccess;
   const int pass = refine ? 1 : 0;
   const Geo& g = L.geo;
-  const double* red = ws_ptr<double>(L.wsp, L.ws.gram_red);
-  double* l64 = ws_ptr<double>(L.wsp, L.ws.linv64);
+  double* red = ws_ptr<double>(L.wsp, L.ws.gram_red);
   uint16_t* lf = ws_ptr<uint16_t>(L.wsp, L.ws.lfrag);
   uint32_t* st = ws_ptr<uint32_t>(L.wsp, L.ws.status);
   uint32_t* uf = ws_ptr<uint32_t>(L.wsp, L.ws.uflags);
+  const double* wsc = ws_ptr<double>(L.wsp, L.ws.wscale);
   const double ridge = (double)L.cfg->ridge;
-  // fp32-accumulated Gram (bf16 path) carries ~1e-6 relative noise; the fp64
-  // path ~1e-15.
-  const double piv_rel = L.ws.mfma ? 1e-4 : 1e-12;
   if (L.ws.mfma) {
-    if (g.D == 128) factor_kernel<128, true><<<g.U, kFactorThreads, 0, L.stream>>>(g, red, ridge, ws_ptr<double>(L.wsp, L.ws.wscale), piv_rel, pass, l64, lf, st, uf);
-    else factor_kernel<64, true><<<g.U, kFactorThreads, 0, L.stream>>>(g, red, ridge, ws_ptr<double>(L.wsp, L.ws.wscale), piv_rel, pass, l64, lf, st, uf);
+    if (g.D == 128) factor_kernel<128, true><<<g.U, kFactorThreads, 0, L.stream>>>(g, red, ridge, wsc, pass, lf, st, uf);
+    else factor_kernel<64, true><<<g.U, kFactorThreads, 0, L.stream>>>(g, red, ridge, wsc, pass, lf, st, uf);
   } else {
-    if (g.D == 128) factor_kernel<128, false><<<g.U, kFactorThreads, 0, L.stream>>>(g, red, ridge, ws_ptr<double>(L.wsp, L.ws.wscale), piv_rel, pass, l64, lf, st, uf);
-    else factor_kernel<64, false><<<g.U, kFactorThreads, 0, L.stream>>>(g, red, ridge, ws_ptr<double>(L.wsp, L.ws.wscale), piv_rel, pass, l64, lf, st, uf);
+    if (g.D == 128) factor_kernel<128, false><<<g.U, kFactorThreads, 0, L.stream>>>(g, red, ridge, wsc, pass, lf, st, uf);
+    else factor_kernel<64, false><<<g.U, kFactorThreads, 0, L.stream>>>(g, red, ridge, wsc, pass, lf, st, uf);
   }
   return hipGetLastError();
 }

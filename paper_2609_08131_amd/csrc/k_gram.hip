@@ -8,13 +8,13 @@
 //
 // bf16 inputs: MFMA 16x16x32 bf16 with fp32 accumulation; the contraction runs
 // over tokens. V is exact in bf16; the weighted operand x = w v (fp32) is split
-// into bf16 terms, so M = sum_t V^T X_t. The first pass uses two terms rounded
-// to nearest (x = x1 + x2 to 2^-17 relative); the factor kernel then marks
-// the units whose capacity matrix is ill-conditioned enough for that to show
-// in the scores, and a second pass recomputes only those with an exact
-// three-term split by truncation.
+// into two bf16 terms rounded to nearest (x = x1 + x2 to 2^-17 relative), so
+// M = V^T X1 + V^T X2. The factor kernel then marks the units whose capacity
+// matrix is ill-conditioned enough for the fp32 rounding to show in the
+// scores, and a second pass recomputes only those in fp64.
 //
-// fp32 inputs: fp64 VALU accumulation (register tiles), same partial layout.
+// fp64 pass (every unit of fp32 inputs; the marked units of bf16 inputs): fp64
+// VALU accumulation of exact products (register tiles), same partial layout.
 #include <type_traits>
 
 #include "jacap_internal.hpp"
@@ -27,35 +27,6 @@ typedef uint16_t u16x8 __attribute__((ext_vector_type(8)));
 typedef short s16x4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float float2v __attribute__((ext_vector_type(2)));
-
-// Three-term exact split of x into bf16 pieces by truncation: each piece takes
-// the next 8 significant bits, the remainder of the last one is exactly zero.
-__device__ __forceinline__ void split3(float x, uint16_t& h1, uint16_t& h2, uint16_t& h3) {
-  const uint32_t b0 = __float_as_uint(x) & 0xFFFF0000u;
-  const float r1 = x - __uint_as_float(b0);
-  const uint32_t b1 = __float_as_uint(r1) & 0xFFFF0000u;
-  const float r2 = r1 - __uint_as_float(b1);
-  h1 = (uint16_t)(b0 >> 16);
-  h2 = (uint16_t)(b1 >> 16);
-  h3 = (uint16_t)(__float_as_uint(r2) >> 16);
-}
-
-// Split x into NT bf16 terms, smallest first (x = sum of the terms up to the
-// split error): NT = 2 rounds to nearest (error <= 2^-17 |x|); NT = 3
-// truncates (exact).
-template <int NT>
-__device__ __forceinline__ void split_terms(float x, uint16_t (&h)[NT]) {
-  if constexpr (NT == 2) {
-    const __bf16 a = (__bf16)x;
-    const __bf16 b = (__bf16)(x - (float)a);
-    h[0] = __builtin_bit_cast(uint16_t, b);
-    h[1] = __builtin_bit_cast(uint16_t, a);
-  } else {
-    uint16_t h1, h2, h3;
-    split3(x, h1, h2, h3);
-    h[0] = h3; h[1] = h2; h[2] = h1;
-  }
-}
 
 // Transposing 64-bit LDS read (gfx950): inside each group of 16 lanes, lane i
 // receives element i % 4 of the 4 x 16-bit values addressed by lanes
@@ -175,7 +146,8 @@ __device__ __forceinline__ void gram_wave(const GramArgs& ga, uint16_t* tiles, f
     constexpr int J = decltype(jc)::value, PBASE = decltype(pbc)::value;
     constexpr bool FIRST = decltype(firstc)::value;
     u16x8 xt[NT];
-    if constexpr (NT == 2) {
+    static_assert(NT == 2, "two bf16 terms");
+    {
       // Pairwise: hi = RNE(x) for two elements with one packed convert, the
       // residual x - hi from an fma on the exact product.
 #pragma unroll
@@ -189,14 +161,6 @@ __device__ __forceinline__ void gram_wave(const GramArgs& ga, uint16_t* tiles, f
         const uint32_t lb = __builtin_bit_cast(uint32_t, __builtin_convertvector(r, bf16x2));
         xt[0][q] = (uint16_t)lb; xt[0][q + 1] = (uint16_t)(lb >> 16);
         xt[1][q] = (uint16_t)hb; xt[1][q + 1] = (uint16_t)(hb >> 16);
-      }
-    } else {
-#pragma unroll
-      for (int q = 0; q < 8; ++q) {
-        uint16_t h[NT];
-        split_terms<NT>(bf16_to_f32(a[J][q]) * wl[q], h);
-#pragma unroll
-        for (int t = 0; t < NT; ++t) xt[t][q] = h[t];
       }
     }
     // term-outer order, so that consecutive MFMAs write different
@@ -308,8 +272,7 @@ __device__ __forceinline__ void gram_wave(const GramArgs& ga, uint16_t* tiles, f
   if constexpr (HAS_B) emit(std::integral_constant<int, JB>{}, std::integral_constant<int, PA>{});
 }
 
-// NT = 2: first pass over every unit. NT = 3: refinement pass over the units
-// the factor kernel marked (kUnitRefine), which rewrites their partials.
+// NT = 2 bf16 terms of the weighted operand, every unit.
 // POL: cache policy of the V loads (streamed, or kept in L2 for the other
 // query-head units of the same KV head).
 template <int D, int NT, int POL>
@@ -321,7 +284,6 @@ __global__ __launch_bounds__(kThreads, 2) void gram_mfma_kernel(
   constexpr int TILE = kGramStep * kGramPitch;
   int u, chunk;
   if (!grid_unit_chunk<true>(g, gchunks, u, chunk)) return;
-  if (NT == 3 && !(uflags[u] & kUnitRefine)) return;
   const Unit un = decode_unit(g, u);
   const int base = chunk * gchunk;
   if (base >= un.n) return;
@@ -344,26 +306,31 @@ __global__ __launch_bounds__(kThreads, 2) void gram_mfma_kernel(
   }
 }
 
-// fp64 Gram for fp32 inputs: thread (ty, tx) of a 16 x 16 grid owns a
-// (D/16) x (D/16) register tile of M; V is staged 32 tokens at a time.
-template <int D>
+// fp64 Gram: every unit of fp32 inputs, and (REFINE_ONLY) the units of bf16
+// inputs that the factorisation marked kUnitRefine. Products w_i v_ij v_ik are
+// exact in fp64 (a bf16 or fp32 value times an fp32 weight, times a bf16 or
+// fp32 value), the sums fp64. Thread (ty, tx) of a 16 x 16 grid owns a
+// (D/16) x (D/16) register tile of M; V is staged 32 tokens at a time. One
+// partial per chunk of `pchunk` tokens, in the block-lane layout.
+template <typename T, int D, bool REFINE_ONLY>
 __global__ __launch_bounds__(kThreads) void gram_precise_kernel(
-    Geo g, const float* __restrict__ v, const float* __restrict__ wbuf,
-    double* __restrict__ partials, int gchunks) {
+    Geo g, const T* __restrict__ v, const float* __restrict__ wbuf,
+    const uint32_t* __restrict__ uflags, double* __restrict__ partials, int pchunks, int pchunk) {
   constexpr int R = D / 16;
   constexpr int NB = D / 16;
   constexpr int NPAIR = NB * (NB + 1) / 2;
   int u, chunk;
-  if (!grid_unit_chunk<true>(g, gchunks, u, chunk)) return;
+  if (!grid_unit_chunk<true>(g, pchunks, u, chunk)) return;
+  if (REFINE_ONLY && !(uflags[u] & kUnitRefine)) return;
   const Unit un = decode_unit(g, u);
-  const int base = chunk * kGChunkPrecise;
+  const int base = chunk * pchunk;
   if (base >= un.n) return;
   const int tid = threadIdx.x, ty = tid / 16, tx = tid % 16;
   __shared__ float vs[32][D];
   __shared__ double ws[32];
-  const float* vb = v + un.l * g.vsl + un.h * g.vsh;
+  const T* vb = v + un.l * g.vsl + un.h * g.vsh;
   const int64_t trow = token_row(g, un);
-  const int end = min(un.n, base + kGChunkPrecise);
+  const int end = min(un.n, base + pchunk);
   double acc[R][R];
 #pragma unroll
   for (int a = 0; a < R; ++a)
@@ -373,7 +340,7 @@ __global__ __launch_bounds__(kThreads) void gram_precise_kernel(
     __syncthreads();
     for (int e = tid; e < 32 * D; e += kThreads) {
       const int tok = e / D, c = e % D;
-      vs[tok][c] = (t0 + tok < end) ? vb[(un.t0 + t0 + tok) * g.vst + c] : 0.0f;
+      vs[tok][c] = (t0 + tok < end) ? to_f32(vb[(un.t0 + t0 + tok) * g.vst + c]) : 0.0f;
     }
     if (tid < 32) {
       const int t = t0 + tid;
@@ -393,7 +360,7 @@ __global__ __launch_bounds__(kThreads) void gram_precise_kernel(
         for (int b = 0; b < R; ++b) acc[a][b] += xa[a] * vb2[b];
     }
   }
-  double* out = partials + ((int64_t)u * gchunks + chunk) * (NPAIR * 256);
+  double* out = partials + ((int64_t)u * pchunks + chunk) * (NPAIR * 256);
 #pragma unroll
   for (int a = 0; a < R; ++a)
 #pragma unroll
@@ -409,32 +376,37 @@ __global__ __launch_bounds__(kThreads) void gram_precise_kernel(
 
 hipError_t launch_gram(const Launch& L, const void* v, bool refine) {
   const Geo& g = L.geo;
-  const dim3 grid((unsigned)chunked_grid(g, L.ws.gchunks));
   const float* wb = ws_ptr<float>(L.wsp, L.ws.wgt);
   const uint32_t* uf = ws_ptr<uint32_t>(L.wsp, L.ws.uflags);
-  if (L.ws.mfma) {
+  if (L.ws.mfma && !refine) {
+    const dim3 grid((unsigned)chunked_grid(g, L.ws.gchunks));
     float* part = ws_ptr<float>(L.wsp, L.ws.gram);
     const uint16_t* vv = (const uint16_t*)v;
     auto go = [&](auto kern) {
       kern<<<grid, kThreads, 0, L.stream>>>(g, vv, wb, uf, part, L.ws.gchunks, L.ws.gchunk);
     };
-    // The refinement pass is rare and always streams.
     if (g.D == 128) {
-      if (refine) go(gram_mfma_kernel<128, 3, kPolicyStream>);
-      else if (g.V > 1) go(gram_mfma_kernel<128, 2, kPolicyShared>);
+      if (g.V > 1) go(gram_mfma_kernel<128, 2, kPolicyShared>);
       else go(gram_mfma_kernel<128, 2, kPolicyStream>);
     } else {
-      if (refine) go(gram_mfma_kernel<64, 3, kPolicyStream>);
-      else if (g.V > 1) go(gram_mfma_kernel<64, 2, kPolicyShared>);
+      if (g.V > 1) go(gram_mfma_kernel<64, 2, kPolicyShared>);
       else go(gram_mfma_kernel<64, 2, kPolicyStream>);
     }
+    return hipGetLastError();
+  }
+  if (!L.ws.mfma && refine) return hipSuccess;
+  // fp64: all units of fp32 inputs, or the marked units of bf16 inputs
+  const dim3 grid((unsigned)chunked_grid(g, L.ws.pchunks));
+  double* part = ws_ptr<double>(L.wsp, L.ws.gram);
+  auto go = [&](auto kern, auto vv) {
+    kern<<<grid, kThreads, 0, L.stream>>>(g, vv, wb, uf, part, L.ws.pchunks, L.ws.pchunk);
+  };
+  if (L.ws.mfma) {
+    if (g.D == 128) go(gram_precise_kernel<uint16_t, 128, true>, (const uint16_t*)v);
+    else go(gram_precise_kernel<uint16_t, 64, true>, (const uint16_t*)v);
   } else {
-    if (refine) return hipSuccess;
-    double* part = ws_ptr<double>(L.wsp, L.ws.gram);
-    if (g.D == 128)
-      gram_precise_kernel<128><<<grid, kThreads, 0, L.stream>>>(g, (const float*)v, wb, part, L.ws.gchunks);
-    else
-      gram_precise_kernel<64><<<grid, kThreads, 0, L.stream>>>(g, (const float*)v, wb, part, L.ws.gchunks);
+    if (g.D == 128) go(gram_precise_kernel<float, 128, false>, (const float*)v);
+    else go(gram_precise_kernel<float, 64, false>, (const float*)v);
   }
   return hipGetLastError();
 }
@@ -469,14 +441,14 @@ hipError_t launch_gram_reduce(const Launch& L, bool refine) {
   const int NB = g.D / 16, npair = NB * (NB + 1) / 2;
   const dim3 grid(g.U, npair);
   double* red = ws_ptr<double>(L.wsp, L.ws.gram_red);
-  if (L.ws.mfma) {
+  if (L.ws.mfma && !refine) {
     const float* part = ws_ptr<float>(L.wsp, L.ws.gram);
     if (g.D == 128) gram_reduce_kernel<float, 128><<<grid, kThreads, 0, L.stream>>>(g, part, L.ws.gchunks, L.ws.gchunk, uf, rf, red);
     else gram_reduce_kernel<float, 64><<<grid, kThreads, 0, L.stream>>>(g, part, L.ws.gchunks, L.ws.gchunk, uf, rf, red);
-  } else {
+  } else {  // fp64 partials
     const double* part = ws_ptr<double>(L.wsp, L.ws.gram);
-    if (g.D == 128) gram_reduce_kernel<double, 128><<<grid, kThreads, 0, L.stream>>>(g, part, L.ws.gchunks, L.ws.gchunk, uf, rf, red);
-    else gram_reduce_kernel<double, 64><<<grid, kThreads, 0, L.stream>>>(g, part, L.ws.gchunks, L.ws.gchunk, uf, rf, red);
+    if (g.D == 128) gram_reduce_kernel<double, 128><<<grid, kThreads, 0, L.stream>>>(g, part, L.ws.pchunks, L.ws.pchunk, uf, rf, red);
+    else gram_reduce_kernel<double, 64><<<grid, kThreads, 0, L.stream>>>(g, part, L.ws.pchunks, L.ws.pchunk, uf, rf, red);
   }
   return hipGetLastError();
 }

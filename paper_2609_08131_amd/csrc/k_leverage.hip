@@ -8,7 +8,9 @@
 // triangle are multiplied. The squared row norm is reduced across the 16
 // lanes that share a token.
 //
-// fp32 inputs: fp64 VALU, L^{-1} in LDS, 8 threads per token.
+// fp64 pass (every unit of fp32 inputs; the units of bf16 inputs that the
+// factorisation sent to the fp64 path): fp64 VALU, L^{-1} in LDS, 8 threads
+// per token.
 #include "jacap_internal.hpp"
 
 namespace jacap {
@@ -37,7 +39,9 @@ __global__ __launch_bounds__(kThreads, 2) void leverage_mfma_kernel(
   const int64_t trow = token_row(g, un);
   const int end = min(un.n, base + kLChunkMfma);
 
-  if (uflags[u] & kUnitFailed) {  // unit failed (non-finite input or singular A): NaN scores
+  const uint32_t uf = uflags[u];
+  if (uf & kUnitRefine) return;  // scored by the fp64 pass
+  if (uf & kUnitFailed) {  // unit failed (non-finite input): NaN scores
     for (int t = base + threadIdx.x; t < end; t += kThreads) scores[trow + t] = __builtin_nanf("");
     return;
   }
@@ -148,37 +152,52 @@ __global__ __launch_bounds__(kThreads, 2) void leverage_mfma_kernel(
   }
 }
 
-template <int D>
+// fp64 leverage: every unit (fp32 inputs), or only the units marked
+// kUnitRefine (REFINE_ONLY, bf16 inputs). L^{-1} comes from the reduced-Gram
+// buffer in the lower-block layout written by the fp64 factorisation.
+template <typename T, int D, bool REFINE_ONLY>
 __global__ __launch_bounds__(kThreads) void leverage_precise_kernel(
-    Geo g, const float* __restrict__ v, const float* __restrict__ wbuf,
-    const double* __restrict__ linv64, const uint32_t* __restrict__ uflags,
-    float* __restrict__ scores, int lchunks) {
+    Geo g, const T* __restrict__ v, const float* __restrict__ wbuf,
+    const double* __restrict__ xred, const uint32_t* __restrict__ uflags,
+    float* __restrict__ scores, int lchunks, int lchunk) {
   constexpr int LD = D + 1;
+  constexpr int NB = D / 16;
+  constexpr int NPAIR = NB * (NB + 1) / 2;
   constexpr int TPT = 8;                 // threads per token
   constexpr int TOK = kThreads / TPT;    // tokens per tile
   int u, chunk;
   if (!grid_unit_chunk<true>(g, lchunks, u, chunk)) return;
+  const uint32_t uf = uflags[u];
+  if (REFINE_ONLY && !(uf & kUnitRefine)) return;
   const Unit un = decode_unit(g, u);
-  const int base = chunk * kLChunkPrecise;
+  const int base = chunk * lchunk;
   if (base >= un.n) return;
   const int tid = threadIdx.x;
   const int64_t trow = token_row(g, un);
-  const int end = min(un.n, base + kLChunkPrecise);
-  if (uflags[u] & kUnitFailed) {
+  const int end = min(un.n, base + lchunk);
+  if (uf & kUnitFailed) {  // non-finite input or singular A: NaN scores
     for (int t = base + tid; t < end; t += kThreads) scores[trow + t] = __builtin_nanf("");
     return;
   }
   __shared__ double X[D * LD];
   __shared__ float vs[TOK][D];
-  const double* Li = linv64 + (int64_t)u * D * D;
-  for (int e = tid; e < D * D; e += kThreads) X[(e / D) * LD + (e % D)] = Li[e];
-  const float* vb = v + un.l * g.vsl + un.h * g.vsh;
+  // lower blocks of L^{-1}: pair p = (bi <= bj) holds X[16 bj + r][16 bi + c]
+  const double* Xb = xred + (int64_t)u * (NPAIR * 256);
+  for (int e = tid; e < NPAIR * 256; e += kThreads) {
+    int p = e >> 8, bi = 0;
+#pragma unroll
+    for (int q = 0; q < NB; ++q)
+      if (p >= NB - bi) { p -= NB - bi; ++bi; }
+    const int bj = bi + p;
+    X[(16 * bj + ((e >> 4) & 15)) * LD + 16 * bi + (e & 15)] = Xb[e];
+  }
+  const T* vb = v + un.l * g.vsl + un.h * g.vsh;
   const int my_tok = tid / TPT, sub = tid % TPT;
   for (int t0 = base; t0 < end; t0 += TOK) {
     __syncthreads();
     for (int e = tid; e < TOK * D; e += kThreads) {
       const int tk = e / D, c = e % D;
-      vs[tk][c] = (t0 + tk < end) ? vb[(un.t0 + t0 + tk) * g.vst + c] : 0.0f;
+      vs[tk][c] = (t0 + tk < end) ? to_f32(vb[(un.t0 + t0 + tk) * g.vst + c]) : 0.0f;
     }
     __syncthreads();
     double ss = 0.0;
@@ -214,11 +233,28 @@ hipError_t launch_leverage(const Launch& L, const void* v, float* scores) {
       else go(leverage_mfma_kernel<64, kPolicyStream>);
     }
   } else {
-    const double* l64 = ws_ptr<double>(L.wsp, L.ws.linv64);
-    if (g.D == 128)
-      leverage_precise_kernel<128><<<grid, kThreads, 0, L.stream>>>(g, (const float*)v, wb, l64, uf, scores, L.ws.lchunks);
-    else
-      leverage_precise_kernel<64><<<grid, kThreads, 0, L.stream>>>(g, (const float*)v, wb, l64, uf, scores, L.ws.lchunks);
+    return launch_leverage_precise(L, v, scores);
+  }
+  return hipGetLastError();
+}
+
+// fp64 leverage: every unit of fp32 inputs, or the marked units of bf16 inputs.
+hipError_t launch_leverage_precise(const Launch& L, const void* v, float* scores) {
+  const Geo& g = L.geo;
+  const dim3 grid((unsigned)chunked_grid(g, L.ws.plchunks));
+  const float* wb = ws_ptr<float>(L.wsp, L.ws.wgt);
+  const uint32_t* uf = ws_ptr<uint32_t>(L.wsp, L.ws.uflags);
+  const double* xr = ws_ptr<double>(L.wsp, L.ws.gram_red);
+  const int lchunk = L.ws.mfma ? kLChunkRefine : kLChunkPrecise;
+  auto go = [&](auto kern, auto vv) {
+    kern<<<grid, kThreads, 0, L.stream>>>(g, vv, wb, xr, uf, scores, L.ws.plchunks, lchunk);
+  };
+  if (L.ws.mfma) {
+    if (g.D == 128) go(leverage_precise_kernel<uint16_t, 128, true>, (const uint16_t*)v);
+    else go(leverage_precise_kernel<uint16_t, 64, true>, (const uint16_t*)v);
+  } else {
+    if (g.D == 128) go(leverage_precise_kernel<float, 128, false>, (const float*)v);
+    else go(leverage_precise_kernel<float, 64, false>, (const float*)v);
   }
   return hipGetLastError();
 }

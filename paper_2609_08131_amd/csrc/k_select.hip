@@ -374,24 +374,41 @@ hipError_t launch_select(const Launch& L, const float* scores, int32_t* idx) {
 // ---------------------------------------------------------------------------
 // Evicted slots: the positions of each unit that the selection does not keep,
 // ascending, then -1 up to the list's capacity. The kept positions come
-// ascending from select_kernel; the evicted ones are the gaps between them:
-// the gap before kept entry j (after entry j - 1) holds positions whose rank
-// among the evicted ones is their index minus j. Thread t takes the gaps
-// j = t, t + kThreads, ... (coalesced reads of the kept list).
+// ascending from select_kernel; an evicted position i goes to slot i - r,
+// r = the number of kept positions below i. Workgroup (tile, unit) takes the
+// positions [p0, p0 + kEvTile): two binary searches of the kept list bound the
+// kept positions inside the tile, which are staged in LDS, and each thread
+// places the positions p0 + tid, p0 + tid + kThreads, ... (consecutive
+// threads write consecutive slots between kept positions). The tile also
+// writes the -1 padding of the slots [p0, p0 + kEvTile) at or past n - kept,
+// and the last tile every padding slot beyond.
 // ---------------------------------------------------------------------------
+constexpr int kEvTile = 4096;
+
 __global__ __launch_bounds__(kThreads) void evicted_kernel(Geo g, const int32_t* __restrict__ kept,
                                                            int budget, int32_t* __restrict__ slots,
                                                            int cap) {
-  const int u = blockIdx.x, tid = threadIdx.x;
+  const int u = blockIdx.y, tile = blockIdx.x, tid = threadIdx.x;
   const Unit un = decode_unit(g, u);
   const int n = un.n, kk = min(budget, n), ne = n - kk;
   const int32_t* kp = kept + (int64_t)u * budget;
   int32_t* out = slots + (int64_t)u * cap;
-  for (int j = ne + tid; j < cap; j += kThreads) out[j] = -1;
-  for (int j = tid; j <= kk; j += kThreads) {
-    const int a = j == 0 ? 0 : kp[j - 1] + 1;
-    const int b = j == kk ? n : kp[j];
-    for (int i = max(a, j); i < b && i - j < ne; ++i) out[i - j] = i;  // i - j >= 0 always
+  const int p0 = tile * kEvTile;
+  const int pad_hi = tile == (int)gridDim.x - 1 ? cap : min(cap, p0 + kEvTile);
+  for (int j = max(ne, p0) + tid; j < pad_hi; j += kThreads) out[j] = -1;
+  if (p0 >= n) return;
+  const int p1 = min(n, p0 + kEvTile);
+  __shared__ int32_t ks[kEvTile];
+  __shared__ int bounds[2];
+  if (tid < 2) bounds[tid] = lower_bound_lds(kp, kk, tid == 0 ? p0 : p1);
+  __syncthreads();
+  const int lo = bounds[0], cnt = bounds[1] - bounds[0];  // distinct positions: cnt <= kEvTile
+  for (int j = tid; j < cnt; j += kThreads) ks[j] = kp[lo + j];
+  __syncthreads();
+  for (int i = p0 + tid; i < p1; i += kThreads) {
+    const int r = lower_bound_lds(ks, cnt, i);
+    if (r < cnt && ks[r] == i) continue;  // kept
+    out[i - (lo + r)] = i;                // i - (lo + r) < ne for an evicted i
   }
 }
 
@@ -402,7 +419,8 @@ hipError_t launch_select_evicted(const Launch& L, const float* scores, int32_t* 
     const hipError_t e = launch_select(L, scores, kept);
     if (e != hipSuccess) return e;
   }
-  evicted_kernel<<<L.geo.U, kThreads, 0, L.stream>>>(L.geo, kept, budget, slots, cap);
+  const int tiles = std::max(1, (L.geo.maxn + kEvTile - 1) / kEvTile);
+  evicted_kernel<<<dim3(tiles, L.geo.U), kThreads, 0, L.stream>>>(L.geo, kept, budget, slots, cap);
   return hipGetLastError();
 }
 

@@ -1,16 +1,20 @@
 """Full-size workloads in the benchmark's launch configuration.
 
 Every unit (sequence, layer, KV head) is scored in one jacap_evict call at the
-real shape; sampled units are checked against the fp64 oracle one by one, and
-properties that hold at any size are checked on every unit:
+real shape. For prefill32k (budgets 128 and 2048), long128k (ridge 1 and 0)
+and ragged16 every unit is checked against the fp64 oracle (run in parallel
+worker processes): every score within the bf16 tolerance, jacap_select on the
+oracle's fp32 scores bit-equal to the oracle's selection, the GPU selection
+equal to the select rule on the GPU's own scores, and the overlap of the GPU's
+selection with the oracle's reported. The other full-size runs check sampled
+units against the oracle, plus properties that hold at any size on every unit:
   * ridge > 0: every score lies in [0, 1) (ridge leverage, Eq. 10 with A >= ridge I);
-  * the selection is the select rule applied to the GPU's own scores
-    (checked exactly on the sampled units; on all units: ascending, in range,
-    -1 padding exactly past min(k, n));
+  * the selection is ascending, in range, with -1 padding exactly past min(k, n);
   * K', V' are exact gathers (sampled units).
 """
 
 import gc
+import time
 
 import numpy as np
 import pytest
@@ -21,6 +25,7 @@ from oracle import jacap_oracle as jo
 
 from helpers import (BF16_TOL, gpu_unit_idx, gpu_unit_scores, oracle_unit, overlap, run_gpu,
                      score_errors, token_slice)
+from oracle_pool import oracle_all_units
 
 pytestmark = pytest.mark.gpu
 
@@ -78,16 +83,78 @@ def _check_sampled(case, prob, budget, ridge, label, mode="diag", gqa="pooled"):
           f"overlap with oracle selection {np.round(ovs, 4).tolist()}", flush=True)
 
 
+def _check_every_unit(case, probs, ridge, label, select_budgets):
+    """Every unit against the oracle. probs: {budget: GPU problem after
+    jacap_evict}; the scores do not depend on the budget, so those of the
+    first are compared. For the budgets in select_budgets, jacap_select runs
+    on the oracle's fp32 scores and must reproduce the oracle's selection."""
+    from paper_2609_08131_amd import jacap
+    budgets = list(probs)
+    first = probs[budgets[0]]
+    gsc = first.scores.cpu()
+    gidx = {bud: p.idx.cpu() for bud, p in probs.items()}
+    ref32 = torch.zeros_like(gsc)
+    orc_idx = {}
+    worst, worst_unit, ovs = 0.0, None, {bud: [] for bud in budgets}
+    t0 = time.time()
+    count = 0
+    for (b, l, h, s32, idx, singular) in oracle_all_units(case, budgets=budgets, ridge=ridge):
+        assert not singular, (label, (b, l, h))
+        lo, hi = token_slice(case, b)
+        g = gsc[l, h, lo:hi].double().numpy()
+        ref32[l, h, lo:hi] = torch.from_numpy(s32)
+        # the oracle's fp64 scores rounded once to fp32: within 2^-24 of them
+        err = score_errors(g, s32.astype(np.float64))
+        e = float(err.max()) if err.size else 0.0
+        if e > worst:
+            worst, worst_unit = e, (b, l, h)
+        assert e <= BF16_TOL - 2.0 ** -23, (label, (b, l, h), e, int(err.argmax()))
+        n = hi - lo
+        for bud in budgets:
+            kk = min(bud, n)
+            row = gidx[bud][b, l, h].numpy()
+            assert np.all(row[kk:] == -1)
+            assert np.array_equal(row[:kk], jo.select_top(g.astype(np.float32), bud)), \
+                (label, bud, (b, l, h))
+            ovs[bud].append(overlap(row[:kk], idx[bud]) if kk else 1.0)
+        for bud in select_budgets:
+            orc_idx[(b, l, h, bud)] = idx[bud]
+        count += 1
+    w = case.workload
+    assert count == case.num_seqs * w.num_layers * w.num_kv_heads
+    for bud in select_budgets:
+        p = probs[bud]
+        idx2 = torch.empty_like(p.idx)
+        jacap.select(p.cfg, p.batch, ref32.to(p.scores.device), idx2)
+        torch.cuda.synchronize()
+        idx2 = idx2.cpu()
+        for (b, l, h, bb), o_idx in orc_idx.items():
+            if bb != bud:
+                continue
+            kk = len(o_idx)
+            got = idx2[b, l, h].numpy()
+            assert np.array_equal(got[:kk], o_idx), ("select on oracle scores", label, bud, (b, l, h))
+            assert np.all(got[kk:] == -1)
+    ovtxt = ", ".join(f"k={bud}: min {min(v):.4f} mean {np.mean(v):.4f}" for bud, v in ovs.items())
+    print(f"\n[fullsize] {label} ridge={ridge:g}: all {count} units, worst rel err {worst:.3e} "
+          f"at {worst_unit}; jacap_select on the oracle's scores bit-exact at k in "
+          f"{list(select_budgets)}; overlap of the GPU selection with the oracle's: {ovtxt} "
+          f"(oracle {time.time() - t0:.0f} s)", flush=True)
+
+
 def test_prefill32k_budget_sweep():
     case = make_case("prefill32k", device="cuda")
+    probs = {}
     for budget in case.workload.budget_sweep:
         prob, flags = run_gpu(case, budget, ridge=1.0)
         assert flags == 0
         _check_all_units_properties(case, prob, budget, 1.0)
         if budget in (128, 2048):
-            _check_sampled(case, prob, budget, 1.0, f"prefill32k k={budget}")
-        del prob
-    del case
+            probs[budget] = prob
+        else:
+            del prob
+    _check_every_unit(case, probs, 1.0, "prefill32k", select_budgets=(128, 2048))
+    del probs, case
     _free()
 
 
@@ -98,7 +165,7 @@ def test_long128k(ridge):
     prob, flags = run_gpu(case, budget, ridge=ridge)
     assert flags == 0
     _check_all_units_properties(case, prob, budget, ridge)
-    _check_sampled(case, prob, budget, ridge, "long128k")
+    _check_every_unit(case, {budget: prob}, ridge, "long128k", select_budgets=(budget,))
     del prob, case
     _free()
 
@@ -109,7 +176,7 @@ def test_ragged16():
     prob, flags = run_gpu(case, budget, ridge=1.0)
     assert flags == 0
     _check_all_units_properties(case, prob, budget, 1.0)
-    _check_sampled(case, prob, budget, 1.0, "ragged16")
+    _check_every_unit(case, {budget: prob}, 1.0, "ragged16", select_budgets=(budget,))
     del prob, case
     _free()
 

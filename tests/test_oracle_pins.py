@@ -489,7 +489,7 @@ def test_select_decides_on_fp32():
 # ---------------------------------------------------------------------------
 
 def test_wo_group_projection_matches_full_output_projection():
-    """Sec. 2.1: the layer output is W_O applied to the concatenated per-head
+    """Sec. 3.1 (Preliminary): the layer output is W_O applied to the concatenated per-head
     outputs. When the G heads of a KV group share one attention output y_h,
     that equals sum_h W~_h y_h with W~_h = group_output_projection(...)."""
     rng = np.random.default_rng(11)
