@@ -50,7 +50,8 @@
  *   host pointers read (or written) during the call only.
  * - The caller owns every buffer. The library allocates no memory, keeps no
  *   pointer after returning and holds no global state (apart from the
- *   optional timing records of jacap_timing_*); all work is enqueued
+ *   optional timing records of jacap_timing_* and the static scratch array of
+ *   jacap_evict_noalloc, on each device that call uses); all work is enqueued
  *   asynchronously on `stream` (a hipStream_t; NULL = the null stream).
  *   Calls on different streams are independent if they use distinct
  *   workspaces.
@@ -237,6 +238,28 @@ jacap_status jacap_evict(const jacap_config* cfg, const jacap_batch* batch,
                          const void* q_win, const void* k, const void* v, float* scores,
                          int32_t* idx, void* k_out, void* v_out, void* ws, size_t ws_bytes,
                          void* stream);
+
+/* jacap_evict for callers that cannot allocate device memory -- code under HIP
+ * graph capture, tight serving loops, harnesses that forbid hipMalloc: the
+ * same launch sequence and results, with the library's own workspace instead
+ * of the caller's. That workspace is a static device array of 64 MiB which
+ * every GPU the library runs on holds until the process ends (looked up on
+ * the call's first use of a device; nothing is allocated by any call). It
+ * serves problems whose jacap_workspace_size() is at most 64 MiB (one
+ * Llama-3-8B layer of 8 KV heads x 8192 tokens needs about 6 MiB, one 32-layer
+ * sequence of about 2000 tokens about 55 MiB); larger ones return
+ * JACAP_ERR_WORKSPACE and enqueue nothing. All calls on one GPU share the
+ * array: calls that overlap on one GPU (several streams or host threads)
+ * race, so they must be ordered by the caller. Per-phase timing is never
+ * recorded for this call.
+ *   status : optional (NULL = not written) device uint32, 4-byte aligned: the
+ *            call's sticky flags (enum jacap_flags), written by its last
+ *            kernel; jacap_read_status does not apply to this call.
+ * Other arguments and errors as jacap_evict. */
+jacap_status jacap_evict_noalloc(const jacap_config* cfg, const jacap_batch* batch,
+                                 const void* q_win, const void* k, const void* v, float* scores,
+                                 int32_t* idx, void* k_out, void* v_out, uint32_t* status,
+                                 void* stream);
 
 /* The complement of jacap_select, for caches refilled in place during
  * decoding (the periodic re-eviction of the decoding-stage setting, Sec. 4.3):

@@ -32,7 +32,7 @@ CFLAGS = [
 ]
 
 SOURCES = ["jacap_host.hip", "jacap_timing.hip", "k_stats.hip", "k_gram.hip", "k_factor.hip",
-           "k_leverage.hip", "k_select.hip", "k_greedy.hip"]
+           "k_leverage.hip", "k_select.hip", "k_greedy.hip", "jacap_noalloc.hip"]
 
 
 def _compile(src: str, verbose: bool) -> str:

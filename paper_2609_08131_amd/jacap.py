@@ -96,6 +96,7 @@ def _load() -> ctypes.CDLL:
         "jacap_greedy_workspace_size": [C, B, ctypes.POINTER(sz)],
         "jacap_greedy": [C, B, P, P, P, P, P, P, P, sz, P],
         "jacap_stream_read": [P, sz, P, P],
+        "jacap_evict_noalloc": [C, B, P, P, P, P, P, P, P, P, P],
     }
     for name, args in sigs.items():
         fn = getattr(lib, name)
@@ -117,7 +118,7 @@ EXPORTED = ("jacap_workspace_size", "jacap_score", "jacap_score_from_stats", "ja
             "jacap_compact", "jacap_evict", "jacap_read_status", "jacap_status_string",
             "jacap_timing_start", "jacap_timing_stop", "jacap_phase_name",
             "jacap_greedy_workspace_size", "jacap_greedy", "jacap_stream_read",
-            "jacap_select_evicted", "jacap_evict_slots")
+            "jacap_select_evicted", "jacap_evict_slots", "jacap_evict_noalloc")
 NUM_PHASES = 13   # enum jacap_phase
 
 
@@ -269,6 +270,15 @@ def evict(cfg, batch, q_win, k, v, scores, idx, k_out, v_out, ws, stream=None) -
     _check("jacap_evict", _lib.jacap_evict(
         ctypes.byref(cfg), ctypes.byref(batch), _ptr(q_win), _ptr(k), _ptr(v), _ptr(scores),
         _ptr(idx), _ptr(k_out), _ptr(v_out), _ptr(ws), ws.numel(), _stream(stream)))
+
+
+def evict_noalloc(cfg, batch, q_win, k, v, scores, idx, k_out, v_out, status=None,
+                  stream=None) -> None:
+    """jacap_evict with the library's own scratch memory (no workspace);
+    status: optional int32 device tensor of one element receiving the flags."""
+    _check("jacap_evict_noalloc", _lib.jacap_evict_noalloc(
+        ctypes.byref(cfg), ctypes.byref(batch), _ptr(q_win), _ptr(k), _ptr(v), _ptr(scores),
+        _ptr(idx), _ptr(k_out), _ptr(v_out), _ptr(status), _stream(stream)))
 
 
 def select_evicted(cfg, batch, scores, slots, ws, stream=None) -> None:
