@@ -62,6 +62,10 @@ def parse():
     ap.add_argument("--inplace", action="store_true",
                     help="evicted-slot lists instead of the compacted cache "
                          "(jacap_evict_slots: a decoding round whose cache is refilled in place)")
+    ap.add_argument("--flush", action="store_true",
+                    help="before every step (outside its timed events) read a 1 GiB buffer "
+                         "with the default cache policy, so that inputs smaller than the "
+                         "256 MB MALL are not measured cache-warm")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="first run a plain 1 GiB elementwise copy (torch.neg; the "
                          "reference kernel for scaling rocprofv3 FETCH_SIZE / WRITE_SIZE)")
@@ -69,6 +73,7 @@ def parse():
 
 
 COPY_BYTES = 1 << 30
+FLUSH_BYTES = 1 << 30
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic.json")
 # Source files whose kernels each phase launches (a change voids recorded counters).
 # Source file, kernel (the DIAG bf16 one on long128k) and launch function of
@@ -372,10 +377,14 @@ def main():
     # Timed region: K steps; the library records the dominant phase only.
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
           for _ in range(args.steps)]
+    flush_buf = torch.ones(FLUSH_BYTES // 4, dtype=torch.float32, device="cuda") if args.flush else None
+    flush_sink = torch.zeros((), dtype=torch.float32, device="cuda")
     torch.cuda.synchronize()
     jacap.timing_start([dominant])
     t_wall = time.perf_counter()
     for s, e in ev:
+        if flush_buf is not None:
+            torch.sum(flush_buf, dim=0, out=flush_sink)   # evicts the MALL; outside the events
         s.record(stream)
         run()
         e.record(stream)
@@ -421,6 +430,9 @@ def main():
             "tokens": case.total_tokens, "window": w.window, "budget_k": budget,
             "tau": args.tau, "ridge": args.ridge, "cov_mode": args.cov, "gqa": args.gqa,
             "inplace": args.inplace,
+            "cache": "flushed before every step" if args.flush else (
+                "warm (inputs fit in the 256 MB MALL)" if step_bytes < (256 << 20) else
+                "cold (inputs exceed the MALL)"),
         },
         "roofline": {
             "bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",

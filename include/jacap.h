@@ -246,8 +246,8 @@ jacap_status jacap_evict(const jacap_config* cfg, const jacap_batch* batch,
  * every GPU the library runs on holds until the process ends (looked up on
  * the call's first use of a device; nothing is allocated by any call). It
  * serves problems whose jacap_workspace_size() is at most 64 MiB (one
- * Llama-3-8B layer of 8 KV heads x 8192 tokens needs about 6 MiB, one 32-layer
- * sequence of about 2000 tokens about 55 MiB); larger ones return
+ * Llama-3-8B layer of 8 KV heads x 8192 tokens needs about 20 MiB, 32 layers
+ * of one 1024-token sequence about 50 MiB); larger ones return
  * JACAP_ERR_WORKSPACE and enqueue nothing. All calls on one GPU share the
  * array: calls that overlap on one GPU (several streams or host threads)
  * race, so they must be ordered by the caller. Per-phase timing is never

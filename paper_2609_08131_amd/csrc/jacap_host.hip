@@ -96,8 +96,14 @@ Workspace layout(const jacap_config* c, const jacap_batch* b, bool greedy = fals
   }
   w.gchunks = (maxn + w.gchunk - 1) / w.gchunk;
   w.gparts = 1;
-  const int lchunk = w.mfma ? kLChunkMfma : kLChunkPrecise;
-  w.lchunks = (maxn + lchunk - 1) / lchunk;
+  // Leverage chunks: kLChunkMfma tokens, halved (down to kLChunkMfmaMin) while
+  // the grid would have fewer than kLevMinBlocks blocks.
+  w.lchunk = w.mfma ? kLChunkMfma : kLChunkPrecise;
+  if (w.mfma)
+    while (w.lchunk > kLChunkMfmaMin &&
+           U * (int64_t)((maxn + w.lchunk - 1) / w.lchunk) < kLevMinBlocks)
+      w.lchunk /= 2;
+  w.lchunks = (maxn + w.lchunk - 1) / w.lchunk;
   // The fp64 Gram pass (every unit of fp32 keys; the units of bf16 keys that
   // need it): about kPrecisePartials partials per batch, so that its buffer
   // stays bounded at any unit count, and no chunk below kGChunkPrecise tokens
@@ -110,8 +116,15 @@ Workspace layout(const jacap_config* c, const jacap_batch* b, bool greedy = fals
     w.pchunk = (int)per;
     w.pchunks = maxn > 0 ? (int)((maxn + per - 1) / per) : 0;
   }
-  const int plchunk = w.mfma ? kLChunkRefine : kLChunkPrecise;
-  w.plchunks = (maxn + plchunk - 1) / plchunk;
+  // fp64 leverage chunks: kLChunkRefine tokens for the marked bf16 units;
+  // for fp32 inputs kLChunkPrecise, halved (down to kLChunkPreciseMin) while
+  // the grid would have fewer than kLevMinBlocks blocks.
+  w.plchunk = w.mfma ? kLChunkRefine : kLChunkPrecise;
+  if (!w.mfma)
+    while (w.plchunk > kLChunkPreciseMin &&
+           U * (int64_t)((maxn + w.plchunk - 1) / w.plchunk) < kLevMinBlocks)
+      w.plchunk /= 2;
+  w.plchunks = (maxn + w.plchunk - 1) / w.plchunk;
   const int64_t NB = D / 16;
   const int64_t npair = NB * (NB + 1) / 2;
   const int64_t nlp = (NB / 2) * (NB / 2 + 1);
@@ -229,8 +242,7 @@ jacap_status score_pass(const Launch& L, const void* q, const void* k, const voi
   if (L.ws.mfma) {  // the units marked by the factorisation, again in fp64
     TimedPhase tp(L.stream, JACAP_PHASE_REFINE, L.timed);
     JACAP_TRY(launch_gram(L, v, true));
-    JACAP_TRY(launch_gram_reduce(L, true));
-    JACAP_TRY(launch_factor(L, true));
+    JACAP_TRY(launch_factor(L, true));  // sums the fp64 partials itself
     JACAP_TRY(launch_leverage_precise(L, v, scores));
   }
   JACAP_PHASE(JACAP_PHASE_LEVERAGE, launch_leverage(L, v, scores));

@@ -15,14 +15,17 @@ namespace jacap {
 constexpr int kThreads = 256;        // 4 wave64 per workgroup
 constexpr int kKChunk = 1024;        // tokens per workgroup in the K pass
 constexpr int kFullMaxQ = 256;       // window queries the FULL-covariance MFMA K pass stages
-constexpr int kGChunkMfma = 4096;    // tokens per workgroup in the MFMA Gram pass: at least
+constexpr int kGChunkMfma = 512;     // tokens per workgroup in the MFMA Gram pass: at least
 constexpr int kGChunkMfmaMax = 16384; // ... and at most (larger chunks: fewer partial Grams)
 constexpr int kGramMinBlocks = 2048;  // chunks are as large as this many blocks in the grid allow
 constexpr int kGramSpan = 128;       // tokens between two flushes of the Gram's short fp32 chains
-constexpr int kGChunkPrecise = 1024; // tokens per workgroup in the fp64 Gram pass: at least
+constexpr int kGChunkPrecise = 128;  // tokens per workgroup in the fp64 Gram pass: at least
 constexpr int kPrecisePartials = 256;  // fp64 Gram partials per batch the chunking aims at
-constexpr int kLChunkMfma = 4096;    // tokens per workgroup in the MFMA leverage pass
-constexpr int kLChunkPrecise = 1024; // tokens per workgroup in the fp64 leverage pass (fp32 keys)
+constexpr int kLChunkMfma = 4096;    // tokens per workgroup in the MFMA leverage pass: at most
+constexpr int kLChunkMfmaMin = 256;  // ... and at least (batches too small to fill the chip)
+constexpr int kLevMinBlocks = 2048;  // leverage chunks shrink until the grid has this many blocks
+constexpr int kLChunkPrecise = 1024; // tokens per workgroup in the fp64 leverage pass (fp32 keys):
+constexpr int kLChunkPreciseMin = 64; // ... at most, and at least (small batches)
 constexpr int kLChunkRefine = 4096;  // ... and over the bf16 units that take the fp64 path
 constexpr int kWChunk = 4096;        // tokens per workgroup in the weight pass
 // The K pass sums a chunk's exp(z - max) terms (all but the max's own) as
@@ -102,8 +105,9 @@ __device__ __forceinline__ int64_t token_row(const Geo& g, const Unit& un) {
 // time, and every read after the first hits that XCD's L2. False for the
 // padding past the last pair.
 template <bool CHUNK_MAJOR>
-__device__ __forceinline__ bool grid_unit_chunk(const Geo& g, int nchunks, int& u, int& chunk) {
-  int p = blockIdx.x, s = 0;
+__device__ __forceinline__ bool grid_unit_chunk_at(const Geo& g, int nchunks, int p, int& u,
+                                                   int& chunk) {
+  int s = 0;
   if (g.V > 1) {
     const int r = p % (8 * g.V);
     s = r >> 3;
@@ -121,6 +125,17 @@ __device__ __forceinline__ bool grid_unit_chunk(const Geo& g, int nchunks, int& 
   u = uk * g.V + s;
   return uk < nk && chunk < nchunks;
 }
+
+template <bool CHUNK_MAJOR>
+__device__ __forceinline__ bool grid_unit_chunk(const Geo& g, int nchunks, int& u, int& chunk) {
+  return grid_unit_chunk_at<CHUNK_MAJOR>(g, nchunks, blockIdx.x, u, chunk);
+}
+
+// Workgroups of the kernels that serve only the units marked for the fp64 path
+// (usually none or few): they walk the (unit, chunk) items in a grid-stride
+// loop and skip unmarked units, so a launch costs a few microseconds however
+// many units and chunks the batch has.
+constexpr int kRefineBlocks = 512;
 
 inline int64_t chunked_grid(const Geo& g, int nchunks) {
   const int64_t pairs = (int64_t)nchunks * (g.U / g.V);
@@ -154,9 +169,9 @@ struct Workspace {
   size_t gst;      // int32  [L][H][T]       greedy: picks made at that time (-1 = taken)
   size_t gent;     // GreedyEntry [U][ceil(maxn / 256)]  greedy: best of each 256-position block
   size_t total;
-  int kchunks, wchunks, gchunks, gchunk, gparts, lchunks;
+  int kchunks, wchunks, gchunks, gchunk, gparts, lchunks, lchunk;
   int pchunks, pchunk;  // chunks of the fp64 Gram pass
-  int plchunks;         // chunks of the fp64 leverage pass
+  int plchunks, plchunk;  // chunks of the fp64 leverage pass
   bool mfma;       // bf16 path (MFMA Gram and leverage)
 };
 

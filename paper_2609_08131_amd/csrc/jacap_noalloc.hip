@@ -20,8 +20,8 @@ namespace jacap {
 namespace {
 
 // Largest workspace the entry point serves (see jacap_workspace_size): one
-// Llama-3-8B layer of 8 KV heads x 8192 tokens needs about 6 MiB, one 32-layer
-// sequence of about 2000 tokens about 55 MiB.
+// Llama-3-8B layer of 8 KV heads x 8192 tokens needs about 20 MiB, 32 layers
+// of one 1024-token sequence about 50 MiB.
 constexpr size_t kScratchBytes = size_t(64) << 20;
 constexpr int kMaxDevices = 64;
 

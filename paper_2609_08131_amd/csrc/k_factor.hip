@@ -26,20 +26,23 @@
 //   Inverse X = L^{-1}:
 //     4. the diagonal 16x16 blocks are inverted independently (one column per
 //        lane);
-//     5. recursive doubling: for blocks of h = 16, 32, 64 rows, each pair
-//        [L11 0; L21 L22] gets X21 = -X22 L21 X11 from the halves' inverses
-//        (two triangular products, 4x4 register tiles).
-// LDS holds A (pitch D + 1) with L in its lower triangle; X replaces L there
-// block by block as each part of L is consumed. The upper triangle holds
-// temporaries.
+//     5. block columns J from right to left: X_IJ = -(sum_{M > J} X_IM L_MJ)
+//        X_JJ for every I > J at once (16x16 products on the fp64 MFMA).
+// LDS holds only the lower 16x16 blocks of A (about 78 KB at d = 128, so two
+// workgroups share a compute unit); L replaces A and X replaces L there,
+// block by block as each part is consumed.
+#include <algorithm>
+
 #include "jacap_internal.hpp"
 
 namespace jacap {
 
-// cond(A) bound above which the bf16 path recomputes the unit in fp64: the
+// Bound on cond(A) above which the bf16 path recomputes the unit in fp64: the
 // fp32-accumulated two-term Gram and the two-term L^{-1} products carry errors
-// that A^{-1} amplifies by up to cond(A) (~1e-8 cond(A) in the scores).
-constexpr double kRefineCond = 2e3;
+// that A^{-1} amplifies by up to cond(A) (~1e-8 cond(A) in the scores, so at
+// most ~2e-4 below the threshold; the bound itself can exceed cond(A) by one
+// or two orders of magnitude).
+constexpr double kRefineCond = 2e4;
 // Smallest pivot, relative to its diagonal entry, taken as positive. On the
 // fp32-accumulated Gram a smaller one sends the unit to the fp64 path. On an
 // fp64 Gram it means A is numerically singular at the score tolerance: a
@@ -73,6 +76,18 @@ __device__ __forceinline__ double rsqrt_f64(double x) {
 
 typedef double f64x4 __attribute__((ext_vector_type(4)));
 
+// LDS layout of A (and of L, then X = L^{-1}, which replace it): only the
+// lower 16x16 blocks (I >= J), packed by rows of blocks; block (I, J) starts
+// at (I (I + 1) / 2 + J) * kBlk and holds element (r, c) at r * kBP + c. The
+// pitch of 17 doubles puts the 16 rows of a block column in distinct banks.
+// Diagonal blocks are stored whole (their upper halves serve as scratch).
+constexpr int kBP = 17;
+constexpr int kBlk = 16 * kBP;
+__device__ __forceinline__ int lidx(int row, int col) {
+  const int I = row >> 4, J = col >> 4;
+  return (I * (I + 1) / 2 + J) * kBlk + (row & 15) * kBP + (col & 15);
+}
+
 // D += A B on the fp64 MFMA (16x16x4): lane l supplies A[l % 16][l / 16] and
 // B[l / 16][l % 16]; element i of lane l's result is D[4 i + l / 16][l % 16].
 __device__ __forceinline__ f64x4 mfma64(double a, double b, f64x4 acc) {
@@ -88,20 +103,20 @@ __device__ __forceinline__ void tri_index(int e, int& i, int& j) {
   j = e - r * (r + 1) / 2;
 }
 
-// PASS 0: first factorisation (all units). PASS 1: the units marked
-// kUnitRefine by pass 0 (bf16 path), from their fp64 Gram. FRAGS: bf16 inputs.
+// One unit. PASS 0: first factorisation (all units), from the reduced Gram
+// `red`. PASS 1: a unit marked kUnitRefine by pass 0 (bf16 path), from its fp64
+// partial Grams `part` (pchunks per unit), summed here in chunk order. FRAGS:
+// bf16 inputs.
 template <int D, bool FRAGS>
-__global__ __launch_bounds__(kFactorThreads) void factor_kernel(Geo g, double* __restrict__ red,
-                                                          double ridge,
-                                                          const double* __restrict__ wscale,
-                                                          int pass,
-                                                          uint16_t* __restrict__ lfrag,
-                                                          uint32_t* status, uint32_t* uflags) {
-  constexpr int LD = D + 1;
+__device__ __forceinline__ void factor_unit(const Geo& g, int u, double* __restrict__ red,
+                                            const double* __restrict__ part, int pchunks,
+                                            int pchunk, double ridge,
+                                            const double* __restrict__ wscale, int pass,
+                                            uint16_t* __restrict__ lfrag, uint32_t* status,
+                                            uint32_t* uflags) {
   constexpr int NB = D / 16;
   constexpr int NPAIR = NB * (NB + 1) / 2;
-  const int u = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  if (pass == 1 && !(uflags[u] & kUnitRefine)) return;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const Unit un = decode_unit(g, u);
   if (un.n == 0) return;
   // The fp32-accumulated Gram of bf16 inputs may be redone in fp64 later;
@@ -110,7 +125,7 @@ __global__ __launch_bounds__(kFactorThreads) void factor_kernel(Geo g, double* _
   const double piv_rel =
       may_refine ? kPivRelRefine : (FRAGS ? kPivRelSingularBf16 : kPivRelSingularFp32);
 
-  __shared__ double A[D * LD];
+  __shared__ double A[NB * (NB + 1) / 2 * kBlk];  // lower 16x16 blocks, see lidx
   __shared__ double dg[D];   // diagonal of A before factorisation
   __shared__ double idg[D];  // 1 / L_rr
   __shared__ double red_sh[kFactorThreads / 64];
@@ -123,10 +138,28 @@ __global__ __launch_bounds__(kFactorThreads) void factor_kernel(Geo g, double* _
   constexpr int NE2 = NPAIR * 128;  // entry pairs
   constexpr int PER = (NE2 + kFactorThreads - 1) / kFactorThreads;
   double2 rv[PER];
+  if (part == nullptr) {
 #pragma unroll
-  for (int k = 0; k < PER; ++k) {
-    const int e2 = tid + k * kFactorThreads;
-    if (e2 < NE2) rv[k] = reinterpret_cast<const double2*>(R)[e2];
+    for (int k = 0; k < PER; ++k) {
+      const int e2 = tid + k * kFactorThreads;
+      if (e2 < NE2) rv[k] = reinterpret_cast<const double2*>(R)[e2];
+    }
+  } else {  // fixed-order sum of the unit's fp64 partials
+    const int nch = (un.n + pchunk - 1) / pchunk;
+    const double2* P = reinterpret_cast<const double2*>(part + (int64_t)u * pchunks * (NPAIR * 256));
+#pragma unroll
+    for (int k = 0; k < PER; ++k) rv[k] = make_double2(0.0, 0.0);
+    for (int c = 0; c < nch; ++c) {
+#pragma unroll
+      for (int k = 0; k < PER; ++k) {
+        const int e2 = tid + k * kFactorThreads;
+        if (e2 < NE2) {
+          const double2 x = P[(int64_t)c * NE2 + e2];
+          rv[k].x += x.x;
+          rv[k].y += x.y;
+        }
+      }
+    }
   }
 #pragma unroll
   for (int k = 0; k < PER; ++k) {
@@ -141,8 +174,8 @@ __global__ __launch_bounds__(kFactorThreads) void factor_kernel(Geo g, double* _
       const int ln = (e & 255) / 4, r = e % 4;  // r even: entries r and r + 1 of lane ln
       const int row = bi * 16 + (ln >> 4) * 4 + r;
       const int col = bj * 16 + (ln & 15);
-      if (row <= col) A[col * LD + row] = rv[k].x;  // diagonal block: upper half only
-      if (row + 1 <= col) A[col * LD + row + 1] = rv[k].y;
+      if (row <= col) A[lidx(col, row)] = rv[k].x;  // diagonal block: upper half only
+      if (row + 1 <= col) A[lidx(col, row + 1)] = rv[k].y;
     }
   }
   if (tid == 0) bad = 0;
@@ -155,13 +188,13 @@ __global__ __launch_bounds__(kFactorThreads) void factor_kernel(Geo g, double* _
     const double* Rm = g.ridge_mat + ((int64_t)un.l * g.H + un.h) * D * D;
     for (int e = tid; e < D * D; e += kFactorThreads) {
       const int r = e / D, cc = e % D;
-      if (cc <= r) A[r * LD + cc] += Rm[e] * sc;
+      if (cc <= r) A[lidx(r, cc)] += Rm[e] * sc;
     }
     __syncthreads();
   }
   for (int a = tid; a < D; a += kFactorThreads) {
-    if (!g.ridge_mat) A[a * LD + a] += ridge * sc;
-    dg[a] = A[a * LD + a];
+    if (!g.ridge_mat) A[lidx(a, a)] += ridge * sc;
+    dg[a] = A[lidx(a, a)];
     if (!isfinite(dg[a])) atomicOr(&bad, (int)kUnitNonfinite);
   }
   __syncthreads();
@@ -184,10 +217,11 @@ __global__ __launch_bounds__(kFactorThreads) void factor_kernel(Geo g, double* _
     for (int w = 1; w < kFactorThreads / 64; ++w) m = fmax(m, red_sh[w]);
     return m;
   };
+
   double anorm = 0.0;
   if (may_refine) {
     double sr = 0.0;
-    for (int b = ppart; b < D; b += TPR) sr += fabs((b <= prow) ? A[prow * LD + b] : A[b * LD + prow]);
+    for (int b = ppart; b < D; b += TPR) sr += fabs((b <= prow) ? A[lidx(prow, b)] : A[lidx(b, prow)]);
 #pragma unroll
     for (int o = 1; o < TPR; o <<= 1) sr += __shfl_xor(sr, o);
     anorm = block_max(sr);
@@ -201,7 +235,7 @@ __global__ __launch_bounds__(kFactorThreads) void factor_kernel(Geo g, double* _
       const int s = lane & 15;
       double a[16];
 #pragma unroll
-      for (int q = 0; q < 16; ++q) a[q] = (q <= s) ? A[(c + s) * LD + c + q] : 0.0;
+      for (int q = 0; q < 16; ++q) a[q] = (q <= s) ? A[lidx((c + s), c + q)] : 0.0;
       // No early exit (the loop must stay fully unrolled so that a[] lives in
       // registers): after a failed pivot the rest is computed on a stand-in
       // pivot and discarded.
@@ -267,7 +301,7 @@ __global__ __launch_bounds__(kFactorThreads) void factor_kernel(Geo g, double* _
       } else if (lane < 16) {
 #pragma unroll
         for (int q = 0; q < 16; ++q)
-          if (q <= s) A[(c + s) * LD + c + q] = a[q];
+          if (q <= s) A[lidx((c + s), c + q)] = a[q];
       }
     }
     __syncthreads();
@@ -282,18 +316,18 @@ __global__ __launch_bounds__(kFactorThreads) void factor_kernel(Geo g, double* _
     for (int r = c + 16 + tid; r < D; r += kFactorThreads) {
       double x[16];
 #pragma unroll
-      for (int t = 0; t < 16; ++t) x[t] = A[r * LD + c + t];
+      for (int t = 0; t < 16; ++t) x[t] = A[lidx(r, c + t)];
 #pragma unroll
       for (int t = 0; t < 16; ++t) {
         // x[t] = (A[r][c+t] - sum_q x[q] L[c+t][c+q]) / L[c+t][c+t]; the sum in
         // four independent chains (latency, not order, bounds this loop)
         double sp[4] = {x[t], 0.0, 0.0, 0.0};
 #pragma unroll
-        for (int q = 0; q < t; ++q) sp[q & 3] = fma(-x[q], A[(c + t) * LD + c + q], sp[q & 3]);
+        for (int q = 0; q < t; ++q) sp[q & 3] = fma(-x[q], A[lidx((c + t), c + q)], sp[q & 3]);
         x[t] = ((sp[0] + sp[1]) + (sp[2] + sp[3])) * idg[c + t];
       }
 #pragma unroll
-      for (int t = 0; t < 16; ++t) A[r * LD + c + t] = x[t];
+      for (int t = 0; t < 16; ++t) A[lidx(r, c + t)] = x[t];
     }
     __syncthreads();
     // 3. Trailing update A_IJ -= L_Ik L_Jk^T for the 16x16 blocks I >= J > k,
@@ -311,10 +345,10 @@ __global__ __launch_bounds__(kFactorThreads) void factor_kernel(Geo g, double* _
 #pragma unroll
         for (int kq = 0; kq < 4; ++kq) {
           const int t = c + 4 * kq + q4;
-          acc = mfma64(A[(I + r16) * LD + t], A[(J + r16) * LD + t], acc);
+          acc = mfma64(A[lidx((I + r16), t)], A[lidx((J + r16), t)], acc);
         }
 #pragma unroll
-        for (int i = 0; i < 4; ++i) A[(I + 4 * i + q4) * LD + J + r16] -= acc[i];
+        for (int i = 0; i < 4; ++i) A[lidx((I + 4 * i + q4), J + r16)] -= acc[i];
       }
     }
     __syncthreads();
@@ -332,66 +366,88 @@ __global__ __launch_bounds__(kFactorThreads) void factor_kernel(Geo g, double* _
     for (int i = 0; i < 16; ++i) {
       double sum = 0.0;
 #pragma unroll
-      for (int q = 0; q < i; ++q) sum += A[(c + i) * LD + c + q] * x[q];
+      for (int q = 0; q < i; ++q) sum += A[lidx((c + i), c + q)] * x[q];
       x[i] = i < t ? 0.0 : (i == t ? idg[c + i] : -idg[c + i] * sum);
     }
 #pragma unroll
     for (int i = 1; i < 16; ++i)
-      if (i > t) A[(c + t) * LD + c + i] = x[i];
+      if (i > t) A[lidx((c + t), c + i)] = x[i];
   }
   __syncthreads();
   for (int e = tid; e < NB * 256; e += kFactorThreads) {
     const int c = 16 * (e >> 8), i = (e >> 4) & 15, t = e & 15;
-    if (i > t) A[(c + i) * LD + c + t] = A[(c + t) * LD + c + i];
-    else if (i == t) A[(c + i) * LD + c + i] = idg[c + i];
+    if (i > t) A[lidx((c + i), c + t)] = A[lidx((c + t), c + i)];
+    else if (i == t) A[lidx((c + i), c + i)] = idg[c + i];
   }
   __syncthreads();
-  // 5. Recursive doubling. Pair at offset o, halves of h rows:
-  //    T = X22 L21 (into the pair's upper off-diagonal block, free), then
-  //    X21 = -T X11 (over L21). 16x16 output blocks, one per wave at a time,
-  //    on the fp64 MFMA; the triangular operands are masked to zero above
-  //    their diagonal.
+  // 5. Off-diagonal blocks of X, block column J from right to left, in place:
+  //    X_IJ = -(sum_{M=J+1..I} X_IM L_MJ) X_JJ for I > J ((X L)_IJ = 0), where
+  //    the blocks X_IM (M > J) are final and L_MJ still in place. One 16x16
+  //    output block per wave on the fp64 MFMA; each product is held in
+  //    registers until every wave has read its operands, then stored over
+  //    L_IJ. The triangular X blocks are masked above their diagonal (their
+  //    upper halves hold the temporaries of step 4).
   {
     const int r16 = lane & 15, q4 = lane >> 4;
-    for (int h = 16; h < D; h *= 2) {
-      const int hb = h / 16, nout = (D / (2 * h)) * hb * hb;
-      for (int e = wave; e < nout; e += kFactorThreads / 64) {
-        const int o = (e / (hb * hb)) * 2 * h, ab = (e % (hb * hb)) / hb, bb = e % hb;
-        f64x4 acc = {0.0, 0.0, 0.0, 0.0};
-        for (int mb = 0; mb <= ab; ++mb) {  // X22 block (ab, mb) is zero for mb > ab
+    constexpr int NW = kFactorThreads / 64;
+    constexpr int PW = (NB - 1 + NW - 1) / NW;  // output blocks per wave, at most
+    for (int J = NB - 2; J >= 0; --J) {
+      // output blocks I = J + 1 + wave + NW p, p < PW
+      f64x4 acc[PW];
 #pragma unroll
-          for (int kq = 0; kq < 4; ++kq) {
-            const int t = 4 * kq + q4;
-            const double x = (mb < ab || r16 >= t) ? A[(o + h + 16 * ab + r16) * LD + o + h + 16 * mb + t] : 0.0;
-            const double l = A[(o + h + 16 * mb + t) * LD + o + 16 * bb + r16];
-            acc = mfma64(x, l, acc);
+      for (int p = 0; p < PW; ++p) {
+        acc[p] = f64x4{0.0, 0.0, 0.0, 0.0};
+        const int I = J + 1 + wave + NW * p;
+        if (I < NB) {
+          for (int M = J + 1; M <= I; ++M) {
+#pragma unroll
+            for (int kq = 0; kq < 4; ++kq) {
+              const int t = 4 * kq + q4;
+              const double x = (M < I || r16 >= t) ? A[lidx(16 * I + r16, 16 * M + t)] : 0.0;
+              const double l = A[lidx(16 * M + t, 16 * J + r16)];
+              acc[p] = mfma64(x, l, acc[p]);
+            }
           }
         }
-#pragma unroll
-        for (int i = 0; i < 4; ++i)  // T[a][b] at A[o + b][o + h + a]
-          A[(o + 16 * bb + r16) * LD + o + h + 16 * ab + 4 * i + q4] = acc[i];
       }
       __syncthreads();
-      for (int e = wave; e < nout; e += kFactorThreads / 64) {
-        const int o = (e / (hb * hb)) * 2 * h, ab = (e % (hb * hb)) / hb, bb = e % hb;
-        f64x4 acc = {0.0, 0.0, 0.0, 0.0};
-        for (int mb = bb; mb < hb; ++mb) {  // X11 block (mb, bb) is zero for mb < bb
+#pragma unroll
+      for (int p = 0; p < PW; ++p) {
+        const int I = J + 1 + wave + NW * p;
+        if (I < NB) {
+#pragma unroll
+          for (int i = 0; i < 4; ++i) A[lidx(16 * I + 4 * i + q4, 16 * J + r16)] = acc[p][i];
+        }
+      }
+      __syncthreads();
+#pragma unroll
+      for (int p = 0; p < PW; ++p) {
+        acc[p] = f64x4{0.0, 0.0, 0.0, 0.0};
+        const int I = J + 1 + wave + NW * p;
+        if (I < NB) {
 #pragma unroll
           for (int kq = 0; kq < 4; ++kq) {
             const int t = 4 * kq + q4;
-            const double tv = A[(o + 16 * mb + t) * LD + o + h + 16 * ab + r16];  // T[a][m]
-            const double x = (mb > bb || t >= r16) ? A[(o + 16 * mb + t) * LD + o + 16 * bb + r16] : 0.0;
-            acc = mfma64(tv, x, acc);
+            const double tv = A[lidx(16 * I + r16, 16 * J + t)];
+            const double x = t >= r16 ? A[lidx(16 * J + t, 16 * J + r16)] : 0.0;
+            acc[p] = mfma64(tv, x, acc[p]);
           }
         }
+      }
+      __syncthreads();
 #pragma unroll
-        for (int i = 0; i < 4; ++i) A[(o + h + 16 * ab + 4 * i + q4) * LD + o + 16 * bb + r16] = -acc[i];
+      for (int p = 0; p < PW; ++p) {
+        const int I = J + 1 + wave + NW * p;
+        if (I < NB) {
+#pragma unroll
+          for (int i = 0; i < 4; ++i) A[lidx(16 * I + 4 * i + q4, 16 * J + r16)] = -acc[p][i];
+        }
       }
       __syncthreads();
     }
   }
   // X[r][c] (zero above the diagonal).
-  auto xat = [&](int r, int cc) -> double { return r >= cc ? A[r * LD + cc] : 0.0; };
+  auto xat = [&](int r, int cc) -> double { return r >= cc ? A[lidx(r, cc)] : 0.0; };
 
   auto xinv = xat;
 
@@ -460,6 +516,21 @@ __global__ __launch_bounds__(kFactorThreads) void factor_kernel(Geo g, double* _
   }
 }
 
+// PASS 0: one workgroup per unit. PASS 1: a grid-stride walk over the units
+// that skips those not marked kUnitRefine.
+template <int D, bool FRAGS>
+__global__ __launch_bounds__(kFactorThreads) void factor_kernel(
+    Geo g, double* __restrict__ red, const double* __restrict__ part, int pchunks, int pchunk,
+    double ridge, const double* __restrict__ wscale, int pass, uint16_t* __restrict__ lfrag,
+    uint32_t* status, uint32_t* uflags) {
+  for (int u = blockIdx.x; u < g.U; u += gridDim.x) {
+    if (pass == 1 && !(uflags[u] & kUnitRefine)) continue;
+    factor_unit<D, FRAGS>(g, u, red, pass == 1 ? part : nullptr, pchunks, pchunk,
+                                          ridge, wscale, pass, lfrag, status, uflags);
+    __syncthreads();  // LDS of this unit fully consumed before the next one's loads
+  }
+}
+
 hipError_t launch_factor(const Launch& L, bool refine) {
   if (refine && !L.ws.mfma) return hipSuccess;
   const int pass = refine ? 1 : 0;
@@ -470,12 +541,18 @@ hipError_t launch_factor(const Launch& L, bool refine) {
   uint32_t* uf = ws_ptr<uint32_t>(L.wsp, L.ws.uflags);
   const double* wsc = ws_ptr<double>(L.wsp, L.ws.wscale);
   const double ridge = (double)L.cfg->ridge;
+  const double* part = ws_ptr<double>(L.wsp, L.ws.gram);
+  const int blocks = refine ? std::min(g.U, kRefineBlocks) : g.U;
+  auto go = [&](auto kern) {
+    kern<<<blocks, kFactorThreads, 0, L.stream>>>(g, red, part, L.ws.pchunks, L.ws.pchunk, ridge,
+                                                  wsc, pass, lf, st, uf);
+  };
   if (L.ws.mfma) {
-    if (g.D == 128) factor_kernel<128, true><<<g.U, kFactorThreads, 0, L.stream>>>(g, red, ridge, wsc, pass, lf, st, uf);
-    else factor_kernel<64, true><<<g.U, kFactorThreads, 0, L.stream>>>(g, red, ridge, wsc, pass, lf, st, uf);
+    if (g.D == 128) go(factor_kernel<128, true>);
+    else go(factor_kernel<64, true>);
   } else {
-    if (g.D == 128) factor_kernel<128, false><<<g.U, kFactorThreads, 0, L.stream>>>(g, red, ridge, wsc, pass, lf, st, uf);
-    else factor_kernel<64, false><<<g.U, kFactorThreads, 0, L.stream>>>(g, red, ridge, wsc, pass, lf, st, uf);
+    if (g.D == 128) go(factor_kernel<128, false>);
+    else go(factor_kernel<64, false>);
   }
   return hipGetLastError();
 }

@@ -17,6 +17,8 @@
 // VALU accumulation of exact products (register tiles), same partial layout.
 #include <type_traits>
 
+#include <algorithm>
+
 #include "jacap_internal.hpp"
 
 namespace jacap {
@@ -315,19 +317,22 @@ __global__ __launch_bounds__(kThreads, 2) void gram_mfma_kernel(
 template <typename T, int D, bool REFINE_ONLY>
 __global__ __launch_bounds__(kThreads) void gram_precise_kernel(
     Geo g, const T* __restrict__ v, const float* __restrict__ wbuf,
-    const uint32_t* __restrict__ uflags, double* __restrict__ partials, int pchunks, int pchunk) {
+    const uint32_t* __restrict__ uflags, double* __restrict__ partials, int pchunks, int pchunk,
+    int items) {
   constexpr int R = D / 16;
   constexpr int NB = D / 16;
   constexpr int NPAIR = NB * (NB + 1) / 2;
-  int u, chunk;
-  if (!grid_unit_chunk<true>(g, pchunks, u, chunk)) return;
-  if (REFINE_ONLY && !(uflags[u] & kUnitRefine)) return;
-  const Unit un = decode_unit(g, u);
-  const int base = chunk * pchunk;
-  if (base >= un.n) return;
-  const int tid = threadIdx.x, ty = tid / 16, tx = tid % 16;
   __shared__ float vs[32][D];
   __shared__ double ws[32];
+  // one (unit, chunk) item per workgroup, or (REFINE_ONLY) a grid-stride walk
+  for (int item = blockIdx.x; item < items; item += gridDim.x) {
+  int u, chunk;
+  if (!grid_unit_chunk_at<true>(g, pchunks, item, u, chunk)) continue;
+  if (REFINE_ONLY && !(uflags[u] & kUnitRefine)) continue;
+  const Unit un = decode_unit(g, u);
+  const int base = chunk * pchunk;
+  if (base >= un.n) continue;
+  const int tid = threadIdx.x, ty = tid / 16, tx = tid % 16;
   const T* vb = v + un.l * g.vsl + un.h * g.vsh;
   const int64_t trow = token_row(g, un);
   const int end = min(un.n, base + pchunk);
@@ -372,6 +377,8 @@ __global__ __launch_bounds__(kThreads) void gram_precise_kernel(
       const int ln = ((row % 16) / 4) * 16 + (col % 16);
       out[p * 256 + ln * 4 + (row % 4)] = acc[a][b];
     }
+  __syncthreads();  // the staged tokens of this item are read before the next item's
+  }
 }
 
 hipError_t launch_gram(const Launch& L, const void* v, bool refine) {
@@ -396,10 +403,12 @@ hipError_t launch_gram(const Launch& L, const void* v, bool refine) {
   }
   if (!L.ws.mfma && refine) return hipSuccess;
   // fp64: all units of fp32 inputs, or the marked units of bf16 inputs
-  const dim3 grid((unsigned)chunked_grid(g, L.ws.pchunks));
+  const int64_t items = chunked_grid(g, L.ws.pchunks);
+  const dim3 grid((unsigned)(L.ws.mfma ? std::min<int64_t>(items, kRefineBlocks) : items));
   double* part = ws_ptr<double>(L.wsp, L.ws.gram);
   auto go = [&](auto kern, auto vv) {
-    kern<<<grid, kThreads, 0, L.stream>>>(g, vv, wb, uf, part, L.ws.pchunks, L.ws.pchunk);
+    kern<<<grid, kThreads, 0, L.stream>>>(g, vv, wb, uf, part, L.ws.pchunks, L.ws.pchunk,
+                                          (int)items);
   };
   if (L.ws.mfma) {
     if (g.D == 128) go(gram_precise_kernel<uint16_t, 128, true>, (const uint16_t*)v);
@@ -418,12 +427,10 @@ hipError_t launch_gram(const Launch& L, const void* v, bool refine) {
 template <typename P, int D>
 __global__ __launch_bounds__(kThreads) void gram_reduce_kernel(Geo g, const P* __restrict__ partials,
                                                                int gchunks, int gchunk,
-                                                               const uint32_t* __restrict__ uflags,
-                                                               int refine, double* __restrict__ red) {
+                                                               double* __restrict__ red) {
   constexpr int NB = D / 16;
   constexpr int NPAIR = NB * (NB + 1) / 2;
   const int u = blockIdx.x, p = blockIdx.y;
-  if (refine && !(uflags[u] & kUnitRefine)) return;
   const Unit un = decode_unit(g, u);
   const int nch = (un.n + gchunk - 1) / gchunk;
   const P* src = partials + (int64_t)u * gchunks * (NPAIR * 256) + p * 256 + threadIdx.x;
@@ -433,22 +440,22 @@ __global__ __launch_bounds__(kThreads) void gram_reduce_kernel(Geo g, const P* _
   red[(int64_t)u * (NPAIR * 256) + p * 256 + threadIdx.x] = s;
 }
 
+// refine: nothing to launch (the fp64 path's second factorisation sums its
+// own partials).
 hipError_t launch_gram_reduce(const Launch& L, bool refine) {
   const Geo& g = L.geo;
-  if (refine && !L.ws.mfma) return hipSuccess;
-  const uint32_t* uf = ws_ptr<uint32_t>(L.wsp, L.ws.uflags);
-  const int rf = refine ? 1 : 0;
+  if (refine) return hipSuccess;
   const int NB = g.D / 16, npair = NB * (NB + 1) / 2;
   const dim3 grid(g.U, npair);
   double* red = ws_ptr<double>(L.wsp, L.ws.gram_red);
-  if (L.ws.mfma && !refine) {
+  if (L.ws.mfma) {
     const float* part = ws_ptr<float>(L.wsp, L.ws.gram);
-    if (g.D == 128) gram_reduce_kernel<float, 128><<<grid, kThreads, 0, L.stream>>>(g, part, L.ws.gchunks, L.ws.gchunk, uf, rf, red);
-    else gram_reduce_kernel<float, 64><<<grid, kThreads, 0, L.stream>>>(g, part, L.ws.gchunks, L.ws.gchunk, uf, rf, red);
+    if (g.D == 128) gram_reduce_kernel<float, 128><<<grid, kThreads, 0, L.stream>>>(g, part, L.ws.gchunks, L.ws.gchunk, red);
+    else gram_reduce_kernel<float, 64><<<grid, kThreads, 0, L.stream>>>(g, part, L.ws.gchunks, L.ws.gchunk, red);
   } else {  // fp64 partials
     const double* part = ws_ptr<double>(L.wsp, L.ws.gram);
-    if (g.D == 128) gram_reduce_kernel<double, 128><<<grid, kThreads, 0, L.stream>>>(g, part, L.ws.pchunks, L.ws.pchunk, uf, rf, red);
-    else gram_reduce_kernel<double, 64><<<grid, kThreads, 0, L.stream>>>(g, part, L.ws.pchunks, L.ws.pchunk, uf, rf, red);
+    if (g.D == 128) gram_reduce_kernel<double, 128><<<grid, kThreads, 0, L.stream>>>(g, part, L.ws.pchunks, L.ws.pchunk, red);
+    else gram_reduce_kernel<double, 64><<<grid, kThreads, 0, L.stream>>>(g, part, L.ws.pchunks, L.ws.pchunk, red);
   }
   return hipGetLastError();
 }

@@ -11,6 +11,8 @@
 // fp64 pass (every unit of fp32 inputs; the units of bf16 inputs that the
 // factorisation sent to the fp64 path): fp64 VALU, L^{-1} in LDS, 8 threads
 // per token.
+#include <algorithm>
+
 #include "jacap_internal.hpp"
 
 namespace jacap {
@@ -24,20 +26,20 @@ template <int D, int POL>
 __global__ __launch_bounds__(kThreads, 2) void leverage_mfma_kernel(
     Geo g, const uint16_t* __restrict__ v, const float* __restrict__ wbuf,
     const uint16_t* __restrict__ lfrag, const uint32_t* __restrict__ uflags,
-    float* __restrict__ scores, int lchunks) {
+    float* __restrict__ scores, int lchunks, int lchunk) {
   constexpr int NB = D / 16;                    // output blocks of 16 channels (a)
   constexpr int NK = D / 32;                    // K blocks of 32 channels (b)
   constexpr int NLP = (NB / 2) * (NB / 2 + 1);  // lower (j, kb) block pairs
   int u, chunk;
   if (!grid_unit_chunk<true>(g, lchunks, u, chunk)) return;
   const Unit un = decode_unit(g, u);
-  const int base = chunk * kLChunkMfma;
+  const int base = chunk * lchunk;
   if (base >= un.n) return;
   const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int ch = lane & 15, kg = lane >> 4;
   const int rl = 2 * (ch >> 3) + ((ch >> 2) & 1);  // token (of 4) whose score this lane ends with
   const int64_t trow = token_row(g, un);
-  const int end = min(un.n, base + kLChunkMfma);
+  const int end = min(un.n, base + lchunk);
 
   const uint32_t uf = uflags[u];
   if (uf & kUnitRefine) return;  // scored by the fp64 pass
@@ -159,28 +161,31 @@ template <typename T, int D, bool REFINE_ONLY>
 __global__ __launch_bounds__(kThreads) void leverage_precise_kernel(
     Geo g, const T* __restrict__ v, const float* __restrict__ wbuf,
     const double* __restrict__ xred, const uint32_t* __restrict__ uflags,
-    float* __restrict__ scores, int lchunks, int lchunk) {
+    float* __restrict__ scores, int lchunks, int lchunk, int items) {
   constexpr int LD = D + 1;
   constexpr int NB = D / 16;
   constexpr int NPAIR = NB * (NB + 1) / 2;
   constexpr int TPT = 8;                 // threads per token
   constexpr int TOK = kThreads / TPT;    // tokens per tile
+  __shared__ double X[D * LD];
+  __shared__ float vs[TOK][D + 1];  // padded: the wave's 8 token rows in distinct banks
+  // one (unit, chunk) item per workgroup, or (REFINE_ONLY) a grid-stride walk
+  for (int item = blockIdx.x; item < items; item += gridDim.x) {
   int u, chunk;
-  if (!grid_unit_chunk<true>(g, lchunks, u, chunk)) return;
+  if (!grid_unit_chunk_at<true>(g, lchunks, item, u, chunk)) continue;
   const uint32_t uf = uflags[u];
-  if (REFINE_ONLY && !(uf & kUnitRefine)) return;
+  if (REFINE_ONLY && !(uf & kUnitRefine)) continue;
   const Unit un = decode_unit(g, u);
   const int base = chunk * lchunk;
-  if (base >= un.n) return;
+  if (base >= un.n) continue;
   const int tid = threadIdx.x;
   const int64_t trow = token_row(g, un);
   const int end = min(un.n, base + lchunk);
   if (uf & kUnitFailed) {  // non-finite input or singular A: NaN scores
     for (int t = base + tid; t < end; t += kThreads) scores[trow + t] = __builtin_nanf("");
-    return;
+    continue;
   }
-  __shared__ double X[D * LD];
-  __shared__ float vs[TOK][D];
+  __syncthreads();  // the previous item's X and staged tokens are no longer read
   // lower blocks of L^{-1}: pair p = (bi <= bj) holds X[16 bj + r][16 bi + c]
   const double* Xb = xred + (int64_t)u * (NPAIR * 256);
   for (int e = tid; e < NPAIR * 256; e += kThreads) {
@@ -202,8 +207,15 @@ __global__ __launch_bounds__(kThreads) void leverage_precise_kernel(
     __syncthreads();
     double ss = 0.0;
     for (int a = sub; a < D; a += TPT) {
-      double y = 0.0;
-      for (int b = 0; b <= a; ++b) y += X[a * LD + b] * (double)vs[my_tok][b];
+      // four independent chains over b (latency, not order, bounds this loop)
+      double y4[4] = {0.0, 0.0, 0.0, 0.0};
+      int b = 0;
+      for (; b + 3 <= a; b += 4) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) y4[q] = fma(X[a * LD + b + q], (double)vs[my_tok][b + q], y4[q]);
+      }
+      for (; b <= a; ++b) y4[0] = fma(X[a * LD + b], (double)vs[my_tok][b], y4[0]);
+      const double y = (y4[0] + y4[1]) + (y4[2] + y4[3]);
       ss += y * y;
     }
 #pragma unroll
@@ -212,6 +224,7 @@ __global__ __launch_bounds__(kThreads) void leverage_precise_kernel(
     if (sub == 0 && t < end) {
       scores[trow + t] = (float)((double)wbuf[trow + t] * ss);
     }
+  }
   }
 }
 
@@ -223,7 +236,8 @@ hipError_t launch_leverage(const Launch& L, const void* v, float* scores) {
   if (L.ws.mfma) {
     const uint16_t* lf = ws_ptr<uint16_t>(L.wsp, L.ws.lfrag);
     auto go = [&](auto kern) {
-      kern<<<grid, kThreads, 0, L.stream>>>(g, (const uint16_t*)v, wb, lf, uf, scores, L.ws.lchunks);
+      kern<<<grid, kThreads, 0, L.stream>>>(g, (const uint16_t*)v, wb, lf, uf, scores, L.ws.lchunks,
+                                            L.ws.lchunk);
     };
     if (g.D == 128) {
       if (g.V > 1) go(leverage_mfma_kernel<128, kPolicyShared>);
@@ -241,13 +255,14 @@ hipError_t launch_leverage(const Launch& L, const void* v, float* scores) {
 // fp64 leverage: every unit of fp32 inputs, or the marked units of bf16 inputs.
 hipError_t launch_leverage_precise(const Launch& L, const void* v, float* scores) {
   const Geo& g = L.geo;
-  const dim3 grid((unsigned)chunked_grid(g, L.ws.plchunks));
+  const int64_t items = chunked_grid(g, L.ws.plchunks);
+  const dim3 grid((unsigned)(L.ws.mfma ? std::min<int64_t>(items, kRefineBlocks) : items));
   const float* wb = ws_ptr<float>(L.wsp, L.ws.wgt);
   const uint32_t* uf = ws_ptr<uint32_t>(L.wsp, L.ws.uflags);
   const double* xr = ws_ptr<double>(L.wsp, L.ws.gram_red);
-  const int lchunk = L.ws.mfma ? kLChunkRefine : kLChunkPrecise;
   auto go = [&](auto kern, auto vv) {
-    kern<<<grid, kThreads, 0, L.stream>>>(g, vv, wb, xr, uf, scores, L.ws.plchunks, lchunk);
+    kern<<<grid, kThreads, 0, L.stream>>>(g, vv, wb, xr, uf, scores, L.ws.plchunks, L.ws.plchunk,
+                                          (int)items);
   };
   if (L.ws.mfma) {
     if (g.D == 128) go(leverage_precise_kernel<uint16_t, 128, true>, (const uint16_t*)v);
