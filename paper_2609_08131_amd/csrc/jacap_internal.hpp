@@ -15,6 +15,10 @@ namespace jacap {
 constexpr int kThreads = 256;        // 4 wave64 per workgroup
 constexpr int kKChunk = 1024;        // tokens per workgroup in the K pass
 constexpr int kFullMaxQ = 256;       // window queries the FULL-covariance MFMA K pass stages
+// FULL covariance: units of at least this many tokens take kappa from the
+// triangular factor of Lambda_Q (a fixed per-unit cost that long units repay).
+constexpr int kTriMinTokens = 8192;
+constexpr int kTriChunks = 4;         // K-pass chunks per workgroup on that path: at most
 constexpr int kGChunkMfma = 512;     // tokens per workgroup in the MFMA Gram pass: at least
 constexpr int kGChunkMfmaMax = 16384; // ... and at most (larger chunks: fewer partial Grams)
 constexpr int kGramMinBlocks = 2048;  // chunks are as large as this many blocks in the grid allow
@@ -44,6 +48,10 @@ constexpr uint32_t kUnitSingular = JACAP_FLAG_SINGULAR;
 // and the bf16 leverage products could miss the score tolerance; its Gram,
 // factor and leverage scores are recomputed in fp64.
 constexpr uint32_t kUnitRefine = 1u << 8;
+// Internal (FULL covariance on the triangular path): the unit's K pass takes
+// the window tile instead -- too few tokens to repay factoring Lambda_Q, a
+// numerically rank-deficient Lambda_Q, or non-finite queries.
+constexpr uint32_t kUnitKTile = 1u << 9;
 constexpr uint32_t kUnitFailed = kUnitNonfinite | kUnitSingular;
 
 // ---------------------------------------------------------------------------
@@ -353,6 +361,16 @@ inline bool full_kpass_on_mfma(const Launch& L, const void* q) {
   return L.cfg->cov_mode == JACAP_COV_FULL && L.cfg->dtype == JACAP_DTYPE_BF16 && q != nullptr &&
          L.geo.G * L.geo.w <= kFullMaxQ;
 }
+// ... and with at least 2 d window queries, where ||X k||^2 (Lambda_Q = X^T X,
+// X lower triangular: about 1.1 d^2 bf16 MACs per token in two terms) costs
+// less than the window tile's N_s d, when some unit is long enough: Lambda_Q
+// is formed and factored per unit first (launch_qfactor), and the units it
+// marks kUnitKTile keep the window tile.
+inline bool full_kpass_tri(const Launch& L, const void* q) {
+  return full_kpass_on_mfma(L, q) && L.geo.G * L.geo.w >= 2 * L.geo.D &&
+         L.geo.maxn >= kTriMinTokens;
+}
+hipError_t launch_qfactor(const Launch& L, const void* q);
 hipError_t launch_softmax_weights(const Launch& L);
 hipError_t launch_head_mean(const Launch& L, const float* hs, float* scores);
 hipError_t launch_gram(const Launch& L, const void* v, bool refine);

@@ -103,6 +103,180 @@ __device__ __forceinline__ void tri_index(int e, int& i, int& j) {
   j = e - r * (r + 1) / 2;
 }
 
+// Elements (u16) of one unit's two-term B fragments of a lower-triangular
+// d x d matrix (see store_lower_frags).
+__host__ __device__ constexpr int lower_frag_elems(int d) {
+  return (d / 32) * (d / 32 + 1) * 2 * 64 * 8;
+}
+
+// A lower-triangular matrix X (x(a, b) = X[a][b] for b <= a) rounded to fp32
+// and split into bf16 hi + lo terms, stored in the per-lane B-fragment order
+// of the 16x16x32 MFMA for Y = V X^T: B fragment of output block j
+// (a = 16 j + ch) and K block kb (b = 32 kb + 8 kg + q), only the pairs with
+// kb <= j / 2 (the rest of X^T is zero); lane (ch, kg) holds 8 bf16, hi then
+// lo.
+template <int D, typename F>
+__device__ __forceinline__ void store_lower_frags(uint16_t* __restrict__ out, F x) {
+  constexpr int NB = D / 16;
+  constexpr int NLP = (NB / 2) * (NB / 2 + 1);  // lower (j, kb) pairs: sum_j (j/2 + 1)
+  static_assert(NLP * 2 * 64 * 8 == lower_frag_elems(D), "fragment count");
+  for (int e = threadIdx.x; e < NLP * 64; e += blockDim.x) {
+    const int qp = e / 64, ln = e % 64, ch = ln & 15, kg = ln >> 4;
+    int j = 0, kb = 0, q = qp;
+    for (int jj = 0; jj < NB; ++jj) {
+      const int cnt = jj / 2 + 1;
+      if (q < cnt) { j = jj; kb = q; break; }
+      q -= cnt;
+    }
+    const int a = 16 * j + ch;
+    uint16_t hi[8], lo[8];
+#pragma unroll
+    for (int t = 0; t < 8; ++t) {
+      const int b = 32 * kb + 8 * kg + t;
+      const float xv = (b <= a) ? (float)x(a, b) : 0.0f;
+      const __bf16 h = (__bf16)xv;
+      const __bf16 l = (__bf16)(xv - (float)h);
+      hi[t] = __builtin_bit_cast(uint16_t, h);
+      lo[t] = __builtin_bit_cast(uint16_t, l);
+    }
+    uint16_t* dh = out + ((int64_t)(qp * 2 + 0) * 64 + ln) * 8;
+    uint16_t* dl = out + ((int64_t)(qp * 2 + 1) * 64 + ln) * 8;
+#pragma unroll
+    for (int t = 0; t < 8; ++t) { dh[t] = hi[t]; dl[t] = lo[t]; }
+  }
+}
+
+// Blocked Cholesky A = L L^T in place on the lower blocks in LDS (see lidx),
+// given dg = diag(A) before factorisation and *bad == 0 (both visible to
+// every thread). idg receives 1 / L_rr. Returns 0, or the flag that stopped
+// it -- kUnitNonfinite for a non-finite pivot, `fail` for a pivot at or below
+// piv_rel times its diagonal entry -- the same value in every thread.
+template <int D>
+__device__ __forceinline__ int cholesky_lds(double* A, const double* dg, double* idg, int* bad,
+                                            double piv_rel, int fail) {
+  constexpr int NB = D / 16;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  for (int kb = 0; kb < NB; ++kb) {
+    const int c = 16 * kb;
+    // 1. Diagonal block, in registers of wave 0: lane s (mod 16) holds row s.
+    if (wave == 0) {
+      const int s = lane & 15;
+      double a[16];
+#pragma unroll
+      for (int q = 0; q < 16; ++q) a[q] = (q <= s) ? A[lidx((c + s), c + q)] : 0.0;
+      // No early exit (the loop must stay fully unrolled so that a[] lives in
+      // registers): after a failed pivot the rest is computed on a stand-in
+      // pivot and discarded.
+      int code = 0;
+#pragma unroll
+      for (int t = 0; t < 16; ++t) {
+        double piv;  // A[t][t], from lane t of the row
+        switch (t) {
+          case 0: piv = row_bcast_f64<0>(a[t]); break;
+          case 1: piv = row_bcast_f64<1>(a[t]); break;
+          case 2: piv = row_bcast_f64<2>(a[t]); break;
+          case 3: piv = row_bcast_f64<3>(a[t]); break;
+          case 4: piv = row_bcast_f64<4>(a[t]); break;
+          case 5: piv = row_bcast_f64<5>(a[t]); break;
+          case 6: piv = row_bcast_f64<6>(a[t]); break;
+          case 7: piv = row_bcast_f64<7>(a[t]); break;
+          case 8: piv = row_bcast_f64<8>(a[t]); break;
+          case 9: piv = row_bcast_f64<9>(a[t]); break;
+          case 10: piv = row_bcast_f64<10>(a[t]); break;
+          case 11: piv = row_bcast_f64<11>(a[t]); break;
+          case 12: piv = row_bcast_f64<12>(a[t]); break;
+          case 13: piv = row_bcast_f64<13>(a[t]); break;
+          case 14: piv = row_bcast_f64<14>(a[t]); break;
+          default: piv = row_bcast_f64<15>(a[t]); break;
+        }
+        // A pivot that has lost all but piv_rel of its diagonal entry is within
+        // the rounding noise of the accumulated Gram: A is numerically singular
+        // at the path's working precision (rank-deficient M with ridge 0).
+        const bool ok = piv > piv_rel * dg[c + t] && piv > 0.0;
+        if (!ok && code == 0)
+          code = !isfinite(piv) ? (int)kUnitNonfinite : fail;
+        const double y = rsqrt_f64(ok ? piv : 1.0);
+        if (lane == 0) idg[c + t] = y;
+        a[t] = (s == t) ? piv * y : a[t] * y;  // column t of L (rows s < t: unused)
+        // a[q] -= L[s][t] L[q][t] for q > t; L[q][t] is lane q's a[t]. Entries
+        // with q > s are outside row s's lower part and never stored.
+#pragma unroll
+        for (int q = t + 1; q < 16; ++q) {
+          double lq;
+          switch (q) {
+            case 1: lq = row_bcast_f64<1>(a[t]); break;
+            case 2: lq = row_bcast_f64<2>(a[t]); break;
+            case 3: lq = row_bcast_f64<3>(a[t]); break;
+            case 4: lq = row_bcast_f64<4>(a[t]); break;
+            case 5: lq = row_bcast_f64<5>(a[t]); break;
+            case 6: lq = row_bcast_f64<6>(a[t]); break;
+            case 7: lq = row_bcast_f64<7>(a[t]); break;
+            case 8: lq = row_bcast_f64<8>(a[t]); break;
+            case 9: lq = row_bcast_f64<9>(a[t]); break;
+            case 10: lq = row_bcast_f64<10>(a[t]); break;
+            case 11: lq = row_bcast_f64<11>(a[t]); break;
+            case 12: lq = row_bcast_f64<12>(a[t]); break;
+            case 13: lq = row_bcast_f64<13>(a[t]); break;
+            case 14: lq = row_bcast_f64<14>(a[t]); break;
+            default: lq = row_bcast_f64<15>(a[t]); break;
+          }
+          a[q] = fma(-a[t], lq, a[q]);
+        }
+      }
+      if (code) {
+        if (lane == 0) *bad = code;
+      } else if (lane < 16) {
+#pragma unroll
+        for (int q = 0; q < 16; ++q)
+          if (q <= s) A[lidx((c + s), c + q)] = a[q];
+      }
+    }
+    __syncthreads();
+    if (*bad) return *bad;
+    // 2. Panel rows r >= c + 16: L[r, c:c+16] = A[r, c:c+16] L_kk^{-T}.
+    for (int r = c + 16 + tid; r < D; r += kFactorThreads) {
+      double x[16];
+#pragma unroll
+      for (int t = 0; t < 16; ++t) x[t] = A[lidx(r, c + t)];
+#pragma unroll
+      for (int t = 0; t < 16; ++t) {
+        // x[t] = (A[r][c+t] - sum_q x[q] L[c+t][c+q]) / L[c+t][c+t]; the sum in
+        // four independent chains (latency, not order, bounds this loop)
+        double sp[4] = {x[t], 0.0, 0.0, 0.0};
+#pragma unroll
+        for (int q = 0; q < t; ++q) sp[q & 3] = fma(-x[q], A[lidx((c + t), c + q)], sp[q & 3]);
+        x[t] = ((sp[0] + sp[1]) + (sp[2] + sp[3])) * idg[c + t];
+      }
+#pragma unroll
+      for (int t = 0; t < 16; ++t) A[lidx(r, c + t)] = x[t];
+    }
+    __syncthreads();
+    // 3. Trailing update A_IJ -= L_Ik L_Jk^T for the 16x16 blocks I >= J > k,
+    //    one block per wave at a time on the fp64 MFMA (K = 16 in four
+    //    slices). Diagonal blocks also update their upper half, which is
+    //    unused until the inverse overwrites it.
+    const int m = NB - kb - 1;
+    if (m > 0) {
+      const int r16 = lane & 15, q4 = lane >> 4;
+      for (int e = wave; e < m * (m + 1) / 2; e += kFactorThreads / 64) {
+        int bi, bj;
+        tri_index(e, bi, bj);
+        const int I = 16 * (kb + 1 + bi), J = 16 * (kb + 1 + bj);
+        f64x4 acc = {0.0, 0.0, 0.0, 0.0};
+#pragma unroll
+        for (int kq = 0; kq < 4; ++kq) {
+          const int t = c + 4 * kq + q4;
+          acc = mfma64(A[lidx((I + r16), t)], A[lidx((J + r16), t)], acc);
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i) A[lidx((I + 4 * i + q4), J + r16)] -= acc[i];
+      }
+    }
+    __syncthreads();
+  }
+  return 0;
+}
+
 // One unit. PASS 0: first factorisation (all units), from the reduced Gram
 // `red`. PASS 1: a unit marked kUnitRefine by pass 0 (bf16 path), from its fp64
 // partial Grams `part` (pchunks per unit), summed here in chunk order. FRAGS:
@@ -228,130 +402,14 @@ __device__ __forceinline__ void factor_unit(const Geo& g, int u, double* __restr
   }
 
   // ---------------- Cholesky A = L L^T (L overwrites the lower triangle) ----
-  for (int kb = 0; kb < NB; ++kb) {
-    const int c = 16 * kb;
-    // 1. Diagonal block, in registers of wave 0: lane s (mod 16) holds row s.
-    if (wave == 0) {
-      const int s = lane & 15;
-      double a[16];
-#pragma unroll
-      for (int q = 0; q < 16; ++q) a[q] = (q <= s) ? A[lidx((c + s), c + q)] : 0.0;
-      // No early exit (the loop must stay fully unrolled so that a[] lives in
-      // registers): after a failed pivot the rest is computed on a stand-in
-      // pivot and discarded.
-      int code = 0;
-#pragma unroll
-      for (int t = 0; t < 16; ++t) {
-        double piv;  // A[t][t], from lane t of the row
-        switch (t) {
-          case 0: piv = row_bcast_f64<0>(a[t]); break;
-          case 1: piv = row_bcast_f64<1>(a[t]); break;
-          case 2: piv = row_bcast_f64<2>(a[t]); break;
-          case 3: piv = row_bcast_f64<3>(a[t]); break;
-          case 4: piv = row_bcast_f64<4>(a[t]); break;
-          case 5: piv = row_bcast_f64<5>(a[t]); break;
-          case 6: piv = row_bcast_f64<6>(a[t]); break;
-          case 7: piv = row_bcast_f64<7>(a[t]); break;
-          case 8: piv = row_bcast_f64<8>(a[t]); break;
-          case 9: piv = row_bcast_f64<9>(a[t]); break;
-          case 10: piv = row_bcast_f64<10>(a[t]); break;
-          case 11: piv = row_bcast_f64<11>(a[t]); break;
-          case 12: piv = row_bcast_f64<12>(a[t]); break;
-          case 13: piv = row_bcast_f64<13>(a[t]); break;
-          case 14: piv = row_bcast_f64<14>(a[t]); break;
-          default: piv = row_bcast_f64<15>(a[t]); break;
-        }
-        // A pivot that has lost all but piv_rel of its diagonal entry is within
-        // the rounding noise of the accumulated Gram: A is numerically singular
-        // at the path's working precision (rank-deficient M with ridge 0).
-        const bool ok = piv > piv_rel * dg[c + t] && piv > 0.0;
-        if (!ok && code == 0)
-          code = !isfinite(piv) ? (int)kUnitNonfinite
-                                : (may_refine ? (int)kUnitRefine : (int)kUnitSingular);
-        const double y = rsqrt_f64(ok ? piv : 1.0);
-        if (lane == 0) idg[c + t] = y;
-        a[t] = (s == t) ? piv * y : a[t] * y;  // column t of L (rows s < t: unused)
-        // a[q] -= L[s][t] L[q][t] for q > t; L[q][t] is lane q's a[t]. Entries
-        // with q > s are outside row s's lower part and never stored.
-#pragma unroll
-        for (int q = t + 1; q < 16; ++q) {
-          double lq;
-          switch (q) {
-            case 1: lq = row_bcast_f64<1>(a[t]); break;
-            case 2: lq = row_bcast_f64<2>(a[t]); break;
-            case 3: lq = row_bcast_f64<3>(a[t]); break;
-            case 4: lq = row_bcast_f64<4>(a[t]); break;
-            case 5: lq = row_bcast_f64<5>(a[t]); break;
-            case 6: lq = row_bcast_f64<6>(a[t]); break;
-            case 7: lq = row_bcast_f64<7>(a[t]); break;
-            case 8: lq = row_bcast_f64<8>(a[t]); break;
-            case 9: lq = row_bcast_f64<9>(a[t]); break;
-            case 10: lq = row_bcast_f64<10>(a[t]); break;
-            case 11: lq = row_bcast_f64<11>(a[t]); break;
-            case 12: lq = row_bcast_f64<12>(a[t]); break;
-            case 13: lq = row_bcast_f64<13>(a[t]); break;
-            case 14: lq = row_bcast_f64<14>(a[t]); break;
-            default: lq = row_bcast_f64<15>(a[t]); break;
-          }
-          a[q] = fma(-a[t], lq, a[q]);
-        }
-      }
-      if (code) {
-        if (lane == 0) bad = code;
-      } else if (lane < 16) {
-#pragma unroll
-        for (int q = 0; q < 16; ++q)
-          if (q <= s) A[lidx((c + s), c + q)] = a[q];
-      }
+  const int code =
+      cholesky_lds<D>(A, dg, idg, &bad, piv_rel, may_refine ? (int)kUnitRefine : (int)kUnitSingular);
+  if (code) {
+    if (tid == 0) {
+      if (code == (int)kUnitRefine) atomicOr(uflags + u, kUnitRefine);
+      else raise_flags(status, uflags, u, (uint32_t)code);
     }
-    __syncthreads();
-    if (bad) {
-      if (tid == 0) {
-        if (bad == (int)kUnitRefine) atomicOr(uflags + u, kUnitRefine);
-        else raise_flags(status, uflags, u, (uint32_t)bad);
-      }
-      return;
-    }
-    // 2. Panel rows r >= c + 16: L[r, c:c+16] = A[r, c:c+16] L_kk^{-T}.
-    for (int r = c + 16 + tid; r < D; r += kFactorThreads) {
-      double x[16];
-#pragma unroll
-      for (int t = 0; t < 16; ++t) x[t] = A[lidx(r, c + t)];
-#pragma unroll
-      for (int t = 0; t < 16; ++t) {
-        // x[t] = (A[r][c+t] - sum_q x[q] L[c+t][c+q]) / L[c+t][c+t]; the sum in
-        // four independent chains (latency, not order, bounds this loop)
-        double sp[4] = {x[t], 0.0, 0.0, 0.0};
-#pragma unroll
-        for (int q = 0; q < t; ++q) sp[q & 3] = fma(-x[q], A[lidx((c + t), c + q)], sp[q & 3]);
-        x[t] = ((sp[0] + sp[1]) + (sp[2] + sp[3])) * idg[c + t];
-      }
-#pragma unroll
-      for (int t = 0; t < 16; ++t) A[lidx(r, c + t)] = x[t];
-    }
-    __syncthreads();
-    // 3. Trailing update A_IJ -= L_Ik L_Jk^T for the 16x16 blocks I >= J > k,
-    //    one block per wave at a time on the fp64 MFMA (K = 16 in four
-    //    slices). Diagonal blocks also update their upper half, which is
-    //    unused until the inverse overwrites it.
-    const int m = NB - kb - 1;
-    if (m > 0) {
-      const int r16 = lane & 15, q4 = lane >> 4;
-      for (int e = wave; e < m * (m + 1) / 2; e += kFactorThreads / 64) {
-        int bi, bj;
-        tri_index(e, bi, bj);
-        const int I = 16 * (kb + 1 + bi), J = 16 * (kb + 1 + bj);
-        f64x4 acc = {0.0, 0.0, 0.0, 0.0};
-#pragma unroll
-        for (int kq = 0; kq < 4; ++kq) {
-          const int t = c + 4 * kq + q4;
-          acc = mfma64(A[lidx((I + r16), t)], A[lidx((J + r16), t)], acc);
-        }
-#pragma unroll
-        for (int i = 0; i < 4; ++i) A[lidx((I + 4 * i + q4), J + r16)] -= acc[i];
-      }
-    }
-    __syncthreads();
+    return;
   }
 
   // ---------------- Inverse X = L^{-1} --------------------------------------
@@ -485,34 +543,7 @@ __device__ __forceinline__ void factor_unit(const Geo& g, int u, double* __restr
       o64[e] = xinv(16 * bj + ((e >> 4) & 15), 16 * bi + (e & 15));
     }
   } else {
-    // B fragment of output block j (a = 16 j + ch) and K block kb
-    // (b = 32 kb + 8 kg + q): lane (ch, kg) holds 8 bf16; hi then lo.
-    constexpr int NLP = (NB / 2) * (NB / 2 + 1);  // lower (j, kb) pairs: sum_j (j/2 + 1)
-    uint16_t* out = lfrag + (int64_t)u * NLP * 2 * 64 * 8;
-    for (int e = tid; e < NLP * 64; e += kFactorThreads) {
-      const int qp = e / 64, ln = e % 64, ch = ln & 15, kg = ln >> 4;
-      int j = 0, kb = 0, q = qp;
-      for (int jj = 0; jj < NB; ++jj) {
-        const int cnt = jj / 2 + 1;
-        if (q < cnt) { j = jj; kb = q; break; }
-        q -= cnt;
-      }
-      const int a = 16 * j + ch;
-      uint16_t hi[8], lo[8];
-#pragma unroll
-      for (int t = 0; t < 8; ++t) {
-        const int b = 32 * kb + 8 * kg + t;
-        const float x = (b <= a) ? (float)xinv(a, b) : 0.0f;
-        const __bf16 h = (__bf16)x;
-        const __bf16 l = (__bf16)(x - (float)h);
-        hi[t] = __builtin_bit_cast(uint16_t, h);
-        lo[t] = __builtin_bit_cast(uint16_t, l);
-      }
-      uint16_t* dh = out + ((int64_t)(qp * 2 + 0) * 64 + ln) * 8;
-      uint16_t* dl = out + ((int64_t)(qp * 2 + 1) * 64 + ln) * 8;
-#pragma unroll
-      for (int t = 0; t < 8; ++t) { dh[t] = hi[t]; dl[t] = lo[t]; }
-    }
+    store_lower_frags<D>(lfrag + (int64_t)u * lower_frag_elems(D), xinv);
   }
 }
 
@@ -554,6 +585,147 @@ hipError_t launch_factor(const Launch& L, bool refine) {
     if (g.D == 128) go(factor_kernel<128, false>);
     else go(factor_kernel<64, false>);
   }
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// FULL covariance, triangular K pass (full_kpass_tri): per unit, Lambda_Q of
+// the pooled window in fp64 and a factor Lambda_Q = X^T X with X lower
+// triangular, stored as two-term bf16 B fragments (store_lower_frags) in the
+// L^{-1} fragment buffer, which is free until the capacity matrix is factored.
+// Then kappa_i = k_i^T Lambda_Q k_i = ||X k_i||^2 (Sec. 3.4, full query
+// covariance) takes the leverage pass's triangular MFMA product.
+//
+// X comes from the Cholesky factorisation of the order-reversed matrix:
+// P Lambda_Q P = C C^T (P reverses the channel order, C lower triangular)
+// gives Lambda_Q = (P C P)(P C P)^T with P C P upper triangular, so
+// X = (P C P)^T, X[i][j] = C[d-1-j][d-1-i].
+//
+// Lambda_Q = (1/N_s) sum_r (q_r - mu)(q_r - mu)^T: the centred window rows
+// (fp64, kQRows at a time in LDS) go through the fp64 MFMA, each wave
+// accumulating its share of the 16x16 lower blocks in registers; the blocks
+// are then written to the factor's LDS layout already reversed.
+//
+// The unit is marked kUnitKTile (the K pass takes the window tile) if it has
+// fewer than kTriMinTokens tokens, non-finite window statistics, or a pivot at
+// most kPivRelTri of its diagonal entry: a numerically rank-deficient
+// Lambda_Q, whose factor would not carry kappa to the tolerance in two bf16
+// terms.
+// ---------------------------------------------------------------------------
+constexpr double kPivRelTri = 1e-3;
+constexpr int kQRows = 32;
+
+template <int D>
+__device__ __forceinline__ void qfactor_unit(const Geo& g, int u, const uint16_t* __restrict__ q,
+                                             const double* __restrict__ mu,
+                                             uint16_t* __restrict__ xfrag,
+                                             uint32_t* __restrict__ uflags) {
+  constexpr int NB = D / 16;
+  constexpr int NPAIR = NB * (NB + 1) / 2;
+  constexpr int NW = kFactorThreads / 64;
+  constexpr int PW = (NPAIR + NW - 1) / NW;  // lower 16x16 blocks of Lambda_Q per wave
+  constexpr int QP = D + 16;  // doubles per staged row: the pad puts consecutive rows on the two halves of the banks
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int r16 = lane & 15, q4 = lane >> 4;
+  const Unit un = decode_unit(g, u);
+  if (un.n == 0) return;
+  if (un.n < kTriMinTokens || (uflags[u] & kUnitNonfinite)) {
+    if (tid == 0) atomicOr(uflags + u, kUnitKTile);
+    return;
+  }
+  __shared__ double A[NPAIR * kBlk];  // lower 16x16 blocks, see lidx
+  __shared__ double dg[D];
+  __shared__ double idg[D];
+  __shared__ double smu[D];
+  __shared__ double qc[kQRows * QP];
+  __shared__ int bad;
+
+  const int Ns = g.G * g.w;
+  const uint16_t* qb =
+      q + un.b * g.qss + un.l * g.qsl + (int64_t)(un.h * g.V + un.s) * g.G * g.qsh;
+  for (int c = tid; c < D; c += kFactorThreads) smu[c] = mu[(int64_t)u * D + c];
+  if (tid == 0) bad = 0;
+  f64x4 acc[PW];
+#pragma unroll
+  for (int p = 0; p < PW; ++p) acc[p] = f64x4{0.0, 0.0, 0.0, 0.0};
+  for (int r0 = 0; r0 < Ns; r0 += kQRows) {
+    __syncthreads();  // the previous rows are consumed (and smu is visible)
+    for (int e = tid; e < kQRows * D; e += kFactorThreads) {
+      const int rr = e / D, c = e - rr * D, r = r0 + rr;
+      double x = 0.0;  // rows past N_s add nothing
+      if (r < Ns) {
+        const int gq = r / g.w, p = r - gq * g.w;
+        x = (double)bf16_to_f32(qb[gq * g.qsh + p * g.qsp + c]) - smu[c];
+      }
+      qc[rr * QP + c] = x;
+    }
+    __syncthreads();
+    // block (bi, bj), bi >= bj: sum_r qc[r][16 bi + i] qc[r][16 bj + j], four
+    // rows per MFMA (lane (r16, q4) supplies row 4 s + q4, column r16 of each)
+#pragma unroll
+    for (int p = 0; p < PW; ++p) {
+      const int e = wave + NW * p;
+      if (e < NPAIR) {
+        int bi, bj;
+        tri_index(e, bi, bj);
+#pragma unroll
+        for (int ks = 0; ks < kQRows / 4; ++ks) {
+          const double* row = qc + (4 * ks + q4) * QP;
+          acc[p] = mfma64(row[16 * bi + r16], row[16 * bj + r16], acc[p]);
+        }
+      }
+    }
+  }
+  // Lambda_Q[row][col] (row >= col) goes to the reversed matrix at
+  // (d-1-col, d-1-row), a lower entry; diagonal blocks are written whole.
+  const double invn = 1.0 / (double)Ns;
+#pragma unroll
+  for (int p = 0; p < PW; ++p) {
+    const int e = wave + NW * p;
+    if (e < NPAIR) {
+      int bi, bj;
+      tri_index(e, bi, bj);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int row = 16 * bi + 4 * i + q4, col = 16 * bj + r16;
+        A[lidx(D - 1 - col, D - 1 - row)] = acc[p][i] * invn;
+      }
+    }
+  }
+  __syncthreads();
+  for (int a = tid; a < D; a += kFactorThreads) dg[a] = A[lidx(a, a)];
+  __syncthreads();
+  if (cholesky_lds<D>(A, dg, idg, &bad, kPivRelTri, (int)kUnitKTile) != 0) {
+    if (tid == 0) atomicOr(uflags + u, kUnitKTile);
+    return;
+  }
+  store_lower_frags<D>(xfrag + (int64_t)u * lower_frag_elems(D),
+                       [&](int a, int b) { return A[lidx(D - 1 - b, D - 1 - a)]; });
+}
+
+// One workgroup per unit (a grid-stride walk if the grid is smaller).
+template <int D>
+__global__ __launch_bounds__(kFactorThreads) void qfactor_kernel(Geo g, const uint16_t* __restrict__ q,
+                                                                 const double* __restrict__ mu,
+                                                                 uint16_t* __restrict__ xfrag,
+                                                                 uint32_t* __restrict__ uflags) {
+  for (int u = blockIdx.x; u < g.U; u += gridDim.x) {
+    qfactor_unit<D>(g, u, q, mu, xfrag, uflags);
+    __syncthreads();  // LDS of this unit fully consumed before the next one's
+  }
+}
+
+hipError_t launch_qfactor(const Launch& L, const void* q) {
+  const Geo& g = L.geo;
+  if (g.U == 0) return hipSuccess;
+  auto go = [&](auto kern) {
+    kern<<<g.U, kFactorThreads, 0, L.stream>>>(g, (const uint16_t*)q,
+                                                ws_ptr<double>(L.wsp, L.ws.mu),
+                                                ws_ptr<uint16_t>(L.wsp, L.ws.lfrag),
+                                                ws_ptr<uint32_t>(L.wsp, L.ws.uflags));
+  };
+  if (g.D == 128) go(qfactor_kernel<128>);
+  else go(qfactor_kernel<64>);
   return hipGetLastError();
 }
 

@@ -176,7 +176,9 @@ hipError_t launch_qstats(const Launch& L, const void* q) {
     else
       qstats_kernel<float, 64><<<g.U, kThreads, 0, L.stream>>>(g, (const float*)q, mu, lam, lf, full, st, uf);
   }
-  return hipGetLastError();
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess || !full_kpass_tri(L, q)) return e;
+  return launch_qfactor(L, q);  // Lambda_Q and its factor for the K pass
 }
 
 // ---------------------------------------------------------------------------
@@ -537,31 +539,28 @@ __device__ __forceinline__ float row_sum16_f32(float v) {
   return v;
 }
 
+// LDS of the window tile: the staged window (u16 rows of QP = d + 8).
 template <int D>
-__global__ __launch_bounds__(kThreads, 2) void kpass_full_mfma_kernel(
-    Geo g, const uint16_t* __restrict__ k, const uint16_t* __restrict__ q,
-    const double* __restrict__ mu, float* __restrict__ zout, float* __restrict__ kout,
-    float2* __restrict__ cstat, int kchunks, double inv_scale, uint32_t* status,
-    uint32_t* uflags) {
+constexpr int kWindowLds = kFullMaxQ * (D + 8);
+
+// One chunk (unit u, tokens base ..) of the window-tile K pass; LDS from the
+// caller (qsh: kWindowLds<D> u16; zsh, ksq: kKChunk floats; red).
+template <int D>
+__device__ __forceinline__ void kpass_tile_chunk(
+    const Geo& g, int u, const Unit& un, int chunk, const uint16_t* __restrict__ k,
+    const uint16_t* __restrict__ q, const double* __restrict__ mu, float* __restrict__ zout,
+    float* __restrict__ kout, float2* __restrict__ cstat, int kchunks, double inv_scale,
+    uint32_t* status, uint32_t* uflags, uint16_t* qsh, float* zsh, float* ksq, float* red) {
   constexpr int NK = D / 32;            // K-blocks of 32 channels
   constexpr int QP = D + 8;             // u16 per staged query row
   constexpr int TT = 2;                 // 16-token tiles per wave pass
   constexpr int WT = kKChunk / (kThreads / 64);  // tokens per wave per chunk
   static_assert(WT % (2 * 16 * TT) == 0, "whole pairs of passes per wave");
-  int u, chunk;
-  if (!grid_unit_chunk<false>(g, kchunks, u, chunk)) return;
-  const Unit un = decode_unit(g, u);
   const int base = chunk * kKChunk;
-  if (base >= un.n) return;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int ch = lane & 15, kg = lane >> 4;
   const int Ns = g.G * g.w, nqt = (Ns + 15) / 16;
-
-  __shared__ __attribute__((aligned(16))) uint16_t qsh[kFullMaxQ * QP];
-  __shared__ float zsh[kKChunk];
-  __shared__ float ksq[kKChunk];
-  __shared__ float red[kThreads / 64];
 
   // The pooled window: row r = gq * w + p (query head gq of the group,
   // position p); rows N_s .. 16 nqt - 1 are zero and masked below.
@@ -699,6 +698,213 @@ __global__ __launch_bounds__(kThreads, 2) void kpass_full_mfma_kernel(
                  chunk);
 }
 
+
+template <int D>
+__global__ __launch_bounds__(kThreads, 2) void kpass_full_mfma_kernel(
+    Geo g, const uint16_t* __restrict__ k, const uint16_t* __restrict__ q,
+    const double* __restrict__ mu, float* __restrict__ zout, float* __restrict__ kout,
+    float2* __restrict__ cstat, int kchunks, double inv_scale, uint32_t* status,
+    uint32_t* uflags) {
+  __shared__ __attribute__((aligned(16))) uint16_t qsh[kWindowLds<D>];
+  __shared__ float zsh[kKChunk];
+  __shared__ float ksq[kKChunk];
+  __shared__ float red[kThreads / 64];
+  int u, chunk;
+  if (!grid_unit_chunk<false>(g, kchunks, u, chunk)) return;
+  const Unit un = decode_unit(g, u);
+  if (chunk * kKChunk >= un.n) return;
+  kpass_tile_chunk<D>(g, u, un, chunk, k, q, mu, zout, kout, cstat, kchunks, inv_scale, status,
+                      uflags, qsh, zsh, ksq, red);
+}
+
+// ---------------------------------------------------------------------------
+// K pass for bf16 keys with the FULL window covariance, triangular path
+// (full_kpass_tri): kappa_i = ||X k_i||^2 with Lambda_Q = X^T X, X lower
+// triangular in two-term bf16 B fragments from launch_qfactor, on MFMA
+// 16x16x32 as in the leverage pass (tokens are the MFMA rows; only the
+// K-blocks of the lower triangle). z_i = mu . k_i / (tau sqrt d) comes from
+// one more MFMA chain, whose B columns 0, 1 and 2 hold mu (rounded to fp32)
+// split exactly into three bf16 terms: the three column sums add to the
+// fp32-accumulated dot product. Units marked kUnitKTile take the window tile
+// inside the same launch (the two paths share the LDS).
+//
+// Each wave takes 16-token steps of the chunk (rows read whole, non-temporal
+// or cached per POL, two steps ahead in three rotating buffers), as the
+// leverage pass does; the rows pass through a wave-private LDS tile into the
+// MFMA operand layout.
+// ---------------------------------------------------------------------------
+template <int D, int POL>
+__global__ __launch_bounds__(kThreads, 2) void kpass_tri_kernel(
+    Geo g, const uint16_t* __restrict__ k, const uint16_t* __restrict__ q,
+    const double* __restrict__ mu, const uint16_t* __restrict__ xfrag,
+    float* __restrict__ zout, float* __restrict__ kout, float2* __restrict__ cstat, int kchunks,
+    int sub, double inv_scale, uint32_t* status, uint32_t* uflags) {
+  constexpr int NB = D / 16;                    // output blocks of 16 channels
+  constexpr int NK = D / 32;                    // K blocks of 32 channels
+  constexpr int NLP = (NB / 2) * (NB / 2 + 1);  // lower (j, kb) block pairs
+  constexpr int PITCH = D * 2 + 16;             // bytes per tile row (the pad spreads the banks)
+  constexpr int TILE_BYTES = (kThreads / 64) * 16 * PITCH;
+  static_assert(TILE_BYTES + NK * 64 * 16 <= kWindowLds<D> * 2, "tri path fits the window LDS");
+  __shared__ __attribute__((aligned(16))) uint16_t qsh[kWindowLds<D>];
+  __shared__ float zsh[kKChunk];
+  __shared__ float ksq[kKChunk];
+  __shared__ float red[kThreads / 64];
+  // `sub` consecutive chunks of one unit per workgroup
+  int u, grp;
+  if (!grid_unit_chunk<false>(g, (kchunks + sub - 1) / sub, u, grp)) return;
+  const Unit un = decode_unit(g, u);
+  const int chunk0 = grp * sub;
+  const int base0 = chunk0 * kKChunk;
+  if (base0 >= un.n) return;
+  const int nsub = min(sub, (un.n - base0 + kKChunk - 1) / kKChunk);
+  if (uflags[u] & kUnitKTile) {
+    for (int c = 0; c < nsub; ++c)
+      kpass_tile_chunk<D>(g, u, un, chunk0 + c, k, q, mu, zout, kout, cstat, kchunks, inv_scale,
+                          status, uflags, qsh, zsh, ksq, red);
+    return;
+  }
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int ch = lane & 15, kg = lane >> 4;
+  const int rl = 2 * (ch >> 3) + ((ch >> 2) & 1);  // token (of 4) whose kappa this lane ends with
+  const int lim = base0 + nsub * kKChunk;
+  const int end = min(un.n, lim);
+  const int64_t trow = token_row(g, un);
+
+  const uint16_t* kb0 = k + un.l * g.ksl + un.h * g.ksh + un.t0 * g.kst;
+  const int32_t kstb = (int32_t)g.kst * 2;
+  constexpr int LPR = D / 8;                    // lanes per whole row (16 bytes each)
+  constexpr int RPL = 64 / LPR;                 // rows per wave load
+  static_assert(RPL * NK == 16, "a step's 16 rows in NK whole-row loads");
+  const int rrow = lane / LPR, rpc = lane % LPR;
+  int32_t koff[NK];
+#pragma unroll
+  for (int i = 0; i < NK; ++i) koff[i] = (RPL * i + rrow) * kstb + rpc * 16;
+  struct Buf { uint4 a[NK]; };
+  // Rows past the unit's last one read as zeros (the range ends there).
+  auto load = [&](int t0, Buf& bf) {
+    const int32_t rows = min(end - t0, 16);
+    const auto kr = buffer_range(kb0 + (int64_t)t0 * g.kst, rows_bytes(rows, kstb, D * 2));
+#pragma unroll
+    for (int i = 0; i < NK; ++i) bf.a[i] = buffer_load16<POL>(kr, koff[i]);
+    __builtin_amdgcn_sched_barrier(0);
+  };
+  // The key stream starts first: the prologue's loads below wait behind it.
+  constexpr int WSTRIDE = 16 * (kThreads / 64);
+  const int t_first = base0 + wave * 16;
+  Buf b0, b1, b2;
+  load(t_first, b0);
+  load(t_first + WSTRIDE, b1);
+
+  char* tile = reinterpret_cast<char*>(qsh) + wave * 16 * PITCH;
+  kbf16x8* mub = reinterpret_cast<kbf16x8*>(reinterpret_cast<char*>(qsh) + TILE_BYTES);
+  // B fragments of the mu block: lane (c, kg) of K-block kb holds column c,
+  // channels 32 kb + 8 kg + t: mu's hi, mid and lo bf16 terms in columns 0,
+  // 1, 2 and zeros elsewhere.
+  for (int e = tid; e < NK * 64; e += kThreads) {
+    const int kb = e >> 6, c = e & 15, g4 = (e >> 4) & 3;
+    kbf16x8 f;
+#pragma unroll
+    for (int t = 0; t < 8; ++t) {
+      const float m = (float)mu[(int64_t)u * D + 32 * kb + 8 * g4 + t];
+      const __bf16 hi = (__bf16)m;
+      const __bf16 mid = (__bf16)(m - (float)hi);
+      const __bf16 lo = (__bf16)((m - (float)hi) - (float)mid);
+      f[t] = c == 0 ? hi : c == 1 ? mid : c == 2 ? lo : (__bf16)0.0f;
+    }
+    mub[e] = f;
+  }
+  // X's B fragments, in registers (as the leverage pass holds L^{-1}).
+  kbf16x8 bh[NLP], bl[NLP];
+  const uint16_t* xf = xfrag + (int64_t)u * NLP * 2 * 64 * 8;
+#pragma unroll
+  for (int p = 0; p < NLP; ++p) {
+    bh[p] = *reinterpret_cast<const kbf16x8*>(xf + ((int64_t)(p * 2 + 0) * 64 + lane) * 8);
+    bl[p] = *reinterpret_cast<const kbf16x8*>(xf + ((int64_t)(p * 2 + 1) * 64 + lane) * 8);
+  }
+  drain_vmem();
+  __syncthreads();  // mu fragments visible
+
+  auto step = [&](int t0, const Buf& bf) {
+#pragma unroll
+    for (int i = 0; i < NK; ++i)
+      *reinterpret_cast<uint4*>(tile + (RPL * i + rrow) * PITCH + rpc * 16) = bf.a[i];
+    kbf16x8 cur[NK];
+#pragma unroll
+    for (int kb = 0; kb < NK; ++kb)
+      cur[kb] = *reinterpret_cast<const kbf16x8*>(tile + ch * PITCH + kb * 64 + kg * 16);
+    kfloatx4 zc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int kb = 0; kb < NK; ++kb)
+      zc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(cur[kb], mub[kb * 64 + lane], zc, 0, 0, 0);
+    float ss[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int jp = 0; jp < NB / 2; ++jp) {
+      kfloatx4 y0 = {0.f, 0.f, 0.f, 0.f}, y1 = {0.f, 0.f, 0.f, 0.f};
+      const int q0 = jp * (jp + 1);             // pair index of (2 jp, 0)
+      const int q1 = jp * (jp + 1) + (jp + 1);  // pair index of (2 jp + 1, 0)
+#pragma unroll
+      for (int kb = 0; kb <= jp; ++kb) {
+        y0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(cur[kb], bh[q0 + kb], y0, 0, 0, 0);
+        y1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(cur[kb], bh[q1 + kb], y1, 0, 0, 0);
+        y0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(cur[kb], bl[q0 + kb], y0, 0, 0, 0);
+        y1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(cur[kb], bl[q1 + kb], y1, 0, 0, 0);
+      }
+#pragma unroll
+      for (int r = 0; r < 4; ++r) ss[r] += y0[r] * y0[r] + y1[r] * y1[r];
+    }
+    // The step's place in its chunk (steps never straddle two chunks).
+    const int tc = (t0 - base0) & (kKChunk - 1);
+    // kappa: ss[r] is this lane's output channel's part of token 4 kg + r;
+    // the transposing row reduction of the leverage pass leaves token rl's
+    // sum in lane ch (ch % 4 == 0 stores it).
+    const bool hi8 = ch >= 8, hi4 = (ch & 4) != 0;
+    const float m0 = (hi8 ? ss[2] : ss[0]) + dpp_f32<kDppMirror>(hi8 ? ss[0] : ss[2]);
+    const float m1 = (hi8 ? ss[3] : ss[1]) + dpp_f32<kDppMirror>(hi8 ? ss[1] : ss[3]);
+    float sv = (hi4 ? m1 : m0) + dpp_f32<kDppHalfMirror>(hi4 ? m0 : m1);
+    sv += dpp_f32<kDppQuadXor1>(sv);
+    sv += dpp_f32<kDppQuadXor2>(sv);
+    if ((ch & 3) == 0) ksq[tc + 4 * kg + rl] = sv;
+    // z: columns 0..3 of the mu block sit in lanes ch = 0..3 (column 3 is
+    // zero); a quad sum leaves token 4 kg + r's dot product in lane ch = 0.
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      float zv = zc[r];
+      zv += dpp_f32<kDppQuadXor1>(zv);
+      zv += dpp_f32<kDppQuadXor2>(zv);
+      if (ch == 0)
+        zsh[tc + 4 * kg + r] = t0 + 4 * kg + r < end ? (float)((double)zv * inv_scale) : -INFINITY;
+    }
+  };
+  // Every step of the chunks runs (steps past the unit's end store -inf
+  // logits), so that each chunk's epilogue sees the whole chunk; the
+  // epilogue follows the chunk's last step (the same step count in every
+  // wave), while the loads for the next chunk are already in flight.
+  constexpr int SPC = kKChunk / WSTRIDE;  // steps per wave per chunk
+  static_assert((kKChunk & (kKChunk - 1)) == 0 && kKChunk % WSTRIDE == 0, "chunks of whole steps");
+  int done = 0;
+  auto after = [&]() {
+    if (++done % SPC == 0) {
+      const int c = done / SPC - 1;
+      kpass_epilogue(un, u, base0 + c * kKChunk, trow, zsh, ksq, red, zout, kout, cstat, kchunks,
+                     status, uflags, chunk0 + c);
+    }
+  };
+  for (int t0 = t_first; t0 < lim; t0 += 3 * WSTRIDE) {
+    load(t0 + 2 * WSTRIDE, b2);
+    step(t0, b0);
+    after();
+    if (t0 + WSTRIDE >= lim) break;
+    load(t0 + 3 * WSTRIDE, b0);
+    step(t0 + WSTRIDE, b1);
+    after();
+    if (t0 + 2 * WSTRIDE >= lim) break;
+    load(t0 + 4 * WSTRIDE, b1);
+    step(t0 + 2 * WSTRIDE, b2);
+    after();
+  }
+}
+
 template <typename T, int D>
 static void kpass_dispatch(const Launch& L, const void* k, bool full, dim3 grid, double inv_scale) {
   const Geo& g = L.geo;
@@ -728,6 +934,29 @@ hipError_t launch_kpass(const Launch& L, const void* k, const void* q) {
   const double inv_scale = 1.0 / ((double)L.cfg->temperature * sqrt((double)g.D));
   const dim3 grid((unsigned)chunked_grid(g, L.ws.kchunks));
   const bool bf = L.cfg->dtype == JACAP_DTYPE_BF16;
+  if (full_kpass_tri(L, q)) {  // ||X k||^2 from Lambda_Q's factor (launch_qfactor)
+    // up to kTriChunks chunks per workgroup, fewer while the grid would
+    // otherwise hold under kLevMinBlocks workgroups
+    int sub = kTriChunks;
+    while (sub > 1 && (int64_t)(L.ws.kchunks + sub - 1) / sub * (g.U / g.V) < kLevMinBlocks) sub /= 2;
+    const dim3 tgrid((unsigned)chunked_grid(g, (L.ws.kchunks + sub - 1) / sub));
+    auto go = [&](auto kern) {
+      kern<<<tgrid, kThreads, 0, L.stream>>>(
+          g, (const uint16_t*)k, (const uint16_t*)q, ws_ptr<double>(L.wsp, L.ws.mu),
+          ws_ptr<uint16_t>(L.wsp, L.ws.lfrag), ws_ptr<float>(L.wsp, L.ws.z),
+          ws_ptr<float>(L.wsp, L.ws.kappa), ws_ptr<float2>(L.wsp, L.ws.cstat), L.ws.kchunks, sub,
+          inv_scale, ws_ptr<uint32_t>(L.wsp, L.ws.status), ws_ptr<uint32_t>(L.wsp, L.ws.uflags));
+    };
+    // K rows read once (pooled group): streamed; by the V units of a KV head: cached
+    if (g.V == 1) {
+      if (g.D == 128) go(kpass_tri_kernel<128, kPolicyStream>);
+      else go(kpass_tri_kernel<64, kPolicyStream>);
+    } else {
+      if (g.D == 128) go(kpass_tri_kernel<128, kPolicyShared>);
+      else go(kpass_tri_kernel<64, kPolicyShared>);
+    }
+    return hipGetLastError();
+  }
   if (full_kpass_on_mfma(L, q)) {  // window queries at hand: the MFMA tile
     auto go = [&](auto kern) {
       kern<<<grid, kThreads, 0, L.stream>>>(

@@ -1,8 +1,8 @@
 """Full-size workloads in the benchmark's launch configuration.
 
 Every unit (sequence, layer, KV head) is scored in one jacap_evict call at the
-real shape. For prefill32k (budgets 128 and 2048), long128k (ridge 1 and 0)
-and ragged16 every unit is checked against the fp64 oracle (run in parallel
+real shape. For prefill32k (budgets 128 and 2048), long128k (ridge 1 and 0;
+FULL covariance at ridge 1) and ragged16 every unit is checked against the fp64 oracle (run in parallel
 worker processes): every score within the bf16 tolerance, jacap_select on the
 oracle's fp32 scores bit-equal to the oracle's selection, the GPU selection
 equal to the select rule on the GPU's own scores, and the overlap of the GPU's
@@ -83,7 +83,7 @@ def _check_sampled(case, prob, budget, ridge, label, mode="diag", gqa="pooled"):
           f"overlap with oracle selection {np.round(ovs, 4).tolist()}", flush=True)
 
 
-def _check_every_unit(case, probs, ridge, label, select_budgets):
+def _check_every_unit(case, probs, ridge, label, select_budgets, cov_mode="diag"):
     """Every unit against the oracle. probs: {budget: GPU problem after
     jacap_evict}; the scores do not depend on the budget, so those of the
     first are compared. For the budgets in select_budgets, jacap_select runs
@@ -98,7 +98,8 @@ def _check_every_unit(case, probs, ridge, label, select_budgets):
     worst, worst_unit, ovs = 0.0, None, {bud: [] for bud in budgets}
     t0 = time.time()
     count = 0
-    for (b, l, h, s32, idx, singular) in oracle_all_units(case, budgets=budgets, ridge=ridge):
+    for (b, l, h, s32, idx, singular) in oracle_all_units(case, budgets=budgets, ridge=ridge,
+                                                          cov_mode=cov_mode):
         assert not singular, (label, (b, l, h))
         lo, hi = token_slice(case, b)
         g = gsc[l, h, lo:hi].double().numpy()
@@ -196,14 +197,20 @@ def test_per_head_gqa_long128k():
 
 @pytest.mark.parametrize("wl", ["prefill32k", "long128k"])
 def test_full_covariance_fullsize(wl):
-    """FULL covariance at full size (N_s = 128 and 256 pooled window queries):
-    the MFMA K pass, sampled units against the oracle, properties on all."""
+    """FULL covariance at full size. prefill32k (N_s = 128 pooled window
+    queries) takes the window tile: sampled units against the oracle,
+    properties on all. long128k (N_s = 256 = 2 d, 131072 tokens) takes kappa
+    from the triangular factor of Lambda_Q: every unit against the oracle."""
     case = make_case(wl, device="cuda")
     budget = case.workload.budget_k
     prob, flags = run_gpu(case, budget, cov_mode=1)
     assert flags == 0, flags
     _check_all_units_properties(case, prob, budget, 1.0)
-    _check_sampled(case, prob, budget, 1.0, f"{wl} full", mode="full")
+    if wl == "long128k":
+        _check_every_unit(case, {budget: prob}, 1.0, f"{wl} full", select_budgets=(),
+                          cov_mode="full")
+    else:
+        _check_sampled(case, prob, budget, 1.0, f"{wl} full", mode="full")
     del prob
     del case
     _free()

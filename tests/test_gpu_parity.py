@@ -148,6 +148,43 @@ def test_full_covariance_window_shapes_bf16(jacap, d, heads, window):
     check_case(case, 64, 1.0, "full", label=f"full d={d} N_s={heads * window}", jacap=jacap)
 
 
+def _low_rank_window(case, b, l, h, rank, noise, seed):
+    """Replace the pooled window of unit (b, l, h) by queries spanning `rank`
+    directions plus isotropic noise of standard deviation `noise` (0: a
+    Lambda_Q of rank `rank`, up to the bf16 rounding of the queries)."""
+    w = case.workload
+    g = w.num_q_heads // w.num_kv_heads
+    gen = torch.Generator().manual_seed(seed)
+    basis = torch.randn((rank, w.head_dim), generator=gen)
+    coef = torch.randn((g, w.window, rank), generator=gen)
+    centre = torch.randn((w.head_dim,), generator=gen)
+    q = centre + coef @ basis / rank ** 0.5
+    q = q + noise * torch.randn((g, w.window, w.head_dim), generator=gen)
+    case.q_win[b, l, h * g:(h + 1) * g] = q.to(case.q_win.dtype)
+
+
+@pytest.mark.parametrize("d,heads,window", [(128, 4, 64), (64, 4, 32), (64, 8, 32)])
+def test_full_covariance_triangular_path(jacap, d, heads, window):
+    """FULL covariance with bf16 keys, N_s >= 2 d and units of at least 8192
+    tokens: kappa = ||X k||^2 from the factor Lambda_Q = X^T X. In the same
+    launch the window tile scores the shorter units (3000 and 1 tokens; an
+    empty sequence), a unit whose window spans d / 8 directions (rank-deficient
+    Lambda_Q) and one with no query noise beyond bf16 rounding in d / 2 of
+    them; a unit whose window spans d / 2 directions plus noise at 0.06 of
+    their scale (pivot ratios ~4e-3, just above the factor's cut) stays on the
+    triangular path."""
+    case = make_case("ragged16", seq_lens=(9000, 0, 3000, 1, 8192), num_layers=2,
+                     num_kv_heads=2, num_q_heads=2 * heads, window=window, head_dim=d,
+                     dtype="bf16")
+    _low_rank_window(case, 0, 1, 0, d // 8, 0.0, seed=11)
+    _low_rank_window(case, 4, 0, 1, d // 2, 0.0, seed=12)
+    _low_rank_window(case, 4, 1, 1, d // 2, 0.06, seed=13)
+    case = case.to("cuda")
+    for ridge in (1.0, 0.0):
+        check_case(case, 256, ridge, "full", label=f"full-tri d={d} N_s={heads * window}",
+                   jacap=jacap)
+
+
 @pytest.mark.parametrize("dtype,d", [("bf16", 128), ("bf16", 64), ("fp32", 64), ("fp32", 128)])
 def test_ragged_small(jacap, dtype, d):
     lens = [0, 1, 17, 255, 256, 257, 1000, 8193]
