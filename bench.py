@@ -81,6 +81,9 @@ TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic.json")
 PHASE_SOURCES = {
     "qstats": ("k_stats.hip", "qstats_kernel", "launch_qstats"),
     "kpass": ("k_stats.hip", "kpass_quad_kernel", "launch_kpass"),
+    # FULL covariance on the triangular path: the K pass and the factor of Lambda_Q
+    "kpass_tri": ("k_stats.hip", "kpass_tri_kernel", "launch_kpass"),
+    "qfactor": ("k_factor.hip", "qfactor_kernel", "launch_qfactor"),
     "weights": ("k_stats.hip", "softmax_weights_kernel", "launch_softmax_weights"),
     "gram": ("k_gram.hip", "gram_mfma_kernel", "launch_gram"),
     "gram_reduce": ("k_gram.hip", "gram_reduce_kernel", "launch_gram_reduce"),
@@ -150,6 +153,18 @@ def source_sha(phase):
         parts.append(funcs[name])
         todo.extend(f for f in funcs if f not in seen and re.search(r"\b%s\b" % f, funcs[name]))
     return hashlib.sha256("\n".join(parts).encode()).hexdigest()[:16]
+
+
+def traffic_key(phase, cov, gqa, w, case):
+    """The counter record of `phase`'s kernel in this configuration: FULL
+    covariance with bf16 keys, 2 d <= N_s <= 256 window queries per scored
+    unit and a sequence of at least 8192 tokens runs the triangular K pass."""
+    ns = w.window if gqa == "per_head" else (w.num_q_heads // w.num_kv_heads) * w.window
+    if phase == "kpass" and cov == "full":
+        tri = (w.dtype == "bf16" and 2 * w.head_dim <= ns <= 256 and
+               max(case.seq_lens) >= 8192)
+        return "kpass_tri" if tri else "kpass_full"
+    return phase
 
 
 def recorded_traffic(phase, workload):
@@ -402,7 +417,7 @@ def main():
     tokens_per_s = case.total_tokens / (ms * 1e-3)
     dom_bytes = phase_bytes(dominant, case, budget, prob)
     achieved = dom_bytes / (dom_avg * 1e-3) / 1e9 if dom_bytes else None
-    traffic = recorded_traffic(dominant, w.name)
+    traffic = recorded_traffic(traffic_key(dominant, args.cov, args.gqa, w, case), w.name)
     # measured ceiling for streaming reads: the probe over the K cache
     probe_bytes, probe_gbs = read_probe(jacap, case.k, stream)
 

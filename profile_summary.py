@@ -36,6 +36,8 @@ COPY_BYTES = 1 << 30
 PHASE_KERNELS = {
     "qstats": r"jacap::qstats_kernel",
     "kpass": r"jacap::kpass_(quad_)?kernel",
+    "kpass_tri": r"jacap::kpass_tri_kernel",
+    "qfactor": r"jacap::qfactor_kernel",
     "weights": r"jacap::softmax_weights_kernel",
     "gram": r"jacap::gram_mfma_kernel<\d+, 2, \d+>",
     "leverage": r"jacap::leverage_mfma_kernel",
