@@ -144,6 +144,7 @@ __device__ __forceinline__ bool grid_unit_chunk(const Geo& g, int nchunks, int& 
 // loop and skip unmarked units, so a launch costs a few microseconds however
 // many units and chunks the batch has.
 constexpr int kRefineBlocks = 512;
+constexpr int kComputeUnits = 256;  // MI355X
 
 inline int64_t chunked_grid(const Geo& g, int nchunks) {
   const int64_t pairs = (int64_t)nchunks * (g.U / g.V);

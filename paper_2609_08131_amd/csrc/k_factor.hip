@@ -56,7 +56,8 @@ constexpr double kPivRelSingularBf16 = 1e-10;
 constexpr double kPivRelSingularFp32 = 1e-8;
 
 // Eight waves: two per SIMD, so that one wave's LDS and fp64 latencies
-// overlap the other's work.
+// overlap the other's work (the capacity factorisation also has a
+// four-wave shape, see factor_kernel).
 constexpr int kFactorThreads = 512;
 
 // Lane N of each 16-lane row, broadcast to the row (one 64-bit DPP move,
@@ -151,7 +152,7 @@ __device__ __forceinline__ void store_lower_frags(uint16_t* __restrict__ out, F 
 // every thread). idg receives 1 / L_rr. Returns 0, or the flag that stopped
 // it -- kUnitNonfinite for a non-finite pivot, `fail` for a pivot at or below
 // piv_rel times its diagonal entry -- the same value in every thread.
-template <int D>
+template <int D, int NT>
 __device__ __forceinline__ int cholesky_lds(double* A, const double* dg, double* idg, int* bad,
                                             double piv_rel, int fail) {
   constexpr int NB = D / 16;
@@ -234,7 +235,7 @@ __device__ __forceinline__ int cholesky_lds(double* A, const double* dg, double*
     __syncthreads();
     if (*bad) return *bad;
     // 2. Panel rows r >= c + 16: L[r, c:c+16] = A[r, c:c+16] L_kk^{-T}.
-    for (int r = c + 16 + tid; r < D; r += kFactorThreads) {
+    for (int r = c + 16 + tid; r < D; r += NT) {
       double x[16];
 #pragma unroll
       for (int t = 0; t < 16; ++t) x[t] = A[lidx(r, c + t)];
@@ -258,7 +259,7 @@ __device__ __forceinline__ int cholesky_lds(double* A, const double* dg, double*
     const int m = NB - kb - 1;
     if (m > 0) {
       const int r16 = lane & 15, q4 = lane >> 4;
-      for (int e = wave; e < m * (m + 1) / 2; e += kFactorThreads / 64) {
+      for (int e = wave; e < m * (m + 1) / 2; e += NT / 64) {
         int bi, bj;
         tri_index(e, bi, bj);
         const int I = 16 * (kb + 1 + bi), J = 16 * (kb + 1 + bj);
@@ -281,7 +282,7 @@ __device__ __forceinline__ int cholesky_lds(double* A, const double* dg, double*
 // `red`. PASS 1: a unit marked kUnitRefine by pass 0 (bf16 path), from its fp64
 // partial Grams `part` (pchunks per unit), summed here in chunk order. FRAGS:
 // bf16 inputs.
-template <int D, bool FRAGS>
+template <int D, bool FRAGS, int NT>
 __device__ __forceinline__ void factor_unit(const Geo& g, int u, double* __restrict__ red,
                                             const double* __restrict__ part, int pchunks,
                                             int pchunk, double ridge,
@@ -302,7 +303,7 @@ __device__ __forceinline__ void factor_unit(const Geo& g, int u, double* __restr
   __shared__ double A[NB * (NB + 1) / 2 * kBlk];  // lower 16x16 blocks, see lidx
   __shared__ double dg[D];   // diagonal of A before factorisation
   __shared__ double idg[D];  // 1 / L_rr
-  __shared__ double red_sh[kFactorThreads / 64];
+  __shared__ double red_sh[NT / 64];
   __shared__ int bad;        // 0, or the unit flag that stops the factorisation
 
   // Lower triangle of A = ridge I + M from the upper blocks of M. Entries
@@ -310,12 +311,12 @@ __device__ __forceinline__ void factor_unit(const Geo& g, int u, double* __restr
   // pairs first (all loads in flight), then places them.
   const double* R = red + (int64_t)u * (NPAIR * 256);
   constexpr int NE2 = NPAIR * 128;  // entry pairs
-  constexpr int PER = (NE2 + kFactorThreads - 1) / kFactorThreads;
+  constexpr int PER = (NE2 + NT - 1) / NT;
   double2 rv[PER];
   if (part == nullptr) {
 #pragma unroll
     for (int k = 0; k < PER; ++k) {
-      const int e2 = tid + k * kFactorThreads;
+      const int e2 = tid + k * NT;
       if (e2 < NE2) rv[k] = reinterpret_cast<const double2*>(R)[e2];
     }
   } else {  // fixed-order sum of the unit's fp64 partials
@@ -326,7 +327,7 @@ __device__ __forceinline__ void factor_unit(const Geo& g, int u, double* __restr
     for (int c = 0; c < nch; ++c) {
 #pragma unroll
       for (int k = 0; k < PER; ++k) {
-        const int e2 = tid + k * kFactorThreads;
+        const int e2 = tid + k * NT;
         if (e2 < NE2) {
           const double2 x = P[(int64_t)c * NE2 + e2];
           rv[k].x += x.x;
@@ -337,7 +338,7 @@ __device__ __forceinline__ void factor_unit(const Geo& g, int u, double* __restr
   }
 #pragma unroll
   for (int k = 0; k < PER; ++k) {
-    const int e2 = tid + k * kFactorThreads;
+    const int e2 = tid + k * NT;
     if (e2 < NE2) {
       const int e = 2 * e2;
       int p = e >> 8, bi = 0;  // block pair p -> block (bi, bj), bi <= bj, row-major
@@ -360,13 +361,13 @@ __device__ __forceinline__ void factor_unit(const Geo& g, int u, double* __restr
   const double sc = wscale[u];
   if (g.ridge_mat) {  // output-projection variant: A = R + M
     const double* Rm = g.ridge_mat + ((int64_t)un.l * g.H + un.h) * D * D;
-    for (int e = tid; e < D * D; e += kFactorThreads) {
+    for (int e = tid; e < D * D; e += NT) {
       const int r = e / D, cc = e % D;
       if (cc <= r) A[lidx(r, cc)] += Rm[e] * sc;
     }
     __syncthreads();
   }
-  for (int a = tid; a < D; a += kFactorThreads) {
+  for (int a = tid; a < D; a += NT) {
     if (!g.ridge_mat) A[lidx(a, a)] += ridge * sc;
     dg[a] = A[lidx(a, a)];
     if (!isfinite(dg[a])) atomicOr(&bad, (int)kUnitNonfinite);
@@ -379,7 +380,7 @@ __device__ __forceinline__ void factor_unit(const Geo& g, int u, double* __restr
 
   // max over rows of sum_c |A[r][c]| (>= lambda_max(A), A symmetric with its
   // lower triangle stored); TPR threads per row.
-  constexpr int TPR = kFactorThreads / D;
+  constexpr int TPR = NT / D;
   const int prow = tid / TPR, ppart = tid % TPR;
   auto block_max = [&](double v) {
     v = wave_max_f64(v);
@@ -388,7 +389,7 @@ __device__ __forceinline__ void factor_unit(const Geo& g, int u, double* __restr
     __syncthreads();
     double m = red_sh[0];
 #pragma unroll
-    for (int w = 1; w < kFactorThreads / 64; ++w) m = fmax(m, red_sh[w]);
+    for (int w = 1; w < NT / 64; ++w) m = fmax(m, red_sh[w]);
     return m;
   };
 
@@ -403,7 +404,7 @@ __device__ __forceinline__ void factor_unit(const Geo& g, int u, double* __restr
 
   // ---------------- Cholesky A = L L^T (L overwrites the lower triangle) ----
   const int code =
-      cholesky_lds<D>(A, dg, idg, &bad, piv_rel, may_refine ? (int)kUnitRefine : (int)kUnitSingular);
+      cholesky_lds<D, NT>(A, dg, idg, &bad, piv_rel, may_refine ? (int)kUnitRefine : (int)kUnitSingular);
   if (code) {
     if (tid == 0) {
       if (code == (int)kUnitRefine) atomicOr(uflags + u, kUnitRefine);
@@ -432,7 +433,7 @@ __device__ __forceinline__ void factor_unit(const Geo& g, int u, double* __restr
       if (i > t) A[lidx((c + t), c + i)] = x[i];
   }
   __syncthreads();
-  for (int e = tid; e < NB * 256; e += kFactorThreads) {
+  for (int e = tid; e < NB * 256; e += NT) {
     const int c = 16 * (e >> 8), i = (e >> 4) & 15, t = e & 15;
     if (i > t) A[lidx((c + i), c + t)] = A[lidx((c + t), c + i)];
     else if (i == t) A[lidx((c + i), c + i)] = idg[c + i];
@@ -447,7 +448,7 @@ __device__ __forceinline__ void factor_unit(const Geo& g, int u, double* __restr
   //    upper halves hold the temporaries of step 4).
   {
     const int r16 = lane & 15, q4 = lane >> 4;
-    constexpr int NW = kFactorThreads / 64;
+    constexpr int NW = NT / 64;
     constexpr int PW = (NB - 1 + NW - 1) / NW;  // output blocks per wave, at most
     for (int J = NB - 2; J >= 0; --J) {
       // output blocks I = J + 1 + wave + NW p, p < PW
@@ -534,7 +535,7 @@ __device__ __forceinline__ void factor_unit(const Geo& g, int u, double* __restr
   // Store L^{-1}.
   if (!may_refine) {  // fp64, over the reduced Gram (already in LDS)
     double* o64 = red + (int64_t)u * (NPAIR * 256);
-    for (int e = tid; e < NPAIR * 256; e += kFactorThreads) {
+    for (int e = tid; e < NPAIR * 256; e += NT) {
       int p = e >> 8, bi = 0;  // block pair p -> (bi, bj), bi <= bj
 #pragma unroll
       for (int q = 0; q < NB; ++q)
@@ -548,16 +549,19 @@ __device__ __forceinline__ void factor_unit(const Geo& g, int u, double* __restr
 }
 
 // PASS 0: one workgroup per unit. PASS 1: a grid-stride walk over the units
-// that skips those not marked kUnitRefine.
-template <int D, bool FRAGS>
-__global__ __launch_bounds__(kFactorThreads) void factor_kernel(
+// that skips those not marked kUnitRefine. NT threads: 512 (eight waves)
+// when the units fit the compute units in one round; 256 (bounded to 256
+// VGPRs, so that two workgroups share a compute unit and one's sequential
+// steps overlap the other's) when there are more.
+template <int D, bool FRAGS, int NT>
+__global__ __launch_bounds__(NT, 512 / NT) void factor_kernel(
     Geo g, double* __restrict__ red, const double* __restrict__ part, int pchunks, int pchunk,
     double ridge, const double* __restrict__ wscale, int pass, uint16_t* __restrict__ lfrag,
     uint32_t* status, uint32_t* uflags) {
   for (int u = blockIdx.x; u < g.U; u += gridDim.x) {
     if (pass == 1 && !(uflags[u] & kUnitRefine)) continue;
-    factor_unit<D, FRAGS>(g, u, red, pass == 1 ? part : nullptr, pchunks, pchunk,
-                                          ridge, wscale, pass, lfrag, status, uflags);
+    factor_unit<D, FRAGS, NT>(g, u, red, pass == 1 ? part : nullptr, pchunks, pchunk, ridge,
+                              wscale, pass, lfrag, status, uflags);
     __syncthreads();  // LDS of this unit fully consumed before the next one's loads
   }
 }
@@ -574,16 +578,17 @@ hipError_t launch_factor(const Launch& L, bool refine) {
   const double ridge = (double)L.cfg->ridge;
   const double* part = ws_ptr<double>(L.wsp, L.ws.gram);
   const int blocks = refine ? std::min(g.U, kRefineBlocks) : g.U;
-  auto go = [&](auto kern) {
-    kern<<<blocks, kFactorThreads, 0, L.stream>>>(g, red, part, L.ws.pchunks, L.ws.pchunk, ridge,
-                                                  wsc, pass, lf, st, uf);
+  const bool pairs = !refine && g.U > kComputeUnits;  // two workgroups per compute unit
+  auto go = [&](auto kern, int nt) {
+    kern<<<blocks, nt, 0, L.stream>>>(g, red, part, L.ws.pchunks, L.ws.pchunk, ridge, wsc, pass,
+                                      lf, st, uf);
   };
   if (L.ws.mfma) {
-    if (g.D == 128) go(factor_kernel<128, true>);
-    else go(factor_kernel<64, true>);
+    if (g.D == 128) pairs ? go(factor_kernel<128, true, 256>, 256) : go(factor_kernel<128, true, 512>, 512);
+    else pairs ? go(factor_kernel<64, true, 256>, 256) : go(factor_kernel<64, true, 512>, 512);
   } else {
-    if (g.D == 128) go(factor_kernel<128, false>);
-    else go(factor_kernel<64, false>);
+    if (g.D == 128) pairs ? go(factor_kernel<128, false, 256>, 256) : go(factor_kernel<128, false, 512>, 512);
+    else pairs ? go(factor_kernel<64, false, 256>, 256) : go(factor_kernel<64, false, 512>, 512);
   }
   return hipGetLastError();
 }
@@ -695,7 +700,7 @@ __device__ __forceinline__ void qfactor_unit(const Geo& g, int u, const uint16_t
   __syncthreads();
   for (int a = tid; a < D; a += kFactorThreads) dg[a] = A[lidx(a, a)];
   __syncthreads();
-  if (cholesky_lds<D>(A, dg, idg, &bad, kPivRelTri, (int)kUnitKTile) != 0) {
+  if (cholesky_lds<D, kFactorThreads>(A, dg, idg, &bad, kPivRelTri, (int)kUnitKTile) != 0) {
     if (tid == 0) atomicOr(uflags + u, kUnitKTile);
     return;
   }
