@@ -160,15 +160,23 @@ __device__ __forceinline__ int cholesky_lds(double* A, const double* dg, double*
   for (int kb = 0; kb < NB; ++kb) {
     const int c = 16 * kb;
     // 1. Diagonal block, in registers of wave 0: lane s (mod 16) holds row s.
+    //    The chain from one pivot to the next is a broadcast, a reciprocal
+    //    square root and one broadcast-FMA; the pivot thresholds are read
+    //    before it starts and the checks stay off it.
     if (wave == 0) {
       const int s = lane & 15;
-      double a[16];
+      double a[16], thr[16], yv[16];
 #pragma unroll
       for (int q = 0; q < 16; ++q) a[q] = (q <= s) ? A[lidx((c + s), c + q)] : 0.0;
+      // A pivot that has lost all but piv_rel of its diagonal entry is within
+      // the rounding noise of A: A is numerically singular at the working
+      // precision (or the caller's fail condition holds).
+#pragma unroll
+      for (int t = 0; t < 16; ++t) thr[t] = piv_rel * dg[c + t];
       // No early exit (the loop must stay fully unrolled so that a[] lives in
-      // registers): after a failed pivot the rest is computed on a stand-in
-      // pivot and discarded.
-      int code = 0;
+      // registers): after a failed pivot the rest is computed on whatever it
+      // produced and discarded; the flag is the first failure's kind.
+      bool failed = false, nonfinite = false;
 #pragma unroll
       for (int t = 0; t < 16; ++t) {
         double piv;  // A[t][t], from lane t of the row
@@ -190,14 +198,11 @@ __device__ __forceinline__ int cholesky_lds(double* A, const double* dg, double*
           case 14: piv = row_bcast_f64<14>(a[t]); break;
           default: piv = row_bcast_f64<15>(a[t]); break;
         }
-        // A pivot that has lost all but piv_rel of its diagonal entry is within
-        // the rounding noise of the accumulated Gram: A is numerically singular
-        // at the path's working precision (rank-deficient M with ridge 0).
-        const bool ok = piv > piv_rel * dg[c + t] && piv > 0.0;
-        if (!ok && code == 0)
-          code = !isfinite(piv) ? (int)kUnitNonfinite : fail;
-        const double y = rsqrt_f64(ok ? piv : 1.0);
-        if (lane == 0) idg[c + t] = y;
+        const bool ok = piv > thr[t] && piv > 0.0;
+        if (!ok && !failed) nonfinite = !isfinite(piv);
+        failed = failed || !ok;
+        const double y = rsqrt_f64(piv);
+        yv[t] = y;
         a[t] = (s == t) ? piv * y : a[t] * y;  // column t of L (rows s < t: unused)
         // a[q] -= L[s][t] L[q][t] for q > t; L[q][t] is lane q's a[t]. Entries
         // with q > s are outside row s's lower part and never stored.
@@ -224,12 +229,17 @@ __device__ __forceinline__ int cholesky_lds(double* A, const double* dg, double*
           a[q] = fma(-a[t], lq, a[q]);
         }
       }
+      const int code = failed ? (nonfinite ? (int)kUnitNonfinite : fail) : 0;
       if (code) {
         if (lane == 0) *bad = code;
       } else if (lane < 16) {
 #pragma unroll
         for (int q = 0; q < 16; ++q)
           if (q <= s) A[lidx((c + s), c + q)] = a[q];
+        if (lane == 0) {
+#pragma unroll
+          for (int t = 0; t < 16; ++t) idg[c + t] = yv[t];
+        }
       }
     }
     __syncthreads();
@@ -239,14 +249,24 @@ __device__ __forceinline__ int cholesky_lds(double* A, const double* dg, double*
       double x[16];
 #pragma unroll
       for (int t = 0; t < 16; ++t) x[t] = A[lidx(r, c + t)];
+      // Row t of L_kk (columns < t) and 1 / L_tt are read one row ahead, so
+      // that the chain does not wait on LDS.
+      double lr[2][16], il[2];
+      il[0] = idg[c];
 #pragma unroll
       for (int t = 0; t < 16; ++t) {
+        const int cur = t & 1, nxt = cur ^ 1;
+        if (t + 1 < 16) {
+#pragma unroll
+          for (int q = 0; q <= t; ++q) lr[nxt][q] = A[lidx((c + t + 1), c + q)];
+          il[nxt] = idg[c + t + 1];
+        }
         // x[t] = (A[r][c+t] - sum_q x[q] L[c+t][c+q]) / L[c+t][c+t]; the sum in
         // four independent chains (latency, not order, bounds this loop)
         double sp[4] = {x[t], 0.0, 0.0, 0.0};
 #pragma unroll
-        for (int q = 0; q < t; ++q) sp[q & 3] = fma(-x[q], A[lidx((c + t), c + q)], sp[q & 3]);
-        x[t] = ((sp[0] + sp[1]) + (sp[2] + sp[3])) * idg[c + t];
+        for (int q = 0; q < t; ++q) sp[q & 3] = fma(-x[q], lr[cur][q], sp[q & 3]);
+        x[t] = ((sp[0] + sp[1]) + (sp[2] + sp[3])) * il[cur];
       }
 #pragma unroll
       for (int t = 0; t < 16; ++t) A[lidx(r, c + t)] = x[t];
