@@ -64,7 +64,29 @@ constexpr int kFactorThreads = 512;
 // row_newbcast).
 template <int N>
 __device__ __forceinline__ double row_bcast_f64(double v) {
-  return __builtin_amdgcn_update_dpp(v, v, 0x150 + N, 0xF, 0xF, false);
+  return __builtin_amdgcn_mov_dpp(v, 0x150 + N, 0xF, 0xF, false);
+}
+// The same for a lane index that is a constant once the caller's loop is
+// unrolled.
+__device__ __forceinline__ double row_bcast_f64_at(double v, int n) {
+  switch (n) {
+    case 0: return row_bcast_f64<0>(v);
+    case 1: return row_bcast_f64<1>(v);
+    case 2: return row_bcast_f64<2>(v);
+    case 3: return row_bcast_f64<3>(v);
+    case 4: return row_bcast_f64<4>(v);
+    case 5: return row_bcast_f64<5>(v);
+    case 6: return row_bcast_f64<6>(v);
+    case 7: return row_bcast_f64<7>(v);
+    case 8: return row_bcast_f64<8>(v);
+    case 9: return row_bcast_f64<9>(v);
+    case 10: return row_bcast_f64<10>(v);
+    case 11: return row_bcast_f64<11>(v);
+    case 12: return row_bcast_f64<12>(v);
+    case 13: return row_bcast_f64<13>(v);
+    case 14: return row_bcast_f64<14>(v);
+    default: return row_bcast_f64<15>(v);
+  }
 }
 
 // 1 / sqrt(x) to full fp64 accuracy: hardware estimate, two Newton steps.
@@ -156,94 +178,87 @@ template <int D, int NT>
 __device__ __forceinline__ int cholesky_lds(double* A, const double* dg, double* idg, int* bad,
                                             double piv_rel, int fail) {
   constexpr int NB = D / 16;
+  constexpr int NW = NT / 64;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  for (int kb = 0; kb < NB; ++kb) {
+  // 1. Diagonal block, in registers of wave 0: lane s (mod 16) holds row s.
+  //    The chain from one pivot to the next is a broadcast, a reciprocal
+  //    square root and one broadcast-FMA; the pivot thresholds are read
+  //    before it starts and the checks stay off it.
+  auto diag = [&](int kb) {
     const int c = 16 * kb;
-    // 1. Diagonal block, in registers of wave 0: lane s (mod 16) holds row s.
-    //    The chain from one pivot to the next is a broadcast, a reciprocal
-    //    square root and one broadcast-FMA; the pivot thresholds are read
-    //    before it starts and the checks stay off it.
-    if (wave == 0) {
-      const int s = lane & 15;
-      double a[16], thr[16], yv[16];
+    const int s = lane & 15;
+    double a[16], thr[16], yv[16];
 #pragma unroll
-      for (int q = 0; q < 16; ++q) a[q] = (q <= s) ? A[lidx((c + s), c + q)] : 0.0;
-      // A pivot that has lost all but piv_rel of its diagonal entry is within
-      // the rounding noise of A: A is numerically singular at the working
-      // precision (or the caller's fail condition holds).
+    for (int q = 0; q < 16; ++q) a[q] = (q <= s) ? A[lidx((c + s), c + q)] : 0.0;
+    // A pivot that has lost all but piv_rel of its diagonal entry is within
+    // the rounding noise of A: A is numerically singular at the working
+    // precision (or the caller's fail condition holds).
 #pragma unroll
-      for (int t = 0; t < 16; ++t) thr[t] = piv_rel * dg[c + t];
-      // No early exit (the loop must stay fully unrolled so that a[] lives in
-      // registers): after a failed pivot the rest is computed on whatever it
-      // produced and discarded; the flag is the first failure's kind.
-      bool failed = false, nonfinite = false;
+    for (int t = 0; t < 16; ++t) thr[t] = piv_rel * dg[c + t];
+    // No early exit (the loop must stay fully unrolled so that a[] lives in
+    // registers): after a failed pivot the rest is computed on whatever it
+    // produced and discarded; the flag is the first failure's kind.
+    bool failed = false, nonfinite = false;
+    double piv = row_bcast_f64<0>(a[0]);  // A[t][t], from lane t of the row
+    double y = rsqrt_f64(piv);
 #pragma unroll
-      for (int t = 0; t < 16; ++t) {
-        double piv;  // A[t][t], from lane t of the row
-        switch (t) {
-          case 0: piv = row_bcast_f64<0>(a[t]); break;
-          case 1: piv = row_bcast_f64<1>(a[t]); break;
-          case 2: piv = row_bcast_f64<2>(a[t]); break;
-          case 3: piv = row_bcast_f64<3>(a[t]); break;
-          case 4: piv = row_bcast_f64<4>(a[t]); break;
-          case 5: piv = row_bcast_f64<5>(a[t]); break;
-          case 6: piv = row_bcast_f64<6>(a[t]); break;
-          case 7: piv = row_bcast_f64<7>(a[t]); break;
-          case 8: piv = row_bcast_f64<8>(a[t]); break;
-          case 9: piv = row_bcast_f64<9>(a[t]); break;
-          case 10: piv = row_bcast_f64<10>(a[t]); break;
-          case 11: piv = row_bcast_f64<11>(a[t]); break;
-          case 12: piv = row_bcast_f64<12>(a[t]); break;
-          case 13: piv = row_bcast_f64<13>(a[t]); break;
-          case 14: piv = row_bcast_f64<14>(a[t]); break;
-          default: piv = row_bcast_f64<15>(a[t]); break;
-        }
-        const bool ok = piv > thr[t] && piv > 0.0;
-        if (!ok && !failed) nonfinite = !isfinite(piv);
-        failed = failed || !ok;
-        const double y = rsqrt_f64(piv);
-        yv[t] = y;
-        a[t] = (s == t) ? piv * y : a[t] * y;  // column t of L (rows s < t: unused)
-        // a[q] -= L[s][t] L[q][t] for q > t; L[q][t] is lane q's a[t]. Entries
-        // with q > s are outside row s's lower part and never stored.
-#pragma unroll
-        for (int q = t + 1; q < 16; ++q) {
-          double lq;
-          switch (q) {
-            case 1: lq = row_bcast_f64<1>(a[t]); break;
-            case 2: lq = row_bcast_f64<2>(a[t]); break;
-            case 3: lq = row_bcast_f64<3>(a[t]); break;
-            case 4: lq = row_bcast_f64<4>(a[t]); break;
-            case 5: lq = row_bcast_f64<5>(a[t]); break;
-            case 6: lq = row_bcast_f64<6>(a[t]); break;
-            case 7: lq = row_bcast_f64<7>(a[t]); break;
-            case 8: lq = row_bcast_f64<8>(a[t]); break;
-            case 9: lq = row_bcast_f64<9>(a[t]); break;
-            case 10: lq = row_bcast_f64<10>(a[t]); break;
-            case 11: lq = row_bcast_f64<11>(a[t]); break;
-            case 12: lq = row_bcast_f64<12>(a[t]); break;
-            case 13: lq = row_bcast_f64<13>(a[t]); break;
-            case 14: lq = row_bcast_f64<14>(a[t]); break;
-            default: lq = row_bcast_f64<15>(a[t]); break;
-          }
-          a[q] = fma(-a[t], lq, a[q]);
-        }
+    for (int t = 0; t < 16; ++t) {
+      const bool ok = piv > thr[t] && piv > 0.0;
+      if (!ok && !failed) nonfinite = !isfinite(piv);
+      failed = failed || !ok;
+      yv[t] = y;
+      a[t] = (s == t) ? piv * y : a[t] * y;  // column t of L (rows s < t: unused)
+      // a[q] -= L[s][t] L[q][t] for q > t; L[q][t] is lane q's a[t]. Entries
+      // with q > s are outside row s's lower part and never stored. Row
+      // t + 1 goes first, and the next pivot's reciprocal square root is
+      // issued before the other rows' updates, which then fill its latency.
+      double pn = 0.0, yn = 0.0;
+      if (t + 1 < 16) {
+        a[t + 1] = fma(-a[t], row_bcast_f64_at(a[t], t + 1), a[t + 1]);
+        pn = row_bcast_f64_at(a[t + 1], t + 1);
+        yn = rsqrt_f64(pn);
       }
-      const int code = failed ? (nonfinite ? (int)kUnitNonfinite : fail) : 0;
-      if (code) {
-        if (lane == 0) *bad = code;
-      } else if (lane < 16) {
 #pragma unroll
-        for (int q = 0; q < 16; ++q)
-          if (q <= s) A[lidx((c + s), c + q)] = a[q];
-        if (lane == 0) {
+      for (int q = t + 2; q < 16; ++q) a[q] = fma(-a[t], row_bcast_f64_at(a[t], q), a[q]);
+      piv = pn;
+      y = yn;
+    }
+    const int code = failed ? (nonfinite ? (int)kUnitNonfinite : fail) : 0;
+    if (code) {
+      if (lane == 0) *bad = code;
+    } else if (lane < 16) {
 #pragma unroll
-          for (int t = 0; t < 16; ++t) idg[c + t] = yv[t];
-        }
+      for (int q = 0; q < 16; ++q)
+        if (q <= s) A[lidx((c + s), c + q)] = a[q];
+      if (lane == 0) {
+#pragma unroll
+        for (int t = 0; t < 16; ++t) idg[c + t] = yv[t];
       }
     }
-    __syncthreads();
-    if (*bad) return *bad;
+  };
+  // 3. Trailing update A_IJ -= L_Ik L_Jk^T of one 16x16 block (I >= J > k,
+  //    block e of the trailing lower triangle, row-major) by one wave on the
+  //    fp64 MFMA (K = 16 in four slices). Diagonal blocks also update their
+  //    upper half, which is unused until the inverse overwrites it.
+  auto update = [&](int kb, int e) {
+    const int c = 16 * kb, r16 = lane & 15, q4 = lane >> 4;
+    int bi, bj;
+    tri_index(e, bi, bj);
+    const int I = 16 * (kb + 1 + bi), J = 16 * (kb + 1 + bj);
+    f64x4 acc = {0.0, 0.0, 0.0, 0.0};
+#pragma unroll
+    for (int kq = 0; kq < 4; ++kq) {
+      const int t = c + 4 * kq + q4;
+      acc = mfma64(A[lidx((I + r16), t)], A[lidx((J + r16), t)], acc);
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) A[lidx((I + 4 * i + q4), J + r16)] -= acc[i];
+  };
+  if (wave == 0) diag(0);
+  __syncthreads();
+  if (*bad) return *bad;
+  for (int kb = 0; kb < NB; ++kb) {
+    const int c = 16 * kb;
     // 2. Panel rows r >= c + 16: L[r, c:c+16] = A[r, c:c+16] L_kk^{-T}.
     for (int r = c + 16 + tid; r < D; r += NT) {
       double x[16];
@@ -272,28 +287,20 @@ __device__ __forceinline__ int cholesky_lds(double* A, const double* dg, double*
       for (int t = 0; t < 16; ++t) A[lidx(r, c + t)] = x[t];
     }
     __syncthreads();
-    // 3. Trailing update A_IJ -= L_Ik L_Jk^T for the 16x16 blocks I >= J > k,
-    //    one block per wave at a time on the fp64 MFMA (K = 16 in four
-    //    slices). Diagonal blocks also update their upper half, which is
-    //    unused until the inverse overwrites it.
+    // Look-ahead: wave 0 updates the next diagonal block and factors it at
+    // once, while the other waves take the rest of the trailing update, so
+    // that the update is hidden behind the pivot chain.
     const int m = NB - kb - 1;
     if (m > 0) {
-      const int r16 = lane & 15, q4 = lane >> 4;
-      for (int e = wave; e < m * (m + 1) / 2; e += NT / 64) {
-        int bi, bj;
-        tri_index(e, bi, bj);
-        const int I = 16 * (kb + 1 + bi), J = 16 * (kb + 1 + bj);
-        f64x4 acc = {0.0, 0.0, 0.0, 0.0};
-#pragma unroll
-        for (int kq = 0; kq < 4; ++kq) {
-          const int t = c + 4 * kq + q4;
-          acc = mfma64(A[lidx((I + r16), t)], A[lidx((J + r16), t)], acc);
-        }
-#pragma unroll
-        for (int i = 0; i < 4; ++i) A[lidx((I + 4 * i + q4), J + r16)] -= acc[i];
+      if (wave == 0) {
+        update(kb, 0);  // block (kb + 1, kb + 1)
+        diag(kb + 1);
+      } else {
+        for (int e = wave; e < m * (m + 1) / 2; e += NW - 1) update(kb, e);
       }
+      __syncthreads();
+      if (*bad) return *bad;
     }
-    __syncthreads();
   }
   return 0;
 }
