@@ -331,6 +331,7 @@ __device__ __forceinline__ void factor_unit(const Geo& g, int u, double* __restr
   __shared__ double dg[D];   // diagonal of A before factorisation
   __shared__ double idg[D];  // 1 / L_rr
   __shared__ double red_sh[NT / 64];
+  __shared__ double red_sh2[NT / 64];
   __shared__ int bad;        // 0, or the unit flag that stops the factorisation
 
   // Lower triangle of A = ridge I + M from the upper blocks of M. Entries
@@ -409,6 +410,24 @@ __device__ __forceinline__ void factor_unit(const Geo& g, int u, double* __restr
   // lower triangle stored); TPR threads per row.
   constexpr int TPR = NT / D;
   const int prow = tid / TPR, ppart = tid % TPR;
+  // Row prow's entries and column prow's entries at b = ppart + TPR j: with
+  // TPR dividing 16, b's block (TPR j / 16) and offset in it (TPR j mod 16,
+  // plus ppart) are constants of j, so each address is a per-thread base plus
+  // a constant. row_at(j): entry (prow, b), stored for b <= prow; col_at(j):
+  // entry (b, prow), stored for b >= prow (other j give in-range addresses
+  // whose values are not used).
+  static_assert(16 % TPR == 0, "threads per row divide a block row");
+  const int pI = prow >> 4, pr = prow & 15;
+  const int rbase = (pI * (pI + 1) / 2) * kBlk + pr * kBP + ppart;
+  const int cbase = pI * kBlk + ppart * kBP + pr;
+  auto row_at = [&](int j) {
+    const int Ib = (TPR * j) >> 4, o = (TPR * j) & 15;
+    return rbase + Ib * kBlk + o;
+  };
+  auto col_at = [&](int j) {
+    const int Ib = (TPR * j) >> 4, o = (TPR * j) & 15;
+    return cbase + (Ib * (Ib + 1) / 2) * kBlk + o * kBP;
+  };
   auto block_max = [&](double v) {
     v = wave_max_f64(v);
     __syncthreads();
@@ -423,7 +442,11 @@ __device__ __forceinline__ void factor_unit(const Geo& g, int u, double* __restr
   double anorm = 0.0;
   if (may_refine) {
     double sr = 0.0;
-    for (int b = ppart; b < D; b += TPR) sr += fabs((b <= prow) ? A[lidx(prow, b)] : A[lidx(b, prow)]);
+#pragma unroll 8
+    for (int j = 0; j < D / TPR; ++j) {
+      const int b = ppart + TPR * j;
+      sr += fabs((b <= prow) ? A[row_at(j)] : A[col_at(j)]);
+    }
 #pragma unroll
     for (int o = 1; o < TPR; o <<= 1) sr += __shfl_xor(sr, o);
     anorm = block_max(sr);
@@ -469,10 +492,12 @@ __device__ __forceinline__ void factor_unit(const Geo& g, int u, double* __restr
   // 5. Off-diagonal blocks of X, block column J from right to left, in place:
   //    X_IJ = -(sum_{M=J+1..I} X_IM L_MJ) X_JJ for I > J ((X L)_IJ = 0), where
   //    the blocks X_IM (M > J) are final and L_MJ still in place. One 16x16
-  //    output block per wave on the fp64 MFMA; each product is held in
-  //    registers until every wave has read its operands, then stored over
-  //    L_IJ. The triangular X blocks are masked above their diagonal (their
-  //    upper halves hold the temporaries of step 4).
+  //    output block per wave on the fp64 MFMA; the sum is held in registers
+  //    until every wave has read its operands, then stored over L_IJ, and
+  //    the wave multiplies its own stored block by X_JJ at once (no other
+  //    wave reads it until the next block column). The triangular X blocks
+  //    are masked above their diagonal (their upper halves hold the
+  //    temporaries of step 4).
   {
     const int r16 = lane & 15, q4 = lane >> 4;
     constexpr int NW = NT / 64;
@@ -486,50 +511,41 @@ __device__ __forceinline__ void factor_unit(const Geo& g, int u, double* __restr
         const int I = J + 1 + wave + NW * p;
         if (I < NB) {
           for (int M = J + 1; M <= I; ++M) {
+            // the block step's operands, all loaded before its MFMAs
+            double x[4], l[4];
 #pragma unroll
             for (int kq = 0; kq < 4; ++kq) {
               const int t = 4 * kq + q4;
-              const double x = (M < I || r16 >= t) ? A[lidx(16 * I + r16, 16 * M + t)] : 0.0;
-              const double l = A[lidx(16 * M + t, 16 * J + r16)];
-              acc[p] = mfma64(x, l, acc[p]);
+              x[kq] = (M < I || r16 >= t) ? A[lidx(16 * I + r16, 16 * M + t)] : 0.0;
+              l[kq] = A[lidx(16 * M + t, 16 * J + r16)];
             }
+#pragma unroll
+            for (int kq = 0; kq < 4; ++kq) acc[p] = mfma64(x[kq], l[kq], acc[p]);
           }
         }
       }
-      __syncthreads();
+      __syncthreads();  // every wave's reads of L_.J done
 #pragma unroll
       for (int p = 0; p < PW; ++p) {
         const int I = J + 1 + wave + NW * p;
         if (I < NB) {
 #pragma unroll
           for (int i = 0; i < 4; ++i) A[lidx(16 * I + 4 * i + q4, 16 * J + r16)] = acc[p][i];
-        }
-      }
-      __syncthreads();
-#pragma unroll
-      for (int p = 0; p < PW; ++p) {
-        acc[p] = f64x4{0.0, 0.0, 0.0, 0.0};
-        const int I = J + 1 + wave + NW * p;
-        if (I < NB) {
+          double tv[4], x[4];
 #pragma unroll
           for (int kq = 0; kq < 4; ++kq) {
             const int t = 4 * kq + q4;
-            const double tv = A[lidx(16 * I + r16, 16 * J + t)];
-            const double x = t >= r16 ? A[lidx(16 * J + t, 16 * J + r16)] : 0.0;
-            acc[p] = mfma64(tv, x, acc[p]);
+            tv[kq] = A[lidx(16 * I + r16, 16 * J + t)];
+            x[kq] = t >= r16 ? A[lidx(16 * J + t, 16 * J + r16)] : 0.0;
           }
+          f64x4 out = {0.0, 0.0, 0.0, 0.0};
+#pragma unroll
+          for (int kq = 0; kq < 4; ++kq) out = mfma64(tv[kq], x[kq], out);
+#pragma unroll
+          for (int i = 0; i < 4; ++i) A[lidx(16 * I + 4 * i + q4, 16 * J + r16)] = -out[i];
         }
       }
-      __syncthreads();
-#pragma unroll
-      for (int p = 0; p < PW; ++p) {
-        const int I = J + 1 + wave + NW * p;
-        if (I < NB) {
-#pragma unroll
-          for (int i = 0; i < 4; ++i) A[lidx(16 * I + 4 * i + q4, 16 * J + r16)] = -acc[p][i];
-        }
-      }
-      __syncthreads();
+      __syncthreads();  // X_.J visible to the next block column's products
     }
   }
   // X[r][c] (zero above the diagonal).
@@ -542,17 +558,28 @@ __device__ __forceinline__ void factor_unit(const Geo& g, int u, double* __restr
   // so no ill-conditioned unit escapes the refinement.
   if (may_refine) {
     double rs = 0.0, cs = 0.0;  // row prow's and column prow's absolute sums
-    for (int b = ppart; b < D; b += TPR) {
-      rs += fabs(xat(prow, b));
-      cs += fabs(xat(b, prow));
+#pragma unroll 8
+    for (int j = 0; j < D / TPR; ++j) {
+      const int b = ppart + TPR * j;
+      rs += fabs(b <= prow ? A[row_at(j)] : 0.0);
+      cs += fabs(b >= prow ? A[col_at(j)] : 0.0);
     }
 #pragma unroll
     for (int o = 1; o < TPR; o <<= 1) {
       rs += __shfl_xor(rs, o);
       cs += __shfl_xor(cs, o);
     }
-    const double xinf = block_max(rs);
-    const double x1 = block_max(cs);
+    // both maxima in one exchange (red_sh was last read before step 5's
+    // barriers)
+    const double wr = wave_max_f64(rs), wc = wave_max_f64(cs);
+    if (lane == 0) { red_sh[wave] = wr; red_sh2[wave] = wc; }
+    __syncthreads();
+    double xinf = red_sh[0], x1 = red_sh2[0];
+#pragma unroll
+    for (int w = 1; w < NT / 64; ++w) {
+      xinf = fmax(xinf, red_sh[w]);
+      x1 = fmax(x1, red_sh2[w]);
+    }
     if (anorm * x1 * xinf > kRefineCond) {
       if (tid == 0) atomicOr(uflags + u, kUnitRefine);
       return;  // pass 1 writes this unit's L^{-1}
