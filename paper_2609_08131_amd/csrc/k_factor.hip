@@ -89,11 +89,13 @@ __device__ __forceinline__ double row_bcast_f64_at(double v, int n) {
   }
 }
 
-// 1 / sqrt(x) to full fp64 accuracy: hardware estimate, two Newton steps.
+// 1 / sqrt(x): the hardware estimate (relative error 2^-24.2, measured on
+// the device) and Newton steps, one (2^-47.8) or two (2^-51.9, full fp64).
+template <bool FULL>
 __device__ __forceinline__ double rsqrt_f64(double x) {
   double y = __builtin_amdgcn_rsq(x);
   y = y * (1.5 - 0.5 * x * y * y);
-  y = y * (1.5 - 0.5 * x * y * y);
+  if constexpr (FULL) y = y * (1.5 - 0.5 * x * y * y);
   return y;
 }
 
@@ -174,7 +176,9 @@ __device__ __forceinline__ void store_lower_frags(uint16_t* __restrict__ out, F 
 // every thread). idg receives 1 / L_rr. Returns 0, or the flag that stopped
 // it -- kUnitNonfinite for a non-finite pivot, `fail` for a pivot at or below
 // piv_rel times its diagonal entry -- the same value in every thread.
-template <int D, int NT>
+// FULL: the pivots' reciprocal square roots to full fp64 accuracy; else to
+// 2^-47.8, for factors that are rounded to two bf16 terms afterwards.
+template <int D, int NT, bool FULL>
 __device__ __forceinline__ int cholesky_lds(double* A, const double* dg, double* idg, int* bad,
                                             double piv_rel, int fail) {
   constexpr int NB = D / 16;
@@ -200,7 +204,7 @@ __device__ __forceinline__ int cholesky_lds(double* A, const double* dg, double*
     // produced and discarded; the flag is the first failure's kind.
     bool failed = false, nonfinite = false;
     double piv = row_bcast_f64<0>(a[0]);  // A[t][t], from lane t of the row
-    double y = rsqrt_f64(piv);
+    double y = rsqrt_f64<FULL>(piv);
 #pragma unroll
     for (int t = 0; t < 16; ++t) {
       const bool ok = piv > thr[t] && piv > 0.0;
@@ -216,7 +220,7 @@ __device__ __forceinline__ int cholesky_lds(double* A, const double* dg, double*
       if (t + 1 < 16) {
         a[t + 1] = fma(-a[t], row_bcast_f64_at(a[t], t + 1), a[t + 1]);
         pn = row_bcast_f64_at(a[t + 1], t + 1);
-        yn = rsqrt_f64(pn);
+        yn = rsqrt_f64<FULL>(pn);
       }
 #pragma unroll
       for (int q = t + 2; q < 16; ++q) a[q] = fma(-a[t], row_bcast_f64_at(a[t], q), a[q]);
@@ -453,8 +457,11 @@ __device__ __forceinline__ void factor_unit(const Geo& g, int u, double* __restr
   }
 
   // ---------------- Cholesky A = L L^T (L overwrites the lower triangle) ----
+  // The first factorisation of bf16 inputs ends in two-term bf16 fragments
+  // of L^{-1}; the fp64 paths keep full precision.
   const int code =
-      cholesky_lds<D, NT>(A, dg, idg, &bad, piv_rel, may_refine ? (int)kUnitRefine : (int)kUnitSingular);
+      may_refine ? cholesky_lds<D, NT, false>(A, dg, idg, &bad, piv_rel, (int)kUnitRefine)
+                 : cholesky_lds<D, NT, true>(A, dg, idg, &bad, piv_rel, (int)kUnitSingular);
   if (code) {
     if (tid == 0) {
       if (code == (int)kUnitRefine) atomicOr(uflags + u, kUnitRefine);
@@ -754,7 +761,7 @@ __device__ __forceinline__ void qfactor_unit(const Geo& g, int u, const uint16_t
   __syncthreads();
   for (int a = tid; a < D; a += kFactorThreads) dg[a] = A[lidx(a, a)];
   __syncthreads();
-  if (cholesky_lds<D, kFactorThreads>(A, dg, idg, &bad, kPivRelTri, (int)kUnitKTile) != 0) {
+  if (cholesky_lds<D, kFactorThreads, false>(A, dg, idg, &bad, kPivRelTri, (int)kUnitKTile) != 0) {
     if (tid == 0) atomicOr(uflags + u, kUnitKTile);
     return;
   }
