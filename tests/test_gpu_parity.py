@@ -195,6 +195,20 @@ def test_ragged_small(jacap, dtype, d):
         check_case(case, 64, ridge, "diag", label=f"ragged/{dtype}/d{d}", jacap=jacap)
 
 
+@pytest.mark.parametrize("dtype,d", [("bf16", 128), ("fp32", 128), ("bf16", 64)])
+def test_more_units_than_compute_units(jacap, dtype, d):
+    """A batch of 288 units (more than the 256 compute units): the capacity
+    factorisation takes its four-wave shape, two workgroups per compute
+    unit, on the first pass (and on every unit of fp32 inputs); at ridge 0
+    many units go on to the fp64 path. Every unit against the oracle."""
+    lens = [(37 * i) % 200 + 1 for i in range(24)]
+    case = make_case("ragged16", seq_lens=lens, num_layers=3, num_kv_heads=4,
+                     num_q_heads=8, head_dim=d, window=8, dtype=dtype).to("cuda")
+    assert case.num_seqs * 3 * 4 == 288
+    for ridge in (1.0, 0.0):
+        check_case(case, 32, ridge, "diag", label=f"288 units/{dtype}/d{d}", jacap=jacap)
+
+
 def test_budget_edges(jacap):
     case = make_case("ragged16", device="cuda", seq_lens=[3, 40, 700], num_layers=1,
                      num_kv_heads=2, num_q_heads=2, head_dim=128, window=4)
