@@ -149,6 +149,8 @@ Workspace layout(const jacap_config* c, const jacap_batch* b, bool greedy = fals
     w.gc = take(8 * LHT);
     w.gst = take(4 * LHT);
     w.gent = take(sizeof(GreedyEntry) * U * nblk);
+    // the factor of Lambda_Q on the FULL covariance's triangular K pass
+    w.lfrag = take(w.mfma && c->cov_mode == JACAP_COV_FULL ? 2 * U * nlp * 2 * 64 * 8 : 8);
     w.total = o;
     return w;
   }

@@ -784,6 +784,9 @@ __global__ __launch_bounds__(kFactorThreads) void qfactor_kernel(Geo g, const ui
 hipError_t launch_qfactor(const Launch& L, const void* q) {
   const Geo& g = L.geo;
   if (g.U == 0) return hipSuccess;
+  // The fragments go to the L^{-1} fragment section, which every layout that
+  // can take this path reserves (offset 0 is the status word's).
+  if (L.ws.lfrag == 0) return hipErrorInvalidValue;
   auto go = [&](auto kern) {
     kern<<<g.U, kFactorThreads, 0, L.stream>>>(g, (const uint16_t*)q,
                                                 ws_ptr<double>(L.wsp, L.ws.mu),

@@ -142,6 +142,16 @@ def test_greedy_full_covariance(jacap):
     check_greedy(jacap, case, 128, cov_mode="full", label="full covariance")
 
 
+def test_greedy_full_covariance_triangular_path(jacap):
+    """FULL covariance with N_s = 2d pooled window queries and a unit of 9000
+    tokens: the greedy picks run on weights whose kappa comes from the
+    triangular factor of Lambda_Q (the eviction path's launches); the 700-token
+    units take the window tile."""
+    case = make_case("ragged16", device="cuda", seq_lens=(9000, 700), num_layers=1,
+                     num_kv_heads=2, num_q_heads=8, window=32, head_dim=64, dtype="bf16")
+    check_greedy(jacap, case, 96, cov_mode="full", label="full covariance, triangular path")
+
+
 def test_greedy_deterministic(jacap):
     case = make_case("llama8b_layer", device="cuda")
     a, _ = run_greedy(jacap, case, 512)

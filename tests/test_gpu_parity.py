@@ -185,6 +185,18 @@ def test_full_covariance_triangular_path(jacap, d, heads, window):
                    jacap=jacap)
 
 
+def test_full_covariance_triangular_path_per_head(jacap):
+    """Per-head GQA on the FULL triangular path: every query head is a unit of
+    its own with N_s = w = 128 = 2d window queries (d = 64), and the K rows of
+    a KV head are read by its G query-head units together (cached loads). A
+    sequence of 8200 tokens takes the triangular path, one of 500 the window
+    tile, in the same launch."""
+    case = make_case("ragged16", seq_lens=(8200, 500), num_layers=1, num_kv_heads=2,
+                     num_q_heads=4, window=128, head_dim=64, dtype="bf16").to("cuda")
+    check_case(case, 128, 1.0, "full", gqa="per_head", label="full-tri per-head d=64",
+               jacap=jacap)
+
+
 @pytest.mark.parametrize("dtype,d", [("bf16", 128), ("bf16", 64), ("fp32", 64), ("fp32", 128)])
 def test_ragged_small(jacap, dtype, d):
     lens = [0, 1, 17, 255, 256, 257, 1000, 8193]
