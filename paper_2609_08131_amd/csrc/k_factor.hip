@@ -667,10 +667,11 @@ hipError_t launch_factor(const Launch& L, bool refine) {
 // gives Lambda_Q = (P C P)(P C P)^T with P C P upper triangular, so
 // X = (P C P)^T, X[i][j] = C[d-1-j][d-1-i].
 //
-// Lambda_Q = (1/N_s) sum_r (q_r - mu)(q_r - mu)^T: the centred window rows
-// (fp64, kQRows at a time in LDS) go through the fp64 MFMA, each wave
-// accumulating its share of the 16x16 lower blocks in registers; the blocks
-// are then written to the factor's LDS layout already reversed.
+// Lambda_Q = (1/N_s) sum_r (q_r - mu)(q_r - mu)^T: the window (raw bf16, all
+// of it in LDS) goes through the fp64 MFMA, each row centred in fp64 as it is
+// read, each wave accumulating its share of the 16x16 lower blocks in
+// registers; the blocks are then written to the factor's LDS layout already
+// reversed.
 //
 // The unit is marked kUnitKTile (the K pass takes the window tile) if it has
 // fewer than kTriMinTokens tokens, non-finite window statistics, or a pivot at
@@ -679,7 +680,6 @@ hipError_t launch_factor(const Launch& L, bool refine) {
 // terms.
 // ---------------------------------------------------------------------------
 constexpr double kPivRelTri = 1e-3;
-constexpr int kQRows = 32;
 
 template <int D>
 __device__ __forceinline__ void qfactor_unit(const Geo& g, int u, const uint16_t* __restrict__ q,
@@ -690,8 +690,9 @@ __device__ __forceinline__ void qfactor_unit(const Geo& g, int u, const uint16_t
   constexpr int NPAIR = NB * (NB + 1) / 2;
   constexpr int NW = kFactorThreads / 64;
   constexpr int PW = (NPAIR + NW - 1) / NW;  // lower 16x16 blocks of Lambda_Q per wave
-  constexpr int QP = D + 16;  // doubles per staged row: the pad puts consecutive rows on the two halves of the banks
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  constexpr int QPB = D + 8;  // u16 per staged window row
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int r16 = lane & 15, q4 = lane >> 4;
   const Unit un = decode_unit(g, u);
   if (un.n == 0) return;
@@ -703,7 +704,7 @@ __device__ __forceinline__ void qfactor_unit(const Geo& g, int u, const uint16_t
   __shared__ double dg[D];
   __shared__ double idg[D];
   __shared__ double smu[D];
-  __shared__ double qc[kQRows * QP];
+  __shared__ __attribute__((aligned(16))) uint16_t qs[kFullMaxQ * QPB];  // the window, raw bf16
   __shared__ int bad;
 
   const int Ns = g.G * g.w;
@@ -711,35 +712,65 @@ __device__ __forceinline__ void qfactor_unit(const Geo& g, int u, const uint16_t
       q + un.b * g.qss + un.l * g.qsl + (int64_t)(un.h * g.V + un.s) * g.G * g.qsh;
   for (int c = tid; c < D; c += kFactorThreads) smu[c] = mu[(int64_t)u * D + c];
   if (tid == 0) bad = 0;
-  f64x4 acc[PW];
-#pragma unroll
-  for (int p = 0; p < PW; ++p) acc[p] = f64x4{0.0, 0.0, 0.0, 0.0};
-  for (int r0 = 0; r0 < Ns; r0 += kQRows) {
-    __syncthreads();  // the previous rows are consumed (and smu is visible)
-    for (int e = tid; e < kQRows * D; e += kFactorThreads) {
-      const int rr = e / D, c = e - rr * D, r = r0 + rr;
-      double x = 0.0;  // rows past N_s add nothing
-      if (r < Ns) {
-        const int gq = r / g.w, p = r - gq * g.w;
-        x = (double)bf16_to_f32(qb[gq * g.qsh + p * g.qsp + c]) - smu[c];
-      }
-      qc[rr * QP + c] = x;
+  // The whole window in one round of 16-byte loads (N_s <= kFullMaxQ rows),
+  // then the products over it with no further barrier. Rows N_s .. N_s4 - 1
+  // are padding and masked.
+  const int Ns4 = (Ns + 3) & ~3;
+  for (int e = tid; e < Ns4 * (D / 8); e += kFactorThreads) {
+    const int r = e / (D / 8), pc = e - r * (D / 8);
+    uint4 x = make_uint4(0u, 0u, 0u, 0u);
+    if (r < Ns) {
+      const int gq = r / g.w, p = r - gq * g.w;
+      x = *reinterpret_cast<const uint4*>(qb + gq * g.qsh + p * g.qsp + pc * 8);
     }
-    __syncthreads();
-    // block (bi, bj), bi >= bj: sum_r qc[r][16 bi + i] qc[r][16 bj + j], four
-    // rows per MFMA (lane (r16, q4) supplies row 4 s + q4, column r16 of each)
+    *reinterpret_cast<uint4*>(qs + r * QPB + pc * 8) = x;
+  }
+  __syncthreads();  // window and smu visible
+  // block (bi, bj), bi >= bj: sum_r (q_r - mu)[16 bi + i] (q_r - mu)[16 bj + j],
+  // four rows per MFMA (lane (r16, q4) supplies row 4 s + q4, column r16 of
+  // each), centred in fp64 as they are read; the wave's blocks take turns so
+  // that their accumulation chains interleave.
+  f64x4 acc[PW];
+  int cbi[PW], cbj[PW];
+  double mbi[PW], mbj[PW];
+  // A wave's slots past the last block repeat that block (no branch in the
+  // loop below); their sums are not stored.
+#pragma unroll
+  for (int p = 0; p < PW; ++p) {
+    acc[p] = f64x4{0.0, 0.0, 0.0, 0.0};
+    const int e = min(wave + NW * p, NPAIR - 1);
+    int bi, bj;
+    tri_index(e, bi, bj);
+    cbi[p] = 16 * bi + r16;
+    cbj[p] = 16 * bj + r16;
+    mbi[p] = smu[cbi[p]];
+    mbj[p] = smu[cbj[p]];
+  }
+  // Each row group's raw values are read while the previous group's MFMAs
+  // run (the last read repeats the last group and is not used).
+  uint16_t na[PW], nb[PW];
+#pragma unroll
+  for (int p = 0; p < PW; ++p) {
+    na[p] = qs[q4 * QPB + cbi[p]];
+    nb[p] = qs[q4 * QPB + cbj[p]];
+  }
+  for (int r = q4; r < Ns4; r += 4) {
+    uint16_t ca[PW], cb[PW];
+#pragma unroll
+    for (int p = 0; p < PW; ++p) { ca[p] = na[p]; cb[p] = nb[p]; }
+    const uint16_t* nrow = qs + min(r + 4, Ns4 - 4 + q4) * QPB;
 #pragma unroll
     for (int p = 0; p < PW; ++p) {
-      const int e = wave + NW * p;
-      if (e < NPAIR) {
-        int bi, bj;
-        tri_index(e, bi, bj);
+      na[p] = nrow[cbi[p]];
+      nb[p] = nrow[cbj[p]];
+    }
+    __builtin_amdgcn_sched_barrier(0);  // the next group's reads stay ahead of these MFMAs
+    const double live = r < Ns ? 1.0 : 0.0;  // a factor, not a branch
 #pragma unroll
-        for (int ks = 0; ks < kQRows / 4; ++ks) {
-          const double* row = qc + (4 * ks + q4) * QP;
-          acc[p] = mfma64(row[16 * bi + r16], row[16 * bj + r16], acc[p]);
-        }
-      }
+    for (int p = 0; p < PW; ++p) {
+      const double xa = ((double)bf16_to_f32(ca[p]) - mbi[p]) * live;
+      const double xb = (double)bf16_to_f32(cb[p]) - mbj[p];
+      acc[p] = mfma64(xa, xb, acc[p]);
     }
   }
   // Lambda_Q[row][col] (row >= col) goes to the reversed matrix at
