@@ -199,7 +199,8 @@ def phase_bytes(phase, case, budget, prob):
         "leverage": entries * (d * e + 8),                  # V rows, w; score out
         "select": entries * 4 + units * budget * 4,         # scores in; idx out
         "compact": 2 * kept * d * e * 2,                    # K, V rows in and out
-        "gram_reduce": None, "factor": units * npair * 256 * 8, "refine": None, "init": None,
+        "gram_reduce": None, "factor": units * npair * 256 * 8,  # each unit's Gram (fp64 size)
+        "refine": None, "init": None,
         "greedy_init": entries * (d * e + 4 + 12),          # V rows, w; c, stamp out
         "greedy": None,
     }.get(phase)

@@ -346,9 +346,9 @@ enum jacap_phase {
   JACAP_PHASE_KPASS = 2,       /* centre logits and query response per token */
   JACAP_PHASE_WEIGHTS = 3,     /* softmax normaliser and Eq. 8 weights */
   JACAP_PHASE_GRAM = 4,        /* weighted Gram partials (Eq. 9) */
-  JACAP_PHASE_GRAM_REDUCE = 5, /* fixed-order sum of the Gram partials */
+  JACAP_PHASE_GRAM_REDUCE = 5, /* fixed-order sum of the Gram partials (units of many chunks) */
   JACAP_PHASE_FACTOR = 6,      /* Cholesky factor and L^{-1} */
-  JACAP_PHASE_REFINE = 7,      /* exact-split Gram, reduce and factor of ill-conditioned units */
+  JACAP_PHASE_REFINE = 7,      /* fp64 Gram, factor and leverage of ill-conditioned units */
   JACAP_PHASE_LEVERAGE = 8,    /* leverage scores (Eq. 10) */
   JACAP_PHASE_SELECT = 9,      /* TOP-B selection */
   JACAP_PHASE_COMPACT = 10,    /* K/V compaction */

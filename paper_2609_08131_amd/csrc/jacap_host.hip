@@ -239,7 +239,7 @@ jacap_status score_pass(const Launch& L, const void* q, const void* k, const voi
   JACAP_PHASE(JACAP_PHASE_KPASS, launch_kpass(L, k, mu ? nullptr : q));
   JACAP_PHASE(JACAP_PHASE_WEIGHTS, launch_softmax_weights(L));
   JACAP_PHASE(JACAP_PHASE_GRAM, launch_gram(L, v, false));
-  JACAP_PHASE(JACAP_PHASE_GRAM_REDUCE, launch_gram_reduce(L, false));
+  if (gram_reduced(L)) JACAP_PHASE(JACAP_PHASE_GRAM_REDUCE, launch_gram_reduce(L));
   JACAP_PHASE(JACAP_PHASE_FACTOR, launch_factor(L, false));
   if (L.ws.mfma) {  // the units marked by the factorisation, again in fp64
     TimedPhase tp(L.stream, JACAP_PHASE_REFINE, L.timed);

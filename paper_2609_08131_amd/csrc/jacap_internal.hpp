@@ -171,8 +171,9 @@ struct Workspace {
   size_t kept;     // int32  [B][L][H][budget] kept positions, staged by jacap_select_evicted
   size_t gram;     // per-chunk partial Grams: [U][gchunks][NPAIR*256] fp32 (bf16 MFMA pass)
                    // or [U][pchunks][NPAIR*256] fp64 (fp64 pass); one buffer for both
-  size_t gram_red; // double [U][NPAIR*256]  reduced Gram, block-lane layout; after an fp64
-                   // factorisation, L^{-1} in the lower-block layout (see k_factor.hip)
+  size_t gram_red; // double [U][NPAIR*256]  the reduced Gram (gram_reduced), block-lane
+                   // layout; after an fp64 factorisation, L^{-1} in the lower-block
+                   // layout (see k_factor.hip)
   size_t lfrag;    // bf16 [U][NLP][2][64][8] L^{-1} hi/lo MFMA B fragments, bf16 path
   size_t gc;       // double [L][H][T]       greedy: c_i when last computed
   size_t gst;      // int32  [L][H][T]       greedy: picks made at that time (-1 = taken)
@@ -375,7 +376,15 @@ hipError_t launch_qfactor(const Launch& L, const void* q);
 hipError_t launch_softmax_weights(const Launch& L);
 hipError_t launch_head_mean(const Launch& L, const float* hs, float* scores);
 hipError_t launch_gram(const Launch& L, const void* v, bool refine);
-hipError_t launch_gram_reduce(const Launch& L, bool refine);
+// The first factorisation sums each unit's Gram partials itself when units
+// have at most kFactorSumChunks chunks (the loads of a few chunks stay in
+// flight together); with more, a reduce kernel sums them over many
+// workgroups first and the factorisation reads the reduced Gram.
+constexpr int kFactorSumChunks = 4;
+inline bool gram_reduced(const Launch& L) {
+  return (L.ws.mfma ? L.ws.gchunks : L.ws.pchunks) > kFactorSumChunks;
+}
+hipError_t launch_gram_reduce(const Launch& L);
 hipError_t launch_factor(const Launch& L, bool refine);
 hipError_t launch_leverage(const Launch& L, const void* v, float* scores);
 hipError_t launch_leverage_precise(const Launch& L, const void* v, float* scores);

@@ -3,14 +3,16 @@
 // the triangular inverse L^{-1}, one workgroup per unit, in fp64 in LDS.
 // ||L^{-1} v||^2 = v^T A^{-1} v is what the leverage score of Eq. 10 needs.
 //
-// Input: the reduced Gram in block-lane layout (upper 16x16 blocks, see
-// k_gram.hip). Output, after the first factorisation of an fp32-accumulated
+// Input: the unit's Gram in block-lane layout (upper 16x16 blocks, see
+// k_gram.hip): its per-chunk partials, summed here in chunk order in fp64, or
+// (units of many chunks) the reduce kernel's sum of them. Output, after the
+// first factorisation of an fp32-accumulated
 // Gram (bf16 inputs): L^{-1} rounded to fp32 and split into bf16 hi + lo
 // terms, stored directly in the per-lane B-fragment order of the 16x16x32
 // MFMA (only the K-blocks that touch the lower triangle). After a
 // factorisation of an fp64 Gram (fp32 inputs; the bf16 units marked for the
-// fp64 path): L^{-1} in fp64, written over the unit's reduced Gram in the
-// lower-block layout -- block pair p = pair_index(i, j), i <= j, holds the
+// fp64 path): L^{-1} in fp64, over the unit's slot of the reduced-Gram buffer
+// in the lower-block layout -- block pair p = pair_index(i, j), i <= j, holds the
 // 16x16 block X[16 j + r][16 i + c] at p * 256 + 16 r + c (zero above the
 // diagonal of a diagonal block).
 //
@@ -309,14 +311,18 @@ __device__ __forceinline__ int cholesky_lds(double* A, const double* dg, double*
   return 0;
 }
 
-// One unit. PASS 0: first factorisation (all units), from the reduced Gram
-// `red`. PASS 1: a unit marked kUnitRefine by pass 0 (bf16 path), from its fp64
-// partial Grams `part` (pchunks per unit), summed here in chunk order. FRAGS:
-// bf16 inputs.
+// One unit. Its Gram: PASS 0 (all units) reads the reduced Gram `red` if the
+// reduce kernel ran (`reduced`), else sums here, in chunk order, in fp64, the
+// fp32 MFMA partials `part32` (bf16 inputs; gchunks per unit of gchunk tokens)
+// or the fp64 partials `part` (fp32 inputs; pchunks of pchunk tokens) -- the
+// reduce kernel's arithmetic; PASS 1 (the units of bf16 inputs that pass 0
+// marked kUnitRefine) sums its fp64 partials. FRAGS: bf16 inputs.
 template <int D, bool FRAGS, int NT>
 __device__ __forceinline__ void factor_unit(const Geo& g, int u, double* __restrict__ red,
                                             const double* __restrict__ part, int pchunks,
-                                            int pchunk, double ridge,
+                                            int pchunk, const float* __restrict__ part32,
+                                            int gchunks, int gchunk, bool reduced,
+                                            double ridge,
                                             const double* __restrict__ wscale, int pass,
                                             uint16_t* __restrict__ lfrag, uint32_t* status,
                                             uint32_t* uflags) {
@@ -341,21 +347,40 @@ __device__ __forceinline__ void factor_unit(const Geo& g, int u, double* __restr
   // Lower triangle of A = ridge I + M from the upper blocks of M. Entries
   // (2 e', 2 e' + 1) share a block pair and a lane: each thread loads its
   // pairs first (all loads in flight), then places them.
-  const double* R = red + (int64_t)u * (NPAIR * 256);
   constexpr int NE2 = NPAIR * 128;  // entry pairs
   constexpr int PER = (NE2 + NT - 1) / NT;
   double2 rv[PER];
-  if (part == nullptr) {
+  // Fixed-order sum of the unit's partials (the chunk loop unrolled so that
+  // about 18 of a thread's loads are in flight; more spills registers).
+  constexpr int CHU = PER <= 9 ? 2 : 1;
+#pragma unroll
+  for (int k = 0; k < PER; ++k) rv[k] = make_double2(0.0, 0.0);
+  if (reduced && pass == 0) {
+    const double2* R = reinterpret_cast<const double2*>(red + (int64_t)u * (NPAIR * 256));
 #pragma unroll
     for (int k = 0; k < PER; ++k) {
       const int e2 = tid + k * NT;
-      if (e2 < NE2) rv[k] = reinterpret_cast<const double2*>(R)[e2];
+      if (e2 < NE2) rv[k] = R[e2];
     }
-  } else {  // fixed-order sum of the unit's fp64 partials
+  } else if (may_refine) {  // fp32 MFMA partials
+    const int nch = (un.n + gchunk - 1) / gchunk;
+    const float2* P = reinterpret_cast<const float2*>(part32 + (int64_t)u * gchunks * (NPAIR * 256));
+#pragma unroll CHU
+    for (int c = 0; c < nch; ++c) {
+#pragma unroll
+      for (int k = 0; k < PER; ++k) {
+        const int e2 = tid + k * NT;
+        if (e2 < NE2) {
+          const float2 x = P[(int64_t)c * NE2 + e2];
+          rv[k].x += (double)x.x;
+          rv[k].y += (double)x.y;
+        }
+      }
+    }
+  } else {  // fp64 partials
     const int nch = (un.n + pchunk - 1) / pchunk;
     const double2* P = reinterpret_cast<const double2*>(part + (int64_t)u * pchunks * (NPAIR * 256));
-#pragma unroll
-    for (int k = 0; k < PER; ++k) rv[k] = make_double2(0.0, 0.0);
+#pragma unroll CHU
     for (int c = 0; c < nch; ++c) {
 #pragma unroll
       for (int k = 0; k < PER; ++k) {
@@ -594,7 +619,7 @@ __device__ __forceinline__ void factor_unit(const Geo& g, int u, double* __restr
   }
 
   // Store L^{-1}.
-  if (!may_refine) {  // fp64, over the reduced Gram (already in LDS)
+  if (!may_refine) {  // fp64, over the unit's slot of the reduced-Gram buffer
     double* o64 = red + (int64_t)u * (NPAIR * 256);
     for (int e = tid; e < NPAIR * 256; e += NT) {
       int p = e >> 8, bi = 0;  // block pair p -> (bi, bj), bi <= bj
@@ -617,12 +642,13 @@ __device__ __forceinline__ void factor_unit(const Geo& g, int u, double* __restr
 template <int D, bool FRAGS, int NT>
 __global__ __launch_bounds__(NT, 512 / NT) void factor_kernel(
     Geo g, double* __restrict__ red, const double* __restrict__ part, int pchunks, int pchunk,
-    double ridge, const double* __restrict__ wscale, int pass, uint16_t* __restrict__ lfrag,
-    uint32_t* status, uint32_t* uflags) {
+    const float* __restrict__ part32, int gchunks, int gchunk, int reduced, double ridge,
+    const double* __restrict__ wscale, int pass, uint16_t* __restrict__ lfrag, uint32_t* status,
+    uint32_t* uflags) {
   for (int u = blockIdx.x; u < g.U; u += gridDim.x) {
     if (pass == 1 && !(uflags[u] & kUnitRefine)) continue;
-    factor_unit<D, FRAGS, NT>(g, u, red, pass == 1 ? part : nullptr, pchunks, pchunk, ridge,
-                              wscale, pass, lfrag, status, uflags);
+    factor_unit<D, FRAGS, NT>(g, u, red, part, pchunks, pchunk, part32, gchunks, gchunk,
+                              reduced != 0, ridge, wscale, pass, lfrag, status, uflags);
     __syncthreads();  // LDS of this unit fully consumed before the next one's loads
   }
 }
@@ -637,12 +663,16 @@ hipError_t launch_factor(const Launch& L, bool refine) {
   uint32_t* uf = ws_ptr<uint32_t>(L.wsp, L.ws.uflags);
   const double* wsc = ws_ptr<double>(L.wsp, L.ws.wscale);
   const double ridge = (double)L.cfg->ridge;
+  // the Gram partials: fp64 (fp32 inputs, and the refine pass), fp32 (the
+  // first pass of bf16 inputs); both in the Gram buffer
   const double* part = ws_ptr<double>(L.wsp, L.ws.gram);
+  const float* part32 = ws_ptr<float>(L.wsp, L.ws.gram);
   const int blocks = refine ? std::min(g.U, kRefineBlocks) : g.U;
   const bool pairs = !refine && g.U > kComputeUnits;  // two workgroups per compute unit
   auto go = [&](auto kern, int nt) {
-    kern<<<blocks, nt, 0, L.stream>>>(g, red, part, L.ws.pchunks, L.ws.pchunk, ridge, wsc, pass,
-                                      lf, st, uf);
+    kern<<<blocks, nt, 0, L.stream>>>(g, red, part, L.ws.pchunks, L.ws.pchunk, part32,
+                                      L.ws.gchunks, L.ws.gchunk, gram_reduced(L) ? 1 : 0, ridge,
+                                      wsc, pass, lf, st, uf);
   };
   if (L.ws.mfma) {
     if (g.D == 128) pairs ? go(factor_kernel<128, true, 256>, 256) : go(factor_kernel<128, true, 512>, 512);

@@ -1,6 +1,7 @@
 // Weighted Gram M = sum_i w_i v_i v_i^T over a unit's tokens (the data term of
 // the capacity matrix, Eq. 9), as one partial per workgroup (a chunk of
-// tokens) that the reduce kernel adds in a fixed order.
+// tokens), added in a fixed order by the factorisation itself or, for units
+// of many chunks, by the reduce kernel below.
 //
 // Partial layout ("block-lane"): the upper-triangular 16x16 blocks (i <= j) of
 // M, block pair p = pair_index(i, j), 256 entries per block in MFMA 16x16
@@ -440,11 +441,11 @@ __global__ __launch_bounds__(kThreads) void gram_reduce_kernel(Geo g, const P* _
   red[(int64_t)u * (NPAIR * 256) + p * 256 + threadIdx.x] = s;
 }
 
-// refine: nothing to launch (the fp64 path's second factorisation sums its
-// own partials).
-hipError_t launch_gram_reduce(const Launch& L, bool refine) {
+// Batches whose units have more than kFactorSumChunks chunks; with fewer the
+// first factorisation sums its unit's partials itself (see launch_factor).
+hipError_t launch_gram_reduce(const Launch& L) {
   const Geo& g = L.geo;
-  if (refine) return hipSuccess;
+  if (!gram_reduced(L)) return hipSuccess;
   const int NB = g.D / 16, npair = NB * (NB + 1) / 2;
   const dim3 grid(g.U, npair);
   double* red = ws_ptr<double>(L.wsp, L.ws.gram_red);

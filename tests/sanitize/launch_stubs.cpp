@@ -29,7 +29,7 @@ hipError_t launch_kpass(const Launch& L, const void*, const void*) { return note
 hipError_t launch_softmax_weights(const Launch& L) { return note(stub::kWeights, L); }
 hipError_t launch_head_mean(const Launch& L, const float*, float*) { return note(stub::kHeadMean, L); }
 hipError_t launch_gram(const Launch& L, const void*, bool) { return note(stub::kGram, L); }
-hipError_t launch_gram_reduce(const Launch& L, bool) { return note(stub::kGramReduce, L); }
+hipError_t launch_gram_reduce(const Launch& L) { return note(stub::kGramReduce, L); }
 hipError_t launch_factor(const Launch& L, bool) { return note(stub::kFactor, L); }
 hipError_t launch_leverage(const Launch& L, const void*, float*) { return note(stub::kLeverage, L); }
 hipError_t launch_leverage_precise(const Launch& L, const void*, float*) { return note(stub::kLeveragePrecise, L); }
