@@ -191,9 +191,15 @@ jacap_status jacap_workspace_size(const jacap_config* cfg, const jacap_batch* ba
  * flags first. Precision: with bf16 inputs A is accumulated in fp32 from
  * exact bf16 products of a two-term split of w_i v_i, and the leverage
  * products use a two-term bf16 L^{-1}; a unit whose capacity matrix the fp64
- * factorisation finds ill-conditioned (a bound on cond(A) above 2e3, or a
+ * factorisation finds ill-conditioned (a bound on cond(A) above 2e4, or a
  * pivot below 1e-4 of its diagonal entry) is recomputed in fp64 throughout
- * (Gram, Cholesky, L^{-1} v). fp32 inputs take the fp64 path for every unit. */
+ * (Gram, Cholesky, L^{-1} v). fp32 inputs take the fp64 path for every unit.
+ * FULL covariance with bf16 keys: kappa_i = k_i^T Lambda_Q k_i comes either
+ * from the bf16 MFMA tile of the keys against the window queries (exact
+ * products, fp32 sums) or, for units of at least 8192 tokens with at least
+ * 2d window queries, as ||X k_i||^2 with Lambda_Q = X^T X factored in fp64 and
+ * X held in two bf16 terms; a numerically rank-deficient Lambda_Q (a pivot
+ * at most 1e-3 of its diagonal entry) keeps the tile. */
 jacap_status jacap_score(const jacap_config* cfg, const jacap_batch* batch,
                          const void* q_win, const void* k, const void* v, float* scores,
                          void* ws, size_t ws_bytes, void* stream);
