@@ -325,6 +325,17 @@ __global__ __launch_bounds__(kThreads) void gram_precise_kernel(
   constexpr int NPAIR = NB * (NB + 1) / 2;
   __shared__ float vs[32][D];
   __shared__ double ws[32];
+  if constexpr (REFINE_ONLY) {
+    // The flags of all the walk's items at once (a load per thread, not one
+    // per item in turn): a workgroup with no marked unit ends here.
+    bool any = false;
+    for (int item = blockIdx.x + threadIdx.x * gridDim.x; item < items;
+         item += gridDim.x * kThreads) {
+      int u, chunk;
+      any |= grid_unit_chunk_at<true>(g, pchunks, item, u, chunk) && (uflags[u] & kUnitRefine);
+    }
+    if (!__syncthreads_or(any)) return;
+  }
   // one (unit, chunk) item per workgroup, or (REFINE_ONLY) a grid-stride walk
   for (int item = blockIdx.x; item < items; item += gridDim.x) {
   int u, chunk;

@@ -171,6 +171,17 @@ __global__ __launch_bounds__(kThreads) void leverage_precise_kernel(
   constexpr int TOK = kThreads / TPT;    // tokens per tile
   __shared__ double X[D * LD];
   __shared__ float vs[TOK][D + 1];  // padded: the wave's 8 token rows in distinct banks
+  if constexpr (REFINE_ONLY) {
+    // The flags of all the walk's items at once (a load per thread, not one
+    // per item in turn): a workgroup with no marked unit ends here.
+    bool any = false;
+    for (int item = blockIdx.x + threadIdx.x * gridDim.x; item < items;
+         item += gridDim.x * kThreads) {
+      int u, chunk;
+      any |= grid_unit_chunk_at<true>(g, lchunks, item, u, chunk) && (uflags[u] & kUnitRefine);
+    }
+    if (!__syncthreads_or(any)) return;
+  }
   // one (unit, chunk) item per workgroup, or (REFINE_ONLY) a grid-stride walk
   for (int item = blockIdx.x; item < items; item += gridDim.x) {
   int u, chunk;
